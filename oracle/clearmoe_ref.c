@@ -1,0 +1,229 @@
+/*
+ * CPU oracle of the CLEAR-MoE FFN forward (arxiv 2606.28516).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg load this library.  The GPU library never
+ * links, calls or includes anything from here, and this file includes nothing
+ * of the GPU library's.
+ *
+ * Everything is computed in IEEE double from the stored inputs (float32, or
+ * bfloat16 widened exactly by the caller), with plain loops, no blocking and
+ * no reordering beyond the definition.  OpenMP only splits independent tokens.
+ *
+ * Paper passages followed:
+ *   router        Sec. III Phase 4 (linear router; Table C5 counts its bias),
+ *                 Algorithm 3 step "a <- argmax(g(x))"
+ *   top-k / gates Appendix A glossary (router = distribution, top-k < E);
+ *                 top-2 with the selected softmax renormalised
+ *   dispatch      Sec. III "Dispatch Backends" (Grouped: sort tokens by expert
+ *                 index, contiguous sub-batches); Algorithm 3 sort step
+ *   fc1 + GELU    Eq. (2), z = GELU(fc1(x)); Algorithm 3 first step
+ *   shared basis  Eq. (2) with W_shared = U_r Sigma_r V_r^T (Sec. III Phase 3),
+ *                 applied as (z V_r)(U_r Sigma_r)^T
+ *   residual      Eq. (2) residual term; Algorithm 3 per-expert step, here
+ *                 token by token with a mask (the paper's Naive backend style)
+ *   output        Algorithm 3 last step, y = h_sh + h_res
+ *
+ * Readings where the paper is silent (router bias, tie-break, gate weighting,
+ * stable order, b2 placement, exact-erf GELU, low-rank residual factors) are
+ * listed in the design notes; each function states the one it uses.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+int ref_num_threads(void) {
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+void ref_set_num_threads(int n) {
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
+/* Exact-erf GELU, v * Phi(v) = 0.5 v (1 + erf(v / sqrt 2)). */
+double ref_gelu(double v) { return 0.5 * v * (1.0 + erf(v * M_SQRT1_2)); }
+
+/* Router logits l[t,e] = sum_d x[t,d] Wg[e,d] + bg[e]  (bg may be NULL). */
+void ref_router_logits(int64_t T, int D, int E, const double* x, const double* Wg,
+                       const double* bg, double* logits) {
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t) {
+        for (int e = 0; e < E; ++e) {
+            double s = 0.0;
+            for (int d = 0; d < D; ++d) s += x[t * D + d] * Wg[(int64_t)e * D + d];
+            logits[t * E + e] = s + (bg ? bg[e] : 0.0);
+        }
+    }
+}
+
+/* Top-k: experts ordered by logit descending, ties to the lower index; slot 0
+ * is the best.  Gates: softmax over the k selected logits,
+ * gate_j = exp(l_(j) - l_(0)) / sum_{i<k} exp(l_(i) - l_(0)); k = 1 gives 1. */
+void ref_topk(int64_t T, int E, int k, const double* logits, int32_t* idx, double* gate) {
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t) {
+        const double* l = logits + t * E;
+        int taken[64];
+        memset(taken, 0, sizeof taken);
+        for (int j = 0; j < k; ++j) {
+            int best = -1;
+            for (int e = 0; e < E; ++e) {
+                if (taken[e]) continue;
+                if (best < 0 || l[e] > l[best]) best = e;   /* strict: ties keep lower e */
+            }
+            taken[best] = 1;
+            idx[t * k + j] = best;
+        }
+        double den = 0.0;
+        for (int j = 0; j < k; ++j) den += exp(l[idx[t * k + j]] - l[idx[t * k]]);
+        for (int j = 0; j < k; ++j) gate[t * k + j] = exp(l[idx[t * k + j]] - l[idx[t * k]]) / den;
+    }
+}
+
+/* Dispatch by direct counting.  Assignment a = t*k + j goes to expert idx[a].
+ * counts[e] = #{a : idx[a] = e};  offsets[0] = 0, offsets[e+1] = offsets[e] + counts[e];
+ * perm lists, expert by expert, the assignments of that expert in ascending a
+ * (a stable sort by expert); inv is the inverse of perm.  Returns -1 if an
+ * index is outside [0, E), else 0. */
+int ref_dispatch(int64_t T, int E, int k, const int32_t* idx, int32_t* counts,
+                 int32_t* offsets, int32_t* perm, int32_t* inv) {
+    const int64_t A = T * k;
+    for (int e = 0; e < E; ++e) counts[e] = 0;
+    for (int64_t a = 0; a < A; ++a) {
+        if (idx[a] < 0 || idx[a] >= E) return -1;
+        counts[idx[a]]++;
+    }
+    offsets[0] = 0;
+    for (int e = 0; e < E; ++e) offsets[e + 1] = offsets[e] + counts[e];
+    int64_t p = 0;
+    for (int e = 0; e < E; ++e)
+        for (int64_t a = 0; a < A; ++a)
+            if (idx[a] == e) { perm[p] = (int32_t)a; inv[a] = (int32_t)p; ++p; }
+    return 0;
+}
+
+/* Row copy into expert order: xperm[p, :] = x[perm[p] / k, :]. */
+void ref_permute_rows(int64_t T, int D, int k, const double* x, const int32_t* perm, double* xperm) {
+    for (int64_t p = 0; p < T * k; ++p)
+        memcpy(xperm + p * D, x + (int64_t)(perm[p] / k) * D, sizeof(double) * (size_t)D);
+}
+
+/* z[t,h] = GELU(sum_d x[t,d] W1[h,d] + b1[h])  (b1 may be NULL). */
+void ref_fc1_gelu(int64_t T, int D, int H, const double* x, const double* W1, const double* b1,
+                  double* z) {
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t)
+        for (int h = 0; h < H; ++h) {
+            double s = 0.0;
+            for (int d = 0; d < D; ++d) s += x[t * D + d] * W1[(int64_t)h * D + d];
+            z[t * H + h] = ref_gelu(s + (b1 ? b1[h] : 0.0));
+        }
+}
+
+/* Shared path h_sh = (z Vt^T) US^T + b2, with Vt = V_r^T [r,H] and
+ * US = U_r diag(S_r) [D,r]; the fc2 bias is added once, here (b2 may be NULL). */
+void ref_shared(int64_t T, int D, int H, int r, const double* z, const double* Vt,
+                const double* US, const double* b2, double* hsh) {
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t) {
+        double* tv = (double*)malloc(sizeof(double) * (size_t)(r > 0 ? r : 1));
+        for (int i = 0; i < r; ++i) {
+            double s = 0.0;
+            for (int h = 0; h < H; ++h) s += z[t * H + h] * Vt[(int64_t)i * H + h];
+            tv[i] = s;
+        }
+        for (int d = 0; d < D; ++d) {
+            double s = 0.0;
+            for (int i = 0; i < r; ++i) s += tv[i] * US[(int64_t)d * r + i];
+            hsh[t * D + d] = s + (b2 ? b2[d] : 0.0);
+        }
+        free(tv);
+    }
+}
+
+/* Residual experts, token by token (no permutation):
+ * for each slot j, e = idx[t,j]:  h_res[t] += gate[t,j] * ((z_t Q_e^T) P_e^T),
+ * with Q [E,q,H] and P [E,D,q].  Expert e's full residual is P_e Q_e. */
+void ref_residual(int64_t T, int D, int H, int E, int k, int q, const double* z,
+                  const double* Q, const double* P, const int32_t* idx, const double* gate,
+                  double* hres) {
+    (void)E;
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t) {
+        double* u = (double*)malloc(sizeof(double) * (size_t)(q > 0 ? q : 1));
+        for (int d = 0; d < D; ++d) hres[t * D + d] = 0.0;
+        for (int j = 0; j < k; ++j) {
+            const int e = idx[t * k + j];
+            const double g = gate[t * k + j];
+            const double* Qe = Q + (int64_t)e * q * H;
+            const double* Pe = P + (int64_t)e * D * q;
+            for (int i = 0; i < q; ++i) {
+                double s = 0.0;
+                for (int h = 0; h < H; ++h) s += z[t * H + h] * Qe[(int64_t)i * H + h];
+                u[i] = s;
+            }
+            for (int d = 0; d < D; ++d) {
+                double s = 0.0;
+                for (int i = 0; i < q; ++i) s += u[i] * Pe[(int64_t)d * q + i];
+                hres[t * D + d] += g * s;
+            }
+        }
+        free(u);
+    }
+}
+
+/* Whole layer: route, fc1+GELU, shared basis, residual, y = h_sh + h_res.
+ * Writes y [T,D]; idx/gate/logits if non-NULL.  Returns 0, or -1 on bad shape. */
+int ref_ffn_forward(int64_t T, int D, int H, int E, int k, int r, int q,
+                    const double* x, const double* W1, const double* b1,
+                    const double* US, const double* Vt, const double* b2,
+                    const double* P, const double* Q, const double* Wg, const double* bg,
+                    double* y, int32_t* idx_out, double* gate_out, double* logits_out) {
+    if (T < 0 || D <= 0 || H <= 0 || E < 1 || E > 64 || k < 1 || k > E || r < 0 || q < 0)
+        return -1;
+    double* logits = (double*)malloc(sizeof(double) * (size_t)(T * E + 1));
+    int32_t* idx = (int32_t*)malloc(sizeof(int32_t) * (size_t)(T * k + 1));
+    double* gate = (double*)malloc(sizeof(double) * (size_t)(T * k + 1));
+    double* z = (double*)malloc(sizeof(double) * (size_t)(T * H + 1));
+    double* hres = (double*)malloc(sizeof(double) * (size_t)(T * D + 1));
+    if (!logits || !idx || !gate || !z || !hres) {
+        free(logits); free(idx); free(gate); free(z); free(hres);
+        return -2;
+    }
+    ref_router_logits(T, D, E, x, Wg, bg, logits);
+    ref_topk(T, E, k, logits, idx, gate);
+    ref_fc1_gelu(T, D, H, x, W1, b1, z);
+    ref_shared(T, D, H, r, z, Vt, US, b2, y);
+    ref_residual(T, D, H, E, k, q, z, Q, P, idx, gate, hres);
+    for (int64_t i = 0; i < T * D; ++i) y[i] += hres[i];
+    if (idx_out) memcpy(idx_out, idx, sizeof(int32_t) * (size_t)(T * k));
+    if (gate_out) memcpy(gate_out, gate, sizeof(double) * (size_t)(T * k));
+    if (logits_out) memcpy(logits_out, logits, sizeof(double) * (size_t)(T * E));
+    free(logits); free(idx); free(gate); free(z); free(hres);
+    return 0;
+}
+
+/* Inverse-permute combine: y[t,:] = sum_j gate[t,j] * ye[inv[t*k+j], :]
+ * (ye in expert order, one row per assignment). */
+void ref_combine(int64_t T, int D, int k, const double* ye, const int32_t* inv,
+                 const double* gate, double* y) {
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t)
+        for (int d = 0; d < D; ++d) {
+            double s = 0.0;
+            for (int j = 0; j < k; ++j) s += gate[t * k + j] * ye[(int64_t)inv[t * k + j] * D + d];
+            y[t * D + d] = s;
+        }
+}
