@@ -1,0 +1,129 @@
+/*
+ * clearmoe.h -- C ABI of the CLEAR-MoE FFN forward on MI355X (gfx950).
+ *
+ * The layer (arxiv 2606.28516, Eq. 2 and Algorithm 3):
+ *     z     = GELU(x W1^T + b1)                       shared fc1, all tokens
+ *     h_sh  = (z Vt^T) US^T + b2                      shared SVD basis of fc2,
+ *                                                     US = U_r diag(S_r), Vt = V_r^T
+ *     a     = top-k of the linear router x Wg^T + bg  (k = 1: Algorithm 3's argmax)
+ *     h_res = sum_j gate_j (z Q_{a_j}^T) P_{a_j}^T    per-expert residual, rank q
+ *     y     = h_sh + h_res
+ *
+ * Conventions shared by every entry point
+ *   - Every tensor pointer is a DEVICE pointer owned by the caller; the
+ *     library never allocates, frees or keeps a pointer after a call returns.
+ *   - Matrices are row-major and contiguous.  Weights are stored [out, in]
+ *     (the nn.Linear convention), so every product is A[M,K] B[N,K]^T.
+ *   - x, W1, US, Vt, P, Q, Wg, ye and y have element type shape->dtype
+ *     (CLEARMOE_F32 = float, CLEARMOE_BF16 = bfloat16 bits).  Biases and gates
+ *     are always float32; index arrays are int32.  A NULL bias means zero.
+ *   - Scratch memory comes from the caller's workspace `ws` of `ws_bytes`
+ *     bytes, at least clearmoe_workspace_bytes(shape), 256-byte aligned.
+ *   - All work is enqueued on `stream`; nothing is synchronised and nothing is
+ *     copied to the host.  The call returns once the kernels are enqueued.
+ *   - Arguments are checked on the host before anything is launched: shapes
+ *     (T >= 0; D, H >= 1; 1 <= k <= E <= 64; 0 <= r, q <= min(D, H);
+ *     T*k < 2^31; D, H, r, q multiples of 8 for bf16 and of 4 for float32),
+ *     required pointers non-NULL and 16-byte aligned, the workspace large
+ *     enough.  A failed check returns its status and has no side effect.  A
+ *     launch failure returns CLEARMOE_ERR_HIP (hipGetLastError).
+ *   - No C++ exception crosses this interface.  Calls on one stream are
+ *     ordered; calls that share a workspace must not overlap in time.
+ */
+#ifndef CLEARMOE_H
+#define CLEARMOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    CLEARMOE_OK = 0,
+    CLEARMOE_ERR_INVALID_ARG = 1,   /* bad shape, NULL or misaligned pointer */
+    CLEARMOE_ERR_UNSUPPORTED = 2,   /* valid but not handled (e.g. dtype) */
+    CLEARMOE_ERR_WORKSPACE = 3,     /* ws NULL or smaller than required */
+    CLEARMOE_ERR_HIP = 4            /* a kernel launch failed */
+} clearmoe_status;
+
+typedef enum { CLEARMOE_F32 = 0, CLEARMOE_BF16 = 1 } clearmoe_dtype;
+
+/* Layer shape.  T tokens, D model width, H fc1 width (d_ffn), E experts,
+ * k experts per token, r shared SVD rank, q residual rank per expert. */
+typedef struct {
+    int32_t T, D, H, E, k, r, q;
+    int32_t dtype;                 /* clearmoe_dtype */
+} clearmoe_shape;
+
+/* Flags of clearmoe_dispatch. */
+#define CLEARMOE_DISPATCH_HIST_IN_WS 1u  /* ws already holds the per-tile expert
+                                            histogram of idx, as left there by
+                                            clearmoe_route with the same shape */
+
+/* Library version, (major << 16) | minor. */
+int clearmoe_version(void);
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* clearmoe_status_string(int status);
+
+/* Bytes of workspace clearmoe_ffn_forward needs for this shape (the largest of
+ * all entry points); 0 if the shape is invalid. */
+size_t clearmoe_workspace_bytes(const clearmoe_shape* shape);
+
+/* Router and top-k (Sec. III Phase 4 linear router, with the bias counted in
+ * Table C5; Algorithm 3 "a <- argmax(g(x))"; top-k with renormalised softmax
+ * gates).
+ *   x   [T, D], Wg [E, D] (dtype); bg [E] float32 or NULL.
+ *   idx [T, k] int32 out: experts by logit descending, ties to the lower
+ *       index; slot 0 is the best.
+ *   gate [T, k] float32 out: softmax over the k selected logits (1.0 at k=1).
+ * Logits are accumulated in double, so the choice is exact whenever the
+ * top-k margin exceeds the double rounding of a D-term dot product.
+ * If ws is non-NULL the per-tile expert histogram is also written to ws, for
+ * a following clearmoe_dispatch with CLEARMOE_DISPATCH_HIST_IN_WS.  Uses
+ * shape fields T, D, E, k, dtype. */
+int clearmoe_route(const clearmoe_shape* shape, const void* x, const void* Wg, const float* bg,
+                   int32_t* idx, float* gate, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Dispatch: expert histogram, exclusive scan and stable permutation (Sec. III
+ * "Dispatch Backends", Grouped: tokens sorted by expert into contiguous
+ * sub-batches; Algorithm 3 sort step).
+ *   idx     [T, k] int32 in, every entry in [0, E).
+ *   counts  [E] out; offsets [E+1] out, offsets[0] = 0, offsets[E] = T*k.
+ *   perm    [T*k] out: perm[p] = a = t*k + j, the assignments of expert 0 in
+ *           ascending a, then expert 1, ...  inv [T*k] out: inv[perm[p]] = p.
+ *   x [T, D] and xperm [T*k, D] (dtype): if both non-NULL, xperm[p] = x[perm[p]/k].
+ * An index outside [0, E) is not detected on the device; it is the caller's
+ * contract (clearmoe_route only produces valid ones).  Uses T, D, E, k, dtype. */
+int clearmoe_dispatch(const clearmoe_shape* shape, const int32_t* idx, void* ws, size_t ws_bytes,
+                      int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv,
+                      const void* x, void* xperm, unsigned flags, hipStream_t stream);
+
+/* Inverse-permute combine (Algorithm 3 "unshuffle h_res; y <- h_sh + h_res",
+ * weighted by the gates):  y[t] = sum_j gate[t, j] * ye[inv[t*k + j]],
+ * accumulated in float32 in slot order, stored in dtype.
+ *   ye [T*k, D] (dtype, expert order), inv [T*k], gate [T, k], y [T, D] out.
+ * Uses T, D, k, dtype. */
+int clearmoe_combine(const clearmoe_shape* shape, const void* ye, const int32_t* inv,
+                     const float* gate, void* y, hipStream_t stream);
+
+/* The whole layer (Eq. 2, Algorithm 3), all steps on the device.
+ *   x [T, D]; W1 [H, D], b1 [H]; US [D, r]; Vt [r, H]; b2 [D];
+ *   P [E, D, q], Q [E, q, H] (expert e's residual is P[e] Q[e]);
+ *   Wg [E, D], bg [E];  y [T, D] out.
+ *   idx_out [T, k] / gate_out [T, k]: optional copies of the routing (NULL ok).
+ * bfloat16 mode accumulates in float32; the hidden activation z and the
+ * rank-r / rank-q projections are rounded to bfloat16 between products. */
+int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void* W1,
+                         const float* b1, const void* US, const void* Vt, const float* b2,
+                         const void* P, const void* Q, const void* Wg, const float* bg, void* y,
+                         int32_t* idx_out, float* gate_out, void* ws, size_t ws_bytes,
+                         hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CLEARMOE_H */

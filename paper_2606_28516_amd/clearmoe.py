@@ -1,0 +1,195 @@
+"""Python binding of the CLEAR-MoE C ABI (``include/clearmoe.h``).
+
+Argument marshalling only: every step of the layer runs in the HIP library
+``libclearmoe.so``.  PyTorch supplies device memory and the current stream.
+There is no fallback: if the library is missing or a call fails, an
+exception is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+import torch
+
+__all__ = ["ClearMoEError", "Shape", "lib", "version", "workspace_bytes", "alloc_workspace",
+           "route", "dispatch", "combine", "ffn_forward", "from_stored", "to_stored",
+           "DISPATCH_HIST_IN_WS", "F32", "BF16", "SYMBOLS"]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libclearmoe.so")
+F32, BF16 = 0, 1
+DISPATCH_HIST_IN_WS = 1
+SYMBOLS = ("clearmoe_version", "clearmoe_status_string", "clearmoe_workspace_bytes",
+           "clearmoe_route", "clearmoe_dispatch", "clearmoe_combine", "clearmoe_ffn_forward")
+
+
+class ClearMoEError(RuntimeError):
+    pass
+
+
+class Shape(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in ("T", "D", "H", "E", "k", "r", "q", "dtype")]
+
+
+_lib = None
+
+
+def lib():
+    """Load the in-tree library (building it first only if it does not exist)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            from . import build as _build
+            _build.build()
+        L = ctypes.CDLL(LIB_PATH)
+        vp, sz, u32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_uint
+        sp = ctypes.POINTER(Shape)
+        L.clearmoe_version.restype = ctypes.c_int
+        L.clearmoe_status_string.restype = ctypes.c_char_p
+        L.clearmoe_status_string.argtypes = [ctypes.c_int]
+        L.clearmoe_workspace_bytes.restype = sz
+        L.clearmoe_workspace_bytes.argtypes = [sp]
+        L.clearmoe_route.restype = ctypes.c_int
+        L.clearmoe_route.argtypes = [sp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.clearmoe_dispatch.restype = ctypes.c_int
+        L.clearmoe_dispatch.argtypes = [sp, vp, vp, sz, vp, vp, vp, vp, vp, vp, u32, vp]
+        L.clearmoe_combine.restype = ctypes.c_int
+        L.clearmoe_combine.argtypes = [sp, vp, vp, vp, vp, vp]
+        L.clearmoe_ffn_forward.restype = ctypes.c_int
+        L.clearmoe_ffn_forward.argtypes = [sp] + [vp] * 13 + [vp, sz, vp]
+        _lib = L
+    return _lib
+
+
+def version() -> int:
+    return lib().clearmoe_version()
+
+
+def _check(rc: int, what: str) -> None:
+    if rc != 0:
+        msg = lib().clearmoe_status_string(rc).decode()
+        raise ClearMoEError(f"{what}: {msg} (status {rc})")
+
+
+def _dt(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise ClearMoEError(f"unsupported dtype {t.dtype}")
+
+
+def _p(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ClearMoEError("tensor is not on the GPU")
+    if not t.is_contiguous():
+        raise ClearMoEError("tensor is not contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def make_shape(T, D, E, k, dtype, H=0, r=0, q=0) -> Shape:
+    return Shape(int(T), int(D), int(H), int(E), int(k), int(r), int(q), int(dtype))
+
+
+def workspace_bytes(shape: Shape) -> int:
+    return int(lib().clearmoe_workspace_bytes(ctypes.byref(shape)))
+
+
+def alloc_workspace(shape: Shape, device="cuda") -> torch.Tensor:
+    n = workspace_bytes(shape)
+    if n == 0:
+        raise ClearMoEError("invalid shape")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def route(x, Wg, bg, k: int, ws: Optional[torch.Tensor] = None, stream=None):
+    """clearmoe_route: returns (idx [T,k] int32, gate [T,k] float32)."""
+    T, D = x.shape
+    E = Wg.shape[0]
+    s = make_shape(T, D, E, k, _dt(x))
+    ws = alloc_workspace(s, x.device) if ws is None else ws
+    idx = torch.empty((T, k), dtype=torch.int32, device=x.device)
+    gate = torch.empty((T, k), dtype=torch.float32, device=x.device)
+    rc = lib().clearmoe_route(ctypes.byref(s), _p(x), _p(Wg), _p(bg), _p(idx), _p(gate), _p(ws),
+                              ws.numel(), _stream(stream))
+    _check(rc, "clearmoe_route")
+    return idx, gate
+
+
+def dispatch(idx, E: int, ws: Optional[torch.Tensor] = None, x=None, D: Optional[int] = None,
+             hist_in_ws: bool = False, stream=None):
+    """clearmoe_dispatch: returns (counts, offsets, perm, inv, xperm or None)."""
+    T, k = idx.shape
+    if x is not None:
+        D, dtype = x.shape[1], _dt(x)
+    else:
+        D, dtype = 8, BF16          # no rows to copy: D only has to be valid
+    s = make_shape(T, D, E, k, dtype)
+    ws = alloc_workspace(s, idx.device) if ws is None else ws
+    dev = idx.device
+    counts = torch.empty(E, dtype=torch.int32, device=dev)
+    offsets = torch.empty(E + 1, dtype=torch.int32, device=dev)
+    perm = torch.empty(T * k, dtype=torch.int32, device=dev)
+    inv = torch.empty(T * k, dtype=torch.int32, device=dev)
+    xperm = None if x is None else torch.empty((T * k, D), dtype=x.dtype, device=dev)
+    rc = lib().clearmoe_dispatch(ctypes.byref(s), _p(idx), _p(ws), ws.numel(), _p(counts),
+                                 _p(offsets), _p(perm), _p(inv), _p(x), _p(xperm),
+                                 DISPATCH_HIST_IN_WS if hist_in_ws else 0, _stream(stream))
+    _check(rc, "clearmoe_dispatch")
+    return counts, offsets, perm, inv, xperm
+
+
+def combine(ye, inv, gate, out: Optional[torch.Tensor] = None, stream=None):
+    """clearmoe_combine: y[t] = sum_j gate[t,j] * ye[inv[t*k+j]]."""
+    T, k = gate.shape
+    D = ye.shape[1]
+    E = max(k, 1)
+    s = make_shape(T, D, E, k, _dt(ye))
+    y = torch.empty((T, D), dtype=ye.dtype, device=ye.device) if out is None else out
+    rc = lib().clearmoe_combine(ctypes.byref(s), _p(ye), _p(inv), _p(gate), _p(y),
+                                _stream(stream))
+    _check(rc, "clearmoe_combine")
+    return y
+
+
+def ffn_forward(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int, ws: Optional[torch.Tensor] = None,
+                out: Optional[torch.Tensor] = None, idx_out=None, gate_out=None, stream=None):
+    """clearmoe_ffn_forward: the whole layer.  Returns y [T, D]."""
+    T, D = x.shape
+    H = W1.shape[0]
+    r = US.shape[1]
+    E, _, q = P.shape
+    s = make_shape(T, D, E, k, _dt(x), H=H, r=r, q=q)
+    ws = alloc_workspace(s, x.device) if ws is None else ws
+    y = torch.empty((T, D), dtype=x.dtype, device=x.device) if out is None else out
+    rc = lib().clearmoe_ffn_forward(ctypes.byref(s), _p(x), _p(W1), _p(b1), _p(US), _p(Vt),
+                                    _p(b2), _p(P), _p(Q), _p(Wg), _p(bg), _p(y), _p(idx_out),
+                                    _p(gate_out), _p(ws), ws.numel(), _stream(stream))
+    _check(rc, "clearmoe_ffn_forward")
+    return y
+
+
+def from_stored(a: np.ndarray, device="cuda") -> torch.Tensor:
+    """Stored host array -> device tensor: uint16 = bfloat16 bits, float32, int32."""
+    a = np.ascontiguousarray(a)
+    if a.dtype == np.uint16:
+        return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(device)
+    return torch.from_numpy(a).to(device)
+
+
+def to_stored(t: torch.Tensor) -> np.ndarray:
+    """Device tensor -> host array in the stored convention (bf16 -> uint16 bits)."""
+    t = t.detach().cpu().contiguous()
+    if t.dtype == torch.bfloat16:
+        return t.view(torch.int16).numpy().view(np.uint16)
+    return t.numpy()

@@ -1,0 +1,287 @@
+// C ABI of the CLEAR-MoE FFN forward (declared in include/clearmoe.h).
+// Host side only: argument checks (before any HIP call), workspace carving and
+// the kernel sequence of each entry point on the caller's stream.
+#include "clearmoe.h"
+
+#include <stdint.h>
+
+#include "kernels.h"
+
+using namespace clearmoe;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kMaxDim = 1 << 16;
+
+size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+// Workspace layout.  Prefix shared by every entry point, then the buffers of
+// the whole-layer forward.
+struct Layout {
+    size_t wgT, tile_counts, tile_base;           // route / dispatch
+    size_t counts, offsets, idx, gate, perm, inv;  // ffn_forward
+    size_t z, tproj, hsh, u, hres;
+    size_t route_end, dispatch_end, total;
+};
+
+size_t elem_size(int dtype) { return dtype == CLEARMOE_F32 ? 4 : 2; }
+
+Layout layout(const clearmoe_shape& s) {
+    Layout L{};
+    const int64_t T = s.T, k = s.k, E = s.E;
+    const int64_t ntiles = route_tiles(T);
+    const int64_t Dpad = round_up(s.D, kWgPadD);
+    const size_t es = elem_size(s.dtype);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off += up(bytes);
+        return at;
+    };
+    // The histogram regions come first and depend on T and E only, so route and
+    // dispatch calls with different D (or none) agree on where they are.
+    L.tile_counts = take(sizeof(int32_t) * (ntiles * E > 0 ? ntiles * E : 1));
+    L.tile_base = take(sizeof(int32_t) * (ntiles * E > 0 ? ntiles * E : 1));
+    L.dispatch_end = off;
+    L.wgT = take(sizeof(double) * Dpad * route_emax(s.E));
+    L.route_end = off;
+    L.counts = take(sizeof(int32_t) * E);
+    L.offsets = take(sizeof(int32_t) * (E + 1));
+    L.idx = take(sizeof(int32_t) * T * k);
+    L.gate = take(sizeof(float) * T * k);
+    L.perm = take(sizeof(int32_t) * T * k);
+    L.inv = take(sizeof(int32_t) * T * k);
+    L.z = take(es * T * s.H);
+    L.tproj = take(es * T * s.r);
+    L.hsh = take(sizeof(float) * T * s.D);
+    L.u = take(es * T * k * s.q);
+    L.hres = take(sizeof(float) * T * k * s.D);
+    L.total = off;
+    return L;
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+// Shape checks common to every entry point (which fields matter depends on
+// the entry point; unused fields must still be in range).
+int check_shape(const clearmoe_shape* s, bool layer) {
+    if (s == nullptr) return CLEARMOE_ERR_INVALID_ARG;
+    if (s->dtype != CLEARMOE_F32 && s->dtype != CLEARMOE_BF16) return CLEARMOE_ERR_UNSUPPORTED;
+    if (s->T < 0 || s->D < 1 || s->D > kMaxDim) return CLEARMOE_ERR_INVALID_ARG;
+    if (s->E < 1 || s->E > 64 || s->k < 1 || s->k > s->E) return CLEARMOE_ERR_INVALID_ARG;
+    if (static_cast<int64_t>(s->T) * s->k >= (int64_t{1} << 31)) return CLEARMOE_ERR_INVALID_ARG;
+    const int mult = s->dtype == CLEARMOE_F32 ? 4 : 8;
+    if (s->D % mult != 0) return CLEARMOE_ERR_INVALID_ARG;
+    if (layer) {
+        if (s->H < 1 || s->H > kMaxDim || s->H % mult != 0) return CLEARMOE_ERR_INVALID_ARG;
+        const int mn = s->D < s->H ? s->D : s->H;
+        if (s->r < 0 || s->r > mn || s->q < 0 || s->q > mn) return CLEARMOE_ERR_INVALID_ARG;
+        if (s->r % mult != 0 || s->q % mult != 0) return CLEARMOE_ERR_INVALID_ARG;
+    }
+    return CLEARMOE_OK;
+}
+
+int hip_status(hipError_t e) { return e == hipSuccess ? CLEARMOE_OK : CLEARMOE_ERR_HIP; }
+
+#define CLEARMOE_TRY(expr)                          \
+    do {                                            \
+        const hipError_t e_ = (expr);               \
+        if (e_ != hipSuccess) return CLEARMOE_ERR_HIP; \
+    } while (0)
+
+template <typename P>
+P* at(void* ws, size_t off) {
+    return reinterpret_cast<P*>(static_cast<unsigned char*>(ws) + off);
+}
+
+int route_impl(const clearmoe_shape& s, const Layout& L, const void* x, const void* Wg,
+               const float* bg, int32_t* idx, float* gate, void* ws, hipStream_t st) {
+    const int emax = route_emax(s.E);
+    const int Dpad = static_cast<int>(round_up(s.D, kWgPadD));
+    double* wgT = at<double>(ws, L.wgT);
+    CLEARMOE_TRY(launch_router_weights_f64(s.dtype, Wg, s.D, s.E, emax, Dpad, wgT, st));
+    CLEARMOE_TRY(launch_route(s.dtype, x, wgT, bg, s.T, s.D, Dpad, s.E, emax, s.k, idx, gate,
+                              at<int32_t>(ws, L.tile_counts), st));
+    return CLEARMOE_OK;
+}
+
+int dispatch_impl(const clearmoe_shape& s, const Layout& L, const int32_t* idx, void* ws,
+                  int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv, const void* x,
+                  void* xperm, bool hist_in_ws, hipStream_t st) {
+    int32_t* tc = at<int32_t>(ws, L.tile_counts);
+    int32_t* tb = at<int32_t>(ws, L.tile_base);
+    const int64_t nt = route_tiles(s.T);
+    if (!hist_in_ws) CLEARMOE_TRY(launch_tile_histogram(idx, s.T, s.E, s.k, tc, st));
+    CLEARMOE_TRY(launch_scan(tc, nt, s.E, tb, counts, offsets, st));
+    CLEARMOE_TRY(launch_permute(s.dtype, idx, tb, offsets, s.T, s.E, s.k, perm, inv, x, xperm,
+                                s.D, st));
+    return CLEARMOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int clearmoe_version(void) { return (0 << 16) | 1; }
+
+const char* clearmoe_status_string(int status) {
+    switch (status) {
+        case CLEARMOE_OK: return "ok";
+        case CLEARMOE_ERR_INVALID_ARG: return "invalid argument";
+        case CLEARMOE_ERR_UNSUPPORTED: return "unsupported";
+        case CLEARMOE_ERR_WORKSPACE: return "workspace missing or too small";
+        case CLEARMOE_ERR_HIP: return "HIP launch failed";
+        default: return "unknown status";
+    }
+}
+
+size_t clearmoe_workspace_bytes(const clearmoe_shape* shape) {
+    if (check_shape(shape, false) != CLEARMOE_OK) return 0;
+    clearmoe_shape s = *shape;
+    if (check_shape(shape, true) != CLEARMOE_OK) {  // route / dispatch-only shape
+        s.H = 0;
+        s.r = 0;
+        s.q = 0;
+    }
+    return layout(s).total;
+}
+
+int clearmoe_route(const clearmoe_shape* shape, const void* x, const void* Wg, const float* bg,
+                   int32_t* idx, float* gate, void* ws, size_t ws_bytes, hipStream_t stream) {
+    int rc = check_shape(shape, false);
+    if (rc != CLEARMOE_OK) return rc;
+    const clearmoe_shape& s = *shape;
+    const bool tok = s.T > 0;                 // per-token arrays may be NULL when T == 0
+    if (!Wg || (tok && (!x || !idx || !gate))) return CLEARMOE_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(Wg, 4) || !aligned(idx, 4) || !aligned(gate, 4) ||
+        (bg && !aligned(bg, 4)))
+        return CLEARMOE_ERR_INVALID_ARG;
+    clearmoe_shape sl = s;
+    sl.H = sl.r = sl.q = 0;
+    const Layout L = layout(sl);
+    if (!ws || !aligned(ws, kAlign) || ws_bytes < L.route_end) return CLEARMOE_ERR_WORKSPACE;
+    return route_impl(s, L, x, Wg, bg, idx, gate, ws, stream);
+}
+
+int clearmoe_dispatch(const clearmoe_shape* shape, const int32_t* idx, void* ws, size_t ws_bytes,
+                      int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv,
+                      const void* x, void* xperm, unsigned flags, hipStream_t stream) {
+    int rc = check_shape(shape, false);
+    if (rc != CLEARMOE_OK) return rc;
+    const clearmoe_shape& s = *shape;
+    const bool tok = s.T > 0;
+    if (!counts || !offsets || (tok && (!idx || !perm || !inv))) return CLEARMOE_ERR_INVALID_ARG;
+    if (tok && (x == nullptr) != (xperm == nullptr)) return CLEARMOE_ERR_INVALID_ARG;
+    if (!aligned(idx, 4) || !aligned(counts, 4) || !aligned(offsets, 4) || !aligned(perm, 4) ||
+        !aligned(inv, 4) || (x && (!aligned(x, 16) || !aligned(xperm, 16))))
+        return CLEARMOE_ERR_INVALID_ARG;
+    if (flags & ~static_cast<unsigned>(CLEARMOE_DISPATCH_HIST_IN_WS)) return CLEARMOE_ERR_INVALID_ARG;
+    clearmoe_shape sl = s;
+    sl.H = sl.r = sl.q = 0;
+    const Layout L = layout(sl);
+    if (!ws || !aligned(ws, kAlign) || ws_bytes < L.dispatch_end) return CLEARMOE_ERR_WORKSPACE;
+    return dispatch_impl(s, L, idx, ws, counts, offsets, perm, inv, x, xperm,
+                         (flags & CLEARMOE_DISPATCH_HIST_IN_WS) != 0, stream);
+}
+
+int clearmoe_combine(const clearmoe_shape* shape, const void* ye, const int32_t* inv,
+                     const float* gate, void* y, hipStream_t stream) {
+    int rc = check_shape(shape, false);
+    if (rc != CLEARMOE_OK) return rc;
+    const clearmoe_shape& s = *shape;
+    if (s.T > 0 && (!ye || !inv || !gate || !y)) return CLEARMOE_ERR_INVALID_ARG;
+    if (!aligned(ye, 16) || !aligned(y, 16) || !aligned(inv, 4) || !aligned(gate, 4))
+        return CLEARMOE_ERR_INVALID_ARG;
+    return hip_status(launch_combine_gated(s.dtype, ye, inv, gate, y, s.T, s.D, s.k, stream));
+}
+
+int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void* W1,
+                         const float* b1, const void* US, const void* Vt, const float* b2,
+                         const void* P, const void* Q, const void* Wg, const float* bg, void* y,
+                         int32_t* idx_out, float* gate_out, void* ws, size_t ws_bytes,
+                         hipStream_t stream) {
+    int rc = check_shape(shape, true);
+    if (rc != CLEARMOE_OK) return rc;
+    const clearmoe_shape& s = *shape;
+    if (!W1 || !Wg || (s.T > 0 && (!x || !y))) return CLEARMOE_ERR_INVALID_ARG;
+    if (s.r > 0 && (!US || !Vt)) return CLEARMOE_ERR_INVALID_ARG;
+    if (s.q > 0 && (!P || !Q)) return CLEARMOE_ERR_INVALID_ARG;
+    const void* v16[] = {x, W1, US, Vt, P, Q, y};
+    for (const void* p : v16)
+        if (p && !aligned(p, 16)) return CLEARMOE_ERR_INVALID_ARG;
+    const void* v4[] = {b1, b2, bg, Wg, idx_out, gate_out};
+    for (const void* p : v4)
+        if (p && !aligned(p, 4)) return CLEARMOE_ERR_INVALID_ARG;
+    const Layout L = layout(s);
+    if (!ws || !aligned(ws, kAlign) || ws_bytes < L.total) return CLEARMOE_ERR_WORKSPACE;
+    if (s.T == 0) return CLEARMOE_OK;
+
+    hipStream_t st = stream;
+    const int64_t T = s.T, A = T * s.k;
+    int32_t* idx = idx_out ? idx_out : at<int32_t>(ws, L.idx);
+    float* gate = gate_out ? gate_out : at<float>(ws, L.gate);
+    int32_t* counts = at<int32_t>(ws, L.counts);
+    int32_t* offsets = at<int32_t>(ws, L.offsets);
+    int32_t* perm = at<int32_t>(ws, L.perm);
+    int32_t* inv = at<int32_t>(ws, L.inv);
+    void* z = at<void>(ws, L.z);
+    void* tproj = at<void>(ws, L.tproj);
+    float* hsh = at<float>(ws, L.hsh);
+    void* u = at<void>(ws, L.u);
+    float* hres = at<float>(ws, L.hres);
+
+    // 1. router + top-k + per-tile histogram; 2. scan + stable permutation
+    rc = route_impl(s, L, x, Wg, bg, idx, gate, ws, st);
+    if (rc != CLEARMOE_OK) return rc;
+    rc = dispatch_impl(s, L, idx, ws, counts, offsets, perm, inv, nullptr, nullptr, true, st);
+    if (rc != CLEARMOE_OK) return rc;
+
+    // 3. z = GELU(x W1^T + b1)
+    GemmDesc g{};
+    g.A = x; g.lda = s.D; g.a_div = 1;
+    g.B = W1; g.ldb = s.D;
+    g.C = z; g.ldc = s.H; g.c_f32 = 0;
+    g.bias = b1; g.gelu = 1;
+    g.M = T; g.N = s.H; g.K = s.D;
+    CLEARMOE_TRY(launch_gemm(s.dtype, g, st));
+
+    // 4. shared basis: t = z Vt^T ; h_sh = t US^T + b2
+    g = GemmDesc{};
+    g.A = z; g.lda = s.H; g.a_div = 1;
+    g.B = Vt; g.ldb = s.H;
+    g.C = tproj; g.ldc = s.r; g.c_f32 = 0;
+    g.M = T; g.N = s.r; g.K = s.H;
+    if (s.r > 0) CLEARMOE_TRY(launch_gemm(s.dtype, g, st));
+    g = GemmDesc{};
+    g.A = tproj; g.lda = s.r; g.a_div = 1;
+    g.B = US; g.ldb = s.r;
+    g.C = hsh; g.ldc = s.D; g.c_f32 = 1;
+    g.bias = b2;
+    g.M = T; g.N = s.D; g.K = s.r;
+    CLEARMOE_TRY(launch_gemm(s.dtype, g, st));
+
+    // 5. residual, grouped by expert: u = gate * (z[perm/k] Q_e^T) ; h_res = u P_e^T
+    g = GemmDesc{};
+    g.A = z; g.lda = s.H; g.a_rows = perm; g.a_div = s.k;
+    g.B = Q; g.ldb = s.H; g.b_seg_stride = static_cast<int64_t>(s.q) * s.H;
+    g.C = u; g.ldc = s.q; g.c_f32 = 0;
+    g.row_scale = gate; g.scale_rows = perm;
+    g.M = A; g.N = s.q; g.K = s.H;
+    g.seg_offsets = offsets; g.nseg = s.E;
+    if (s.q > 0) CLEARMOE_TRY(launch_gemm(s.dtype, g, st));
+    g = GemmDesc{};
+    g.A = u; g.lda = s.q; g.a_div = 1;
+    g.B = P; g.ldb = s.q; g.b_seg_stride = static_cast<int64_t>(s.D) * s.q;
+    g.C = hres; g.ldc = s.D; g.c_f32 = 1;
+    g.M = A; g.N = s.D; g.K = s.q;
+    g.seg_offsets = offsets; g.nseg = s.E;
+    CLEARMOE_TRY(launch_gemm(s.dtype, g, st));
+
+    // 6. y[t] = h_sh[t] + sum_j h_res[inv[t*k+j]]
+    CLEARMOE_TRY(launch_combine_residual(s.dtype, hsh, hres, inv, y, T, s.D, s.k, st));
+    return CLEARMOE_OK;
+}
+
+}  // extern "C"

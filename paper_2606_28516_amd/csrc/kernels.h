@@ -1,0 +1,115 @@
+// Internal declarations of the CLEAR-MoE HIP kernels (gfx950) and their host
+// launchers.  Nothing here is part of the public C ABI (include/clearmoe.h).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace clearmoe {
+
+// ---------------------------------------------------------------------------
+// Element types.  bfloat16 is carried as raw 16-bit patterns in memory.
+// ---------------------------------------------------------------------------
+typedef uint16_t bf16_bits;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float bf16_to_f32(bf16_bits b) {
+    return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// float -> bfloat16, round to nearest even (NaN kept quiet).
+__device__ __forceinline__ bf16_bits f32_to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_bits>((u >> 16) | 0x40u);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return static_cast<bf16_bits>(u >> 16);
+}
+
+template <typename T> struct Elem;
+template <> struct Elem<float> {
+    static constexpr int per16 = 4;                 // elements per 16-byte piece
+    __device__ static float load(const float* p, int64_t i) { return p[i]; }
+    __device__ static float to_f32(float v) { return v; }
+    __device__ static float from_f32(float v) { return v; }
+};
+template <> struct Elem<bf16_bits> {
+    static constexpr int per16 = 8;
+    __device__ static float load(const bf16_bits* p, int64_t i) { return bf16_to_f32(p[i]); }
+    __device__ static float to_f32(bf16_bits v) { return bf16_to_f32(v); }
+    __device__ static bf16_bits from_f32(float v) { return f32_to_bf16(v); }
+};
+
+// Exact-erf GELU in float32 (device erff).
+__device__ __forceinline__ float gelu_erf(float v) {
+    return 0.5f * v * (1.0f + erff(v * 0.70710678118654752440f));
+}
+
+// ---------------------------------------------------------------------------
+// Tiling constants shared by host and device code.
+// ---------------------------------------------------------------------------
+constexpr int kRouteTile = 256;      // tokens per routing / dispatch tile (one per thread)
+constexpr int kRouteChunkBytes = 128;// bytes of a token row staged per LDS chunk
+constexpr int kWgPadD = 64;          // router weight rows padded to a multiple of this
+
+inline int64_t route_tiles(int64_t T) { return (T + kRouteTile - 1) / kRouteTile; }
+inline int route_emax(int E) {       // register width of the logit array
+    if (E <= 8) return E;
+    if (E <= 16) return 16;
+    if (E <= 32) return 32;
+    return 64;
+}
+
+// ---------------------------------------------------------------------------
+// Host launchers (return hipError_t of the launch).
+// ---------------------------------------------------------------------------
+// Router weights -> double, transposed and zero padded: wgT[d][e], d < Dpad, e < emax.
+hipError_t launch_router_weights_f64(int dtype, const void* Wg, int D, int E, int emax, int Dpad,
+                                     double* wgT, hipStream_t st);
+// Router logits (double), top-k, gates, per-tile expert histogram.
+hipError_t launch_route(int dtype, const void* x, const double* wgT, const float* bg, int64_t T,
+                        int D, int Dpad, int E, int emax, int k, int32_t* idx, float* gate,
+                        int32_t* tile_counts, hipStream_t st);
+// Per-tile expert histogram of an index array.
+hipError_t launch_tile_histogram(const int32_t* idx, int64_t T, int E, int k,
+                                 int32_t* tile_counts, hipStream_t st);
+// Exclusive scan of tile histograms: tile_base[b][e] = sum_{b'<b} tile_counts[b'][e];
+// counts[e] = column sums; offsets[e] = exclusive scan of counts (offsets[E] = total).
+hipError_t launch_scan(const int32_t* tile_counts, int64_t ntiles, int E, int32_t* tile_base,
+                       int32_t* counts, int32_t* offsets, hipStream_t st);
+// Stable permutation (and optional row copy x -> xperm).
+hipError_t launch_permute(int dtype, const int32_t* idx, const int32_t* tile_base,
+                          const int32_t* offsets, int64_t T, int E, int k, int32_t* perm,
+                          int32_t* inv, const void* x, void* xperm, int D, hipStream_t st);
+// y[t] = sum_j gate[t,j] ye[inv[t*k+j]]  (ye, y in dtype).
+hipError_t launch_combine_gated(int dtype, const void* ye, const int32_t* inv, const float* gate,
+                                void* y, int64_t T, int D, int k, hipStream_t st);
+// y[t] = hsh[t] + sum_j hres[inv[t*k+j]]  (hsh, hres float32; y in dtype).
+hipError_t launch_combine_residual(int dtype, const float* hsh, const float* hres,
+                                   const int32_t* inv, void* y, int64_t T, int D, int k,
+                                   hipStream_t st);
+
+// NT GEMM  C[m, n] = epi( sum_k A[arow(m), k] B_seg(m)[n, k] ).
+struct GemmDesc {
+    const void* A;            // [*, K] in dtype, row stride lda (elements)
+    int64_t lda;
+    const int32_t* a_rows;    // optional gather: A row = a_rows[m] / a_div
+    int a_div;
+    const void* B;            // [N, K] per segment, row stride ldb; segment e at B + e*b_seg_stride
+    int64_t ldb;
+    int64_t b_seg_stride;     // elements
+    void* C;                  // [M, N] output, row stride ldc
+    int64_t ldc;
+    int c_f32;                // 1: C is float32; 0: C is dtype
+    const float* bias;        // optional [N]
+    const float* row_scale;   // optional: C row m scaled by row_scale[scale_rows[m]]
+    const int32_t* scale_rows;
+    int gelu;                 // 1: GELU after bias
+    int64_t M;                // rows (sum of segments when grouped)
+    int N, K;
+    const int32_t* seg_offsets;  // optional [nseg+1] on the device: grouped GEMM
+    int nseg;
+};
+hipError_t launch_gemm(int dtype, const GemmDesc& g, hipStream_t st);
+
+}  // namespace clearmoe

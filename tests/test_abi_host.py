@@ -1,0 +1,134 @@
+"""Host-only checks of the C ABI: the library loads, exports every function
+include/clearmoe.h declares, and rejects bad arguments before touching the GPU
+(every call here fails validation, so no HIP call is made)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2606_28516_amd import clearmoe as cm
+from paper_2606_28516_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "clearmoe.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(clearmoe_[a-z_]+)\s*\(", src)))
+
+
+def test_header_declarations_match_binding():
+    assert _declared() == sorted(cm.SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol():
+    L = cm.lib()
+    for name in _declared():
+        assert hasattr(L, name), name
+    nm = os.popen(f"nm -D --defined-only {cm.LIB_PATH}").read()
+    for name in _declared():
+        assert re.search(rf"\bT {name}\b", nm), name
+
+
+def test_version_and_status_strings():
+    assert cm.version() == 1
+    L = cm.lib()
+    assert L.clearmoe_status_string(0) == b"ok"
+    assert L.clearmoe_status_string(3).startswith(b"workspace")
+    assert L.clearmoe_status_string(99) == b"unknown status"
+
+
+def _shape(**kw):
+    d = dict(T=100, D=64, H=128, E=4, k=2, r=16, q=8, dtype=cm.BF16)
+    d.update(kw)
+    return cm.make_shape(d["T"], d["D"], d["E"], d["k"], d["dtype"], H=d["H"], r=d["r"], q=d["q"])
+
+
+def test_workspace_bytes_grows_with_shape_and_rejects_bad_shapes():
+    a = cm.workspace_bytes(_shape())
+    b = cm.workspace_bytes(_shape(T=1000))
+    assert 0 < a < b and a % 256 == 0
+    assert cm.workspace_bytes(_shape(k=5)) == 0          # k > E
+    assert cm.workspace_bytes(_shape(E=65, k=1)) == 0    # E > 64
+    assert cm.workspace_bytes(_shape(D=12)) == 0         # D not a multiple of 8 for bf16
+    assert cm.workspace_bytes(_shape(D=12, dtype=cm.F32, H=128, r=4, q=4)) > 0
+    assert cm.workspace_bytes(_shape(T=0)) > 0
+    # the configurations of the benchmark and tests are all valid
+    for c in synth.CONFIGS.values():
+        s = cm.make_shape(c.T, c.D, c.E, c.k, cm.F32 if c.dtype == "f32" else cm.BF16,
+                          H=c.H, r=c.r, q=c.q)
+        assert cm.workspace_bytes(s) > 0
+
+
+FAKE = ctypes.c_void_p(0x10000)      # aligned, never dereferenced: validation fails first
+
+
+def test_route_rejects_before_launch():
+    L = cm.lib()
+    s = _shape()
+    ws_n = cm.workspace_bytes(s)
+    # NULL x
+    assert L.clearmoe_route(ctypes.byref(s), None, FAKE, None, FAKE, FAKE, FAKE, ws_n, None) == 1
+    # misaligned x
+    assert L.clearmoe_route(ctypes.byref(s), ctypes.c_void_p(0x10002), FAKE, None, FAKE, FAKE,
+                            FAKE, ws_n, None) == 1
+    # missing / small workspace
+    assert L.clearmoe_route(ctypes.byref(s), FAKE, FAKE, None, FAKE, FAKE, None, ws_n, None) == 3
+    assert L.clearmoe_route(ctypes.byref(s), FAKE, FAKE, None, FAKE, FAKE, FAKE, 16, None) == 3
+    # bad shapes / dtype
+    bad = _shape(k=0)
+    assert L.clearmoe_route(ctypes.byref(bad), FAKE, FAKE, None, FAKE, FAKE, FAKE, ws_n, None) == 1
+    bad = _shape(dtype=7)
+    assert L.clearmoe_route(ctypes.byref(bad), FAKE, FAKE, None, FAKE, FAKE, FAKE, ws_n, None) == 2
+    big = _shape(T=1 << 30, k=2)                                    # T*k >= 2^31
+    assert L.clearmoe_route(ctypes.byref(big), FAKE, FAKE, None, FAKE, FAKE, FAKE, ws_n, None) == 1
+    assert L.clearmoe_route(None, FAKE, FAKE, None, FAKE, FAKE, FAKE, ws_n, None) == 1
+
+
+def test_dispatch_combine_ffn_reject_before_launch():
+    L = cm.lib()
+    s = _shape()
+    n = cm.workspace_bytes(s)
+    # x without xperm
+    assert L.clearmoe_dispatch(ctypes.byref(s), FAKE, FAKE, n, FAKE, FAKE, FAKE, FAKE, FAKE, None,
+                               0, None) == 1
+    # unknown flag
+    assert L.clearmoe_dispatch(ctypes.byref(s), FAKE, FAKE, n, FAKE, FAKE, FAKE, FAKE, None, None,
+                               8, None) == 1
+    assert L.clearmoe_dispatch(ctypes.byref(s), FAKE, FAKE, 4, FAKE, FAKE, FAKE, FAKE, None, None,
+                               0, None) == 3
+    assert L.clearmoe_combine(ctypes.byref(s), None, FAKE, FAKE, FAKE, None) == 1
+    args = [FAKE] * 13
+    # NULL W1
+    a = list(args)
+    a[1] = None
+    assert L.clearmoe_ffn_forward(ctypes.byref(s), *a, FAKE, n, None) == 1
+    # r > min(D, H)
+    bad = _shape(r=72)
+    assert L.clearmoe_ffn_forward(ctypes.byref(bad), *args, FAKE, n, None) == 1
+    # q not a multiple of 8 in bf16
+    bad = _shape(q=6)
+    assert L.clearmoe_ffn_forward(ctypes.byref(bad), *args, FAKE, n, None) == 1
+    # workspace one byte short
+    assert L.clearmoe_ffn_forward(ctypes.byref(s), *args, FAKE, n - 1, None) == 3
+
+
+def _prototypes():
+    src = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
+    out = {}
+    for m in re.finditer(r"\b(clearmoe_[a-z_]+)\s*\(([^)]*)\)\s*;", src):
+        params = m.group(2).strip()
+        out[m.group(1)] = 0 if params in ("", "void") else params.count(",") + 1
+    return out
+
+
+def test_binding_signatures_match_header():
+    L = cm.lib()
+    protos = _prototypes()
+    assert set(protos) == set(cm.SYMBOLS)
+    for name, n in protos.items():
+        argtypes = getattr(L, name).argtypes
+        assert len(argtypes or []) == n, (name, len(argtypes or []), n)
