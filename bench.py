@@ -1,0 +1,337 @@
+#!/usr/bin/env python3
+"""Benchmark of the CLEAR-MoE FFN forward on one MI355X.
+
+A step is one clearmoe_ffn_forward call (router, dispatch, fc1 + GELU, shared
+SVD basis, grouped residual experts, combine) over the DeiT-Small-shaped layer:
+T = 64 x 197 = 12608 tokens, D = 384, H = 1536, E = 8, top-1, r = 128, q = 32,
+bf16 storage with float32 accumulation, synthetic seeded inputs already in HBM.
+
+Prints one JSON line.  Besides the contract fields it carries
+  roofline     the dominant kernel's algorithmic rate (HIP events recorded on
+               its stream around every launch in the timed region) against its
+               MI355X peak, plus measured HBM traffic when counters exist for
+               the current kernel source;
+  cpu_baseline the CPU oracle on a bounded sample of the same workload;
+  stages       per-kernel times of one step;
+  cold         the step with the 256 MB last-level cache flushed before it;
+  dense        the dense fc1 + GELU + fc2 comparator through the same kernels;
+  dispatch     the routing/dispatch-only workload (2^20 tokens, D = 384, E = 8,
+               top-2, Zipf-skewed bias): route -> dispatch (+ rows) -> combine,
+               with its HBM fraction.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum CPU time of the oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="only the timed steps (for profiler runs)")
+    ap.add_argument("--workload", default="C2", choices=["C1", "C2", "C3"])
+    return ap.parse_args()
+
+
+def source_digest():
+    """Hash of the HIP sources: counters taken on other code are not reported."""
+    h = hashlib.sha256()
+    cdir = os.path.join(ROOT, "paper_2606_28516_amd", "csrc")
+    for name in sorted(os.listdir(cdir)):
+        with open(os.path.join(cdir, name), "rb") as f:
+            h.update(name.encode())
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def stage_work(stage, cfg, b):
+    """Algorithmic (flops, bytes) of one launch of a stage of the layer.
+    b = bytes per stored element; h_sh and h_res are float32."""
+    T, D, H, E, k, r, q = cfg.T, cfg.D, cfg.H, cfg.E, cfg.k, cfg.r, cfg.q
+    A = T * k
+    w = {
+        "route": (2 * T * D * E, T * D * b + E * D * b + A * 8),
+        "scan": (0, 8 * ((T + 255) // 256) * E),
+        "permute": (0, A * 4 + A * 8),
+        "fc1_gelu": (2 * T * H * D, T * D * b + H * D * b + T * H * b),
+        "basis_t": (2 * T * r * H, T * H * b + r * H * b + T * r * b),
+        "basis_h": (2 * T * D * r, T * r * b + D * r * b + T * D * 4),
+        "res_u": (2 * A * q * H, A * H * b + E * q * H * b + A * q * b),
+        "res_h": (2 * A * D * q, A * q * b + E * D * q * b + A * D * 4),
+        "combine_res": (0, T * D * 4 + A * D * 4 + A * 4 + T * D * b),
+        "dense_fc2": (2 * T * D * H, T * H * b + D * H * b + T * D * b),
+    }
+    return w.get(stage, (0, 0))
+
+
+def layer_flops(cfg):
+    T, D, H, E, k, r, q = cfg.T, cfg.D, cfg.H, cfg.E, cfg.k, cfg.r, cfg.q
+    return 2 * T * (D * H + H * r + r * D + k * (H * q + q * D) + D * E)
+
+
+def load_traffic(kernel, workload, digest):
+    """Measured HBM bytes per launch from a committed counter summary, if it was
+    taken on the current kernel source."""
+    path = os.path.join(PROFILE_DIR, f"traffic_{kernel}_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_digest") != digest:
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py: this build runs on one GPU only (asked for --gpus {args.gpus}, "
+              f"WORLD_SIZE {world}); the path shards by tokens with no exchange, see the "
+              f"design notes", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2606_28516_amd import clearmoe as cm
+    from paper_2606_28516_amd import synth
+
+    assert torch.cuda.is_available(), "bench.py needs the GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    cfg = synth.CONFIGS[args.workload]
+    b = 4 if cfg.dtype == "f32" else 2
+    L = synth.make_layer(cfg)
+    d = {n: cm.from_stored(L[n]) for n in ("x", "W1", "b1", "US", "Vt", "b2", "P", "Q", "Wg", "bg")}
+    shape = cm.make_shape(cfg.T, cfg.D, cfg.E, cfg.k, cm.F32 if cfg.dtype == "f32" else cm.BF16,
+                          H=cfg.H, r=cfg.r, q=cfg.q)
+    ws = cm.alloc_workspace(shape)
+    y = torch.empty((cfg.T, cfg.D), dtype=d["x"].dtype, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        cm.ffn_forward(d["x"], d["W1"], d["b1"], d["US"], d["Vt"], d["b2"], d["P"], d["Q"],
+                       d["Wg"], d["bg"], cfg.k, ws=ws, out=y)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # Per-stage times of a few steps (all stages timed) to find the dominant kernel.
+    names = cm.stage_names()
+    cm.timing_start(names, 64 * len(names))
+    for _ in range(20):
+        step()
+    per = cm.timing_stop()
+    stages = {s: ms / n for s, (ms, n) in per.items()}
+    dominant = max(stages, key=stages.get)
+
+    # Timed region: exactly K steps; events recorded around the dominant kernel only.
+    cm.timing_start([dominant], args.steps)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(args.steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dom_ms, dom_n = cm.timing_stop()[dominant]
+    ms_step = ev0.elapsed_time(ev1) / args.steps
+    value = cfg.T / (ms_step * 1e-3)
+
+    flops, byts = stage_work(dominant, cfg, b)
+    dom_avg_s = dom_ms / dom_n * 1e-3
+    digest = source_digest()
+    if flops > 0:
+        roof = dict(bound="mfma", achieved=flops / dom_avg_s / 1e12,
+                    peak=MFMA_PEAK_TFLOPS[cfg.dtype], unit="TFLOP/s")
+    else:
+        roof = dict(bound="hbm", achieved=byts / dom_avg_s / 1e9, peak=HBM_PEAK_GBS, unit="GB/s")
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = load_traffic(dominant, args.workload, digest)
+    roof["kernel"] = dominant
+    roof["avg_launch_us"] = dom_avg_s * 1e6
+    roof["algorithmic_per_launch"] = flops if flops > 0 else byts
+
+    out = {
+        "metric": "tokens/sec per CLEAR-MoE FFN layer + % HBM peak (dispatch) / % MFMA peak (GEMM)",
+        "value": value,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": cfg.dtype,
+        "data": "synthetic (seeded Gaussian-cluster tokens, N(0,0.02) weights, SVD-extracted basis)",
+        "config": {"workload": cfg.name, "tokens": cfg.T, "D": cfg.D, "H": cfg.H, "E": cfg.E,
+                   "k": cfg.k, "r": cfg.r, "q": cfg.q, "seed": cfg.seed},
+        "roofline": roof,
+        "layer_tflops": layer_flops(cfg) / (ms_step * 1e-3) / 1e12,
+        "stages_us": {s: v * 1e3 for s, v in sorted(stages.items(), key=lambda kv: -kv[1])},
+        "wall_s": wall,
+        "source_digest": digest,
+    }
+
+    if not args.no_extras:
+        # Cold: flush the 256 MB last-level cache (512 MiB write) before each step.
+        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+        times = []
+        for _ in range(30):
+            flush.fill_(1)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            step()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            times.append(e0.elapsed_time(e1))
+        del flush
+        cold = float(np.median(times))
+        out["cold"] = {"ms_per_step": cold, "tokens_per_s": cfg.T / (cold * 1e-3)}
+
+        # Dense comparator through the same GEMM kernels.
+        W2 = cm.from_stored(L["W2"].astype(np.float32) if cfg.dtype == "f32"
+                            else synth.to_bf16_bits(L["W2"]))
+        yd = torch.empty_like(y)
+
+        def dense():
+            cm.dense_ffn_forward(d["x"], d["W1"], d["b1"], W2, d["b2"], ws=ws, out=yd)
+
+        for _ in range(args.warmup):
+            dense()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            dense()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        dms = e0.elapsed_time(e1) / args.steps
+        out["dense"] = {"ms_per_step": dms, "tokens_per_s": cfg.T / (dms * 1e-3),
+                        "moe_over_dense_time": ms_step / dms,
+                        "tflops": 4 * cfg.T * cfg.D * cfg.H / (dms * 1e-3) / 1e12}
+        del W2, yd
+        out["dispatch"] = bench_dispatch(cm, synth, torch, np, stream, max(10, args.steps // 10))
+
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(L, cfg, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+def bench_dispatch(cm, synth, torch, np, stream, steps):
+    """Route -> dispatch (rows copied into expert order) -> gated combine on the
+    2^20-token workload.  HBM fraction against compulsory bytes (x read once)
+    and against the bytes this design moves (x read by route and by permute)."""
+    L = synth.make_dispatch()
+    c = L["cfg"]
+    T, D, E, k = c["T"], c["D"], c["E"], c["k"]
+    x, Wg, bg = cm.from_stored(L["x"]), cm.from_stored(L["Wg"]), cm.from_stored(L["bg"])
+    del L
+    s = cm.make_shape(T, D, E, k, cm.BF16)
+    ws = cm.alloc_workspace(s)
+    dev = x.device
+    idx = torch.empty((T, k), dtype=torch.int32, device=dev)
+    gate = torch.empty((T, k), dtype=torch.float32, device=dev)
+    counts = torch.empty(E, dtype=torch.int32, device=dev)
+    offsets = torch.empty(E + 1, dtype=torch.int32, device=dev)
+    perm = torch.empty(T * k, dtype=torch.int32, device=dev)
+    inv = torch.empty(T * k, dtype=torch.int32, device=dev)
+    xperm = torch.empty((T * k, D), dtype=x.dtype, device=dev)
+    y = torch.empty_like(x)
+    Lb = cm.lib()
+    import ctypes
+
+    sp = ctypes.byref(s)
+    st = ctypes.c_void_p(stream.cuda_stream)
+    P = lambda t: ctypes.c_void_p(t.data_ptr())  # noqa: E731
+
+    def run():
+        rc = Lb.clearmoe_route(sp, P(x), P(Wg), P(bg), P(idx), P(gate), P(ws), ws.numel(), st)
+        rc |= Lb.clearmoe_dispatch(sp, P(idx), P(ws), ws.numel(), P(counts), P(offsets), P(perm),
+                                   P(inv), P(x), P(xperm), cm.DISPATCH_HIST_IN_WS, st)
+        rc |= Lb.clearmoe_combine(sp, P(xperm), P(inv), P(gate), P(y), st)
+        if rc:
+            raise cm.ClearMoEError("dispatch workload failed")
+
+    for _ in range(3):
+        run()
+    torch.cuda.synchronize()
+    names = cm.stage_names()
+    cm.timing_start(names, steps * len(names))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        run()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    per = cm.timing_stop()
+    ms = e0.elapsed_time(e1) / steps
+    A = T * k
+    b = 2
+    # x read, xperm written and read, y written, idx/gate/perm/inv written, inv/gate read
+    compulsory = T * D * b + 2 * A * D * b + T * D * b + A * 24
+    moved = compulsory + T * D * b
+    kern = {}
+    kbytes = {"route": T * D * b + A * 8, "permute": A * 4 + T * D * b + A * 8 + A * D * b,
+              "combine": A * 8 + A * D * b + T * D * b}
+    for s_, (t_ms, n) in per.items():
+        us = t_ms / n * 1e3
+        e = {"us": us}
+        if s_ in kbytes:
+            e["GBs"] = kbytes[s_] / (us * 1e-6) / 1e9
+            e["hbm_frac"] = e["GBs"] / HBM_PEAK_GBS
+        kern[s_] = e
+    return {"workload": "C4-dispatch-bf16 T=2^20 D=384 E=8 k=2 zipf1.2", "ms": ms,
+            "tokens_per_s": T / (ms * 1e-3),
+            "hbm_frac_compulsory": compulsory / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "hbm_frac_moved": moved / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "compulsory_GB": compulsory / 1e9, "moved_GB": moved / 1e9,
+            "counts": counts.cpu().tolist(), "kernels": kern}
+
+
+def cpu_baseline(L, cfg, min_seconds):
+    """The CPU oracle, as it stands, on whole passes over the same workload's
+    tokens (row blocks of 4096 tokens) until at least min_seconds have run."""
+    import numpy as np
+
+    import oracle
+
+    oracle.lib()
+    threads = oracle.num_threads()
+    blk = 4096
+    done, t_used = 0, 0.0
+    start = 0
+    while t_used < min_seconds:
+        rows = np.arange(start, min(cfg.T, start + blk))
+        t0 = time.perf_counter()
+        oracle.ffn_forward_layer(L, rows=rows)
+        t_used += time.perf_counter() - t0
+        done += rows.size
+        start = (start + blk) % cfg.T
+    return {"value": done / t_used, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{done} tokens of {cfg.name} in blocks of {blk}, {t_used:.1f} s, fp64 "
+                      f"plain loops, OpenMP over tokens"}
+
+
+if __name__ == "__main__":
+    main()

@@ -80,11 +80,13 @@ size_t clearmoe_workspace_bytes(const clearmoe_shape* shape);
  *   idx [T, k] int32 out: experts by logit descending, ties to the lower
  *       index; slot 0 is the best.
  *   gate [T, k] float32 out: softmax over the k selected logits (1.0 at k=1).
- * Logits are accumulated in double, so the choice is exact whenever the
- * top-k margin exceeds the double rounding of a D-term dot product.
- * If ws is non-NULL the per-tile expert histogram is also written to ws, for
- * a following clearmoe_dispatch with CLEARMOE_DISPATCH_HIST_IN_WS.  Uses
- * shape fields T, D, E, k, dtype. */
+ * The choice is exact: logits are accumulated in float32 by MFMA together
+ * with a rigorous bound on their rounding error, and every token whose top-k
+ * gaps do not clear that bound is recomputed in double (so ties are decided
+ * by the index rule on exact sums).  Gates come from the same logits.
+ * ws (required) receives the per-tile expert histogram of the result, which a
+ * following clearmoe_dispatch with CLEARMOE_DISPATCH_HIST_IN_WS and the same
+ * T, E, k reuses instead of recounting.  Uses shape fields T, D, E, k, dtype. */
 int clearmoe_route(const clearmoe_shape* shape, const void* x, const void* Wg, const float* bg,
                    int32_t* idx, float* gate, void* ws, size_t ws_bytes, hipStream_t stream);
 
@@ -122,6 +124,51 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
                          const void* P, const void* Q, const void* Wg, const float* bg, void* y,
                          int32_t* idx_out, float* gate_out, void* ws, size_t ws_bytes,
                          hipStream_t stream);
+
+/* Dense comparator: y = GELU(x W1^T + b1) W2^T + b2, the unexpertised FFN the
+ * paper's dense rows time (Table III, D0), run through the same GEMM kernels.
+ *   x [T, D]; W1 [H, D], b1 [H]; W2 [D, H], b2 [D]; y [T, D] out (dtype).
+ * Uses T, D, H, dtype (E, k, r, q must still be valid); the workspace of
+ * clearmoe_workspace_bytes(shape) suffices. */
+int clearmoe_dense_ffn_forward(const clearmoe_shape* shape, const void* x, const void* W1,
+                               const float* b1, const void* W2, const float* b2, void* y,
+                               void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* ---- Stage timing (measurement support) -----------------------------------
+ * Kernel stages of the entry points above.  While timing is on, every launch
+ * of a selected stage is bracketed by two HIP events recorded on the stream it
+ * runs on, so the elapsed time is the kernel's own.  Off by default: then no
+ * event is recorded and the entry points behave exactly as documented. */
+enum {
+    CLEARMOE_STAGE_ROUTE = 0,          /* logits + top-k + gates + tile histogram */
+    CLEARMOE_STAGE_TILE_HIST = 1,      /* tile histogram of a given idx */
+    CLEARMOE_STAGE_SCAN = 2,           /* exclusive scan of tile histograms */
+    CLEARMOE_STAGE_PERMUTE = 3,        /* stable permutation (+ row copy) */
+    CLEARMOE_STAGE_COMBINE = 4,        /* gated inverse-permute combine */
+    CLEARMOE_STAGE_FC1 = 5,            /* z = GELU(x W1^T + b1) */
+    CLEARMOE_STAGE_BASIS_T = 6,        /* t = z Vt^T */
+    CLEARMOE_STAGE_BASIS_H = 7,        /* h_sh = t US^T + b2 */
+    CLEARMOE_STAGE_RES_U = 8,          /* u = gate * z[perm] Q_e^T (grouped) */
+    CLEARMOE_STAGE_RES_H = 9,          /* h_res = u P_e^T (grouped) */
+    CLEARMOE_STAGE_COMBINE_RES = 10,   /* y = h_sh + unpermuted h_res */
+    CLEARMOE_STAGE_DENSE_FC2 = 11,     /* dense comparator y = z W2^T + b2 */
+    CLEARMOE_N_STAGES = 12
+};
+
+/* Name of a stage (static string; "?" if out of range). */
+const char* clearmoe_stage_name(int stage);
+
+/* Start timing the stages whose bit is set in stage_mask, for at most
+ * max_records launches in total (the events are created here, once).
+ * Returns CLEARMOE_ERR_INVALID_ARG if timing is already on or max_records < 1,
+ * CLEARMOE_ERR_HIP if an event cannot be created.  Not thread-safe. */
+int clearmoe_timing_start(unsigned stage_mask, int max_records);
+
+/* Stop timing: wait for the recorded events, then write per stage the summed
+ * elapsed milliseconds (ms[CLEARMOE_N_STAGES]) and the number of timed
+ * launches (launches[CLEARMOE_N_STAGES]); either pointer may be NULL.  The
+ * events are destroyed and timing is off afterwards. */
+int clearmoe_timing_stop(double* ms, int32_t* launches);
 
 #ifdef __cplusplus
 }

@@ -16,14 +16,18 @@ import torch
 
 __all__ = ["ClearMoEError", "Shape", "lib", "version", "workspace_bytes", "alloc_workspace",
            "route", "dispatch", "combine", "ffn_forward", "from_stored", "to_stored",
-           "DISPATCH_HIST_IN_WS", "F32", "BF16", "SYMBOLS"]
+           "DISPATCH_HIST_IN_WS", "F32", "BF16", "SYMBOLS", "N_STAGES", "stage_names",
+           "timing_start", "timing_stop", "make_shape", "dense_ffn_forward"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libclearmoe.so")
 F32, BF16 = 0, 1
 DISPATCH_HIST_IN_WS = 1
 SYMBOLS = ("clearmoe_version", "clearmoe_status_string", "clearmoe_workspace_bytes",
-           "clearmoe_route", "clearmoe_dispatch", "clearmoe_combine", "clearmoe_ffn_forward")
+           "clearmoe_route", "clearmoe_dispatch", "clearmoe_combine", "clearmoe_ffn_forward",
+           "clearmoe_dense_ffn_forward", "clearmoe_stage_name", "clearmoe_timing_start",
+           "clearmoe_timing_stop")
+N_STAGES = 12
 
 
 class ClearMoEError(RuntimeError):
@@ -60,6 +64,15 @@ def lib():
         L.clearmoe_combine.argtypes = [sp, vp, vp, vp, vp, vp]
         L.clearmoe_ffn_forward.restype = ctypes.c_int
         L.clearmoe_ffn_forward.argtypes = [sp] + [vp] * 13 + [vp, sz, vp]
+        L.clearmoe_dense_ffn_forward.restype = ctypes.c_int
+        L.clearmoe_dense_ffn_forward.argtypes = [sp] + [vp] * 6 + [vp, sz, vp]
+        L.clearmoe_stage_name.restype = ctypes.c_char_p
+        L.clearmoe_stage_name.argtypes = [ctypes.c_int]
+        L.clearmoe_timing_start.restype = ctypes.c_int
+        L.clearmoe_timing_start.argtypes = [u32, ctypes.c_int]
+        L.clearmoe_timing_stop.restype = ctypes.c_int
+        L.clearmoe_timing_stop.argtypes = [ctypes.POINTER(ctypes.c_double),
+                                           ctypes.POINTER(ctypes.c_int32)]
         _lib = L
     return _lib
 
@@ -177,6 +190,41 @@ def ffn_forward(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int, ws: Optional[torch.
                                     _p(gate_out), _p(ws), ws.numel(), _stream(stream))
     _check(rc, "clearmoe_ffn_forward")
     return y
+
+
+def dense_ffn_forward(x, W1, b1, W2, b2, ws: Optional[torch.Tensor] = None,
+                      out: Optional[torch.Tensor] = None, stream=None):
+    """clearmoe_dense_ffn_forward: y = GELU(x W1^T + b1) W2^T + b2."""
+    T, D = x.shape
+    H = W1.shape[0]
+    s = make_shape(T, D, 1, 1, _dt(x), H=H)
+    ws = alloc_workspace(s, x.device) if ws is None else ws
+    y = torch.empty((T, D), dtype=x.dtype, device=x.device) if out is None else out
+    rc = lib().clearmoe_dense_ffn_forward(ctypes.byref(s), _p(x), _p(W1), _p(b1), _p(W2), _p(b2),
+                                          _p(y), _p(ws), ws.numel(), _stream(stream))
+    _check(rc, "clearmoe_dense_ffn_forward")
+    return y
+
+
+def stage_names():
+    return [lib().clearmoe_stage_name(i).decode() for i in range(N_STAGES)]
+
+
+def timing_start(stages, max_records: int) -> None:
+    """Time every launch of the named stages (at most max_records launches)."""
+    names = stage_names()
+    mask = 0
+    for s in stages:
+        mask |= 1 << names.index(s)
+    _check(lib().clearmoe_timing_start(mask, int(max_records)), "clearmoe_timing_start")
+
+
+def timing_stop() -> dict:
+    """Stop timing; {stage: (total_ms, launches)} for the stages that ran."""
+    ms = (ctypes.c_double * N_STAGES)()
+    n = (ctypes.c_int32 * N_STAGES)()
+    _check(lib().clearmoe_timing_stop(ms, n), "clearmoe_timing_stop")
+    return {name: (ms[i], n[i]) for i, name in enumerate(stage_names()) if n[i] > 0}
 
 
 def from_stored(a: np.ndarray, device="cuda") -> torch.Tensor:

@@ -5,6 +5,9 @@
 
 #include <stdint.h>
 
+#include <mutex>
+#include <vector>
+
 #include "kernels.h"
 
 using namespace clearmoe;
@@ -15,15 +18,14 @@ constexpr size_t kAlign = 256;
 constexpr int64_t kMaxDim = 1 << 16;
 
 size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
-int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 
 // Workspace layout.  Prefix shared by every entry point, then the buffers of
 // the whole-layer forward.
 struct Layout {
-    size_t wgT, tile_counts, tile_base;           // route / dispatch
+    size_t tile_counts, tile_base;                // route / dispatch
     size_t counts, offsets, idx, gate, perm, inv;  // ffn_forward
     size_t z, tproj, hsh, u, hres;
-    size_t route_end, dispatch_end, total;
+    size_t dispatch_end, total;
 };
 
 size_t elem_size(int dtype) { return dtype == CLEARMOE_F32 ? 4 : 2; }
@@ -32,7 +34,6 @@ Layout layout(const clearmoe_shape& s) {
     Layout L{};
     const int64_t T = s.T, k = s.k, E = s.E;
     const int64_t ntiles = route_tiles(T);
-    const int64_t Dpad = round_up(s.D, kWgPadD);
     const size_t es = elem_size(s.dtype);
     size_t off = 0;
     auto take = [&](size_t bytes) {
@@ -45,8 +46,6 @@ Layout layout(const clearmoe_shape& s) {
     L.tile_counts = take(sizeof(int32_t) * (ntiles * E > 0 ? ntiles * E : 1));
     L.tile_base = take(sizeof(int32_t) * (ntiles * E > 0 ? ntiles * E : 1));
     L.dispatch_end = off;
-    L.wgT = take(sizeof(double) * Dpad * route_emax(s.E));
-    L.route_end = off;
     L.counts = take(sizeof(int32_t) * E);
     L.offsets = take(sizeof(int32_t) * (E + 1));
     L.idx = take(sizeof(int32_t) * T * k);
@@ -83,12 +82,44 @@ int check_shape(const clearmoe_shape* s, bool layer) {
     return CLEARMOE_OK;
 }
 
-int hip_status(hipError_t e) { return e == hipSuccess ? CLEARMOE_OK : CLEARMOE_ERR_HIP; }
+// ---- stage timing: two events per timed launch, recorded on its stream ----
+struct StageTimer {
+    bool on = false;
+    unsigned mask = 0;
+    int used = 0;
+    std::vector<hipEvent_t> ev;   // 2 per record
+    std::vector<int> stage;
+};
+StageTimer g_timer;
+std::mutex g_timer_mu;
 
-#define CLEARMOE_TRY(expr)                          \
-    do {                                            \
-        const hipError_t e_ = (expr);               \
-        if (e_ != hipSuccess) return CLEARMOE_ERR_HIP; \
+class StageScope {
+  public:
+    StageScope(int stage, hipStream_t st) : st_(st) {
+        if (!g_timer.on || !((g_timer.mask >> stage) & 1u)) return;
+        std::lock_guard<std::mutex> lk(g_timer_mu);
+        if (g_timer.used >= static_cast<int>(g_timer.stage.size())) return;
+        slot_ = g_timer.used++;
+        g_timer.stage[slot_] = stage;
+        (void)hipEventRecord(g_timer.ev[2 * slot_], st_);
+    }
+    ~StageScope() {
+        if (slot_ >= 0) (void)hipEventRecord(g_timer.ev[2 * slot_ + 1], st_);
+    }
+    StageScope(const StageScope&) = delete;
+    StageScope& operator=(const StageScope&) = delete;
+
+  private:
+    hipStream_t st_;
+    int slot_ = -1;
+};
+
+// Launch one stage under its timing scope.
+#define CLEARMOE_STAGE(stage, st, expr)                  \
+    do {                                                  \
+        StageScope scope_(stage, st);                     \
+        const hipError_t e_ = (expr);                     \
+        if (e_ != hipSuccess) return CLEARMOE_ERR_HIP;    \
     } while (0)
 
 template <typename P>
@@ -98,12 +129,9 @@ P* at(void* ws, size_t off) {
 
 int route_impl(const clearmoe_shape& s, const Layout& L, const void* x, const void* Wg,
                const float* bg, int32_t* idx, float* gate, void* ws, hipStream_t st) {
-    const int emax = route_emax(s.E);
-    const int Dpad = static_cast<int>(round_up(s.D, kWgPadD));
-    double* wgT = at<double>(ws, L.wgT);
-    CLEARMOE_TRY(launch_router_weights_f64(s.dtype, Wg, s.D, s.E, emax, Dpad, wgT, st));
-    CLEARMOE_TRY(launch_route(s.dtype, x, wgT, bg, s.T, s.D, Dpad, s.E, emax, s.k, idx, gate,
-                              at<int32_t>(ws, L.tile_counts), st));
+    CLEARMOE_STAGE(CLEARMOE_STAGE_ROUTE, st,
+                   launch_route(s.dtype, x, Wg, bg, s.T, s.D, s.E, s.k, idx, gate,
+                                at<int32_t>(ws, L.tile_counts), st));
     return CLEARMOE_OK;
 }
 
@@ -113,10 +141,13 @@ int dispatch_impl(const clearmoe_shape& s, const Layout& L, const int32_t* idx, 
     int32_t* tc = at<int32_t>(ws, L.tile_counts);
     int32_t* tb = at<int32_t>(ws, L.tile_base);
     const int64_t nt = route_tiles(s.T);
-    if (!hist_in_ws) CLEARMOE_TRY(launch_tile_histogram(idx, s.T, s.E, s.k, tc, st));
-    CLEARMOE_TRY(launch_scan(tc, nt, s.E, tb, counts, offsets, st));
-    CLEARMOE_TRY(launch_permute(s.dtype, idx, tb, offsets, s.T, s.E, s.k, perm, inv, x, xperm,
-                                s.D, st));
+    if (!hist_in_ws)
+        CLEARMOE_STAGE(CLEARMOE_STAGE_TILE_HIST, st,
+                       launch_tile_histogram(idx, s.T, s.E, s.k, tc, st));
+    CLEARMOE_STAGE(CLEARMOE_STAGE_SCAN, st, launch_scan(tc, nt, s.E, tb, counts, offsets, st));
+    CLEARMOE_STAGE(CLEARMOE_STAGE_PERMUTE, st,
+                   launch_permute(s.dtype, idx, tb, offsets, s.T, s.E, s.k, perm, inv, x, xperm,
+                                  s.D, st));
     return CLEARMOE_OK;
 }
 
@@ -155,13 +186,13 @@ int clearmoe_route(const clearmoe_shape* shape, const void* x, const void* Wg, c
     const clearmoe_shape& s = *shape;
     const bool tok = s.T > 0;                 // per-token arrays may be NULL when T == 0
     if (!Wg || (tok && (!x || !idx || !gate))) return CLEARMOE_ERR_INVALID_ARG;
-    if (!aligned(x, 16) || !aligned(Wg, 4) || !aligned(idx, 4) || !aligned(gate, 4) ||
+    if (!aligned(x, 16) || !aligned(Wg, 16) || !aligned(idx, 4) || !aligned(gate, 4) ||
         (bg && !aligned(bg, 4)))
         return CLEARMOE_ERR_INVALID_ARG;
     clearmoe_shape sl = s;
     sl.H = sl.r = sl.q = 0;
     const Layout L = layout(sl);
-    if (!ws || !aligned(ws, kAlign) || ws_bytes < L.route_end) return CLEARMOE_ERR_WORKSPACE;
+    if (!ws || !aligned(ws, kAlign) || ws_bytes < L.dispatch_end) return CLEARMOE_ERR_WORKSPACE;
     return route_impl(s, L, x, Wg, bg, idx, gate, ws, stream);
 }
 
@@ -194,7 +225,9 @@ int clearmoe_combine(const clearmoe_shape* shape, const void* ye, const int32_t*
     if (s.T > 0 && (!ye || !inv || !gate || !y)) return CLEARMOE_ERR_INVALID_ARG;
     if (!aligned(ye, 16) || !aligned(y, 16) || !aligned(inv, 4) || !aligned(gate, 4))
         return CLEARMOE_ERR_INVALID_ARG;
-    return hip_status(launch_combine_gated(s.dtype, ye, inv, gate, y, s.T, s.D, s.k, stream));
+    CLEARMOE_STAGE(CLEARMOE_STAGE_COMBINE, stream,
+                   launch_combine_gated(s.dtype, ye, inv, gate, y, s.T, s.D, s.k, stream));
+    return CLEARMOE_OK;
 }
 
 int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void* W1,
@@ -208,10 +241,10 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
     if (!W1 || !Wg || (s.T > 0 && (!x || !y))) return CLEARMOE_ERR_INVALID_ARG;
     if (s.r > 0 && (!US || !Vt)) return CLEARMOE_ERR_INVALID_ARG;
     if (s.q > 0 && (!P || !Q)) return CLEARMOE_ERR_INVALID_ARG;
-    const void* v16[] = {x, W1, US, Vt, P, Q, y};
+    const void* v16[] = {x, W1, US, Vt, P, Q, Wg, y};
     for (const void* p : v16)
         if (p && !aligned(p, 16)) return CLEARMOE_ERR_INVALID_ARG;
-    const void* v4[] = {b1, b2, bg, Wg, idx_out, gate_out};
+    const void* v4[] = {b1, b2, bg, idx_out, gate_out};
     for (const void* p : v4)
         if (p && !aligned(p, 4)) return CLEARMOE_ERR_INVALID_ARG;
     const Layout L = layout(s);
@@ -245,7 +278,7 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
     g.C = z; g.ldc = s.H; g.c_f32 = 0;
     g.bias = b1; g.gelu = 1;
     g.M = T; g.N = s.H; g.K = s.D;
-    CLEARMOE_TRY(launch_gemm(s.dtype, g, st));
+    CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
 
     // 4. shared basis: t = z Vt^T ; h_sh = t US^T + b2
     g = GemmDesc{};
@@ -253,14 +286,14 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
     g.B = Vt; g.ldb = s.H;
     g.C = tproj; g.ldc = s.r; g.c_f32 = 0;
     g.M = T; g.N = s.r; g.K = s.H;
-    if (s.r > 0) CLEARMOE_TRY(launch_gemm(s.dtype, g, st));
+    if (s.r > 0) CLEARMOE_STAGE(CLEARMOE_STAGE_BASIS_T, st, launch_gemm(s.dtype, g, st));
     g = GemmDesc{};
     g.A = tproj; g.lda = s.r; g.a_div = 1;
     g.B = US; g.ldb = s.r;
     g.C = hsh; g.ldc = s.D; g.c_f32 = 1;
     g.bias = b2;
     g.M = T; g.N = s.D; g.K = s.r;
-    CLEARMOE_TRY(launch_gemm(s.dtype, g, st));
+    CLEARMOE_STAGE(CLEARMOE_STAGE_BASIS_H, st, launch_gemm(s.dtype, g, st));
 
     // 5. residual, grouped by expert: u = gate * (z[perm/k] Q_e^T) ; h_res = u P_e^T
     g = GemmDesc{};
@@ -270,18 +303,105 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
     g.row_scale = gate; g.scale_rows = perm;
     g.M = A; g.N = s.q; g.K = s.H;
     g.seg_offsets = offsets; g.nseg = s.E;
-    if (s.q > 0) CLEARMOE_TRY(launch_gemm(s.dtype, g, st));
+    if (s.q > 0) CLEARMOE_STAGE(CLEARMOE_STAGE_RES_U, st, launch_gemm(s.dtype, g, st));
     g = GemmDesc{};
     g.A = u; g.lda = s.q; g.a_div = 1;
     g.B = P; g.ldb = s.q; g.b_seg_stride = static_cast<int64_t>(s.D) * s.q;
     g.C = hres; g.ldc = s.D; g.c_f32 = 1;
     g.M = A; g.N = s.D; g.K = s.q;
     g.seg_offsets = offsets; g.nseg = s.E;
-    CLEARMOE_TRY(launch_gemm(s.dtype, g, st));
+    CLEARMOE_STAGE(CLEARMOE_STAGE_RES_H, st, launch_gemm(s.dtype, g, st));
 
     // 6. y[t] = h_sh[t] + sum_j h_res[inv[t*k+j]]
-    CLEARMOE_TRY(launch_combine_residual(s.dtype, hsh, hres, inv, y, T, s.D, s.k, st));
+    CLEARMOE_STAGE(CLEARMOE_STAGE_COMBINE_RES, st,
+                   launch_combine_residual(s.dtype, hsh, hres, inv, y, T, s.D, s.k, st));
     return CLEARMOE_OK;
+}
+
+int clearmoe_dense_ffn_forward(const clearmoe_shape* shape, const void* x, const void* W1,
+                               const float* b1, const void* W2, const float* b2, void* y,
+                               void* ws, size_t ws_bytes, hipStream_t stream) {
+    int rc = check_shape(shape, true);
+    if (rc != CLEARMOE_OK) return rc;
+    const clearmoe_shape& s = *shape;
+    if (!W1 || !W2 || (s.T > 0 && (!x || !y))) return CLEARMOE_ERR_INVALID_ARG;
+    const void* v16[] = {x, W1, W2, y};
+    for (const void* p : v16)
+        if (p && !aligned(p, 16)) return CLEARMOE_ERR_INVALID_ARG;
+    if ((b1 && !aligned(b1, 4)) || (b2 && !aligned(b2, 4))) return CLEARMOE_ERR_INVALID_ARG;
+    const Layout L = layout(s);
+    if (!ws || !aligned(ws, kAlign) || ws_bytes < L.total) return CLEARMOE_ERR_WORKSPACE;
+    if (s.T == 0) return CLEARMOE_OK;
+    void* z = at<void>(ws, L.z);
+    GemmDesc g{};
+    g.A = x; g.lda = s.D; g.a_div = 1;
+    g.B = W1; g.ldb = s.D;
+    g.C = z; g.ldc = s.H; g.c_f32 = 0;
+    g.bias = b1; g.gelu = 1;
+    g.M = s.T; g.N = s.H; g.K = s.D;
+    CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, stream, launch_gemm(s.dtype, g, stream));
+    g = GemmDesc{};
+    g.A = z; g.lda = s.H; g.a_div = 1;
+    g.B = W2; g.ldb = s.H;
+    g.C = y; g.ldc = s.D; g.c_f32 = 0;
+    g.bias = b2;
+    g.M = s.T; g.N = s.D; g.K = s.H;
+    CLEARMOE_STAGE(CLEARMOE_STAGE_DENSE_FC2, stream, launch_gemm(s.dtype, g, stream));
+    return CLEARMOE_OK;
+}
+
+const char* clearmoe_stage_name(int stage) {
+    static const char* names[CLEARMOE_N_STAGES] = {
+        "route", "tile_hist", "scan", "permute", "combine", "fc1_gelu",
+        "basis_t", "basis_h", "res_u", "res_h", "combine_res", "dense_fc2"};
+    return (stage >= 0 && stage < CLEARMOE_N_STAGES) ? names[stage] : "?";
+}
+
+int clearmoe_timing_start(unsigned stage_mask, int max_records) {
+    std::lock_guard<std::mutex> lk(g_timer_mu);
+    if (g_timer.on || max_records < 1) return CLEARMOE_ERR_INVALID_ARG;
+    g_timer.ev.assign(2 * static_cast<size_t>(max_records), nullptr);
+    g_timer.stage.assign(static_cast<size_t>(max_records), -1);
+    for (auto& e : g_timer.ev) {
+        if (hipEventCreate(&e) != hipSuccess) {
+            for (auto& f : g_timer.ev)
+                if (f) (void)hipEventDestroy(f);
+            g_timer.ev.clear();
+            g_timer.stage.clear();
+            return CLEARMOE_ERR_HIP;
+        }
+    }
+    g_timer.mask = stage_mask;
+    g_timer.used = 0;
+    g_timer.on = true;
+    return CLEARMOE_OK;
+}
+
+int clearmoe_timing_stop(double* ms, int32_t* launches) {
+    std::lock_guard<std::mutex> lk(g_timer_mu);
+    if (!g_timer.on) return CLEARMOE_ERR_INVALID_ARG;
+    double acc[CLEARMOE_N_STAGES] = {};
+    int32_t cnt[CLEARMOE_N_STAGES] = {};
+    int rc = CLEARMOE_OK;
+    for (int i = 0; i < g_timer.used; ++i) {
+        float t = 0.0f;
+        if (hipEventSynchronize(g_timer.ev[2 * i + 1]) != hipSuccess ||
+            hipEventElapsedTime(&t, g_timer.ev[2 * i], g_timer.ev[2 * i + 1]) != hipSuccess) {
+            rc = CLEARMOE_ERR_HIP;
+            continue;
+        }
+        acc[g_timer.stage[i]] += t;
+        cnt[g_timer.stage[i]] += 1;
+    }
+    for (auto& e : g_timer.ev) (void)hipEventDestroy(e);
+    g_timer.ev.clear();
+    g_timer.stage.clear();
+    g_timer.on = false;
+    for (int i = 0; i < CLEARMOE_N_STAGES; ++i) {
+        if (ms) ms[i] = acc[i];
+        if (launches) launches[i] = cnt[i];
+    }
+    return rc;
 }
 
 }  // extern "C"

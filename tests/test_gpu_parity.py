@@ -261,3 +261,27 @@ def test_dispatch_workload_full_size():
     xs = oracle.widen(L["x"][toks])
     assert np.all(np.abs(got - xs) <= 2.0 ** -7 * np.abs(xs))
     assert np.mean(got == xs) > 0.99
+
+
+@pytest.mark.parametrize("name", ["C1", "C2"])
+def test_dense_comparator(name):
+    """Dense FFN through the same GEMM kernels.  The oracle's layer reduces to
+    it exactly with US = I, Vt = W2 (r = D) and a zero residual."""
+    cfg = synth.CONFIGS[name]
+    L = synth.make_layer(cfg)
+    W2 = L["W2"].astype(np.float32) if cfg.dtype == "f32" else synth.to_bf16_bits(L["W2"])
+    rng = np.random.default_rng(2)
+    b1 = (0.1 * rng.standard_normal(cfg.H)).astype(np.float32)
+    b2 = (0.1 * rng.standard_normal(cfg.D)).astype(np.float32)
+    y = cm.dense_ffn_forward(dev(L["x"]), dev(L["W1"]), dev(b1), dev(W2), dev(b2))
+    torch.cuda.synchronize()
+    rows = _sample_rows(cfg.T, 256, 6)
+    D = cfg.D
+    eye = np.eye(D, dtype=np.float32)
+    ref = oracle.ffn_forward(L["x"][rows], L["W1"], b1, eye, W2, b2, np.zeros((1, D, 8)),
+                             np.zeros((1, 8, cfg.H)), np.zeros((1, D), np.float32), None, 1)
+    got = oracle.widen(cm.to_stored(y))[rows]
+    if cfg.dtype == "f32":
+        assert max_rel(got, ref["y"]) <= F32_MAXREL
+    else:
+        assert frob_rel(got, ref["y"]) <= BF16_FROB_REGRESS
