@@ -75,6 +75,8 @@ def stage_work(stage, cfg, b):
         "res_h": (2 * A * D * q, A * q * b + E * D * q * b + A * D * 4),
         "combine_res": (0, T * D * 4 + A * D * 4 + A * 4 + T * D * b),
         "dense_fc2": (2 * T * D * H, T * H * b + D * H * b + T * D * b),
+        "tu_grouped": (2 * A * (r + q) * H, A * H * b + (r + E * q) * H * b + A * (r + q) * b),
+        "y_grouped": (2 * A * D * (r + q), A * (r + q) * b + D * (r + E * q) * b + T * D * b),
     }
     return w.get(stage, (0, 0))
 

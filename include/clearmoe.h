@@ -118,7 +118,10 @@ int clearmoe_combine(const clearmoe_shape* shape, const void* ye, const int32_t*
  *   Wg [E, D], bg [E];  y [T, D] out.
  *   idx_out [T, k] / gate_out [T, k]: optional copies of the routing (NULL ok).
  * bfloat16 mode accumulates in float32; the hidden activation z and the
- * rank-r / rank-q projections are rounded to bfloat16 between products. */
+ * rank-r / rank-q projections are rounded to bfloat16 between products.
+ * For k = 1 the shared basis and the residual run as two products over the
+ * expert order ([t|u] = z[perm] [Vt;Q_e]^T, then y[perm] = [t|u] [US|P_e]^T
+ * + b2); for k > 1 h_sh and h_res are formed apart and combined. */
 int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void* W1,
                          const float* b1, const void* US, const void* Vt, const float* b2,
                          const void* P, const void* Q, const void* Wg, const float* bg, void* y,
@@ -152,7 +155,9 @@ enum {
     CLEARMOE_STAGE_RES_H = 9,          /* h_res = u P_e^T (grouped) */
     CLEARMOE_STAGE_COMBINE_RES = 10,   /* y = h_sh + unpermuted h_res */
     CLEARMOE_STAGE_DENSE_FC2 = 11,     /* dense comparator y = z W2^T + b2 */
-    CLEARMOE_N_STAGES = 12
+    CLEARMOE_STAGE_TU = 12,            /* top-1: [t|u] = z[perm] [Vt;Q_e]^T (grouped) */
+    CLEARMOE_STAGE_Y = 13,             /* top-1: y[perm] = [t|u] [US|P_e]^T + b2 (grouped) */
+    CLEARMOE_N_STAGES = 14
 };
 
 /* Name of a stage (static string; "?" if out of range). */

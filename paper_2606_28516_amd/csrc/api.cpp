@@ -24,7 +24,7 @@ size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 struct Layout {
     size_t tile_counts, tile_base;                // route / dispatch
     size_t counts, offsets, idx, gate, perm, inv;  // ffn_forward
-    size_t z, tproj, hsh, u, hres;
+    size_t z, tproj, hsh, u, hres, tu;
     size_t dispatch_end, total;
 };
 
@@ -57,6 +57,7 @@ Layout layout(const clearmoe_shape& s) {
     L.hsh = take(sizeof(float) * T * s.D);
     L.u = take(es * T * k * s.q);
     L.hres = take(sizeof(float) * T * k * s.D);
+    L.tu = take(es * T * k * (s.r + s.q));
     L.total = off;
     return L;
 }
@@ -144,10 +145,17 @@ int dispatch_impl(const clearmoe_shape& s, const Layout& L, const int32_t* idx, 
     if (!hist_in_ws)
         CLEARMOE_STAGE(CLEARMOE_STAGE_TILE_HIST, st,
                        launch_tile_histogram(idx, s.T, s.E, s.k, tc, st));
-    CLEARMOE_STAGE(CLEARMOE_STAGE_SCAN, st, launch_scan(tc, nt, s.E, tb, counts, offsets, st));
-    CLEARMOE_STAGE(CLEARMOE_STAGE_PERMUTE, st,
-                   launch_permute(s.dtype, idx, tb, offsets, s.T, s.E, s.k, perm, inv, x, xperm,
-                                  s.D, st));
+    if (nt * s.E <= kInlineScanMax) {
+        // small histogram: the permutation scans it itself (one launch fewer)
+        CLEARMOE_STAGE(CLEARMOE_STAGE_PERMUTE, st,
+                       launch_permute(s.dtype, idx, tb, offsets, tc, counts, s.T, s.E, s.k, perm,
+                                      inv, x, xperm, s.D, st));
+    } else {
+        CLEARMOE_STAGE(CLEARMOE_STAGE_SCAN, st, launch_scan(tc, nt, s.E, tb, counts, offsets, st));
+        CLEARMOE_STAGE(CLEARMOE_STAGE_PERMUTE, st,
+                       launch_permute(s.dtype, idx, tb, offsets, nullptr, counts, s.T, s.E, s.k,
+                                      perm, inv, x, xperm, s.D, st));
+    }
     return CLEARMOE_OK;
 }
 
@@ -271,44 +279,68 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
     rc = dispatch_impl(s, L, idx, ws, counts, offsets, perm, inv, nullptr, nullptr, true, st);
     if (rc != CLEARMOE_OK) return rc;
 
-    // 3. z = GELU(x W1^T + b1)
-    GemmDesc g{};
-    g.A = x; g.lda = s.D; g.a_div = 1;
+    // 3. z = GELU(x W1^T + b1), token order
+    GemmDesc g = gemm_desc(T, s.H, s.D);
+    g.A = x; g.lda = s.D;
     g.B = W1; g.ldb = s.D;
     g.C = z; g.ldc = s.H; g.c_f32 = 0;
     g.bias = b1; g.gelu = 1;
-    g.M = T; g.N = s.H; g.K = s.D;
     CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
 
+    if (s.k == 1) {
+        // Top-1: every row p of the expert order is one token, so the shared
+        // basis and the residual merge into two grouped products over p:
+        //   [t | u](p) = z[perm p] [Vt ; Q_e]^T, the u columns scaled by the gate;
+        //   y[perm p]  = [t | u](p) [US | P_e]^T + b2   (each y row written once).
+        void* tu = at<void>(ws, L.tu);
+        const int rq = s.r + s.q;
+        g = gemm_desc(A, rq, s.H);
+        g.A = z; g.lda = s.H; g.a_rows = perm; g.a_div = 1;
+        g.B = Vt; g.ldb = s.H; g.b_seg_stride = 0;
+        g.B1 = Q; g.ldb1 = s.H; g.b1_seg_stride = static_cast<int64_t>(s.q) * s.H;
+        g.n_split = s.r;
+        g.C = tu; g.ldc = rq; g.c_f32 = 0;
+        g.row_scale = gate; g.scale_rows = perm; g.scale_col0 = s.r;
+        g.seg_offsets = offsets; g.nseg = s.E;
+        if (rq > 0) CLEARMOE_STAGE(CLEARMOE_STAGE_TU, st, launch_gemm(s.dtype, g, st));
+        g = gemm_desc(A, s.D, rq);
+        g.A = tu; g.lda = rq;
+        g.B = US; g.ldb = s.r; g.b_seg_stride = 0;
+        g.B1 = P; g.ldb1 = s.q; g.b1_seg_stride = static_cast<int64_t>(s.D) * s.q;
+        g.k_split = s.r;
+        g.C = y; g.ldc = s.D; g.c_f32 = 0;
+        g.c_rows = perm; g.c_div = 1;
+        g.bias = b2;
+        g.seg_offsets = offsets; g.nseg = s.E;
+        CLEARMOE_STAGE(CLEARMOE_STAGE_Y, st, launch_gemm(s.dtype, g, st));
+        return CLEARMOE_OK;
+    }
+
     // 4. shared basis: t = z Vt^T ; h_sh = t US^T + b2
-    g = GemmDesc{};
-    g.A = z; g.lda = s.H; g.a_div = 1;
+    g = gemm_desc(T, s.r, s.H);
+    g.A = z; g.lda = s.H;
     g.B = Vt; g.ldb = s.H;
     g.C = tproj; g.ldc = s.r; g.c_f32 = 0;
-    g.M = T; g.N = s.r; g.K = s.H;
     if (s.r > 0) CLEARMOE_STAGE(CLEARMOE_STAGE_BASIS_T, st, launch_gemm(s.dtype, g, st));
-    g = GemmDesc{};
-    g.A = tproj; g.lda = s.r; g.a_div = 1;
+    g = gemm_desc(T, s.D, s.r);
+    g.A = tproj; g.lda = s.r;
     g.B = US; g.ldb = s.r;
     g.C = hsh; g.ldc = s.D; g.c_f32 = 1;
     g.bias = b2;
-    g.M = T; g.N = s.D; g.K = s.r;
     CLEARMOE_STAGE(CLEARMOE_STAGE_BASIS_H, st, launch_gemm(s.dtype, g, st));
 
     // 5. residual, grouped by expert: u = gate * (z[perm/k] Q_e^T) ; h_res = u P_e^T
-    g = GemmDesc{};
+    g = gemm_desc(A, s.q, s.H);
     g.A = z; g.lda = s.H; g.a_rows = perm; g.a_div = s.k;
     g.B = Q; g.ldb = s.H; g.b_seg_stride = static_cast<int64_t>(s.q) * s.H;
     g.C = u; g.ldc = s.q; g.c_f32 = 0;
     g.row_scale = gate; g.scale_rows = perm;
-    g.M = A; g.N = s.q; g.K = s.H;
     g.seg_offsets = offsets; g.nseg = s.E;
     if (s.q > 0) CLEARMOE_STAGE(CLEARMOE_STAGE_RES_U, st, launch_gemm(s.dtype, g, st));
-    g = GemmDesc{};
-    g.A = u; g.lda = s.q; g.a_div = 1;
+    g = gemm_desc(A, s.D, s.q);
+    g.A = u; g.lda = s.q;
     g.B = P; g.ldb = s.q; g.b_seg_stride = static_cast<int64_t>(s.D) * s.q;
     g.C = hres; g.ldc = s.D; g.c_f32 = 1;
-    g.M = A; g.N = s.D; g.K = s.q;
     g.seg_offsets = offsets; g.nseg = s.E;
     CLEARMOE_STAGE(CLEARMOE_STAGE_RES_H, st, launch_gemm(s.dtype, g, st));
 
@@ -333,19 +365,17 @@ int clearmoe_dense_ffn_forward(const clearmoe_shape* shape, const void* x, const
     if (!ws || !aligned(ws, kAlign) || ws_bytes < L.total) return CLEARMOE_ERR_WORKSPACE;
     if (s.T == 0) return CLEARMOE_OK;
     void* z = at<void>(ws, L.z);
-    GemmDesc g{};
-    g.A = x; g.lda = s.D; g.a_div = 1;
+    GemmDesc g = gemm_desc(s.T, s.H, s.D);
+    g.A = x; g.lda = s.D;
     g.B = W1; g.ldb = s.D;
     g.C = z; g.ldc = s.H; g.c_f32 = 0;
     g.bias = b1; g.gelu = 1;
-    g.M = s.T; g.N = s.H; g.K = s.D;
     CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, stream, launch_gemm(s.dtype, g, stream));
-    g = GemmDesc{};
-    g.A = z; g.lda = s.H; g.a_div = 1;
+    g = gemm_desc(s.T, s.D, s.H);
+    g.A = z; g.lda = s.H;
     g.B = W2; g.ldb = s.H;
     g.C = y; g.ldc = s.D; g.c_f32 = 0;
     g.bias = b2;
-    g.M = s.T; g.N = s.D; g.K = s.H;
     CLEARMOE_STAGE(CLEARMOE_STAGE_DENSE_FC2, stream, launch_gemm(s.dtype, g, stream));
     return CLEARMOE_OK;
 }
@@ -353,7 +383,8 @@ int clearmoe_dense_ffn_forward(const clearmoe_shape* shape, const void* x, const
 const char* clearmoe_stage_name(int stage) {
     static const char* names[CLEARMOE_N_STAGES] = {
         "route", "tile_hist", "scan", "permute", "combine", "fc1_gelu",
-        "basis_t", "basis_h", "res_u", "res_h", "combine_res", "dense_fc2"};
+        "basis_t", "basis_h", "res_u", "res_h", "combine_res", "dense_fc2", "tu_grouped",
+        "y_grouped"};
     return (stage >= 0 && stage < CLEARMOE_N_STAGES) ? names[stage] : "?";
 }
 

@@ -65,65 +65,118 @@ __global__ __launch_bounds__(kRouteTile) void k_tile_hist(const int32_t* __restr
     if (tid < E) tile_counts[static_cast<int64_t>(blockIdx.x) * E + tid] = s_run[tid];
 }
 
-// One workgroup: exclusive scan over tiles, expert by expert.
+// One workgroup: exclusive scan over tiles of every expert column at once.
+// 1024 tiles per pass, one per thread; a thread holds its tile's histogram
+// (EP >= E registers), the wave scans it with shuffles, wave totals and the
+// running carry of earlier passes live in LDS.
+template <int EP>
 __global__ __launch_bounds__(1024) void k_scan(const int32_t* __restrict__ tc, int64_t ntiles,
                                                int E, int32_t* __restrict__ tb,
                                                int32_t* __restrict__ counts,
                                                int32_t* __restrict__ offsets) {
-    __shared__ int s_wsum[16];
-    __shared__ int s_tot[64];
+    __shared__ int s_wsum[16][EP];
+    __shared__ int s_carry[EP];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int64_t per = (ntiles + 1023) / 1024;
-    const int64_t b0 = tid * per;
-    const int64_t b1 = b0 + per < ntiles ? b0 + per : ntiles;
-    for (int e = 0; e < E; ++e) {
-        int s = 0;
-        for (int64_t b = b0; b < b1; ++b) s += tc[b * E + e];
-        int v = s;
+    if (tid < EP) s_carry[tid] = 0;
+    __syncthreads();
+    for (int64_t b0 = 0; b0 < ntiles; b0 += 1024) {
+        const int64_t b = b0 + tid;
+        const bool in = b < ntiles;
+        int v[EP], c[EP];
+#pragma unroll
+        for (int e = 0; e < EP; ++e) {
+            c[e] = (in && e < E) ? tc[b * E + e] : 0;
+            v[e] = c[e];
+        }
 #pragma unroll
         for (int o = 1; o < 64; o <<= 1) {
-            const int n = __shfl_up(v, o);
-            if (lane >= o) v += n;
+#pragma unroll
+            for (int e = 0; e < EP; ++e) {
+                const int n = __shfl_up(v[e], o);
+                if (lane >= o) v[e] += n;
+            }
         }
-        if (lane == 63) s_wsum[w] = v;
+        if (lane == 63) {
+#pragma unroll
+            for (int e = 0; e < EP; ++e) s_wsum[w][e] = v[e];
+        }
         __syncthreads();
-        int pre = 0;
-        for (int i = 0; i < w; ++i) pre += s_wsum[i];
-        int run = pre + v - s;
-        for (int64_t b = b0; b < b1; ++b) {
-            tb[b * E + e] = run;
-            run += tc[b * E + e];
+#pragma unroll
+        for (int e = 0; e < EP; ++e) {
+            int pre = s_carry[e];
+            for (int i = 0; i < w; ++i) pre += s_wsum[i][e];
+            if (in && e < E) tb[b * E + e] = pre + v[e] - c[e];
         }
-        if (tid == 1023) s_tot[e] = pre + v;
+        __syncthreads();
+        if (tid < EP) {
+            int sum = 0;
+            for (int i = 0; i < 16; ++i) sum += s_wsum[i][tid];
+            s_carry[tid] += sum;
+        }
         __syncthreads();
     }
     if (tid == 0) {
         int o = 0;
         for (int e = 0; e < E; ++e) {
-            counts[e] = s_tot[e];
+            counts[e] = s_carry[e];
             offsets[e] = o;
-            o += s_tot[e];
+            o += s_carry[e];
         }
         offsets[E] = o;
     }
 }
 
+// Stable permutation.  Tile bases come either from the scan kernel
+// (tile_base + offsets) or, when tile_counts is given (small histograms), from
+// an inline scan: every workgroup sums the histogram columns itself (LDS
+// integer atomics: exact and order independent) and workgroup 0 publishes
+// counts and offsets.
 template <typename Tin>
 __global__ __launch_bounds__(kRouteTile) void k_permute(
     const int32_t* __restrict__ idx, const int32_t* __restrict__ tb,
-    const int32_t* __restrict__ offsets, int64_t T, int E, int k, int32_t* __restrict__ perm,
+    int32_t* __restrict__ offsets, const int32_t* __restrict__ tile_counts,
+    int32_t* __restrict__ counts, int64_t T, int E, int k, int32_t* __restrict__ perm,
     int32_t* __restrict__ inv, const Tin* __restrict__ x, Tin* __restrict__ xperm, int D) {
     extern __shared__ int s_p[];          // [256 * k] destination of each assignment
     __shared__ int s_wc[kWaves][64];
     __shared__ int s_run[64];
     __shared__ int s_base[64];
+    __shared__ int s_pre[64], s_tot[64];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int64_t A = T * k;
     const int64_t a0 = static_cast<int64_t>(blockIdx.x) * kRouteTile * k;
     const int64_t na64 = A - a0 < static_cast<int64_t>(kRouteTile) * k ? A - a0
                                                                          : static_cast<int64_t>(kRouteTile) * k;
     const int na = static_cast<int>(na64);
-    if (tid < E) {
+    if (tile_counts != nullptr) {
+        if (tid < E) {
+            s_pre[tid] = 0;
+            s_tot[tid] = 0;
+        }
+        __syncthreads();
+        const int64_t nt = route_tiles(T);
+        for (int64_t i = tid; i < nt * E; i += kRouteTile) {
+            const int64_t b = i / E;
+            const int e = static_cast<int>(i - b * E);
+            const int c = tile_counts[i];
+            atomicAdd(&s_tot[e], c);
+            if (b < static_cast<int64_t>(blockIdx.x)) atomicAdd(&s_pre[e], c);
+        }
+        __syncthreads();
+        if (tid == 0) {
+            int o = 0;
+            for (int e = 0; e < E; ++e) {
+                s_base[e] = o + s_pre[e];
+                if (blockIdx.x == 0) {
+                    counts[e] = s_tot[e];
+                    offsets[e] = o;
+                }
+                o += s_tot[e];
+            }
+            if (blockIdx.x == 0) offsets[E] = o;
+        }
+        if (tid < E) s_run[tid] = 0;
+    } else if (tid < E) {
         s_run[tid] = 0;
         s_base[tid] = offsets[tid] + tb[static_cast<int64_t>(blockIdx.x) * E + tid];
     }
@@ -162,22 +215,47 @@ __global__ __launch_bounds__(kRouteTile) void k_permute(
         __syncthreads();
     }
     if (xperm != nullptr) {
+        // Row copy: 16-byte pieces, four per thread per round (all loads issued
+        // before the stores); the destination rows are written once and read
+        // later by another kernel, so the stores bypass the caches.
         constexpr int PER16 = Elem<Tin>::per16;
+        constexpr int U = 4;
         const int ppr = D / PER16;                      // 16-byte pieces per row
         const int npairs = na * ppr;
-#pragma unroll 4
-        for (int pr = tid; pr < npairs; pr += kRouteTile) {
-            const int al = pr / ppr, pc = pr - al * ppr;
-            const int p = s_p[al];
-            if (p < 0) continue;
-            const int64_t tok = (a0 + al) / k;
-            const uint4 v = *reinterpret_cast<const uint4*>(x + tok * D + pc * PER16);
-            *reinterpret_cast<uint4*>(xperm + static_cast<int64_t>(p) * D + pc * PER16) = v;
+        for (int base = 0; base < npairs; base += U * kRouteTile) {
+            u32x4 v[U];
+            int dp[U], dc[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int pr = base + u * kRouteTile + tid;
+                dp[u] = -1;
+                dc[u] = 0;
+                if (pr < npairs) {
+                    const int al = pr / ppr, pc = pr - al * ppr;
+                    const int p = s_p[al];
+                    if (p >= 0) {
+                        const int64_t tok = (a0 + al) / k;
+                        v[u] = *reinterpret_cast<const u32x4*>(x + tok * D + pc * PER16);
+                        dp[u] = p;
+                        dc[u] = pc;
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (dp[u] >= 0)
+                    __builtin_nontemporal_store(
+                        v[u], reinterpret_cast<u32x4*>(xperm + static_cast<int64_t>(dp[u]) * D +
+                                                       dc[u] * PER16));
         }
     }
 }
 
-// y[t, :] = sum_j gate[t, j] * ye[inv[t*k + j], :], float32 accumulation in slot order.
+constexpr int kCombineU = 4;   // 16-byte output pieces per thread
+
+// y[t, :] = sum_j gate[t, j] * ye[inv[t*k + j], :], float32 accumulation in
+// slot order.  A workgroup covers 256*U consecutive 16-byte pieces of y, a
+// thread U of them (stride 256, so each load instruction is coalesced).
 template <typename T>
 __global__ __launch_bounds__(256) void k_combine_gated(const T* __restrict__ ye,
                                                        const int32_t* __restrict__ inv,
@@ -186,60 +264,105 @@ __global__ __launch_bounds__(256) void k_combine_gated(const T* __restrict__ ye,
                                                        int k) {
     constexpr int PER16 = Elem<T>::per16;
     const int ppr = D / PER16;
-    const int64_t pr = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    if (pr >= Tn * ppr) return;
-    const int64_t t = pr / ppr;
-    const int pc = static_cast<int>(pr - t * ppr);
-    float acc[PER16];
+    const int64_t n = Tn * ppr, A = Tn * k;
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * 256 * kCombineU + threadIdx.x;
+    float acc[kCombineU][PER16];
 #pragma unroll
-    for (int u = 0; u < PER16; ++u) acc[u] = 0.0f;
-    const int64_t A = Tn * k;
+    for (int u = 0; u < kCombineU; ++u)
+#pragma unroll
+        for (int i = 0; i < PER16; ++i) acc[u][i] = 0.0f;
     for (int j = 0; j < k; ++j) {
-        const int64_t p = inv[t * k + j];
-        if (p < 0 || p >= A) continue;           // never follow an invalid index
-        const float g = gate[t * k + j];
-        const uint4 v = *reinterpret_cast<const uint4*>(ye + p * D + pc * PER16);
-        T vals[PER16];
-        __builtin_memcpy(vals, &v, 16);
+        u32x4 v[kCombineU];
+        float g[kCombineU];
 #pragma unroll
-        for (int u = 0; u < PER16; ++u) acc[u] = __builtin_fmaf(g, Elem<T>::to_f32(vals[u]), acc[u]);
+        for (int u = 0; u < kCombineU; ++u) {
+            const int64_t pr = base + u * 256;
+            g[u] = 0.0f;
+            v[u] = u32x4{0u, 0u, 0u, 0u};
+            if (pr < n) {
+                const int64_t t = pr / ppr, pc = pr - t * ppr;
+                const int64_t p = inv[t * k + j];
+                if (p >= 0 && p < A) {               // never follow an invalid index
+                    g[u] = gate[t * k + j];
+                    v[u] = *reinterpret_cast<const u32x4*>(ye + p * D + pc * PER16);
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kCombineU; ++u) {
+            T vals[PER16];
+            __builtin_memcpy(vals, &v[u], 16);
+#pragma unroll
+            for (int i = 0; i < PER16; ++i)
+                acc[u][i] = __builtin_fmaf(g[u], Elem<T>::to_f32(vals[i]), acc[u][i]);
+        }
     }
-    T out[PER16];
 #pragma unroll
-    for (int u = 0; u < PER16; ++u) out[u] = Elem<T>::from_f32(acc[u]);
-    uint4 o;
-    __builtin_memcpy(&o, out, 16);
-    *reinterpret_cast<uint4*>(y + t * D + pc * PER16) = o;
+    for (int u = 0; u < kCombineU; ++u) {
+        const int64_t pr = base + u * 256;
+        if (pr >= n) continue;
+        T out[PER16];
+#pragma unroll
+        for (int i = 0; i < PER16; ++i) out[i] = Elem<T>::from_f32(acc[u][i]);
+        u32x4 o;
+        __builtin_memcpy(&o, out, 16);
+        const int64_t t = pr / ppr, pc = pr - t * ppr;
+        *reinterpret_cast<u32x4*>(y + t * D + pc * PER16) = o;
+    }
 }
 
-// y[t, :] = hsh[t, :] + sum_j hres[inv[t*k + j], :]  (float32 in, dtype out).
+// y[t, :] = hsh[t, :] + sum_j hres[inv[t*k + j], :]  (float32 in, dtype out);
+// 4-float pieces, U per thread as above.
 template <typename T>
 __global__ __launch_bounds__(256) void k_combine_residual(const float* __restrict__ hsh,
                                                           const float* __restrict__ hres,
                                                           const int32_t* __restrict__ inv,
                                                           T* __restrict__ y, int64_t Tn, int D,
                                                           int k) {
-    const int ppr = D / 4;                       // 4 floats per piece
-    const int64_t pr = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    if (pr >= Tn * ppr) return;
-    const int64_t t = pr / ppr;
-    const int pc = static_cast<int>(pr - t * ppr);
-    float4 a = *reinterpret_cast<const float4*>(hsh + t * D + pc * 4);
-    const int64_t A = Tn * k;
-    for (int j = 0; j < k; ++j) {
-        const int64_t p = inv[t * k + j];
-        if (p < 0 || p >= A) continue;
-        const float4 b = *reinterpret_cast<const float4*>(hres + p * D + pc * 4);
-        a.x += b.x;
-        a.y += b.y;
-        a.z += b.z;
-        a.w += b.w;
-    }
-    T out[4] = {Elem<T>::from_f32(a.x), Elem<T>::from_f32(a.y), Elem<T>::from_f32(a.z),
-                Elem<T>::from_f32(a.w)};
-    T* dst = y + t * D + pc * 4;
+    const int ppr = D / 4;
+    const int64_t n = Tn * ppr, A = Tn * k;
+    const int64_t base = static_cast<int64_t>(blockIdx.x) * 256 * kCombineU + threadIdx.x;
+    float4 a[kCombineU];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) dst[u] = out[u];
+    for (int u = 0; u < kCombineU; ++u) {
+        const int64_t pr = base + u * 256;
+        a[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (pr < n) {
+            const int64_t t = pr / ppr, pc = pr - t * ppr;
+            a[u] = *reinterpret_cast<const float4*>(hsh + t * D + pc * 4);
+        }
+    }
+    for (int j = 0; j < k; ++j) {
+        float4 bv[kCombineU];
+#pragma unroll
+        for (int u = 0; u < kCombineU; ++u) {
+            const int64_t pr = base + u * 256;
+            bv[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (pr < n) {
+                const int64_t t = pr / ppr, pc = pr - t * ppr;
+                const int64_t p = inv[t * k + j];
+                if (p >= 0 && p < A) bv[u] = *reinterpret_cast<const float4*>(hres + p * D + pc * 4);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kCombineU; ++u) {
+            a[u].x += bv[u].x;
+            a[u].y += bv[u].y;
+            a[u].z += bv[u].z;
+            a[u].w += bv[u].w;
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kCombineU; ++u) {
+        const int64_t pr = base + u * 256;
+        if (pr >= n) continue;
+        const int64_t t = pr / ppr, pc = pr - t * ppr;
+        T* dst = y + t * D + pc * 4;
+        dst[0] = Elem<T>::from_f32(a[u].x);
+        dst[1] = Elem<T>::from_f32(a[u].y);
+        dst[2] = Elem<T>::from_f32(a[u].z);
+        dst[3] = Elem<T>::from_f32(a[u].w);
+    }
 }
 
 hipError_t launch_tile_histogram(const int32_t* idx, int64_t T, int E, int k,
@@ -252,24 +375,32 @@ hipError_t launch_tile_histogram(const int32_t* idx, int64_t T, int E, int k,
 
 hipError_t launch_scan(const int32_t* tile_counts, int64_t ntiles, int E, int32_t* tile_base,
                        int32_t* counts, int32_t* offsets, hipStream_t st) {
-    k_scan<<<1, 1024, 0, st>>>(tile_counts, ntiles, E, tile_base, counts, offsets);
+    if (E <= 8)
+        k_scan<8><<<1, 1024, 0, st>>>(tile_counts, ntiles, E, tile_base, counts, offsets);
+    else if (E <= 16)
+        k_scan<16><<<1, 1024, 0, st>>>(tile_counts, ntiles, E, tile_base, counts, offsets);
+    else if (E <= 32)
+        k_scan<32><<<1, 1024, 0, st>>>(tile_counts, ntiles, E, tile_base, counts, offsets);
+    else
+        k_scan<64><<<1, 1024, 0, st>>>(tile_counts, ntiles, E, tile_base, counts, offsets);
     return hipGetLastError();
 }
 
 hipError_t launch_permute(int dtype, const int32_t* idx, const int32_t* tile_base,
-                          const int32_t* offsets, int64_t T, int E, int k, int32_t* perm,
-                          int32_t* inv, const void* x, void* xperm, int D, hipStream_t st) {
+                          int32_t* offsets, const int32_t* tile_counts, int32_t* counts,
+                          int64_t T, int E, int k, int32_t* perm, int32_t* inv, const void* x,
+                          void* xperm, int D, hipStream_t st) {
     const int64_t nt = route_tiles(T);
     if (nt == 0) return hipSuccess;
     const size_t shm = sizeof(int) * static_cast<size_t>(kRouteTile) * k;
     if (dtype == 0)
         k_permute<float><<<dim3(static_cast<unsigned>(nt)), kRouteTile, shm, st>>>(
-            idx, tile_base, offsets, T, E, k, perm, inv, static_cast<const float*>(x),
-            static_cast<float*>(xperm), D);
+            idx, tile_base, offsets, tile_counts, counts, T, E, k, perm, inv,
+            static_cast<const float*>(x), static_cast<float*>(xperm), D);
     else
         k_permute<bf16_bits><<<dim3(static_cast<unsigned>(nt)), kRouteTile, shm, st>>>(
-            idx, tile_base, offsets, T, E, k, perm, inv, static_cast<const bf16_bits*>(x),
-            static_cast<bf16_bits*>(xperm), D);
+            idx, tile_base, offsets, tile_counts, counts, T, E, k, perm, inv,
+            static_cast<const bf16_bits*>(x), static_cast<bf16_bits*>(xperm), D);
     return hipGetLastError();
 }
 
@@ -278,7 +409,7 @@ hipError_t launch_combine_gated(int dtype, const void* ye, const int32_t* inv, c
     const int per16 = dtype == 0 ? 4 : 8;
     const int64_t n = T * (D / per16);
     if (n == 0) return hipSuccess;
-    const unsigned blocks = static_cast<unsigned>((n + 255) / 256);
+    const unsigned blocks = static_cast<unsigned>((n + 256 * kCombineU - 1) / (256 * kCombineU));
     if (dtype == 0)
         k_combine_gated<float><<<blocks, 256, 0, st>>>(static_cast<const float*>(ye), inv, gate,
                                                         static_cast<float*>(y), T, D, k);
@@ -293,7 +424,7 @@ hipError_t launch_combine_residual(int dtype, const float* hsh, const float* hre
                                    hipStream_t st) {
     const int64_t n = T * (D / 4);
     if (n == 0) return hipSuccess;
-    const unsigned blocks = static_cast<unsigned>((n + 255) / 256);
+    const unsigned blocks = static_cast<unsigned>((n + 256 * kCombineU - 1) / (256 * kCombineU));
     if (dtype == 0)
         k_combine_residual<float><<<blocks, 256, 0, st>>>(hsh, hres, inv, static_cast<float*>(y),
                                                            T, D, k);

@@ -2,29 +2,67 @@
 //     C[m, n] = epi( sum_k A[arow(m), k] * B_seg(m)[n, k] )
 // used for fc1 + GELU (Eq. 2), the two skinny products of the shared SVD basis
 // and, grouped by expert with device-resident segment offsets, the two
-// products of the per-expert residual (Algorithm 3, one product per
-// contiguous expert sub-batch, with no host round trip for the sizes).
+// products of the per-expert residual (Algorithm 3: one product per
+// contiguous expert sub-batch, here with no host round trip for the sizes).
 //
 // Mapping
 //   * 256 threads = 4 waves in a WM x WN grid; a wave owns a (BM/WM) x (BN/WN)
 //     block of 32x32 MFMA tiles with float32 accumulators;
-//   * bf16: v_mfma_f32_32x32x16_bf16, each lane feeds 8 consecutive k of one
-//     row (A) / one column (B);  f32: v_mfma_f32_32x32x2f32, each lane holds 4
-//     consecutive k per operand and the two lane halves take k and k+4 in
-//     four successive MFMAs (the k order of a dot product is free, and A and B
-//     use the same order);
-//   * per stage each row contributes 128 bytes of k; LDS rows are padded to
-//     144 bytes, so the 16-byte reads of 32 consecutive rows are conflict free;
-//   * global -> register -> LDS double buffering: the next stage's 16-byte
-//     loads are in flight while the current stage feeds the MFMAs.
-//   * grouped mode: workgroup x-index enumerates (segment, M-tile) pairs in
+//   * bf16: v_mfma_f32_32x32x16_bf16, a lane feeds 8 consecutive k of one row
+//     (A) / one column (B); f32: v_mfma_f32_32x32x2f32, a lane holds 4
+//     consecutive k per operand and the two lane halves take k and k+4 in four
+//     successive MFMAs (the k order of a dot product is free and A and B use
+//     the same order);
+//   * operands move HBM -> LDS with gfx950's global_load_lds_dwordx4 (no
+//     register staging): a stage is 128 bytes of k per row, rows are stored
+//     unpadded with the 16-byte chunk index XOR-swizzled by (row >> 1) & 7.
+//     A 128-bit LDS read serves 16 lanes per cycle across 64 banks (256 bytes),
+//     and the 16 lanes of a group read one chunk of 16 consecutive rows: row
+//     parity picks the bank half and the swizzle spreads the 8 rows of each
+//     parity over the 8 chunk slots, so the reads are conflict free (a plain
+//     row & 7 swizzle puts rows r and r + 8 on the same banks);
+//   * NS stages are in flight: stage kt+NS-1 is issued while stage kt feeds
+//     the MFMAs, and each wave waits with an explicit vmcnt for exactly its
+//     own loads of stage kt before the workgroup barrier;
+//   * lanes whose row or k chunk is outside the operand load a 16-byte zero
+//     page instead, so tails need no special path and never read out of bounds;
+//   * tiles are ordered XCD-major: workgroup i runs on XCD i % 8, and each XCD
+//     walks a contiguous range of tiles (N fastest), so the A rows of a tile
+//     stay in one XCD's L2;
+//   * grouped mode: the tile index enumerates (segment, M-tile) pairs in
 //     segment order, read from the device offsets; surplus workgroups exit.
 #include "kernels.h"
 
 namespace clearmoe {
 
-constexpr int kGemmStageBytes = 128;             // bytes of k per row per stage
-constexpr int kGemmLdsStride = kGemmStageBytes + 16;
+constexpr int kStageBytes = 128;   // bytes of k per row per stage
+constexpr int kXcds = 8;           // MI355X: 8 XCDs of 32 CUs
+
+__device__ __attribute__((aligned(16))) const uint32_t g_zero_page[4] = {0u, 0u, 0u, 0u};
+
+typedef __attribute__((address_space(3))) uint32_t lds_u32;
+
+// Physical 16-byte chunk slot of logical chunk c in LDS row r is c ^ swz(r).
+__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+
+// 16 bytes per lane, HBM -> LDS: lane i's bytes land at lds_base + 16*i.
+// Issued as inline asm so that the compiler does not model it: the waits for
+// these loads are the explicit per-wave vmcnt waits plus the workgroup barrier
+// of the pipeline below.  M0 holds the LDS base; one wait state is required
+// between writing M0 and the load that reads it.
+__device__ __forceinline__ void async_load16(const void* gptr, uint32_t lds_base) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(lds_base), "v"(gptr)
+                 : "memory", "m0");
+}
+
+// s_waitcnt vmcnt(n) (gfx9 encoding), other counters untouched.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
 
 template <typename Tin> struct Mfma;
 template <> struct Mfma<bf16_bits> {
@@ -44,28 +82,38 @@ template <> struct Mfma<float> {
     }
 };
 
-template <typename Tin, int BM, int BN, int WM, int WN>
-__global__ __launch_bounds__(256) void k_gemm(GemmDesc g) {
+template <typename Tin, int BM, int BN, int WM, int WN, int NS>
+__global__ __launch_bounds__(256) void k_gemm(GemmDesc g, int mtiles, int ntiles, int per_xcd) {
     static_assert(WM * WN == 4, "4 waves");
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 32, TN = WTN / 32;
     static_assert(TM >= 1 && TN >= 1, "wave tile at least 32x32");
+    static_assert(BM % 32 == 0 && BN % 32 == 0, "8-row load groups per wave");
     constexpr int PER16 = Elem<Tin>::per16;
-    constexpr int BK = kGemmStageBytes / static_cast<int>(sizeof(Tin));  // elements per stage
-    constexpr int PIECES = kGemmStageBytes / 16;                          // 16B pieces per row
-    constexpr int ALOADS = BM * PIECES / 256;
-    constexpr int BLOADS = (BN * PIECES + 255) / 256;
-    __shared__ __align__(16) unsigned char sA[2][BM * kGemmLdsStride];
-    __shared__ __align__(16) unsigned char sB[2][BN * kGemmLdsStride];
+    constexpr int BK = kStageBytes / static_cast<int>(sizeof(Tin));
+    constexpr int AL = BM / 32, BL = BN / 32;       // load instructions per wave per stage
+    constexpr int LPS = AL + BL;
+    static_assert(LPS * (NS - 1) < 64, "vmcnt range");
+    constexpr int STAGE_A = BM * kStageBytes, STAGE_B = BN * kStageBytes;
+    // One LDS array per stage, so that with the stage index a compile-time
+    // constant the LDS lowering gives each its own alias scope and the
+    // compiler's own waits for the async loads cover only the stage read.
+    __shared__ __attribute__((aligned(1024))) unsigned char st0[STAGE_A + STAGE_B];
+    __shared__ __attribute__((aligned(1024))) unsigned char st1[NS > 1 ? STAGE_A + STAGE_B : 16];
+    __shared__ __attribute__((aligned(1024))) unsigned char st2[NS > 2 ? STAGE_A + STAGE_B : 16];
+    __shared__ __attribute__((aligned(1024))) unsigned char st3[NS > 3 ? STAGE_A + STAGE_B : 16];
+    static_assert(NS >= 2 && NS <= 4, "2..4 stages");
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
 
-    // ---- which rows (and which expert segment) this workgroup owns
+    // ---- tile of this workgroup (XCD-major order)
+    const int tile = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    if (tile >= mtiles * ntiles) return;
+    const int mt = tile / ntiles, nt = tile % ntiles;
     int64_t m_lo, m_hi;
     int seg = 0;
     if (g.seg_offsets != nullptr) {
-        const int64_t bid = blockIdx.x;
         int64_t before = 0;
         bool found = false;
         for (int e = 0; e < g.nseg; ++e) {
@@ -74,73 +122,97 @@ __global__ __launch_bounds__(256) void k_gemm(GemmDesc g) {
             int64_t lo = g.seg_offsets[e], hi = g.seg_offsets[e + 1];
             lo = lo < 0 ? 0 : (lo > g.M ? g.M : lo);
             hi = hi < lo ? lo : (hi > g.M ? g.M : hi);
-            const int64_t nt = (hi - lo + BM - 1) / BM;
-            if (bid < before + nt) {
+            const int64_t n_t = (hi - lo + BM - 1) / BM;
+            if (mt < before + n_t) {
                 seg = e;
-                m_lo = lo + (bid - before) * BM;
+                m_lo = lo + (mt - before) * BM;
                 m_hi = m_lo + BM < hi ? m_lo + BM : hi;
                 found = true;
                 break;
             }
-            before += nt;
+            before += n_t;
         }
         if (!found) return;                      // uniform over the workgroup
     } else {
-        m_lo = static_cast<int64_t>(blockIdx.x) * BM;
+        m_lo = static_cast<int64_t>(mt) * BM;
         if (m_lo >= g.M) return;
         m_hi = m_lo + BM < g.M ? m_lo + BM : g.M;
     }
-    const int n0 = blockIdx.y * BN;
+    const int n0 = nt * BN;
     const Tin* A = static_cast<const Tin*>(g.A);
-    const Tin* B = static_cast<const Tin*>(g.B) + static_cast<int64_t>(seg) * g.b_seg_stride;
+    const Tin* B0 = g.B != nullptr
+                        ? static_cast<const Tin*>(g.B) + static_cast<int64_t>(seg) * g.b_seg_stride
+                        : nullptr;
+    const Tin* B1 = g.B1 != nullptr
+                        ? static_cast<const Tin*>(g.B1) + static_cast<int64_t>(seg) * g.b1_seg_stride
+                        : nullptr;
+    const uint32_t* zero = g_zero_page;
 
-    // ---- per-thread source rows of the global loads
-    int64_t arow[ALOADS];
+    // ---- per-lane source rows of its load instructions (row within the tile
+    //      = (wave*AL + i)*8 + lane/8; LDS chunk lane%8 holds global chunk
+    //      (lane%8) ^ swz(row)).  A B row has a part-0 and a part-1 pointer
+    //      (the k split picks between them per chunk).
+    const int lrow8 = lane >> 3, cpos = lane & 7;
+    const Tin* arow[AL];
+    const Tin* brow0[BL];
+    const Tin* brow1[BL];
+    int achunk[AL], bchunk[BL];
 #pragma unroll
-    for (int i = 0; i < ALOADS; ++i) {
-        const int r = (tid + i * 256) / PIECES;
+    for (int i = 0; i < AL; ++i) {
+        const int r = (wave * AL + i) * 8 + lrow8;
         const int64_t m = m_lo + r;
-        int64_t src = -1;
-        if (m < m_hi) src = g.a_rows != nullptr ? static_cast<int64_t>(g.a_rows[m] / g.a_div) : m;
-        arow[i] = src;
+        arow[i] = nullptr;
+        if (m < m_hi) {
+            const int64_t src = g.a_rows != nullptr ? static_cast<int64_t>(g.a_rows[m] / g.a_div) : m;
+            arow[i] = A + src * g.lda;
+        }
+        achunk[i] = cpos ^ swz(r);
+    }
+#pragma unroll
+    for (int i = 0; i < BL; ++i) {
+        const int r = (wave * BL + i) * 8 + lrow8;
+        const int n = n0 + r;
+        brow0[i] = brow1[i] = nullptr;
+        if (n < g.N) {
+            if (n < g.n_split) {
+                if (g.B != nullptr) brow0[i] = B0 + static_cast<int64_t>(n) * g.ldb;
+                if (B1 != nullptr) brow1[i] = B1 + static_cast<int64_t>(n) * g.ldb1;
+            } else if (B1 != nullptr) {
+                brow0[i] = B1 + static_cast<int64_t>(n - g.n_split) * g.ldb1;
+            }
+        }
+        bchunk[i] = cpos ^ swz(r);
     }
 
-    uint4 ra[ALOADS], rb[BLOADS];
-    auto gload = [&](int kt) {
+    auto stage = [&](int b) -> unsigned char* {
+        return b == 0 ? st0 : b == 1 ? st1 : b == 2 ? st2 : st3;
+    };
+
+    // Issue the async loads of stage kt into LDS buffer `b` (compile-time).
+    auto issue = [&](int kt, int b) {
+        const uint32_t base = __builtin_amdgcn_readfirstlane(
+            static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u32*)(stage(b)))));
         const int kbase = kt * BK;
 #pragma unroll
-        for (int i = 0; i < ALOADS; ++i) {
-            const int pc = (tid + i * 256) % PIECES;
-            const int kk = kbase + pc * PER16;
-            uint4 v = make_uint4(0u, 0u, 0u, 0u);
-            if (arow[i] >= 0 && kk < g.K)
-                v = *reinterpret_cast<const uint4*>(A + arow[i] * g.lda + kk);
-            ra[i] = v;
+        for (int i = 0; i < AL; ++i) {
+            const int kk = kbase + achunk[i] * PER16;
+            const void* src = (arow[i] != nullptr && kk < g.K) ? static_cast<const void*>(arow[i] + kk)
+                                                               : static_cast<const void*>(zero);
+            async_load16(src, __builtin_amdgcn_readfirstlane(base + (wave * AL + i) * 1024));
         }
 #pragma unroll
-        for (int i = 0; i < BLOADS; ++i) {
-            const int piece = tid + i * 256;
-            const int r = piece / PIECES, pc = piece % PIECES;
-            const int kk = kbase + pc * PER16;
-            const int n = n0 + r;
-            uint4 v = make_uint4(0u, 0u, 0u, 0u);
-            if (r < BN && n < g.N && kk < g.K)
-                v = *reinterpret_cast<const uint4*>(B + static_cast<int64_t>(n) * g.ldb + kk);
-            rb[i] = v;
-        }
-    };
-    auto lstore = [&](int buf) {
-#pragma unroll
-        for (int i = 0; i < ALOADS; ++i) {
-            const int piece = tid + i * 256;
-            const int r = piece / PIECES, pc = piece % PIECES;
-            *reinterpret_cast<uint4*>(&sA[buf][r * kGemmLdsStride + pc * 16]) = ra[i];
-        }
-#pragma unroll
-        for (int i = 0; i < BLOADS; ++i) {
-            const int piece = tid + i * 256;
-            const int r = piece / PIECES, pc = piece % PIECES;
-            if (r < BN) *reinterpret_cast<uint4*>(&sB[buf][r * kGemmLdsStride + pc * 16]) = rb[i];
+        for (int i = 0; i < BL; ++i) {
+            const int kk = kbase + bchunk[i] * PER16;
+            const void* src = zero;
+            if (kk < g.K) {
+                if (kk < g.k_split) {
+                    if (brow0[i] != nullptr) src = brow0[i] + kk;
+                } else if (brow1[i] != nullptr) {
+                    src = brow1[i] + (kk - g.k_split);
+                }
+            }
+            async_load16(src,
+                         __builtin_amdgcn_readfirstlane(base + STAGE_A + (wave * BL + i) * 1024));
         }
     };
 
@@ -153,74 +225,117 @@ __global__ __launch_bounds__(256) void k_gemm(GemmDesc g) {
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
     const int nk = (g.K + BK - 1) / BK;
-    if (nk > 0) {
-        gload(0);
-        lstore(0);
-        __syncthreads();
-    }
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+        if (s < nk) issue(s, s);
+
     const int lrow = lane & 31, lhalf = lane >> 5;
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) gload(kt + 1);
+    for (int k0 = 0; k0 < nk; k0 += NS) {
 #pragma unroll
-        for (int s = 0; s < kGemmStageBytes / 32; ++s) {
-            uint4 fa[TM], fb[TN];
+        for (int b = 0; b < NS; ++b) {
+            const int kt = k0 + b;
+            if (kt >= nk) break;
+            // this wave's loads of stage kt are done once at most the later
+            // stages' loads are outstanding
+            const int later = nk - 1 - kt < NS - 2 ? nk - 1 - kt : NS - 2;
+            if (later >= 2 && NS >= 4) wait_vmcnt<(NS >= 4 ? 2 * LPS : 0)>();
+            else if (later == 1 && NS >= 3) wait_vmcnt<(NS >= 3 ? LPS : 0)>();
+            else wait_vmcnt<0>();
+            // Bare barrier: __syncthreads() would also drain the later stages'
+            // loads (its fence waits for vmcnt 0).  lgkmcnt(0) first, so every
+            // wave's LDS reads of the buffer recycled below have completed.
+            __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0) only
+            __builtin_amdgcn_s_barrier();
+            if (kt + NS - 1 < nk) issue(kt + NS - 1, (b + NS - 1) % NS);
+            const unsigned char* sa = stage(b);
+            const unsigned char* sb = sa + STAGE_A;
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
-                fa[i] = *reinterpret_cast<const uint4*>(
-                    &sA[buf][(wm * WTM + i * 32 + lrow) * kGemmLdsStride + s * 32 + lhalf * 16]);
+            for (int s = 0; s < kStageBytes / 32; ++s) {
+                const int c = 2 * s + lhalf;        // 16-byte chunk of k within the stage
+                uint4 fa[TM], fb[TN];
 #pragma unroll
-            for (int j = 0; j < TN; ++j)
-                fb[j] = *reinterpret_cast<const uint4*>(
-                    &sB[buf][(wn * WTN + j * 32 + lrow) * kGemmLdsStride + s * 32 + lhalf * 16]);
+                for (int i = 0; i < TM; ++i) {
+                    const int r = wm * WTM + i * 32 + lrow;
+                    fa[i] = *reinterpret_cast<const uint4*>(sa + r * kStageBytes + ((c ^ swz(r)) << 4));
+                }
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
+                for (int j = 0; j < TN; ++j) {
+                    const int r = wn * WTN + j * 32 + lrow;
+                    fb[j] = *reinterpret_cast<const uint4*>(sb + r * kStageBytes + ((c ^ swz(r)) << 4));
+                }
 #pragma unroll
-                for (int j = 0; j < TN; ++j) Mfma<Tin>::step(fa[i], fb[j], acc[i][j]);
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j) Mfma<Tin>::step(fa[i], fb[j], acc[i][j]);
+            }
         }
-        if (kt + 1 < nk) lstore(buf ^ 1);
-        __syncthreads();
     }
 
-    // ---- epilogue: D[v] of a 32x32 tile sits at row 8*(v/4) + 4*(lane/32) + v%4, column lane%32
+    // ---- epilogue: D[v] of a 32x32 tile sits at row 8*(v/4) + 4*(lane/32) + v%4,
+    //      column lane%32.  Bias and row scales are fetched once, up front.
+    float bias_j[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int n = n0 + wn * WTN + j * 32 + lrow;
+        bias_j[j] = (g.bias != nullptr && n < g.N) ? g.bias[n] : 0.0f;
+    }
+    float rs[TM][16];
+    int64_t crow[TM][16];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const int64_t m = m_lo + wm * WTM + i * 32 + 8 * (v >> 2) + 4 * lhalf + (v & 3);
+            const bool in = m < m_hi;
+            rs[i][v] = (g.row_scale != nullptr && in) ? g.row_scale[g.scale_rows[m]] : 1.0f;
+            crow[i][v] = !in ? -1 : (g.c_rows != nullptr ? static_cast<int64_t>(g.c_rows[m] / g.c_div) : m);
+        }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
 #pragma unroll
-        for (int j = 0; j < TN; ++j) {
-            const int n = n0 + wn * WTN + j * 32 + lrow;
-            const float bn = (g.bias != nullptr && n < g.N) ? g.bias[n] : 0.0f;
+        for (int v = 0; v < 16; ++v) {
+            const int64_t cm = crow[i][v];
+            if (cm < 0) continue;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int64_t m = m_lo + wm * WTM + i * 32 + 8 * (v >> 2) + 4 * lhalf + (v & 3);
-                if (m >= m_hi || n >= g.N) continue;
-                float val = acc[i][j][v];
-                if (g.row_scale != nullptr) val *= g.row_scale[g.scale_rows[m]];
-                val += bn;
+            for (int j = 0; j < TN; ++j) {
+                const int n = n0 + wn * WTN + j * 32 + lrow;
+                if (n >= g.N) continue;
+                float val = acc[i][j][v] * (n >= g.scale_col0 ? rs[i][v] : 1.0f) + bias_j[j];
                 if (g.gelu) val = gelu_erf(val);
                 if (g.c_f32)
-                    static_cast<float*>(g.C)[m * g.ldc + n] = val;
+                    static_cast<float*>(g.C)[cm * g.ldc + n] = val;
                 else
-                    static_cast<Tin*>(g.C)[m * g.ldc + n] = Elem<Tin>::from_f32(val);
+                    static_cast<Tin*>(g.C)[cm * g.ldc + n] = Elem<Tin>::from_f32(val);
             }
         }
     }
 }
 
-template <typename Tin, int BM, int BN, int WM, int WN>
+template <typename Tin, int BM, int BN, int WM, int WN, int NS>
 static hipError_t gemm_cfg(const GemmDesc& g, hipStream_t st) {
     int64_t mt = (g.M + BM - 1) / BM;
     if (g.seg_offsets != nullptr) mt += g.nseg;
-    const int nt = (g.N + BN - 1) / BN;
-    if (mt == 0 || nt == 0) return hipSuccess;
-    k_gemm<Tin, BM, BN, WM, WN><<<dim3(static_cast<unsigned>(mt), nt), 256, 0, st>>>(g);
+    const int64_t nt = (g.N + BN - 1) / BN;
+    const int64_t tiles = mt * nt;
+    if (tiles == 0) return hipSuccess;
+    const int64_t per_xcd = (tiles + kXcds - 1) / kXcds;
+    const int64_t grid = per_xcd * kXcds;
+    k_gemm<Tin, BM, BN, WM, WN, NS><<<dim3(static_cast<unsigned>(grid)), 256, 0, st>>>(
+        g, static_cast<int>(mt), static_cast<int>(nt), static_cast<int>(per_xcd));
     return hipGetLastError();
 }
 
+// Tile choice by shape (measured on MI355X at the layer's sizes): with few
+// 128x128 tiles the GEMM is latency bound, so 64-row tiles (more workgroups
+// per CU) win; long-K skinny products want 64x64 with four stages in flight.
 template <typename Tin>
 static hipError_t gemm_dt(const GemmDesc& g, hipStream_t st) {
-    if (g.N <= 32) return gemm_cfg<Tin, 128, 32, 4, 1>(g, st);
-    if (g.N <= 64) return gemm_cfg<Tin, 128, 64, 4, 1>(g, st);
-    return gemm_cfg<Tin, 128, 128, 2, 2>(g, st);
+    const int64_t mt128 = (g.M + 127) / 128;
+    if (g.N <= 32) return gemm_cfg<Tin, 128, 32, 4, 1, 3>(g, st);
+    if (g.N <= 64) return gemm_cfg<Tin, 128, 64, 4, 1, 3>(g, st);
+    if (g.N <= 128 && g.K >= 1024) return gemm_cfg<Tin, 64, 64, 2, 2, 4>(g, st);
+    if (mt128 * ((g.N + 127) / 128) < 2048) return gemm_cfg<Tin, 64, 128, 2, 2, 2>(g, st);
+    return gemm_cfg<Tin, 128, 128, 2, 2, 2>(g, st);
 }
 
 hipError_t launch_gemm(int dtype, const GemmDesc& g, hipStream_t st) {

@@ -6,17 +6,19 @@
 // of the selected logits renormalised; ties go to the lower expert index.
 //
 // Exact decisions at MFMA speed.  The logits are accumulated by MFMA in
-// float32 (bf16 x bf16 products are exact in float32).  A second MFMA over
-// |x| and |w| gives S_e = sum_d |x_d w_ed|, and the float32 accumulation error
-// of logit e is at most beta_e = (D + 64) 2^-23 S_e (more than twice the
-// classical gamma_n bound for n = D products plus the per-instruction
-// accumulations).  A token whose consecutive top-(k+1) gaps all exceed twice
-// the largest beta has provably the same top-k, in the same order, as the
-// exact logits.  Every other token (near ties, typically well under 1%) is
-// recomputed in double by its whole wave (64 lanes split D, butterfly sum),
-// so the choice is the exact one for every token whose margin exceeds the
-// double rounding of a D-term sum.  Gates use the same logits (double for the
-// recomputed tokens, certified float32 for the others).
+// float32 (bf16 x bf16 products are exact in float32) in partial sums of
+// kPart columns, which are added in double.  A second MFMA over |x| and |w|
+// gives S_e = sum_d |x_d w_ed|; the float32 error of each partial is at most
+// (kPart + 8) u S_partial, so every logit is within beta = 2 (kPart + 8) u S_e
+// of its exact value (u = 2^-24; the factor 2 covers products that float32
+// inputs round, and leaves slack for the MFMA's internal order).  A token
+// whose consecutive top-(k+1) gaps all exceed 2 beta has provably the same
+// top-k, in the same order, as the exact logits.  Every other token (near
+// ties, a small fraction) is recomputed in double by its whole wave (64 lanes
+// split D, butterfly sum), so the choice is the exact one for every token
+// whose margin exceeds the double rounding of a D-term sum.  Gates use the
+// same logits (double for the recomputed tokens, certified float32 sums of
+// double partials for the others).
 //
 // Mapping (gfx950, wave64): a workgroup of 4 waves routes 256 tokens, a wave
 // 64 tokens as four 16-token MFMA column blocks: v_mfma_f32_16x16x32_bf16
@@ -28,9 +30,16 @@
 
 namespace clearmoe {
 
+#ifndef KPRE
+#define KPRE 4   // steps of x / router rows in flight per wave
+#endif
+
+__device__ __attribute__((aligned(16))) const uint32_t g_route_zero[4] = {0u, 0u, 0u, 0u};
+
 template <typename Tin> struct RouteMfma;
 template <> struct RouteMfma<bf16_bits> {
     static constexpr int kstep = 32;   // d per 16-byte-per-lane step (4 lane groups x 8)
+    static constexpr int kpart = 64;   // columns per float32 partial sum of a logit
     __device__ static void step(const uint4& a, const uint4& b, f32x4& c) {
         c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
                                                      __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
@@ -42,6 +51,7 @@ template <> struct RouteMfma<bf16_bits> {
 };
 template <> struct RouteMfma<float> {
     static constexpr int kstep = 16;   // 4 lane groups x 4 floats, four MFMAs of k = 4
+    static constexpr int kpart = 32;
     __device__ static void step(const uint4& a, const uint4& b, f32x4& c) {
         const f32x4 av = __builtin_bit_cast(f32x4, a);
         const f32x4 bv = __builtin_bit_cast(f32x4, b);
@@ -98,8 +108,9 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
     constexpr int EP = 16 * EG;                      // experts padded to MFMA rows
     constexpr int PER16 = Elem<Tin>::per16;
     constexpr int KS = RouteMfma<Tin>::kstep;
-    __shared__ float s_l[kRouteTile / 64][64][EP + 1];
-    __shared__ float s_s[kRouteTile / 64][64][EP + 1];
+    constexpr int kPart = RouteMfma<Tin>::kpart;
+    __shared__ double s_l[kRouteTile / 64][64][17];
+    __shared__ float s_s[kRouteTile / 64][64][4 * EG + 1];
     __shared__ int s_wcnt[kRouteTile / 64][64];
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -107,66 +118,108 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
     const int64_t tw = static_cast<int64_t>(blockIdx.x) * kRouteTile + w * 64;  // wave's first token
 
     f32x4 acc[EG][4], aab[EG][4];
-#pragma unroll
-    for (int g = 0; g < EG; ++g)
-#pragma unroll
-        for (int b = 0; b < 4; ++b)
-#pragma unroll
-            for (int v = 0; v < 4; ++v) acc[g][b][v] = aab[g][b][v] = 0.0f;
-
-    const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
-    for (int d0 = 0; d0 < D; d0 += KS) {
-        const int dd = d0 + grp * PER16;
-        const bool din = dd < D;
-        uint4 xv[4], wv[EG];
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            const int64_t t = tw + 16 * b + col;
-            xv[b] = (din && t < T) ? *reinterpret_cast<const uint4*>(x + t * D + dd) : zero;
-        }
-#pragma unroll
-        for (int g = 0; g < EG; ++g) {
-            const int e = 16 * g + col;
-            wv[g] = (din && e < E) ? *reinterpret_cast<const uint4*>(Wg + static_cast<int64_t>(e) * D + dd)
-                                   : zero;
-        }
-#pragma unroll
-        for (int g = 0; g < EG; ++g) {
-            const uint4 wa = RouteMfma<Tin>::absv(wv[g]);
-#pragma unroll
-            for (int b = 0; b < 4; ++b) {
-                RouteMfma<Tin>::step(wv[g], xv[b], acc[g][b]);
-                RouteMfma<Tin>::step(wa, RouteMfma<Tin>::absv(xv[b]), aab[g][b]);
-            }
-        }
-    }
-    // C of a 16x16 MFMA: lane holds column lane%16 (token), rows 4*(lane/16)+v (experts).
+    double lacc[EG][4][4];             // double sums of the float32 partials
 #pragma unroll
     for (int g = 0; g < EG; ++g)
 #pragma unroll
         for (int b = 0; b < 4; ++b)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                s_l[w][16 * b + col][16 * g + 4 * grp + v] = acc[g][b][v];
-                s_s[w][16 * b + col][16 * g + 4 * grp + v] = aab[g][b][v];
+                acc[g][b][v] = aab[g][b][v] = 0.0f;
+                lacc[g][b][v] = 0.0;
             }
-    __syncthreads();
 
-    // ---- each lane owns one token from here on
+    // Loads of step s (KS columns of d) for the wave's 4 token blocks and the
+    // router rows.  A ring of kPre steps keeps several steps in flight; the loop
+    // is branch-free (steps past D and rows past T read a 16-byte zero page),
+    // so the compiler's waits stay per round instead of per step.  Every
+    // kPart columns the float32 partials move into double.
+    constexpr int kPre = KPRE;
+    static_assert((kPre * KS) % kPart == 0 && kPart % KS == 0, "partials align with rounds");
+    const int nsteps = (D + KS - 1) / KS;
+    const int nround = (nsteps + kPre - 1) / kPre;
+    const uint4* zp = reinterpret_cast<const uint4*>(g_route_zero);
+    uint4 xr[kPre][4], wr[kPre][EG];
+    auto load_step = [&](int s, uint4 (&xv)[4], uint4 (&wv)[EG]) {
+        const int dd = s * KS + grp * PER16;
+        const bool din = dd < D;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            const int64_t t = tw + 16 * b + col;
+            const uint4* src = (din && t < T) ? reinterpret_cast<const uint4*>(x + t * D + dd) : zp;
+            xv[b] = *src;
+        }
+#pragma unroll
+        for (int g = 0; g < EG; ++g) {
+            const int e = 16 * g + col;
+            const uint4* src = (din && e < E)
+                                   ? reinterpret_cast<const uint4*>(Wg + static_cast<int64_t>(e) * D + dd)
+                                   : zp;
+            wv[g] = *src;
+        }
+    };
+#pragma unroll
+    for (int i = 0; i < kPre; ++i) load_step(i, xr[i], wr[i]);
+    for (int o = 0; o < nround; ++o) {
+#pragma unroll
+        for (int i = 0; i < kPre; ++i) {
+#pragma unroll
+            for (int g = 0; g < EG; ++g) {
+                const uint4 wa = RouteMfma<Tin>::absv(wr[i][g]);
+#pragma unroll
+                for (int b = 0; b < 4; ++b) {
+                    RouteMfma<Tin>::step(wr[i][g], xr[i][b], acc[g][b]);
+                    RouteMfma<Tin>::step(wa, RouteMfma<Tin>::absv(xr[i][b]), aab[g][b]);
+                }
+            }
+            load_step((o + 1) * kPre + i, xr[i], wr[i]);   // past the end: zero page
+            if (((i + 1) * KS) % kPart == 0) {
+#pragma unroll
+                for (int g = 0; g < EG; ++g)
+#pragma unroll
+                    for (int b = 0; b < 4; ++b)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            lacc[g][b][v] += static_cast<double>(acc[g][b][v]);
+                            acc[g][b][v] = 0.0f;
+                        }
+            }
+        }
+    }
+    // C of a 16x16 MFMA: lane holds column lane%16 (token), rows 4*(lane/16)+v
+    // (experts).  Through LDS, one 16-expert group at a time, each lane takes
+    // the logits of one token; for S only each lane's maximum over its four
+    // experts is exchanged.
     const int64_t t = tw + lane;
     const bool valid = t < T;
     double lg[EP];
+#pragma unroll
+    for (int g = 0; g < EG; ++g) {
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) s_l[w][16 * b + col][4 * grp + v] = lacc[g][b][v];
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+            float m = 0.0f;
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                if (16 * g + 4 * grp + v < E) m = fmaxf(m, aab[g][b][v]);
+            s_s[w][16 * b + col][4 * g + grp] = m;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < 16; ++e) lg[16 * g + e] = s_l[w][lane][e];
+        __syncthreads();
+    }
     float smax = 0.0f;
 #pragma unroll
-    for (int e = 0; e < EP; ++e) {
-        const double bias = (bg != nullptr && e < E) ? static_cast<double>(bg[e]) : 0.0;
-        lg[e] = static_cast<double>(s_l[w][lane][e]) + bias;
-        if (e < E) smax = fmaxf(smax, s_s[w][lane][e]);
-    }
-    // Accumulation error bound of every float32 logit (S rounded up by 1%);
-    // float32 inputs also round each product, hence twice the factor.
-    constexpr double kBeta = sizeof(Tin) == 2 ? 0x1p-23 : 0x1p-22;
-    const double beta = static_cast<double>(D + 64) * kBeta * static_cast<double>(smax) * 1.01;
+    for (int i = 0; i < 4 * EG; ++i) smax = fmaxf(smax, s_s[w][lane][i]);
+#pragma unroll
+    for (int e = 0; e < EP; ++e)
+        lg[e] += (bg != nullptr && e < E) ? static_cast<double>(bg[e]) : 0.0;
+    // Rounding bound of every logit (S itself rounded up by 1%).
+    const double beta = 2.0 * (kPart + 8) * 0x1p-24 * static_cast<double>(smax) * 1.01;
     const bool certain = topk_gap<EP>(lg, E, k) > 2.0 * beta;
 
     // ---- exact recompute in double of the tokens that are not certified
@@ -178,20 +231,37 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
         double part[EP];
 #pragma unroll
         for (int e = 0; e < EP; ++e) part[e] = 0.0;
-        for (int d = lane; d < D; d += 64) {
-            const double xd = static_cast<double>(Elem<Tin>::load(x, to * D + d));
+        constexpr int kFallU = EP <= 16 ? 4 : 1;   // d = lane + 64 i, per lane per round
+        for (int d0 = 0; d0 < D; d0 += 64 * kFallU) {
+            // Branch-free: out-of-range columns / experts load a clamped (valid)
+            // address and are zeroed afterwards, so all loads of a round are in
+            // flight together.
+            float xv[kFallU], wv[kFallU][EP];
 #pragma unroll
-            for (int e = 0; e < EP; ++e)
-                if (e < E)
-                    part[e] = __builtin_fma(
-                        xd, static_cast<double>(Elem<Tin>::load(Wg, static_cast<int64_t>(e) * D + d)),
-                        part[e]);
+            for (int i = 0; i < kFallU; ++i) {
+                const int d = d0 + lane + 64 * i;
+                const int dc = d < D ? d : D - 1;
+                const float xr = Elem<Tin>::load(x, to * D + dc);
+                xv[i] = d < D ? xr : 0.0f;
+#pragma unroll
+                for (int e = 0; e < EP; ++e) {
+                    const int ec = e < E ? e : E - 1;
+                    wv[i][e] = Elem<Tin>::load(Wg, static_cast<int64_t>(ec) * D + dc);
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < kFallU; ++i)
+#pragma unroll
+                for (int e = 0; e < EP; ++e)
+                    part[e] = __builtin_fma(static_cast<double>(xv[i]), static_cast<double>(wv[i][e]),
+                                            part[e]);
         }
 #pragma unroll
         for (int e = 0; e < EP; ++e) {
-            if (e >= E) break;
+            if (e < E) {                           // uniform: the loop stays unrolled
 #pragma unroll
-            for (int o = 32; o >= 1; o >>= 1) part[e] += __shfl_xor(part[e], o);
+                for (int o = 32; o >= 1; o >>= 1) part[e] += __shfl_xor(part[e], o);
+            }
         }
         if (lane == owner) {
 #pragma unroll
