@@ -45,6 +45,9 @@ def parse():
     ap.add_argument("--no-extras", action="store_true",
                     help="only the timed steps (for profiler runs)")
     ap.add_argument("--workload", default="C2", choices=["C1", "C2", "C3"])
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="for counter runs: one 1 GiB device copy from a cache-cold source "
+                         "(known bytes, to scale the counters), then the timed steps only")
     return ap.parse_args()
 
 
@@ -134,6 +137,20 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
+    if args.traffic_probe:
+        src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        flush.fill_(2)                  # evicts src from the 256 MB last-level cache
+        torch.cuda.synchronize()
+        dst.copy_(src)                  # reads and writes exactly 1 GiB
+        torch.cuda.synchronize()
+        del src, dst, flush
+        for _ in range(args.steps):
+            step()
+        torch.cuda.synchronize()
+        print(json.dumps({"traffic_probe": True, "steps": args.steps}), flush=True)
+        return
 
     # Per-stage times of a few steps (all stages timed) to find the dominant kernel.
     names = cm.stage_names()
