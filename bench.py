@@ -80,6 +80,10 @@ def stage_work(stage, cfg, b):
         "dense_fc2": (2 * T * D * H, T * H * b + D * H * b + T * D * b),
         "tu_grouped": (2 * A * (r + q) * H, A * H * b + (r + E * q) * H * b + A * (r + q) * b),
         "y_grouped": (2 * A * D * (r + q), A * (r + q) * b + D * (r + E * q) * b + T * D * b),
+        # x in, y out; W1, [Vt;Q_e] and [US|P_e] once each; b1, b2, perm and gate
+        "fused_top1": (2 * T * (D * H + H * (r + q) + (r + q) * D),
+                       2 * T * D * b + H * D * b + 2 * (r + E * q) * (H + D) * b // 2
+                       + (H + D) * 4 + T * 8),
     }
     return w.get(stage, (0, 0))
 

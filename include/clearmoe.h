@@ -157,7 +157,8 @@ enum {
     CLEARMOE_STAGE_DENSE_FC2 = 11,     /* dense comparator y = z W2^T + b2 */
     CLEARMOE_STAGE_TU = 12,            /* top-1: [t|u] = z[perm] [Vt;Q_e]^T (grouped) */
     CLEARMOE_STAGE_Y = 13,             /* top-1: y[perm] = [t|u] [US|P_e]^T + b2 (grouped) */
-    CLEARMOE_N_STAGES = 14
+    CLEARMOE_STAGE_FUSED_TOP1 = 14,    /* top-1 bf16: fc1+GELU, [t|u] and y in one kernel */
+    CLEARMOE_N_STAGES = 15
 };
 
 /* Name of a stage (static string; "?" if out of range). */

@@ -27,7 +27,7 @@ SYMBOLS = ("clearmoe_version", "clearmoe_status_string", "clearmoe_workspace_byt
            "clearmoe_route", "clearmoe_dispatch", "clearmoe_combine", "clearmoe_ffn_forward",
            "clearmoe_dense_ffn_forward", "clearmoe_stage_name", "clearmoe_timing_start",
            "clearmoe_timing_stop")
-N_STAGES = 14
+N_STAGES = 15
 
 
 class ClearMoEError(RuntimeError):

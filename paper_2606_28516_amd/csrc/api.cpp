@@ -279,6 +279,14 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
     rc = dispatch_impl(s, L, idx, ws, counts, offsets, perm, inv, nullptr, nullptr, true, st);
     if (rc != CLEARMOE_OK) return rc;
 
+    // Top-1 in bf16: fc1 + GELU, [t|u] and y in one kernel (z stays on chip).
+    if (s.k == 1 && s.dtype == CLEARMOE_BF16 && fused_top1_supported(s.D, s.H, s.r, s.q)) {
+        CLEARMOE_STAGE(CLEARMOE_STAGE_FUSED_TOP1, st,
+                       launch_fused_top1(x, W1, b1, US, Vt, b2, P, Q, perm, offsets, gate, y, T,
+                                         s.D, s.H, s.E, s.r, s.q, st));
+        return CLEARMOE_OK;
+    }
+
     // 3. z = GELU(x W1^T + b1), token order
     GemmDesc g = gemm_desc(T, s.H, s.D);
     g.A = x; g.lda = s.D;
@@ -384,7 +392,7 @@ const char* clearmoe_stage_name(int stage) {
     static const char* names[CLEARMOE_N_STAGES] = {
         "route", "tile_hist", "scan", "permute", "combine", "fc1_gelu",
         "basis_t", "basis_h", "res_u", "res_h", "combine_res", "dense_fc2", "tu_grouped",
-        "y_grouped"};
+        "y_grouped", "fused_top1"};
     return (stage >= 0 && stage < CLEARMOE_N_STAGES) ? names[stage] : "?";
 }
 

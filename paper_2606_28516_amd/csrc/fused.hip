@@ -1,0 +1,666 @@
+// Fused top-1 CLEAR-MoE FFN in bfloat16 for gfx950: one kernel from x to y.
+//
+// With k = 1 every row p of the expert order is one token, and the layer is
+//     z      = GELU(x W1^T + b1)                        shared fc1 (Eq. 2)
+//     [t|u]  = z [Vt ; Q_e]^T, the u columns times the gate
+//     y      = [t|u] [US | P_e]^T + b2                  shared basis + residual (Eq. 3-4)
+// A workgroup owns up to 64 consecutive rows of one expert's segment and the
+// whole hidden width, so neither z nor [t|u] ever goes to HBM:
+//   * the 64 gathered x rows are copied to LDS once and stay there;
+//   * wave w walks the 64-wide hidden slices w, w + 4, w + 8, ...: for a slice
+//     it forms z^T (64 hidden x 64 tokens, four 32x32 MFMA tiles), its W1 rows
+//     streamed by DMA into a ring of LDS stages private to the wave (no
+//     workgroup barrier in the loop), applies bias, GELU and bf16 rounding, and
+//     adds [Vt;Q_e]_slice z^T_slice to its own [t|u]^T held in registers;
+//   * the four partial [t|u] are summed in LDS as (w0 + w2) + (w1 + w3)
+//     (fixed order, deterministic), the gate is applied, the sum is rounded to
+//     bf16, and the last product builds the y rows in LDS and writes each row
+//     to its token with 16-byte stores.
+//
+// Register chaining.  For v_mfma_f32_32x32x16_bf16, lane l holds result
+// column l%32, rows 8(v/4) + 4(l/32) + v%4 (v = 0..15), and as a k operand
+// supplies k slots 8(l/32) + i (i = 0..7) of row/column l%32.  Tile q (0, 1)
+// of the z^T block takes W1 row  hb + 32 ((s>>2)&1) + 16 q + 4 (s>>3) + (s&3)
+// in row slot s, which makes lane l's 16 results of tile q the hidden units
+// hb + 32(l/32) + 16q + v.  Across both tiles a lane then holds hidden units
+// hb + 32(l/32) + [0, 32): four runs of 8, i.e. the B operands of four MFMAs
+// whose slot 8(l/32) + i is hidden unit hb + 32(l/32) + 8j + i (j = 0..3).
+// The A operand ([Vt;Q_e] rows) reads the same 8 units: 64 contiguous bytes
+// per lane over j.  Phase-1 products use the analogous k order (slot
+// 8(l/32) + i of MFMA j is input feature 64g + 32(l/32) + 8j + i).
+//
+// Waits.  The W1 DMA is inline asm the compiler does not see; every wave
+// issues its loads in a fixed order (stages, then the [Vt;Q_e] loads of a
+// slice after its first two stages) and waits with vmcnt values computed from
+// that order.  Loads the compiler does see ([Vt;Q_e], b1) are all complete
+// whenever it waits for them, so its own counts never hold back a DMA.
+#include "kernels.h"
+
+namespace clearmoe {
+
+namespace {
+
+constexpr int kFRows = 64;      // rows (tokens) per workgroup
+constexpr int kFHid = 64;       // hidden units per wave per step
+constexpr int kFXcds = 8;
+constexpr int kNS = 3;                  // W1 ring stages per wave
+constexpr int kStageBytes = 64 * 128;   // 64 W1 rows x 64 inputs (bf16)
+constexpr int kCt = 3;                  // y column tiles per wave and pass
+
+__device__ __attribute__((aligned(16))) const uint32_t g_fused_zero[4] = {0u, 0u, 0u, 0u};
+
+typedef __attribute__((address_space(3))) uint32_t lds_word;
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(lds_addr), "v"(gptr)
+                 : "memory", "m0");
+}
+
+// Raw buffer resources: a load whose offset lies outside [0, bytes) returns
+// zero, so tails and absent rows need no pointer selects and no branches.
+constexpr uint32_t kOob = 0x80000000u;          // an offset past every buffer here
+constexpr int kBufWord3 = 0x00020000;           // raw dword access (CDNA)
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf(const void* p, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), static_cast<short>(0),
+                                             static_cast<int>(bytes), kBufWord3);
+}
+__device__ __forceinline__ u32x4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(u32x4,
+                              __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, 0));
+}
+
+// Two floats -> two bf16 (hardware round to nearest even), packed in 32 bits.
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+    const f32x2 v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+}
+
+__device__ __forceinline__ f32x16 mfma(const u32x4& a, const u32x4& b, const f32x16& c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a),
+                                                    __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// Buffer descriptor words for the inline-asm DMA below (uniform values).
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4 dma_desc(const void* p, int64_t bytes) {
+    const uint64_t a = reinterpret_cast<uint64_t>(p);
+    i32x4 d;
+    d.x = __builtin_amdgcn_readfirstlane(static_cast<int>(a & 0xffffffffu));
+    d.y = __builtin_amdgcn_readfirstlane(static_cast<int>((a >> 32) & 0xffffu));   // stride 0
+    d.z = __builtin_amdgcn_readfirstlane(static_cast<int>(bytes));
+    d.w = kBufWord3;
+    return d;
+}
+
+// One W1 ring stage: 8 loads of 16 bytes per lane, buffer -> LDS at
+// base + 1024 i + 16 * lane (zeros for an offset outside the buffer).  Inline
+// asm: the compiler does not count these loads; the kernel waits for them
+// with explicit vmcnt values (vm_wait below).  M0 carries the LDS address; one
+// wait state separates each M0 write from the load that reads it.
+__device__ __forceinline__ void dma_stage8(const i32x4& d, uint32_t base, const uint32_t (&o)[8]) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\ts_nop 0\n\t"
+        "buffer_load_dwordx4 %1, %9, 0 offen lds\n\t"
+        "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\t"
+        "buffer_load_dwordx4 %2, %9, 0 offen lds\n\t"
+        "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\t"
+        "buffer_load_dwordx4 %3, %9, 0 offen lds\n\t"
+        "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\t"
+        "buffer_load_dwordx4 %4, %9, 0 offen lds\n\t"
+        "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\t"
+        "buffer_load_dwordx4 %5, %9, 0 offen lds\n\t"
+        "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\t"
+        "buffer_load_dwordx4 %6, %9, 0 offen lds\n\t"
+        "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\t"
+        "buffer_load_dwordx4 %7, %9, 0 offen lds\n\t"
+        "s_add_u32 m0, m0, 0x400\n\ts_nop 0\n\t"
+        "buffer_load_dwordx4 %8, %9, 0 offen lds"
+        :
+        : "s"(base), "v"(o[0]), "v"(o[1]), "v"(o[2]), "v"(o[3]), "v"(o[4]), "v"(o[5]), "v"(o[6]),
+          "v"(o[7]), "s"(d)
+        : "memory", "m0", "scc");
+}
+
+// Wait until at most N vector-memory loads of this wave are outstanding.  The
+// memory clobber keeps LDS reads of the awaited data below it.
+template <int N>
+__device__ __forceinline__ void vm_wait() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
+}
+
+// Hidden offset (within a 64-slice) of row slot s of z^T tile q.
+__device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
+
+__device__ __forceinline__ int hid_of_slot(int q, int s) {
+    return 32 * ((s >> 2) & 1) + 16 * q + 4 * (s >> 3) + (s & 3);
+}
+
+struct FusedArgs {
+    const bf16_bits* x;
+    const bf16_bits* W1;
+    const float* b1;
+    const bf16_bits* US;
+    const bf16_bits* Vt;
+    const float* b2;
+    const bf16_bits* P;
+    const bf16_bits* Q;
+    const int32_t* perm;
+    const int32_t* offsets;
+    const float* gate;
+    bf16_bits* y;
+    int64_t T;
+    int D, H, E, r, q;
+    int xch;        // LDS pitch of an x row, 16-byte chunks (odd, >= 8 * kgroups)
+    int kgroups;    // ceil(D / 64) rounded up to even
+    int hpad;       // H rounded up to 4 waves x 64
+    int redp;       // LDS pitch (floats) of a token's [t|u] partial sums
+    int tuch;       // LDS pitch of a bf16 [t|u] row, 16-byte chunks (odd)
+    int yp;         // LDS pitch (elements) of a bf16 y row
+    int x_off;      // byte offset of the x rows (after b1)
+    int ring_off;   // byte offset of the four waves' W1 rings (after x)
+    int tu_off;     // byte offset of the bf16 [t|u] rows (after the sums / y rows)
+    int tiles_bound;
+    int per_xcd;
+};
+
+// Wait for stage n of the W1 ring: loads issued after it are stage n + 1 (if
+// it belongs to this slice), stage n + 2 (likewise), and for the first two
+// stages of a slice the slice's 4 NFT [Vt;Q_e] loads.
+template <int NFT>
+__device__ __forceinline__ void wait_stage(bool s1, bool s2, bool vq) {
+    const int key = (s1 ? 1 : 0) + (s2 ? 2 : 0) + (vq ? 4 : 0);
+    switch (key) {
+        case 0: vm_wait<0>(); break;
+        case 1: vm_wait<8>(); break;
+        case 2: vm_wait<8>(); break;
+        case 3: vm_wait<16>(); break;
+        case 4: vm_wait<4 * NFT>(); break;
+        case 5: vm_wait<8 + 4 * NFT>(); break;
+        case 6: vm_wait<8 + 4 * NFT>(); break;
+        default: vm_wait<16 + 4 * NFT>(); break;
+    }
+}
+
+// Bare workgroup barrier: LDS operations complete, outstanding DMA untouched
+// (__syncthreads would also wait for every vector-memory load).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+    __builtin_amdgcn_s_barrier();
+}
+
+// NFT = 32-row tiles of [t|u] features (r + q <= 32 NFT).  KG > 0 fixes the
+// number of 64-wide input groups at compile time (straight-line phase 1).
+template <int NFT, int KG>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
+void k_fused_top1(FusedArgs a) {
+    extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
+    __shared__ int32_t s_tok[kFRows];
+    __shared__ float s_gate[kFRows];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lrow = lane & 31, lh = lane >> 5;
+
+    // ---- tile -> (expert e, rows [m_lo, m_hi)), XCD-major order
+    const int tile = (blockIdx.x % kFXcds) * a.per_xcd + blockIdx.x / kFXcds;
+    if (tile >= a.tiles_bound) return;
+    int e = -1;
+    int64_t m_lo = 0, m_hi = 0;
+    {
+        const int64_t M = a.T;
+        int64_t before = 0;
+        for (int s = 0; s < a.E; ++s) {
+            // offsets are clamped to [0, T]: bad offsets cannot send a
+            // workgroup outside the buffers
+            int64_t lo = a.offsets[s], hi = a.offsets[s + 1];
+            lo = lo < 0 ? 0 : (lo > M ? M : lo);
+            hi = hi < lo ? lo : (hi > M ? M : hi);
+            const int64_t nt = (hi - lo + kFRows - 1) / kFRows;
+            if (tile < before + nt) {
+                e = s;
+                m_lo = lo + (tile - before) * kFRows;
+                m_hi = m_lo + kFRows < hi ? m_lo + kFRows : hi;
+                break;
+            }
+            before += nt;
+        }
+    }
+    if (e < 0) return;                          // uniform over the workgroup
+    const int rows = static_cast<int>(m_hi - m_lo);
+    const int D = a.D, H = a.H, r = a.r, rq = a.r + a.q;
+
+    if (tid < kFRows) {
+        int32_t tok = -1;
+        float g = 0.0f;
+        if (tid < rows) {
+            const int32_t t = a.perm[m_lo + tid];
+            if (t >= 0 && t < a.T) {
+                tok = t;
+                g = a.gate[t];
+            }
+        }
+        s_tok[tid] = tok;
+        s_gate[tid] = g;
+    }
+    __syncthreads();
+
+    float* s_b1 = reinterpret_cast<float*>(smem);
+    const unsigned char* xs = smem + a.x_off;
+    unsigned char* ringp = smem + a.ring_off + wave * (kNS * kStageBytes);
+    const uint32_t ring = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_word*)ringp));
+    const int kgroups = KG > 0 ? KG : a.kgroups;
+    const int n_iter = wave * kFHid < H ? (H - wave * kFHid + 4 * kFHid - 1) / (4 * kFHid) : 0;
+    const i32x4 d_w1 = dma_desc(a.W1, static_cast<int64_t>(H) * D * 2);
+
+    // DMA of W1 ring stage n = slice it, input group g into slot n % kNS: ring
+    // row 32q + s holds W1 row hb + hid_of_slot(q, s), and its 16-byte chunk c
+    // (inputs 64g + 8c .. + 8) sits at slot c ^ swz(row).
+    auto dma_stage = [&](int n) {
+        const int it = n / kgroups, g = n - it * kgroups;
+        const int hb = (it * 4 + wave) * kFHid;
+        const uint32_t m0 = ring + static_cast<uint32_t>(n % kNS) * kStageBytes;
+        uint32_t off[8];
+#pragma unroll
+        for (int ins = 0; ins < 8; ++ins) {
+            const int row = 8 * ins + (lane >> 3);
+            const int c = (lane & 7) ^ swz(row);
+            const int hid = hb + hid_of_slot(row >> 5, row & 31);
+            const int k = 64 * g + 8 * c;
+            off[ins] = ((hid < H) & (k < D)) ? static_cast<uint32_t>(hid * D + k) * 2u : kOob;
+        }
+        // the slot's previous stage must have been read by this wave
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        dma_stage8(d_w1, __builtin_amdgcn_readfirstlane(m0), off);
+    };
+
+    // ---- prologue: x rows -> LDS (DMA), b1 -> LDS, the first two W1 stages
+    {
+        const uint32_t xl = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_word*)xs));
+        const int dch = D / 8;
+        const int slots = kFRows * a.xch;
+        for (int base = wave * 64; base < slots; base += 256) {
+            const int j = base + lane;
+            const int row = j / a.xch, c = j - row * a.xch;
+            const void* src = g_fused_zero;                 // padding chunks read zeros
+            if (j < slots && c < dch) {
+                const int32_t tok = s_tok[row];
+                if (tok >= 0) src = a.x + static_cast<int64_t>(tok) * D + 8 * c;
+            }
+            lds_dma16(src, __builtin_amdgcn_readfirstlane(xl + base * 16));
+        }
+    }
+    // (the compiler waits for these b1 loads, issued after the x copy: that
+    // also completes this wave's x copy)
+    for (int i = tid; i < a.hpad; i += 256) s_b1[i] = (a.b1 != nullptr && i < H) ? a.b1[i] : 0.0f;
+    vm_wait<0>();
+    if (n_iter > 0) {
+        dma_stage(0);
+        dma_stage(1);
+    }
+    lds_barrier();
+
+    const __amdgpu_buffer_rsrc_t r_vt = buf(a.Vt, static_cast<int64_t>(r) * H * 2);
+    const __amdgpu_buffer_rsrc_t r_qe =
+        buf(a.Q + static_cast<int64_t>(e) * a.q * H, static_cast<int64_t>(a.q) * H * 2);
+    // LDS byte offsets of this lane's x chunks for token blocks 0 and 1
+    const int xoff0 = (lrow * a.xch + 4 * lh) * 16;
+    const int xoff1 = xoff0 + 32 * a.xch * 16;
+
+    f32x16 tu[NFT][2];
+#pragma unroll
+    for (int f = 0; f < NFT; ++f)
+#pragma unroll
+        for (int b = 0; b < 2; ++b)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) tu[f][b][v] = 0.0f;
+
+    for (int it = 0; it < n_iter; ++it) {
+        const int hb = (it * 4 + wave) * kFHid;
+        // [Vt;Q_e] operands of this slice, columns hb + 32 lh + 8 j + [0, 8)
+        u32x4 vq[NFT][4];
+#pragma unroll
+        for (int f = 0; f < NFT; ++f) {
+            // r is a multiple of 32: a feature tile is all Vt rows or all Q_e rows
+            const bool tile_vt = 32 * f < r;
+            const int feat = 32 * f + lrow;
+            const uint32_t rowb = static_cast<uint32_t>(tile_vt ? feat : feat - r) * H * 2;
+            const bool live = feat < rq;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int hid = hb + 32 * lh + 8 * j;
+                vq[f][j] = bload16(tile_vt ? r_vt : r_qe, (live & (hid < H)) ? rowb + 2u * hid : kOob);
+            }
+        }
+
+        // ---- phase 1: z^T[64 hidden x 64 tokens] = W1_slice x^T, one ring stage
+        //      (64 inputs) per step; stage n + 2 of the slice is issued before
+        //      stage n is read
+        f32x16 za[2][2];
+#pragma unroll
+        for (int qq = 0; qq < 2; ++qq)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) za[qq][b][v] = 0.0f;
+#pragma unroll
+        for (int g = 0; g < kgroups; ++g) {
+            const int n = it * kgroups + g;
+            if (g + 2 < kgroups) dma_stage(n + 2);
+            wait_stage<NFT>(g + 1 < kgroups, g + 2 < kgroups, g < 2);
+            const unsigned char* st = ringp + (n % kNS) * kStageBytes;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int c = (8 * g + j) * 16;
+                const u32x4 x0 = *reinterpret_cast<const u32x4*>(xs + xoff0 + c);
+                const u32x4 x1 = *reinterpret_cast<const u32x4*>(xs + xoff1 + c);
+#pragma unroll
+                for (int qq = 0; qq < 2; ++qq) {
+                    const int row = 32 * qq + lrow;
+                    const u32x4 w = *reinterpret_cast<const u32x4*>(
+                        st + row * 128 + (((4 * lh + j) ^ swz(row)) << 4));
+                    za[qq][0] = mfma(w, x0, za[qq][0]);
+                    za[qq][1] = mfma(w, x1, za[qq][1]);
+                }
+            }
+        }
+        // The last step's wait left nothing of this wave outstanding, so the
+        // compiler's waits for the [Vt;Q_e] registers (placed here) are free;
+        // then the next slice's first two stages load behind GELU and phase 2.
+#pragma unroll
+        for (int f = 0; f < NFT; ++f)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) asm volatile("" : : "v"(vq[f][j]));
+        if (it + 1 < n_iter) {
+            dma_stage((it + 1) * kgroups);
+            dma_stage((it + 1) * kgroups + 1);
+        }
+
+        // ---- per run j of 8 hidden units (hb + 32 lh + 8 j + i): bias, GELU and
+        //      bf16 turn the lane's z values into the B operand of phase 2, and
+        //      [t|u]^T += [Vt;Q_e]_run z^T_run.  Units >= H have zero [Vt;Q_e]
+        //      columns, so their z values do not count.
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int qq = j >> 1, v0 = 8 * (j & 1);
+            const int hid0 = hb + 32 * lh + 8 * j;      // < H rounded up to 256
+            const float4 b0 = *reinterpret_cast<const float4*>(s_b1 + hid0);
+            const float4 b1v = *reinterpret_cast<const float4*>(s_b1 + hid0 + 4);
+            const float bj[8] = {b0.x, b0.y, b0.z, b0.w, b1v.x, b1v.y, b1v.z, b1v.w};
+            u32x4 zo[2];
+#pragma unroll
+            for (int b = 0; b < 2; ++b) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int v = v0 + 2 * i;
+                    zo[b][i] = pack_bf16x2(gelu_erf(za[qq][b][v] + bj[2 * i]),
+                                           gelu_erf(za[qq][b][v + 1] + bj[2 * i + 1]));
+                }
+            }
+#pragma unroll
+            for (int f = 0; f < NFT; ++f)
+#pragma unroll
+                for (int b = 0; b < 2; ++b) tu[f][b] = mfma(vq[f][j], zo[b], tu[f][b]);
+        }
+    }
+    vm_wait<0>();
+
+    // ---- sum the four waves' [t|u]^T partials: (w0 + w2) + (w1 + w3).  Areas
+    //      hold [token][feature] floats (pitch redp); lane (token 32b + lrow)
+    //      holds features 32f + 8g + 4 lh + [0, 4) of v-group g: 16-byte moves.
+    __syncthreads();                                   // b1, x, rings no longer read
+    float* area0 = reinterpret_cast<float*>(smem);
+    float* area1 = area0 + kFRows * a.redp;
+    auto put = [&](float* area) {
+#pragma unroll
+        for (int f = 0; f < NFT; ++f)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    float4 v;
+                    v.x = tu[f][b][4 * g]; v.y = tu[f][b][4 * g + 1];
+                    v.z = tu[f][b][4 * g + 2]; v.w = tu[f][b][4 * g + 3];
+                    *reinterpret_cast<float4*>(area + (32 * b + lrow) * a.redp + 32 * f + 8 * g + 4 * lh) = v;
+                }
+    };
+    auto add = [&](const float* area) {
+        float4 o[NFT][2][4];
+#pragma unroll
+        for (int f = 0; f < NFT; ++f)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+#pragma unroll
+                for (int g = 0; g < 4; ++g)
+                    o[f][b][g] = *reinterpret_cast<const float4*>(
+                        area + (32 * b + lrow) * a.redp + 32 * f + 8 * g + 4 * lh);
+#pragma unroll
+        for (int f = 0; f < NFT; ++f)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    tu[f][b][4 * g] += o[f][b][g].x;
+                    tu[f][b][4 * g + 1] += o[f][b][g].y;
+                    tu[f][b][4 * g + 2] += o[f][b][g].z;
+                    tu[f][b][4 * g + 3] += o[f][b][g].w;
+                }
+    };
+    if (wave >= 2) put(wave == 2 ? area0 : area1);
+    __syncthreads();
+    if (wave < 2) add(wave == 0 ? area0 : area1);
+    __syncthreads();
+    if (wave == 1) put(area0);
+    __syncthreads();
+    bf16_bits* tul = reinterpret_cast<bf16_bits*>(smem + a.tu_off);
+    if (wave == 0) {
+        add(area0);
+        // gate the u features (r is a multiple of 32: whole tiles), round to
+        // bf16, tul[token][feature]
+#pragma unroll
+        for (int b = 0; b < 2; ++b) {
+            const float gt = s_gate[32 * b + lrow];
+#pragma unroll
+            for (int f = 0; f < NFT; ++f) {
+                const float sc = 32 * f < r ? 1.0f : gt;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    uint2 w;
+                    w.x = pack_bf16x2(tu[f][b][4 * g] * sc, tu[f][b][4 * g + 1] * sc);
+                    w.y = pack_bf16x2(tu[f][b][4 * g + 2] * sc, tu[f][b][4 * g + 3] * sc);
+                    *reinterpret_cast<uint2*>(tul + (32 * b + lrow) * a.tuch * 8 + 32 * f + 8 * g +
+                                              4 * lh) = w;
+                }
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---- y = [t|u] [US | P_e]^T + b2 into LDS rows (the sums' area, free
+    //      now), kCt column tiles of 32 per pass with every operand load
+    //      issued before any store
+    const __amdgpu_buffer_rsrc_t r_us = buf(a.US, static_cast<int64_t>(D) * r * 2);
+    const __amdgpu_buffer_rsrc_t r_pe =
+        buf(a.P + static_cast<int64_t>(e) * D * a.q, static_cast<int64_t>(D) * a.q * 2);
+    bf16_bits* yl = reinterpret_cast<bf16_bits*>(smem);
+    const int rqp = (rq + 15) & ~15;
+    const int nks = rqp / 16;
+    const int nct = (D + 31) / 32;
+    for (int ct0 = wave; ct0 < nct; ct0 += 4 * kCt) {
+        u32x4 bw[kCt][2 * NFT];
+#pragma unroll
+        for (int c = 0; c < kCt; ++c) {
+            const int n = 32 * (ct0 + 4 * c) + lrow;
+#pragma unroll
+            for (int ks = 0; ks < 2 * NFT; ++ks) {
+                // r is a multiple of 16: a k step is all US columns or all P_e columns
+                const int k = 16 * ks + 8 * lh;
+                const bool step_us = 16 * ks < r;
+                const uint32_t off = step_us ? static_cast<uint32_t>(n * r + k) * 2
+                                             : static_cast<uint32_t>(n * a.q + k - r) * 2;
+                bw[c][ks] = bload16(step_us ? r_us : r_pe,
+                                    ((ks < nks) & (n < D) & (k < rq)) ? off : kOob);
+            }
+        }
+        f32x16 ay[kCt][2];
+#pragma unroll
+        for (int c = 0; c < kCt; ++c)
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) ay[c][b][v] = 0.0f;
+#pragma unroll
+        for (int ks = 0; ks < 2 * NFT; ++ks) {
+            if (ks < nks) {
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    const u32x4 av = *reinterpret_cast<const u32x4*>(
+                        tul + ((32 * b + lrow) * a.tuch + 2 * ks + lh) * 8);
+#pragma unroll
+                    for (int c = 0; c < kCt; ++c) ay[c][b] = mfma(av, bw[c][ks], ay[c][b]);
+                }
+            }
+        }
+#pragma unroll
+        for (int c = 0; c < kCt; ++c) {
+            const int n = 32 * (ct0 + 4 * c) + lrow;
+            if (n < D) {
+                const float bn = a.b2 != nullptr ? a.b2[n] : 0.0f;
+#pragma unroll
+                for (int b = 0; b < 2; ++b)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int t = 32 * b + 8 * (v >> 2) + 4 * lh + (v & 3);
+                        yl[t * a.yp + n] = f32_to_bf16(ay[c][b][v] + bn);
+                    }
+            }
+        }
+    }
+    __syncthreads();
+    // ---- y rows -> HBM, 16 bytes per thread and step
+    const int dch = D / 8;
+    for (int i = tid; i < kFRows * dch; i += 256) {
+        const int t = i / dch, c = i - t * dch;
+        const int32_t tok = s_tok[t];
+        if (tok >= 0)
+            *reinterpret_cast<uint4*>(a.y + static_cast<int64_t>(tok) * D + 8 * c) =
+                *reinterpret_cast<const uint4*>(yl + t * a.yp + 8 * c);
+    }
+}
+
+template <int NFT, int KG>
+hipError_t fused_cfg(const FusedArgs& a, size_t lds, int grid, hipStream_t st) {
+    if (lds > 65536) {
+        const hipError_t err = hipFuncSetAttribute(
+            reinterpret_cast<const void*>(&k_fused_top1<NFT, KG>),
+            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+        if (err != hipSuccess) return err;
+    }
+    k_fused_top1<NFT, KG><<<dim3(static_cast<unsigned>(grid)), 256, lds, st>>>(a);
+    return hipGetLastError();
+}
+
+int odd_at_least(int n) { return n | 1; }
+
+constexpr size_t kLdsBytes = 160 * 1024;   // gfx950 LDS per workgroup
+constexpr size_t kStaticLds = 1024;        // s_tok, s_gate (aligned)
+
+// LDS plan: [b1 | x rows | 4 W1 rings] while the hidden loop runs, then
+// [two fp32 [t|u] partial-sum areas, later the bf16 y rows | bf16 [t|u] rows]
+// (aliasing the former).
+struct FusedLds {
+    size_t b1, x, ring, areas, yrows, tu_off, total;
+    int xch, redp, tuch, yp;
+};
+FusedLds fused_lds(int D, int H, int r, int q) {
+    FusedLds L{};
+    const int kgroups = (((D + 63) / 64) + 1) & ~1;
+    const int hpad = (H + 4 * kFHid - 1) / (4 * kFHid) * (4 * kFHid);
+    const int nft = (r + q + 31) / 32;
+    L.xch = odd_at_least(8 * kgroups);
+    // a token's 32 NFT sums, padded so that 16 tokens' 16-byte moves hit 16
+    // different bank groups (pitch = 9 groups mod 16)
+    L.redp = 32 * nft + 4;
+    L.tuch = odd_at_least(4 * nft);
+    L.yp = D + 8;
+    L.b1 = static_cast<size_t>(hpad) * 4;
+    // the x copy issues whole 64-lane rounds of slots: round its region up
+    L.x = ((static_cast<size_t>(kFRows) * L.xch + 63) / 64) * 64 * 16;
+    L.ring = static_cast<size_t>(4) * kNS * kStageBytes;
+    L.areas = static_cast<size_t>(2) * kFRows * L.redp * 4;
+    L.yrows = static_cast<size_t>(kFRows) * L.yp * 2;
+    L.tu_off = ((L.areas > L.yrows ? L.areas : L.yrows) + 15) / 16 * 16;
+    const size_t run = L.b1 + L.x + L.ring;
+    const size_t tail = L.tu_off + static_cast<size_t>(kFRows) * L.tuch * 16;
+    L.total = run > tail ? run : tail;
+    return L;
+}
+
+}  // namespace
+
+bool fused_top1_supported(int D, int H, int r, int q) {
+    if (!(D >= 8 && D <= kFusedMaxD && H >= 8 && H <= kFusedMaxH && r % 32 == 0 && r + q > 0 &&
+          r + q <= kFusedMaxRQ))
+        return false;
+    return fused_lds(D, H, r, q).total <= kLdsBytes - kStaticLds;
+}
+
+hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, const void* US,
+                             const void* Vt, const float* b2, const void* P, const void* Q,
+                             const int32_t* perm, const int32_t* offsets, const float* gate,
+                             void* y, int64_t T, int D, int H, int E, int r, int q,
+                             hipStream_t st) {
+    if (!fused_top1_supported(D, H, r, q)) return hipErrorInvalidValue;
+    if (T == 0) return hipSuccess;
+    FusedArgs a{};
+    a.x = static_cast<const bf16_bits*>(x);
+    a.W1 = static_cast<const bf16_bits*>(W1);
+    a.b1 = b1;
+    a.US = static_cast<const bf16_bits*>(US);
+    a.Vt = static_cast<const bf16_bits*>(Vt);
+    a.b2 = b2;
+    a.P = static_cast<const bf16_bits*>(P);
+    a.Q = static_cast<const bf16_bits*>(Q);
+    a.perm = perm;
+    a.offsets = offsets;
+    a.gate = gate;
+    a.y = static_cast<bf16_bits*>(y);
+    a.T = T;
+    a.D = D;
+    a.H = H;
+    a.E = E;
+    a.r = r;
+    a.q = q;
+    a.kgroups = (((D + 63) / 64) + 1) & ~1;
+    a.hpad = (H + 4 * kFHid - 1) / (4 * kFHid) * (4 * kFHid);
+    const int nft = (r + q + 31) / 32;
+    const FusedLds L = fused_lds(D, H, r, q);
+    a.xch = L.xch;
+    a.redp = L.redp;
+    a.tuch = L.tuch;
+    a.yp = L.yp;
+    a.x_off = static_cast<int>(L.b1);
+    a.ring_off = static_cast<int>(L.b1 + L.x);
+    a.tu_off = static_cast<int>(L.tu_off);
+    const size_t lds = L.total;
+    const int64_t tiles = (T + kFRows - 1) / kFRows + E;
+    a.tiles_bound = static_cast<int>(tiles);
+    a.per_xcd = static_cast<int>((tiles + kFXcds - 1) / kFXcds);
+    const int grid = a.per_xcd * kFXcds;
+    switch (nft) {
+        case 1: return fused_cfg<1, 0>(a, lds, grid, st);
+        case 2: return fused_cfg<2, 0>(a, lds, grid, st);
+        case 3: return fused_cfg<3, 0>(a, lds, grid, st);
+        case 4: return fused_cfg<4, 0>(a, lds, grid, st);
+        case 5: return a.kgroups == 6 ? fused_cfg<5, 6>(a, lds, grid, st)
+                                      : fused_cfg<5, 0>(a, lds, grid, st);
+        default: return fused_cfg<6, 0>(a, lds, grid, st);
+    }
+}
+
+}  // namespace clearmoe

@@ -41,11 +41,25 @@ template <> struct Elem<bf16_bits> {
     __device__ static bf16_bits from_f32(float v) { return f32_to_bf16(v); }
 };
 
-// Exact-erf GELU in float32 (device erff).
+// Exact-erf GELU, v Phi(v) = 0.5 v (1 + erf(v / sqrt 2)), in float32.
+// erf by Abramowitz & Stegun 7.1.26 (|error| <= 1.5e-7 for every argument):
+// for a >= 0, 1 - erf(a) = t P(t) exp(-a^2), t = 1 / (1 + p a), P of degree 4.
+// With a = |v| / sqrt 2 and h = 0.5 v (1 - erf(a)):  GELU(v) = v - h for
+// v >= 0 and h for v < 0 (no cancellation in the negative tail).  The 0.5 is
+// folded into P's coefficients, exp(-a^2) = 2^(-v^2 log2(e) / 2), and the
+// reciprocal and power of two are the hardware instructions (about 1 ulp):
+// 14 FMA-class operations and 2 transcendental ones.
 __device__ __forceinline__ float gelu_erf(float v) {
-    return 0.5f * v * (1.0f + erff(v * 0.70710678118654752440f));
+    const float a = fabsf(v) * 0.70710678118654752440f;
+    const float t = __builtin_amdgcn_rcpf(__builtin_fmaf(0.3275911f, a, 1.0f));
+    float hp = __builtin_fmaf(t, 0.5307027145f, -0.7265760135f);   // 0.5 * (a5, a4)
+    hp = __builtin_fmaf(t, hp, 0.7107068705f);                      // 0.5 * a3
+    hp = __builtin_fmaf(t, hp, -0.142248368f);                      // 0.5 * a2
+    hp = __builtin_fmaf(t, hp, 0.127414796f);                       // 0.5 * a1
+    const float e = __builtin_amdgcn_exp2f(v * v * -0.72134752044448170368f);   // -log2(e) / 2
+    const float h = v * (t * hp) * e;
+    return v >= 0.0f ? v - h : h;
 }
-
 // ---------------------------------------------------------------------------
 // Tiling constants shared by host and device code.
 // ---------------------------------------------------------------------------
@@ -130,5 +144,19 @@ inline GemmDesc gemm_desc(int64_t M, int N, int K) {
     return g;
 }
 hipError_t launch_gemm(int dtype, const GemmDesc& g, hipStream_t st);
+
+// Fused top-1 layer in bfloat16: y[perm p] = [t|u](p) [US | P_e]^T + b2 with
+// [t|u](p) = GELU(x[perm p] W1^T + b1) [Vt ; Q_e]^T (u columns times the gate),
+// every intermediate on chip.  Needs the expert order (perm, offsets) of a
+// top-1 routing.  Shapes outside fused_top1_supported use the GEMM path.
+constexpr int kFusedMaxD = 768;      // x rows of a 64-row tile live in LDS ...
+constexpr int kFusedMaxH = 8192;     // ... beside b1
+constexpr int kFusedMaxRQ = 192;     // [t|u] accumulators live in registers
+bool fused_top1_supported(int D, int H, int r, int q);
+hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, const void* US,
+                             const void* Vt, const float* b2, const void* P, const void* Q,
+                             const int32_t* perm, const int32_t* offsets, const float* gate,
+                             void* y, int64_t T, int D, int H, int E, int r, int q,
+                             hipStream_t st);
 
 }  // namespace clearmoe
