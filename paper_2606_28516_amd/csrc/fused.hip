@@ -20,14 +20,15 @@
 // Register chaining.  For v_mfma_f32_32x32x16_bf16, lane l holds result
 // column l%32, rows 8(v/4) + 4(l/32) + v%4 (v = 0..15), and as a k operand
 // supplies k slots 8(l/32) + i (i = 0..7) of row/column l%32.  Tile q (0, 1)
-// of the z^T block takes W1 row  hb + 32 ((s>>2)&1) + 16 q + 4 (s>>3) + (s&3)
-// in row slot s, which makes lane l's 16 results of tile q the hidden units
-// hb + 32(l/32) + 16q + v.  Across both tiles a lane then holds hidden units
-// hb + 32(l/32) + [0, 32): four runs of 8, i.e. the B operands of four MFMAs
-// whose slot 8(l/32) + i is hidden unit hb + 32(l/32) + 8j + i (j = 0..3).
-// The A operand ([Vt;Q_e] rows) reads the same 8 units: 64 contiguous bytes
-// per lane over j.  Phase-1 products use the analogous k order (slot
-// 8(l/32) + i of MFMA j is input feature 64g + 32(l/32) + 8j + i).
+// of the z^T block takes, in row slot s, W1 row
+//     hb + 32 q + 16 (s>>4) + 8 ((s>>2)&1) + 4 ((s>>3)&1) + (s&3),
+// which makes lane l's result v of tile q the hidden unit
+// hb + 32 q + 16 (v/8) + 8 (l/32) + v%8.  Run j = 2q + v/8 of 8 such values
+// is then the B operand of an MFMA whose slot 8(l/32) + i is hidden unit
+// hb + 16 j + 8 (l/32) + i, and the A operand ([Vt;Q_e] rows) reads those 8
+// units: the two lane halves read 32 contiguous bytes of a row.  Phase-1
+// products use their own k order (slot 8(l/32) + i of MFMA j is input feature
+// 64 g + 32 (l/32) + 8 j + i), matched by the x reads.
 //
 // Waits.  The W1 DMA is inline asm the compiler does not see; every wave
 // issues its loads in a fixed order (stages, then the [Vt;Q_e] loads of a
@@ -97,6 +98,15 @@ __device__ __forceinline__ i32x4 dma_desc(const void* p, int64_t bytes) {
     return d;
 }
 
+// 16 bytes per lane, buffer -> LDS at m0 + 16 * lane (zeros outside the
+// buffer); waited for like the ring stages.
+__device__ __forceinline__ void dma16_buf(const i32x4& d, uint32_t off, uint32_t m0) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :
+                 : "s"(m0), "v"(off), "s"(d)
+                 : "memory", "m0");
+}
+
 // One W1 ring stage: 8 loads of 16 bytes per lane, buffer -> LDS at
 // base + 1024 i + 16 * lane (zeros for an offset outside the buffer).  Inline
 // asm: the compiler does not count these loads; the kernel waits for them
@@ -134,11 +144,13 @@ __device__ __forceinline__ void vm_wait() {
     asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory");
 }
 
-// Hidden offset (within a 64-slice) of row slot s of z^T tile q.
 __device__ __forceinline__ int swz(int row) { return (row >> 1) & 7; }
 
+// Hidden offset (within a 64-slice) of row slot s of z^T tile q.  It makes
+// the lane's result v of tile q (row slot 8(v/4) + 4 lh + v%4) the hidden
+// unit 32 q + 16 (v/8) + 8 lh + v%8.
 __device__ __forceinline__ int hid_of_slot(int q, int s) {
-    return 32 * ((s >> 2) & 1) + 16 * q + 4 * (s >> 3) + (s & 3);
+    return 32 * q + 16 * (s >> 4) + 8 * ((s >> 2) & 1) + 4 * ((s >> 3) & 1) + (s & 3);
 }
 
 struct FusedArgs {
@@ -157,35 +169,39 @@ struct FusedArgs {
     int64_t T;
     int D, H, E, r, q;
     int xch;        // LDS pitch of an x row, 16-byte chunks (odd, >= 8 * kgroups)
-    int kgroups;    // ceil(D / 64) rounded up to even
+    int kgroups;    // ceil(D / 64) rounded up to even, at least 6
     int hpad;       // H rounded up to 4 waves x 64
     int redp;       // LDS pitch (floats) of a token's [t|u] partial sums
     int tuch;       // LDS pitch of a bf16 [t|u] row, 16-byte chunks (odd)
     int yp;         // LDS pitch (elements) of a bf16 y row
-    int x_off;      // byte offset of the x rows (after b1)
+    int b2_off;     // byte offset of b2 (after b1)
+    int b2_chunks;  // 16-byte chunks of the b2 region (a multiple of 64)
+    int x_off;      // byte offset of the x rows (after b2)
     int ring_off;   // byte offset of the four waves' W1 rings (after x)
+    int epi_off;    // byte offset of the [t|u] partial sums, later the y rows (after b2)
     int tu_off;     // byte offset of the bf16 [t|u] rows (after the sums / y rows)
     int tiles_bound;
     int per_xcd;
 };
 
-// Wait for stage n of the W1 ring: loads issued after it are stage n + 1 (if
-// it belongs to this slice), stage n + 2 (likewise), and for the first two
-// stages of a slice the slice's 4 NFT [Vt;Q_e] loads.
-template <int NFT>
-__device__ __forceinline__ void wait_stage(bool s1, bool s2, bool vq) {
-    const int key = (s1 ? 1 : 0) + (s2 ? 2 : 0) + (vq ? 4 : 0);
-    switch (key) {
-        case 0: vm_wait<0>(); break;
-        case 1: vm_wait<8>(); break;
-        case 2: vm_wait<8>(); break;
-        case 3: vm_wait<16>(); break;
-        case 4: vm_wait<4 * NFT>(); break;
-        case 5: vm_wait<8 + 4 * NFT>(); break;
-        case 6: vm_wait<8 + 4 * NFT>(); break;
-        default: vm_wait<16 + 4 * NFT>(); break;
+// [Vt;Q_e] halves (issued in steps 4 and 5 of every block, before that step's
+// W1 stage) issued after stage n was: stage n of step g was issued in step
+// g - 2, of the previous block when negative (the first block has none; its
+// stages 0 and 1 come from the prologue).
+__host__ __device__ constexpr int vq_halves_after(int g, int kgroups, bool first) {
+    const int s = g - 2;
+    int c = 0;
+    for (int p = 4; p <= 5; ++p) {
+        if (s >= 0) c += (p > s && p <= g) ? 1 : 0;
+        else c += ((!first && p > kgroups + s) || p <= g) ? 1 : 0;
     }
+    return c;
 }
+static_assert(vq_halves_after(0, 6, false) == 1 && vq_halves_after(1, 6, false) == 0 &&
+                  vq_halves_after(0, 6, true) == 0 && vq_halves_after(4, 6, false) == 1 &&
+                  vq_halves_after(5, 6, false) == 2 && vq_halves_after(0, 8, false) == 0 &&
+                  vq_halves_after(6, 8, false) == 1 && vq_halves_after(5, 6, true) == 2,
+              "vq issue accounting");
 
 // Bare workgroup barrier: LDS operations complete, outstanding DMA untouched
 // (__syncthreads would also wait for every vector-memory load).
@@ -251,6 +267,7 @@ void k_fused_top1(FusedArgs a) {
     __syncthreads();
 
     float* s_b1 = reinterpret_cast<float*>(smem);
+    const float* s_b2 = reinterpret_cast<const float*>(smem + a.b2_off);
     const unsigned char* xs = smem + a.x_off;
     unsigned char* ringp = smem + a.ring_off + wave * (kNS * kStageBytes);
     const uint32_t ring = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_word*)ringp));
@@ -279,7 +296,19 @@ void k_fused_top1(FusedArgs a) {
         dma_stage8(d_w1, __builtin_amdgcn_readfirstlane(m0), off);
     };
 
-    // ---- prologue: x rows -> LDS (DMA), b1 -> LDS, the first two W1 stages
+    // ---- prologue: b1, b2 and the gathered x rows -> LDS, the first two W1
+    //      stages; all by DMA, one wait
+    {
+        const uint32_t lb = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_word*)smem));
+        const i32x4 d_b1 = dma_desc(a.b1, a.b1 != nullptr ? static_cast<int64_t>(H) * 4 : 0);
+        const i32x4 d_b2 = dma_desc(a.b2, a.b2 != nullptr ? static_cast<int64_t>(D) * 4 : 0);
+        for (int base = wave * 64; base < a.hpad / 4; base += 256)    // zeros past H
+            dma16_buf(d_b1, static_cast<uint32_t>(base + lane) * 16u,
+                      __builtin_amdgcn_readfirstlane(lb + base * 16));
+        for (int base = wave * 64; base < a.b2_chunks; base += 256)   // zeros past D
+            dma16_buf(d_b2, static_cast<uint32_t>(base + lane) * 16u,
+                      __builtin_amdgcn_readfirstlane(lb + a.b2_off + base * 16));
+    }
     {
         const uint32_t xl = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_word*)xs));
         const int dch = D / 8;
@@ -295,13 +324,12 @@ void k_fused_top1(FusedArgs a) {
             lds_dma16(src, __builtin_amdgcn_readfirstlane(xl + base * 16));
         }
     }
-    // (the compiler waits for these b1 loads, issued after the x copy: that
-    // also completes this wave's x copy)
-    for (int i = tid; i < a.hpad; i += 256) s_b1[i] = (a.b1 != nullptr && i < H) ? a.b1[i] : 0.0f;
-    vm_wait<0>();
     if (n_iter > 0) {
         dma_stage(0);
         dma_stage(1);
+        vm_wait<16>();                                 // all but the two W1 stages
+    } else {
+        vm_wait<0>();
     }
     lds_barrier();
 
@@ -320,10 +348,17 @@ void k_fused_top1(FusedArgs a) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) tu[f][b][v] = 0.0f;
 
-    for (int it = 0; it < n_iter; ++it) {
-        const int hb = (it * 4 + wave) * kFHid;
-        // [Vt;Q_e] operands of this slice, columns hb + 32 lh + 8 j + [0, 8)
-        u32x4 vq[NFT][4];
+    // Software pipeline over this wave's slices.  Block k runs phase 1 of
+    // slice k (z^T accumulated in za, one ring stage per step) and, in its
+    // first four steps, GELU + phase 2 of slice k - 1 (one run j of 8 hidden
+    // units per step, from zp), so that the GELU arithmetic overlaps the MFMA
+    // and LDS work of phase 1.  The [Vt;Q_e] operands of slice k are loaded in
+    // step 4 of block k, after the last run of slice k - 1 has used vq.
+    f32x16 za[2][2], zp[2][2];
+    u32x4 vq[NFT][4];
+
+    // [Vt;Q_e] columns hb + 16 j + 8 lh + [0, 8) for j in [j0, j0 + 2)
+    auto load_vq = [&](int hb, int j0) {
 #pragma unroll
         for (int f = 0; f < NFT; ++f) {
             // r is a multiple of 32: a feature tile is all Vt rows or all Q_e rows
@@ -332,89 +367,141 @@ void k_fused_top1(FusedArgs a) {
             const uint32_t rowb = static_cast<uint32_t>(tile_vt ? feat : feat - r) * H * 2;
             const bool live = feat < rq;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int hid = hb + 32 * lh + 8 * j;
+            for (int jj = 0; jj < 2; ++jj) {
+                const int j = j0 + jj;
+                const int hid = hb + 16 * j + 8 * lh;
                 vq[f][j] = bload16(tile_vt ? r_vt : r_qe, (live & (hid < H)) ? rowb + 2u * hid : kOob);
             }
         }
-
-        // ---- phase 1: z^T[64 hidden x 64 tokens] = W1_slice x^T, one ring stage
-        //      (64 inputs) per step; stage n + 2 of the slice is issued before
-        //      stage n is read
-        f32x16 za[2][2];
+    };
+    // Run j of the pending slice (hidden units hb + 16 j + 8 lh + i): GELU and
+    // bf16 turn the lane's z values (bias included) into the B operand, and
+    // [t|u]^T += [Vt;Q_e]_run z^T_run.  Units >= H have zero [Vt;Q_e] columns.
+    auto run = [&](int j) {
+        const int qq = j >> 1, v0 = 8 * (j & 1);
+        u32x4 zo[2];
 #pragma unroll
-        for (int qq = 0; qq < 2; ++qq)
+        for (int b = 0; b < 2; ++b)
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) za[qq][b][v] = 0.0f;
-#pragma unroll
-        for (int g = 0; g < kgroups; ++g) {
-            const int n = it * kgroups + g;
-            if (g + 2 < kgroups) dma_stage(n + 2);
-            wait_stage<NFT>(g + 1 < kgroups, g + 2 < kgroups, g < 2);
-            const unsigned char* st = ringp + (n % kNS) * kStageBytes;
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int c = (8 * g + j) * 16;
-                const u32x4 x0 = *reinterpret_cast<const u32x4*>(xs + xoff0 + c);
-                const u32x4 x1 = *reinterpret_cast<const u32x4*>(xs + xoff1 + c);
-#pragma unroll
-                for (int qq = 0; qq < 2; ++qq) {
-                    const int row = 32 * qq + lrow;
-                    const u32x4 w = *reinterpret_cast<const u32x4*>(
-                        st + row * 128 + (((4 * lh + j) ^ swz(row)) << 4));
-                    za[qq][0] = mfma(w, x0, za[qq][0]);
-                    za[qq][1] = mfma(w, x1, za[qq][1]);
-                }
+            for (int i = 0; i < 4; ++i) {
+                const int v = v0 + 2 * i;
+                zo[b][i] = pack_bf16x2(gelu_erf(zp[qq][b][v]), gelu_erf(zp[qq][b][v + 1]));
             }
-        }
-        // The last step's wait left nothing of this wave outstanding, so the
-        // compiler's waits for the [Vt;Q_e] registers (placed here) are free;
-        // then the next slice's first two stages load behind GELU and phase 2.
 #pragma unroll
         for (int f = 0; f < NFT; ++f)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) asm volatile("" : : "v"(vq[f][j]));
-        if (it + 1 < n_iter) {
-            dma_stage((it + 1) * kgroups);
-            dma_stage((it + 1) * kgroups + 1);
-        }
-
-        // ---- per run j of 8 hidden units (hb + 32 lh + 8 j + i): bias, GELU and
-        //      bf16 turn the lane's z values into the B operand of phase 2, and
-        //      [t|u]^T += [Vt;Q_e]_run z^T_run.  Units >= H have zero [Vt;Q_e]
-        //      columns, so their z values do not count.
+            for (int b = 0; b < 2; ++b) tu[f][b] = mfma(vq[f][j], zo[b], tu[f][b]);
+    };
+    // Phase-1 step: stage n of the ring (inputs 64 g .. 64 g + 63).
+    auto step = [&](int n, int g) {
+        const unsigned char* st = ringp + (n % kNS) * kStageBytes;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int qq = j >> 1, v0 = 8 * (j & 1);
-            const int hid0 = hb + 32 * lh + 8 * j;      // < H rounded up to 256
-            const float4 b0 = *reinterpret_cast<const float4*>(s_b1 + hid0);
-            const float4 b1v = *reinterpret_cast<const float4*>(s_b1 + hid0 + 4);
-            const float bj[8] = {b0.x, b0.y, b0.z, b0.w, b1v.x, b1v.y, b1v.z, b1v.w};
-            u32x4 zo[2];
+            const int c = (8 * g + j) * 16;
+            const u32x4 x0 = *reinterpret_cast<const u32x4*>(xs + xoff0 + c);
+            const u32x4 x1 = *reinterpret_cast<const u32x4*>(xs + xoff1 + c);
 #pragma unroll
-            for (int b = 0; b < 2; ++b) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const int v = v0 + 2 * i;
-                    zo[b][i] = pack_bf16x2(gelu_erf(za[qq][b][v] + bj[2 * i]),
-                                           gelu_erf(za[qq][b][v + 1] + bj[2 * i + 1]));
-                }
+            for (int qq = 0; qq < 2; ++qq) {
+                const int row = 32 * qq + lrow;
+                const u32x4 w = *reinterpret_cast<const u32x4*>(
+                    st + row * 128 + (((4 * lh + j) ^ swz(row)) << 4));
+                za[qq][0] = mfma(w, x0, za[qq][0]);
+                za[qq][1] = mfma(w, x1, za[qq][1]);
             }
+        }
+    };
+    // Block k.  Loads issued after stage n: stages n + 1 and n + 2 (16), plus
+    // the halves of [Vt;Q_e] (2 NFT loads each, issued in steps 4 and 5 before
+    // that step's stage) that came after stage n.  The stages past the last
+    // slice load zeros (every block issues the same loads).
+    auto block = [&](int k, bool p2) {
+        const int hb = (k * 4 + wave) * kFHid;
+        if (p2) {
+            // the compiler's wait for vq goes here, before this block's DMA
 #pragma unroll
             for (int f = 0; f < NFT; ++f)
 #pragma unroll
-                for (int b = 0; b < 2; ++b) tu[f][b] = mfma(vq[f][j], zo[b], tu[f][b]);
+                for (int j = 0; j < 4; ++j) asm volatile("" : : "v"(vq[f][j]));
         }
+        // z^T accumulators start at b1 (lane's value v of tile qq is hidden
+        // unit hb + 32 qq + 16 (v/8) + 8 lh + v%8; the LDS copy of b1 is zero
+        // past H)
+#pragma unroll
+        for (int qq = 0; qq < 2; ++qq) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float4 bv = *reinterpret_cast<const float4*>(
+                    s_b1 + hb + 32 * qq + 16 * (i >> 1) + 8 * lh + 4 * (i & 1));
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    za[qq][b][4 * i] = bv.x;
+                    za[qq][b][4 * i + 1] = bv.y;
+                    za[qq][b][4 * i + 2] = bv.z;
+                    za[qq][b][4 * i + 3] = bv.w;
+                }
+            }
+        }
+#pragma unroll
+        for (int g = 0; g < kgroups; ++g) {
+            const int n = k * kgroups + g;
+            if (g == 4) load_vq(hb, 0);
+            if (g == 5) load_vq(hb, 2);
+            dma_stage(n + 2);
+            switch (vq_halves_after(g, kgroups, !p2)) {
+                case 0: vm_wait<16>(); break;
+                case 1: vm_wait<16 + 2 * NFT>(); break;
+                default: vm_wait<16 + 4 * NFT>(); break;
+            }
+            step(n, g);
+            if (p2 && g < 4) run(g);
+        }
+#pragma unroll
+        for (int qq = 0; qq < 2; ++qq)
+#pragma unroll
+            for (int b = 0; b < 2; ++b) zp[qq][b] = za[qq][b];
+    };
+
+    if (n_iter > 0) {
+        block(0, false);
+        for (int k = 1; k < n_iter; ++k) block(k, true);
+        // drain: GELU + phase 2 of the last slice
+#pragma unroll
+        for (int j = 0; j < 4; ++j) run(j);
     }
     vm_wait<0>();
+
+    // [US | P_e] operands of this wave's first pass of output columns, loaded
+    // now so that their latency hides behind the reduction (whose barriers
+    // therefore leave vector-memory loads alone)
+    const __amdgpu_buffer_rsrc_t r_us = buf(a.US, static_cast<int64_t>(D) * r * 2);
+    const __amdgpu_buffer_rsrc_t r_pe =
+        buf(a.P + static_cast<int64_t>(e) * D * a.q, static_cast<int64_t>(D) * a.q * 2);
+    const int rqp = (rq + 15) & ~15;
+    const int nks = rqp / 16;
+    u32x4 bw[kCt][2 * NFT];
+    auto load_bw = [&](int ct0) {
+#pragma unroll
+        for (int c = 0; c < kCt; ++c) {
+            const int n = 32 * (ct0 + 4 * c) + lrow;
+#pragma unroll
+            for (int ks = 0; ks < 2 * NFT; ++ks) {
+                // r is a multiple of 16: a k step is all US columns or all P_e columns
+                const int k = 16 * ks + 8 * lh;
+                const bool step_us = 16 * ks < r;
+                const uint32_t off = step_us ? static_cast<uint32_t>(n * r + k) * 2
+                                             : static_cast<uint32_t>(n * a.q + k - r) * 2;
+                bw[c][ks] = bload16(step_us ? r_us : r_pe,
+                                    ((ks < nks) & (n < D) & (k < rq)) ? off : kOob);
+            }
+        }
+    };
+    load_bw(wave);
 
     // ---- sum the four waves' [t|u]^T partials: (w0 + w2) + (w1 + w3).  Areas
     //      hold [token][feature] floats (pitch redp); lane (token 32b + lrow)
     //      holds features 32f + 8g + 4 lh + [0, 4) of v-group g: 16-byte moves.
-    __syncthreads();                                   // b1, x, rings no longer read
-    float* area0 = reinterpret_cast<float*>(smem);
+    lds_barrier();                                     // x and the rings no longer read
+    float* area0 = reinterpret_cast<float*>(smem + a.epi_off);
     float* area1 = area0 + kFRows * a.redp;
     auto put = [&](float* area) {
 #pragma unroll
@@ -429,34 +516,34 @@ void k_fused_top1(FusedArgs a) {
                     *reinterpret_cast<float4*>(area + (32 * b + lrow) * a.redp + 32 * f + 8 * g + 4 * lh) = v;
                 }
     };
+    // one feature tile at a time (its 8 reads issued together): bounded registers
     auto add = [&](const float* area) {
-        float4 o[NFT][2][4];
 #pragma unroll
-        for (int f = 0; f < NFT; ++f)
+        for (int f = 0; f < NFT; ++f) {
+            float4 o[2][4];
 #pragma unroll
             for (int b = 0; b < 2; ++b)
 #pragma unroll
                 for (int g = 0; g < 4; ++g)
-                    o[f][b][g] = *reinterpret_cast<const float4*>(
+                    o[b][g] = *reinterpret_cast<const float4*>(
                         area + (32 * b + lrow) * a.redp + 32 * f + 8 * g + 4 * lh);
-#pragma unroll
-        for (int f = 0; f < NFT; ++f)
 #pragma unroll
             for (int b = 0; b < 2; ++b)
 #pragma unroll
                 for (int g = 0; g < 4; ++g) {
-                    tu[f][b][4 * g] += o[f][b][g].x;
-                    tu[f][b][4 * g + 1] += o[f][b][g].y;
-                    tu[f][b][4 * g + 2] += o[f][b][g].z;
-                    tu[f][b][4 * g + 3] += o[f][b][g].w;
+                    tu[f][b][4 * g] += o[b][g].x;
+                    tu[f][b][4 * g + 1] += o[b][g].y;
+                    tu[f][b][4 * g + 2] += o[b][g].z;
+                    tu[f][b][4 * g + 3] += o[b][g].w;
                 }
+        }
     };
     if (wave >= 2) put(wave == 2 ? area0 : area1);
-    __syncthreads();
+    lds_barrier();
     if (wave < 2) add(wave == 0 ? area0 : area1);
-    __syncthreads();
+    lds_barrier();
     if (wave == 1) put(area0);
-    __syncthreads();
+    lds_barrier();
     bf16_bits* tul = reinterpret_cast<bf16_bits*>(smem + a.tu_off);
     if (wave == 0) {
         add(area0);
@@ -479,34 +566,15 @@ void k_fused_top1(FusedArgs a) {
             }
         }
     }
-    __syncthreads();
+    lds_barrier();
 
     // ---- y = [t|u] [US | P_e]^T + b2 into LDS rows (the sums' area, free
     //      now), kCt column tiles of 32 per pass with every operand load
     //      issued before any store
-    const __amdgpu_buffer_rsrc_t r_us = buf(a.US, static_cast<int64_t>(D) * r * 2);
-    const __amdgpu_buffer_rsrc_t r_pe =
-        buf(a.P + static_cast<int64_t>(e) * D * a.q, static_cast<int64_t>(D) * a.q * 2);
-    bf16_bits* yl = reinterpret_cast<bf16_bits*>(smem);
-    const int rqp = (rq + 15) & ~15;
-    const int nks = rqp / 16;
+    bf16_bits* yl = reinterpret_cast<bf16_bits*>(smem + a.epi_off);
     const int nct = (D + 31) / 32;
     for (int ct0 = wave; ct0 < nct; ct0 += 4 * kCt) {
-        u32x4 bw[kCt][2 * NFT];
-#pragma unroll
-        for (int c = 0; c < kCt; ++c) {
-            const int n = 32 * (ct0 + 4 * c) + lrow;
-#pragma unroll
-            for (int ks = 0; ks < 2 * NFT; ++ks) {
-                // r is a multiple of 16: a k step is all US columns or all P_e columns
-                const int k = 16 * ks + 8 * lh;
-                const bool step_us = 16 * ks < r;
-                const uint32_t off = step_us ? static_cast<uint32_t>(n * r + k) * 2
-                                             : static_cast<uint32_t>(n * a.q + k - r) * 2;
-                bw[c][ks] = bload16(step_us ? r_us : r_pe,
-                                    ((ks < nks) & (n < D) & (k < rq)) ? off : kOob);
-            }
-        }
+        if (ct0 != wave) load_bw(ct0);               // the first pass was prefetched
         f32x16 ay[kCt][2];
 #pragma unroll
         for (int c = 0; c < kCt; ++c)
@@ -514,42 +582,58 @@ void k_fused_top1(FusedArgs a) {
             for (int b = 0; b < 2; ++b)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) ay[c][b][v] = 0.0f;
+        // y^T[n][token] = [US|P_e][n][k] [t|u]^T[k][token]: the lane holds, for
+        // token 32 b + lrow, features 32 ct + 8 g + 4 lh + [0, 4) of v-group g
 #pragma unroll
         for (int ks = 0; ks < 2 * NFT; ++ks) {
             if (ks < nks) {
 #pragma unroll
                 for (int b = 0; b < 2; ++b) {
-                    const u32x4 av = *reinterpret_cast<const u32x4*>(
+                    const u32x4 tv = *reinterpret_cast<const u32x4*>(
                         tul + ((32 * b + lrow) * a.tuch + 2 * ks + lh) * 8);
 #pragma unroll
-                    for (int c = 0; c < kCt; ++c) ay[c][b] = mfma(av, bw[c][ks], ay[c][b]);
+                    for (int c = 0; c < kCt; ++c) ay[c][b] = mfma(bw[c][ks], tv, ay[c][b]);
                 }
             }
         }
 #pragma unroll
         for (int c = 0; c < kCt; ++c) {
-            const int n = 32 * (ct0 + 4 * c) + lrow;
-            if (n < D) {
-                const float bn = a.b2 != nullptr ? a.b2[n] : 0.0f;
+            const int ct = ct0 + 4 * c;
 #pragma unroll
-                for (int b = 0; b < 2; ++b)
+            for (int g = 0; g < 4; ++g) {
+                const int n0 = 32 * ct + 8 * g + 4 * lh;
+                if (n0 < D) {                               // D % 8 == 0: all four or none
+                    const float4 bn = *reinterpret_cast<const float4*>(s_b2 + n0);
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        const int t = 32 * b + 8 * (v >> 2) + 4 * lh + (v & 3);
-                        yl[t * a.yp + n] = f32_to_bf16(ay[c][b][v] + bn);
+                    for (int b = 0; b < 2; ++b) {
+                        uint2 w;
+                        w.x = pack_bf16x2(ay[c][b][4 * g] + bn.x, ay[c][b][4 * g + 1] + bn.y);
+                        w.y = pack_bf16x2(ay[c][b][4 * g + 2] + bn.z, ay[c][b][4 * g + 3] + bn.w);
+                        *reinterpret_cast<uint2*>(yl + (32 * b + lrow) * a.yp + n0) = w;
                     }
+                }
             }
         }
     }
     __syncthreads();
-    // ---- y rows -> HBM, 16 bytes per thread and step
+    // ---- y rows -> HBM: wave w writes rows w + 4 i (i < 16), lane c the
+    //      16-byte chunks c, c + 64, ...: all LDS reads of a pass, then its stores
     const int dch = D / 8;
-    for (int i = tid; i < kFRows * dch; i += 256) {
-        const int t = i / dch, c = i - t * dch;
-        const int32_t tok = s_tok[t];
-        if (tok >= 0)
-            *reinterpret_cast<uint4*>(a.y + static_cast<int64_t>(tok) * D + 8 * c) =
-                *reinterpret_cast<const uint4*>(yl + t * a.yp + 8 * c);
+    for (int c = lane; c - lane < dch; c += 64) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {                  // 8 rows per batch
+            u32x4 v[kFRows / 8];
+            const int cc = c < dch ? c : 0;             // lanes past the row read chunk 0
+#pragma unroll
+            for (int i = 0; i < kFRows / 8; ++i)
+                v[i] = *reinterpret_cast<const u32x4*>(yl + (wave + 4 * (8 * h + i)) * a.yp + 8 * cc);
+#pragma unroll
+            for (int i = 0; i < kFRows / 8; ++i) {
+                const int32_t tok = s_tok[wave + 4 * (8 * h + i)];
+                if (tok >= 0 && c < dch)
+                    *reinterpret_cast<u32x4*>(a.y + static_cast<int64_t>(tok) * D + 8 * c) = v[i];
+            }
+        }
     }
 }
 
@@ -567,19 +651,27 @@ hipError_t fused_cfg(const FusedArgs& a, size_t lds, int grid, hipStream_t st) {
 
 int odd_at_least(int n) { return n | 1; }
 
+// 64-wide input groups of phase 1: ceil(D / 64), even, and at least 6 (the
+// pipeline spreads a slice's four GELU runs over the first four steps and
+// loads the next [Vt;Q_e] in step 4; padded groups read zeros).
+int fused_kgroups(int D) {
+    const int g = (((D + 63) / 64) + 1) & ~1;
+    return g < 6 ? 6 : g;
+}
+
 constexpr size_t kLdsBytes = 160 * 1024;   // gfx950 LDS per workgroup
 constexpr size_t kStaticLds = 1024;        // s_tok, s_gate (aligned)
 
-// LDS plan: [b1 | x rows | 4 W1 rings] while the hidden loop runs, then
-// [two fp32 [t|u] partial-sum areas, later the bf16 y rows | bf16 [t|u] rows]
-// (aliasing the former).
+// LDS plan: [b1 | b2 | x rows | 4 W1 rings] while the hidden loop runs, then
+// [b1 | b2 | two fp32 [t|u] partial-sum areas, later the bf16 y rows | bf16
+// [t|u] rows] (aliasing x and the rings).
 struct FusedLds {
-    size_t b1, x, ring, areas, yrows, tu_off, total;
+    size_t b1, b2, x, ring, areas, yrows, epi_off, tu_off, total;
     int xch, redp, tuch, yp;
 };
 FusedLds fused_lds(int D, int H, int r, int q) {
     FusedLds L{};
-    const int kgroups = (((D + 63) / 64) + 1) & ~1;
+    const int kgroups = fused_kgroups(D);
     const int hpad = (H + 4 * kFHid - 1) / (4 * kFHid) * (4 * kFHid);
     const int nft = (r + q + 31) / 32;
     L.xch = odd_at_least(8 * kgroups);
@@ -588,14 +680,16 @@ FusedLds fused_lds(int D, int H, int r, int q) {
     L.redp = 32 * nft + 4;
     L.tuch = odd_at_least(4 * nft);
     L.yp = D + 8;
-    L.b1 = static_cast<size_t>(hpad) * 4;
+    L.b1 = static_cast<size_t>(hpad) * 4;                    // a multiple of 1 KB
+    L.b2 = (static_cast<size_t>(D) * 4 + 1023) / 1024 * 1024;
     // the x copy issues whole 64-lane rounds of slots: round its region up
     L.x = ((static_cast<size_t>(kFRows) * L.xch + 63) / 64) * 64 * 16;
     L.ring = static_cast<size_t>(4) * kNS * kStageBytes;
     L.areas = static_cast<size_t>(2) * kFRows * L.redp * 4;
     L.yrows = static_cast<size_t>(kFRows) * L.yp * 2;
-    L.tu_off = ((L.areas > L.yrows ? L.areas : L.yrows) + 15) / 16 * 16;
-    const size_t run = L.b1 + L.x + L.ring;
+    L.epi_off = L.b1 + L.b2;                                 // past b2, which phase C reads
+    L.tu_off = L.epi_off + ((L.areas > L.yrows ? L.areas : L.yrows) + 15) / 16 * 16;
+    const size_t run = L.b1 + L.b2 + L.x + L.ring;
     const size_t tail = L.tu_off + static_cast<size_t>(kFRows) * L.tuch * 16;
     L.total = run > tail ? run : tail;
     return L;
@@ -636,7 +730,7 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
     a.E = E;
     a.r = r;
     a.q = q;
-    a.kgroups = (((D + 63) / 64) + 1) & ~1;
+    a.kgroups = fused_kgroups(D);
     a.hpad = (H + 4 * kFHid - 1) / (4 * kFHid) * (4 * kFHid);
     const int nft = (r + q + 31) / 32;
     const FusedLds L = fused_lds(D, H, r, q);
@@ -644,8 +738,11 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
     a.redp = L.redp;
     a.tuch = L.tuch;
     a.yp = L.yp;
-    a.x_off = static_cast<int>(L.b1);
-    a.ring_off = static_cast<int>(L.b1 + L.x);
+    a.b2_off = static_cast<int>(L.b1);
+    a.b2_chunks = static_cast<int>(L.b2 / 16);
+    a.x_off = static_cast<int>(L.b1 + L.b2);
+    a.ring_off = static_cast<int>(L.b1 + L.b2 + L.x);
+    a.epi_off = static_cast<int>(L.epi_off);
     a.tu_off = static_cast<int>(L.tu_off);
     const size_t lds = L.total;
     const int64_t tiles = (T + kFRows - 1) / kFRows + E;
@@ -657,9 +754,8 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
         case 2: return fused_cfg<2, 0>(a, lds, grid, st);
         case 3: return fused_cfg<3, 0>(a, lds, grid, st);
         case 4: return fused_cfg<4, 0>(a, lds, grid, st);
-        case 5: return a.kgroups == 6 ? fused_cfg<5, 6>(a, lds, grid, st)
-                                      : fused_cfg<5, 0>(a, lds, grid, st);
-        default: return fused_cfg<6, 0>(a, lds, grid, st);
+        default: return a.kgroups == 6 ? fused_cfg<5, 6>(a, lds, grid, st)
+                                       : fused_cfg<5, 0>(a, lds, grid, st);
     }
 }
 

@@ -44,23 +44,22 @@ template <> struct Elem<bf16_bits> {
 // Exact-erf GELU, v Phi(v) = 0.5 v (1 + erf(v / sqrt 2)), in float32.
 // erf by Abramowitz & Stegun 7.1.26 (|error| <= 1.5e-7 for every argument):
 // for a >= 0, 1 - erf(a) = t P(t) exp(-a^2), t = 1 / (1 + p a), P of degree 4.
-// With a = |v| / sqrt 2 and h = 0.5 v (1 - erf(a)):  GELU(v) = v - h for
-// v >= 0 and h for v < 0 (no cancellation in the negative tail).  The 0.5 is
-// folded into P's coefficients, exp(-a^2) = 2^(-v^2 log2(e) / 2), and the
-// reciprocal and power of two are the hardware instructions (about 1 ulp):
-// 14 FMA-class operations and 2 transcendental ones.
+// With a = |v| / sqrt 2 and h = 0.5 |v| (1 - erf(a)) >= 0, GELU(v) = v - h for
+// v >= 0 and -h for v < 0, i.e. max(v, 0) - h (no cancellation in the
+// negative tail).  The 0.5 is folded into P's coefficients and 1 / sqrt 2
+// into p, exp(-a^2) = 2^(-v^2 log2(e) / 2), and the reciprocal and power of
+// two are the hardware instructions (about 1 ulp): 12 FMA-class operations
+// and 2 transcendental ones.
 __device__ __forceinline__ float gelu_erf(float v) {
-    const float a = fabsf(v) * 0.70710678118654752440f;
-    const float t = __builtin_amdgcn_rcpf(__builtin_fmaf(0.3275911f, a, 1.0f));
+    const float t = __builtin_amdgcn_rcpf(__builtin_fmaf(fabsf(v), 0.23164188827f, 1.0f));   // p / sqrt 2
     float hp = __builtin_fmaf(t, 0.5307027145f, -0.7265760135f);   // 0.5 * (a5, a4)
     hp = __builtin_fmaf(t, hp, 0.7107068705f);                      // 0.5 * a3
     hp = __builtin_fmaf(t, hp, -0.142248368f);                      // 0.5 * a2
     hp = __builtin_fmaf(t, hp, 0.127414796f);                       // 0.5 * a1
     const float e = __builtin_amdgcn_exp2f(v * v * -0.72134752044448170368f);   // -log2(e) / 2
-    const float h = v * (t * hp) * e;
-    return v >= 0.0f ? v - h : h;
-}
-// ---------------------------------------------------------------------------
+    const float h = fabsf(v) * (t * hp) * e;
+    return fmaxf(v, 0.0f) - h;
+}// ---------------------------------------------------------------------------
 // Tiling constants shared by host and device code.
 // ---------------------------------------------------------------------------
 constexpr int kRouteTile = 256;      // tokens per routing / dispatch tile (one per thread)
@@ -151,7 +150,7 @@ hipError_t launch_gemm(int dtype, const GemmDesc& g, hipStream_t st);
 // top-1 routing.  Shapes outside fused_top1_supported use the GEMM path.
 constexpr int kFusedMaxD = 768;      // x rows of a 64-row tile live in LDS ...
 constexpr int kFusedMaxH = 8192;     // ... beside b1
-constexpr int kFusedMaxRQ = 192;     // [t|u] accumulators live in registers
+constexpr int kFusedMaxRQ = 160;     // [t|u] accumulators live in registers
 bool fused_top1_supported(int D, int H, int r, int q);
 hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, const void* US,
                              const void* Vt, const float* b2, const void* P, const void* Q,
