@@ -35,6 +35,8 @@
 // slice after its first two stages) and waits with vmcnt values computed from
 // that order.  Loads the compiler does see ([Vt;Q_e], b1) are all complete
 // whenever it waits for them, so its own counts never hold back a DMA.
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace clearmoe {
@@ -375,11 +377,10 @@ void k_fused_top1(FusedArgs a) {
         }
     };
     // Run j of the pending slice (hidden units hb + 16 j + 8 lh + i): GELU and
-    // bf16 turn the lane's z values (bias included) into the B operand, and
+    // bf16 turn the lane's z values (bias included) into the B operand zo, and
     // [t|u]^T += [Vt;Q_e]_run z^T_run.  Units >= H have zero [Vt;Q_e] columns.
-    auto run = [&](int j) {
+    auto gelu_run = [&](int j, u32x4 (&zo)[2]) {
         const int qq = j >> 1, v0 = 8 * (j & 1);
-        u32x4 zo[2];
 #pragma unroll
         for (int b = 0; b < 2; ++b)
 #pragma unroll
@@ -387,6 +388,8 @@ void k_fused_top1(FusedArgs a) {
                 const int v = v0 + 2 * i;
                 zo[b][i] = pack_bf16x2(gelu_erf(zp[qq][b][v]), gelu_erf(zp[qq][b][v + 1]));
             }
+    };
+    auto phase2_run = [&](int j, const u32x4 (&zo)[2]) {
 #pragma unroll
         for (int f = 0; f < NFT; ++f)
 #pragma unroll
@@ -410,13 +413,20 @@ void k_fused_top1(FusedArgs a) {
             }
         }
     };
-    // Block k.  Loads issued after stage n: stages n + 1 and n + 2 (16), plus
+    // Block k.  In steps 0..3 the GELU of run g of slice k - 1 is computed and
+    // the [t|u] MFMAs of run g - 1 are issued (one step later, so that a step
+    // holds 26 independent MFMAs next to its GELU arithmetic); run 3's MFMAs
+    // come in step 4, before step 5 reloads vq's second half.
+    // Loads issued after stage n: stages n + 1 and n + 2 (16), plus
     // the halves of [Vt;Q_e] (2 NFT loads each, issued in steps 4 and 5 before
     // that step's stage) that came after stage n.  The stages past the last
     // slice load zeros (every block issues the same loads).
-    auto block = [&](int k, bool p2) {
+    // P2 (compile time) keeps a step's phase-1 and GELU work in one basic
+    // block, where the scheduler can interleave them.
+    auto block = [&](int k, auto p2_tag) {
+        constexpr bool p2 = decltype(p2_tag)::value;
         const int hb = (k * 4 + wave) * kFHid;
-        if (p2) {
+        if constexpr (p2) {
             // the compiler's wait for vq goes here, before this block's DMA
 #pragma unroll
             for (int f = 0; f < NFT; ++f)
@@ -441,6 +451,7 @@ void k_fused_top1(FusedArgs a) {
                 }
             }
         }
+        u32x4 zo_prev[2], zo_cur[2];
 #pragma unroll
         for (int g = 0; g < kgroups; ++g) {
             const int n = k * kgroups + g;
@@ -453,7 +464,21 @@ void k_fused_top1(FusedArgs a) {
                 default: vm_wait<16 + 4 * NFT>(); break;
             }
             step(n, g);
-            if (p2 && g < 4) run(g);
+            if constexpr (p2) {
+                if (g >= 1 && g <= 4) phase2_run(g - 1, zo_prev);
+                if (g < 4) {
+                    gelu_run(g, zo_cur);
+#pragma unroll
+                    for (int b = 0; b < 2; ++b) zo_prev[b] = zo_cur[b];
+                    // spread this step's MFMAs (16, plus 10 from g >= 1) evenly
+                    // over its GELU arithmetic, so the matrix pipe never idles
+#pragma unroll
+                    for (int i = 0; i < 26; ++i) {
+                        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);    // one MFMA
+                        __builtin_amdgcn_sched_group_barrier(0x002, 12, 0);   // twelve VALU
+                    }
+                }
+            }
         }
 #pragma unroll
         for (int qq = 0; qq < 2; ++qq)
@@ -462,11 +487,15 @@ void k_fused_top1(FusedArgs a) {
     };
 
     if (n_iter > 0) {
-        block(0, false);
-        for (int k = 1; k < n_iter; ++k) block(k, true);
+        block(0, std::false_type{});
+        for (int k = 1; k < n_iter; ++k) block(k, std::true_type{});
         // drain: GELU + phase 2 of the last slice
 #pragma unroll
-        for (int j = 0; j < 4; ++j) run(j);
+        for (int j = 0; j < 4; ++j) {
+            u32x4 zo[2];
+            gelu_run(j, zo);
+            phase2_run(j, zo);
+        }
     }
     vm_wait<0>();
 

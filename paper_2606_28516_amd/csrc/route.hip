@@ -100,11 +100,26 @@ __device__ __forceinline__ double topk_gap(const double (&lg)[EP], int E, int k)
     return gap;
 }
 
+// 16 bytes per lane, global -> LDS at m0 + 16 * lane.  Inline asm, issued
+// before any other load of the wave: every later wait of the wave (the
+// compiler's, in issue order) also covers it.
+__device__ __forceinline__ void route_dma16(const void* gptr, uint32_t lds_addr) {
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(lds_addr), "v"(gptr)
+                 : "memory", "m0");
+}
+
+typedef __attribute__((address_space(3))) uint32_t route_lds_word;
+
+// w_lds > 0: the router matrix (E x D, w_lds bytes of dynamic LDS) is copied to
+// LDS for the exact recompute of uncertified tokens.
 template <typename Tin, int EG>
 __global__ __launch_bounds__(kRouteTile) void k_route(
     const Tin* __restrict__ x, const Tin* __restrict__ Wg, const float* __restrict__ bg, int64_t T,
     int D, int E, int k, int32_t* __restrict__ idx, float* __restrict__ gate,
-    int32_t* __restrict__ tile_counts) {
+    int32_t* __restrict__ tile_counts, int w_lds) {
+    extern __shared__ __attribute__((aligned(16))) unsigned char s_w[];
     constexpr int EP = 16 * EG;                      // experts padded to MFMA rows
     constexpr int PER16 = Elem<Tin>::per16;
     constexpr int KS = RouteMfma<Tin>::kstep;
@@ -116,6 +131,19 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
     const int64_t tw = static_cast<int64_t>(blockIdx.x) * kRouteTile + w * 64;  // wave's first token
+
+    if (w_lds > 0) {                               // router rows -> LDS (read after a barrier)
+        const int64_t wbytes = static_cast<int64_t>(E) * D * static_cast<int>(sizeof(Tin));
+        const uint32_t base_l =
+            static_cast<uint32_t>(reinterpret_cast<uintptr_t>((route_lds_word*)s_w));
+        for (int base = w * 64; base * 16 < w_lds; base += kRouteTile) {
+            const int64_t off = static_cast<int64_t>(base + lane) * 16;
+            const void* src = off < wbytes ? static_cast<const void*>(
+                                                 reinterpret_cast<const unsigned char*>(Wg) + off)
+                                           : static_cast<const void*>(g_route_zero);
+            route_dma16(src, __builtin_amdgcn_readfirstlane(base_l + base * 16));
+        }
+    }
 
     f32x4 acc[EG][4], aab[EG][4];
     double lacc[EG][4][4];             // double sums of the float32 partials
@@ -231,6 +259,32 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
         double part[EP];
 #pragma unroll
         for (int e = 0; e < EP; ++e) part[e] = 0.0;
+        if (w_lds > 0) {
+            // router rows from LDS: only the token's x row comes from memory
+            const Tin* wl = reinterpret_cast<const Tin*>(s_w);
+            constexpr int kU = 8;                      // d = lane + 64 i, per lane per round
+            for (int d0 = 0; d0 < D; d0 += 64 * kU) {
+                float xv[kU];
+#pragma unroll
+                for (int i = 0; i < kU; ++i) {
+                    const int d = d0 + lane + 64 * i;
+                    const float xr = Elem<Tin>::load(x, to * D + (d < D ? d : D - 1));
+                    xv[i] = d < D ? xr : 0.0f;
+                }
+#pragma unroll
+                for (int i = 0; i < kU; ++i) {
+                    const int d = d0 + lane + 64 * i;
+                    const int dc = d < D ? d : D - 1;
+#pragma unroll
+                    for (int e = 0; e < EP; ++e) {
+                        const int ec = e < E ? e : E - 1;
+                        part[e] = __builtin_fma(static_cast<double>(xv[i]),
+                                                static_cast<double>(Elem<Tin>::load(wl, ec * D + dc)),
+                                                part[e]);
+                    }
+                }
+            }
+        } else {
         constexpr int kFallU = EP <= 16 ? 4 : 1;   // d = lane + 64 i, per lane per round
         for (int d0 = 0; d0 < D; d0 += 64 * kFallU) {
             // Branch-free: out-of-range columns / experts load a clamped (valid)
@@ -255,6 +309,7 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
                 for (int e = 0; e < EP; ++e)
                     part[e] = __builtin_fma(static_cast<double>(xv[i]), static_cast<double>(wv[i][e]),
                                             part[e]);
+        }
         }
 #pragma unroll
         for (int e = 0; e < EP; ++e) {
@@ -308,18 +363,23 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
     }
 }
 
+constexpr int64_t kRouteWLds = 32 * 1024;
+
 template <typename Tin>
 static hipError_t route_dt(const Tin* x, const Tin* Wg, const float* bg, int64_t T, int D, int E,
                            int k, int32_t* idx, float* gate, int32_t* tc, hipStream_t st) {
     const int64_t blocks = route_tiles(T);
     if (blocks == 0) return hipSuccess;
     const dim3 grid(static_cast<unsigned>(blocks));
+    // the router rows go to LDS when they fit in kRouteWLds (whole 1 KB rounds)
+    const int64_t wbytes = static_cast<int64_t>(E) * D * static_cast<int64_t>(sizeof(Tin));
+    const int w_lds = wbytes <= kRouteWLds ? static_cast<int>((wbytes + 1023) / 1024 * 1024) : 0;
     if (E <= 16)
-        k_route<Tin, 1><<<grid, kRouteTile, 0, st>>>(x, Wg, bg, T, D, E, k, idx, gate, tc);
+        k_route<Tin, 1><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, idx, gate, tc, w_lds);
     else if (E <= 32)
-        k_route<Tin, 2><<<grid, kRouteTile, 0, st>>>(x, Wg, bg, T, D, E, k, idx, gate, tc);
+        k_route<Tin, 2><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, idx, gate, tc, w_lds);
     else
-        k_route<Tin, 4><<<grid, kRouteTile, 0, st>>>(x, Wg, bg, T, D, E, k, idx, gate, tc);
+        k_route<Tin, 4><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, idx, gate, tc, w_lds);
     return hipGetLastError();
 }
 
