@@ -17,7 +17,11 @@ Prints one JSON line.  Besides the contract fields it carries
   dense        the dense fc1 + GELU + fc2 comparator through the same kernels;
   dispatch     the routing/dispatch-only workload (2^20 tokens, D = 384, E = 8,
                top-2, Zipf-skewed bias): route -> dispatch (+ rows) -> combine,
-               with its HBM fraction.
+               with its HBM fraction;
+  imbalance    the dispatch-backend sweep: grouped (clearmoe_ffn_forward)
+               against padded batches (clearmoe_ffn_forward_padded) at 0, 40,
+               60 and 80 % load imbalance, E = 4, DeiT-Small widths, top-1 and
+               top-2, 1568 and 12608 tokens.
 """
 import argparse
 import hashlib
@@ -255,6 +259,7 @@ def main():
                         "tflops": 4 * cfg.T * cfg.D * cfg.H / (dms * 1e-3) / 1e12}
         del W2, yd
         out["dispatch"] = bench_dispatch(cm, synth, torch, np, stream, max(10, args.steps // 10))
+        out["imbalance"] = bench_imbalance(cm, synth, torch, np, stream, max(20, args.steps // 5))
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(L, cfg, args.cpu_seconds)
@@ -330,6 +335,57 @@ def bench_dispatch(cm, synth, torch, np, stream, steps):
             "hbm_frac_moved": moved / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
             "compulsory_GB": compulsory / 1e9, "moved_GB": moved / 1e9,
             "counts": counts.cpu().tolist(), "kernels": kern}
+
+
+def bench_imbalance(cm, synth, torch, np, stream, steps):
+    """Grouped against padded dispatch backends under load imbalance (the
+    paper's dispatch benchmark: E = 4, imbalance 0/40/60/80 %, here at the
+    DeiT-Small widths on MI355X).  Imbalance p draws a share p of the tokens
+    from cluster 0 on top of an even spread (synth.imbalance_mixture); the
+    realised expert loads are reported with each point.  Both backends compute
+    the whole layer; tokens/s is per layer call, host waits included."""
+    D, H, E, r, q = 384, 1536, 4, 128, 32
+    out = []
+    for T in (1568, 12608):
+        for p in (0.0, 0.4, 0.6, 0.8):
+            cfg = synth.LayerConfig(f"imbalance-{round(100 * p)}", T=T, D=D, H=H, E=E, k=1, r=r,
+                                    q=q, dtype="bf16", seed=5, n_cal=4000,
+                                    mixture=synth.imbalance_mixture(E, p))
+            L = synth.make_layer(cfg)
+            d = {n: cm.from_stored(L[n])
+                 for n in ("x", "W1", "b1", "US", "Vt", "b2", "P", "Q", "Wg", "bg")}
+            del L
+            y = torch.empty((T, D), dtype=d["x"].dtype, device=d["x"].device)
+            for k in (1, 2):
+                shape = cm.make_shape(T, D, E, k, cm.BF16, H=H, r=r, q=q)
+                ws = torch.empty(cm.padded_workspace_bytes(shape), dtype=torch.uint8,
+                                 device=y.device)
+                idx = torch.empty((T, k), dtype=torch.int32, device=y.device)
+                row = {"tokens": T, "imbalance": p, "k": k}
+                for name, fwd in (("grouped", cm.ffn_forward), ("padded", cm.ffn_forward_padded)):
+                    def run():
+                        fwd(d["x"], d["W1"], d["b1"], d["US"], d["Vt"], d["b2"], d["P"], d["Q"],
+                            d["Wg"], d["bg"], k, ws=ws, out=y, idx_out=idx)
+                    for _ in range(5):
+                        run()
+                    torch.cuda.synchronize()
+                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    e0.record(stream)
+                    for _ in range(steps):
+                        run()
+                    e1.record(stream)
+                    torch.cuda.synchronize()
+                    ms = e0.elapsed_time(e1) / steps
+                    row[name] = {"ms": ms, "tokens_per_s": T / (ms * 1e-3)}
+                counts = torch.bincount(idx.flatten().long(), minlength=E).cpu().numpy()
+                row["counts"] = counts.tolist()
+                row["padded_rows_over_assignments"] = E * int(counts.max()) / (T * k)
+                row["padded_over_grouped_time"] = row["padded"]["ms"] / row["grouped"]["ms"]
+                out.append(row)
+                del ws, idx
+            del d, y
+    return {"workload": "DeiT-Small widths D=384 H=1536 r=128 q=32 bf16, E=4, seed 5",
+            "steps": steps, "points": out}
 
 
 def cpu_baseline(L, cfg, min_seconds):

@@ -69,8 +69,9 @@ int clearmoe_version(void);
 /* Human-readable name of a status code (static string, never NULL). */
 const char* clearmoe_status_string(int status);
 
-/* Bytes of workspace clearmoe_ffn_forward needs for this shape (the largest of
- * all entry points); 0 if the shape is invalid. */
+/* Bytes of workspace clearmoe_ffn_forward needs for this shape (enough for
+ * every entry point but clearmoe_ffn_forward_padded); 0 if the shape is
+ * invalid. */
 size_t clearmoe_workspace_bytes(const clearmoe_shape* shape);
 
 /* Router and top-k (Sec. III Phase 4 linear router, with the bias counted in
@@ -128,6 +129,32 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
                          int32_t* idx_out, float* gate_out, void* ws, size_t ws_bytes,
                          hipStream_t stream);
 
+/* Bytes of workspace clearmoe_ffn_forward_padded needs for this shape (room
+ * for a padded batch of E * T * k rows); 0 if the shape is invalid. */
+size_t clearmoe_padded_workspace_bytes(const clearmoe_shape* shape);
+
+/* The whole layer through the padded batched backend (Sec. III "Dispatch
+ * Backends", the cuBLAS variant: expert sub-batches padded to the largest and
+ * stacked into one 3-D batch; Sec. IV dispatch benchmark, Table C6).  Same
+ * arguments, layouts and results as clearmoe_ffn_forward, up to rounding
+ * order; it exists to measure what padding costs under imbalanced routing.
+ * Route, dispatch, fc1 + GELU and the shared basis run as in the k > 1 path of
+ * clearmoe_ffn_forward; then, with C the largest expert count, expert e owns
+ * rows [e C, e C + C) of a padded batch, its assignments first and zero rows
+ * after, and the residual products run over all E * C rows (padding rows
+ * included) before the combine reads the real rows back.
+ * The host needs C to size the batch: the call copies the counts to pinned
+ * host memory (one small buffer per calling thread, kept until the process
+ * ends) and waits for them on an event, so it blocks the calling thread until
+ * dispatch has finished on the stream (fc1 and the shared basis are queued
+ * first and overlap the wait), and it cannot be captured into a graph.
+ * ws must hold clearmoe_padded_workspace_bytes(shape). */
+int clearmoe_ffn_forward_padded(const clearmoe_shape* shape, const void* x, const void* W1,
+                                const float* b1, const void* US, const void* Vt, const float* b2,
+                                const void* P, const void* Q, const void* Wg, const float* bg,
+                                void* y, int32_t* idx_out, float* gate_out, void* ws,
+                                size_t ws_bytes, hipStream_t stream);
+
 /* Dense comparator: y = GELU(x W1^T + b1) W2^T + b2, the unexpertised FFN the
  * paper's dense rows time (Table III, D0), run through the same GEMM kernels.
  *   x [T, D]; W1 [H, D], b1 [H]; W2 [D, H], b2 [D]; y [T, D] out (dtype).
@@ -158,7 +185,8 @@ enum {
     CLEARMOE_STAGE_TU = 12,            /* top-1: [t|u] = z[perm] [Vt;Q_e]^T (grouped) */
     CLEARMOE_STAGE_Y = 13,             /* top-1: y[perm] = [t|u] [US|P_e]^T + b2 (grouped) */
     CLEARMOE_STAGE_FUSED_TOP1 = 14,    /* top-1 bf16: fc1+GELU, [t|u] and y in one kernel */
-    CLEARMOE_N_STAGES = 15
+    CLEARMOE_STAGE_PAD_INDEX = 15,     /* padded backend: padded row maps */
+    CLEARMOE_N_STAGES = 16
 };
 
 /* Name of a stage (static string; "?" if out of range). */

@@ -17,7 +17,8 @@ import torch
 __all__ = ["ClearMoEError", "Shape", "lib", "version", "workspace_bytes", "alloc_workspace",
            "route", "dispatch", "combine", "ffn_forward", "from_stored", "to_stored",
            "DISPATCH_HIST_IN_WS", "F32", "BF16", "SYMBOLS", "N_STAGES", "stage_names",
-           "timing_start", "timing_stop", "make_shape", "dense_ffn_forward"]
+           "timing_start", "timing_stop", "make_shape", "dense_ffn_forward",
+           "padded_workspace_bytes", "ffn_forward_padded"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libclearmoe.so")
@@ -26,8 +27,9 @@ DISPATCH_HIST_IN_WS = 1
 SYMBOLS = ("clearmoe_version", "clearmoe_status_string", "clearmoe_workspace_bytes",
            "clearmoe_route", "clearmoe_dispatch", "clearmoe_combine", "clearmoe_ffn_forward",
            "clearmoe_dense_ffn_forward", "clearmoe_stage_name", "clearmoe_timing_start",
-           "clearmoe_timing_stop")
-N_STAGES = 15
+           "clearmoe_timing_stop", "clearmoe_padded_workspace_bytes",
+           "clearmoe_ffn_forward_padded")
+N_STAGES = 16
 
 
 class ClearMoEError(RuntimeError):
@@ -64,6 +66,10 @@ def lib():
         L.clearmoe_combine.argtypes = [sp, vp, vp, vp, vp, vp]
         L.clearmoe_ffn_forward.restype = ctypes.c_int
         L.clearmoe_ffn_forward.argtypes = [sp] + [vp] * 13 + [vp, sz, vp]
+        L.clearmoe_padded_workspace_bytes.restype = sz
+        L.clearmoe_padded_workspace_bytes.argtypes = [sp]
+        L.clearmoe_ffn_forward_padded.restype = ctypes.c_int
+        L.clearmoe_ffn_forward_padded.argtypes = [sp] + [vp] * 13 + [vp, sz, vp]
         L.clearmoe_dense_ffn_forward.restype = ctypes.c_int
         L.clearmoe_dense_ffn_forward.argtypes = [sp] + [vp] * 6 + [vp, sz, vp]
         L.clearmoe_stage_name.restype = ctypes.c_char_p
@@ -175,21 +181,44 @@ def combine(ye, inv, gate, out: Optional[torch.Tensor] = None, stream=None):
     return y
 
 
-def ffn_forward(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int, ws: Optional[torch.Tensor] = None,
-                out: Optional[torch.Tensor] = None, idx_out=None, gate_out=None, stream=None):
-    """clearmoe_ffn_forward: the whole layer.  Returns y [T, D]."""
+def padded_workspace_bytes(shape: Shape) -> int:
+    return int(lib().clearmoe_padded_workspace_bytes(ctypes.byref(shape)))
+
+
+def _layer_call(name, ws_bytes, x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k, ws, out, idx_out,
+                gate_out, stream):
     T, D = x.shape
     H = W1.shape[0]
     r = US.shape[1]
     E, _, q = P.shape
     s = make_shape(T, D, E, k, _dt(x), H=H, r=r, q=q)
-    ws = alloc_workspace(s, x.device) if ws is None else ws
+    if ws is None:
+        n = ws_bytes(s)
+        if n == 0:
+            raise ClearMoEError("invalid shape")
+        ws = torch.empty(n, dtype=torch.uint8, device=x.device)
     y = torch.empty((T, D), dtype=x.dtype, device=x.device) if out is None else out
-    rc = lib().clearmoe_ffn_forward(ctypes.byref(s), _p(x), _p(W1), _p(b1), _p(US), _p(Vt),
-                                    _p(b2), _p(P), _p(Q), _p(Wg), _p(bg), _p(y), _p(idx_out),
-                                    _p(gate_out), _p(ws), ws.numel(), _stream(stream))
-    _check(rc, "clearmoe_ffn_forward")
+    rc = getattr(lib(), name)(ctypes.byref(s), _p(x), _p(W1), _p(b1), _p(US), _p(Vt), _p(b2),
+                              _p(P), _p(Q), _p(Wg), _p(bg), _p(y), _p(idx_out), _p(gate_out),
+                              _p(ws), ws.numel(), _stream(stream))
+    _check(rc, name)
     return y
+
+
+def ffn_forward(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int, ws: Optional[torch.Tensor] = None,
+                out: Optional[torch.Tensor] = None, idx_out=None, gate_out=None, stream=None):
+    """clearmoe_ffn_forward: the whole layer.  Returns y [T, D]."""
+    return _layer_call("clearmoe_ffn_forward", workspace_bytes, x, W1, b1, US, Vt, b2, P, Q, Wg,
+                       bg, k, ws, out, idx_out, gate_out, stream)
+
+
+def ffn_forward_padded(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int,
+                       ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                       idx_out=None, gate_out=None, stream=None):
+    """clearmoe_ffn_forward_padded: the whole layer through the padded batched
+    backend (blocks the host until dispatch is done).  Returns y [T, D]."""
+    return _layer_call("clearmoe_ffn_forward_padded", padded_workspace_bytes, x, W1, b1, US, Vt,
+                       b2, P, Q, Wg, bg, k, ws, out, idx_out, gate_out, stream)
 
 
 def dense_ffn_forward(x, W1, b1, W2, b2, ws: Optional[torch.Tensor] = None,

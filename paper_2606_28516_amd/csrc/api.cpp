@@ -26,6 +26,8 @@ struct Layout {
     size_t counts, offsets, idx, gate, perm, inv;  // ffn_forward
     size_t z, tproj, hsh, u, hres, tu;
     size_t dispatch_end, total;
+    // padded-batch backend only (after total): capacity E * T * k rows
+    size_t perm_pad, inv_pad, seg, u_pad, hres_pad, padded_total;
 };
 
 size_t elem_size(int dtype) { return dtype == CLEARMOE_F32 ? 4 : 2; }
@@ -59,6 +61,15 @@ Layout layout(const clearmoe_shape& s) {
     L.hres = take(sizeof(float) * T * k * s.D);
     L.tu = take(es * T * k * (s.r + s.q));
     L.total = off;
+    // A padded batch holds E sub-batches of the largest expert count, which
+    // can be every assignment: room for E * T * k rows.
+    const int64_t cap = E * T * k;
+    L.perm_pad = take(sizeof(int32_t) * (cap > 0 ? cap : 1));
+    L.inv_pad = take(sizeof(int32_t) * (T * k > 0 ? T * k : 1));
+    L.seg = take(sizeof(int32_t) * (E + 1));
+    L.u_pad = take(es * cap * s.q);
+    L.hres_pad = take(sizeof(float) * cap * s.D);
+    L.padded_total = off;
     return L;
 }
 
@@ -159,6 +170,76 @@ int dispatch_impl(const clearmoe_shape& s, const Layout& L, const int32_t* idx, 
     return CLEARMOE_OK;
 }
 
+// Argument checks of the whole-layer entry points (before any HIP call).
+int check_layer_args(const clearmoe_shape* shape, const void* x, const void* W1, const float* b1,
+                     const void* US, const void* Vt, const float* b2, const void* P, const void* Q,
+                     const void* Wg, const float* bg, const void* y, const int32_t* idx_out,
+                     const float* gate_out) {
+    int rc = check_shape(shape, true);
+    if (rc != CLEARMOE_OK) return rc;
+    const clearmoe_shape& s = *shape;
+    if (!W1 || !Wg || (s.T > 0 && (!x || !y))) return CLEARMOE_ERR_INVALID_ARG;
+    if (s.r > 0 && (!US || !Vt)) return CLEARMOE_ERR_INVALID_ARG;
+    if (s.q > 0 && (!P || !Q)) return CLEARMOE_ERR_INVALID_ARG;
+    const void* v16[] = {x, W1, US, Vt, P, Q, Wg, y};
+    for (const void* p : v16)
+        if (p && !aligned(p, 16)) return CLEARMOE_ERR_INVALID_ARG;
+    const void* v4[] = {b1, b2, bg, idx_out, gate_out};
+    for (const void* p : v4)
+        if (p && !aligned(p, 4)) return CLEARMOE_ERR_INVALID_ARG;
+    return CLEARMOE_OK;
+}
+
+// z = GELU(x W1^T + b1), then the shared basis t = z Vt^T, h_sh = t US^T + b2
+// (all in token order).
+int shared_impl(const clearmoe_shape& s, const void* x, const void* W1, const float* b1,
+                const void* US, const void* Vt, const float* b2, void* z, void* tproj, float* hsh,
+                hipStream_t st) {
+    GemmDesc g = gemm_desc(s.T, s.H, s.D);
+    g.A = x; g.lda = s.D;
+    g.B = W1; g.ldb = s.D;
+    g.C = z; g.ldc = s.H; g.c_f32 = 0;
+    g.bias = b1; g.gelu = 1;
+    CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
+    g = gemm_desc(s.T, s.r, s.H);
+    g.A = z; g.lda = s.H;
+    g.B = Vt; g.ldb = s.H;
+    g.C = tproj; g.ldc = s.r; g.c_f32 = 0;
+    if (s.r > 0) CLEARMOE_STAGE(CLEARMOE_STAGE_BASIS_T, st, launch_gemm(s.dtype, g, st));
+    g = gemm_desc(s.T, s.D, s.r);
+    g.A = tproj; g.lda = s.r;
+    g.B = US; g.ldb = s.r;
+    g.C = hsh; g.ldc = s.D; g.c_f32 = 1;
+    g.bias = b2;
+    CLEARMOE_STAGE(CLEARMOE_STAGE_BASIS_H, st, launch_gemm(s.dtype, g, st));
+    return CLEARMOE_OK;
+}
+
+// Residual over row segments seg[0..E] of a row order given by rows (-1 =
+// padding row, which reads zeros):  u = gate * (z[rows/k] Q_e^T) ;
+// h_res = u P_e^T  (M rows in all).
+int residual_impl(const clearmoe_shape& s, int64_t M, const void* z, const int32_t* rows,
+                  const int32_t* seg, const float* gate, const void* P, const void* Q, void* u,
+                  float* hres, hipStream_t st) {
+    GemmDesc g = gemm_desc(M, s.q, s.H);
+    g.A = z; g.lda = s.H; g.a_rows = rows; g.a_div = s.k;
+    g.B = Q; g.ldb = s.H; g.b_seg_stride = static_cast<int64_t>(s.q) * s.H;
+    g.C = u; g.ldc = s.q; g.c_f32 = 0;
+    g.row_scale = gate; g.scale_rows = rows;
+    g.seg_offsets = seg; g.nseg = s.E;
+    if (s.q > 0) CLEARMOE_STAGE(CLEARMOE_STAGE_RES_U, st, launch_gemm(s.dtype, g, st));
+    g = gemm_desc(M, s.D, s.q);
+    g.A = u; g.lda = s.q;
+    g.B = P; g.ldb = s.q; g.b_seg_stride = static_cast<int64_t>(s.D) * s.q;
+    g.C = hres; g.ldc = s.D; g.c_f32 = 1;
+    g.seg_offsets = seg; g.nseg = s.E;
+    CLEARMOE_STAGE(CLEARMOE_STAGE_RES_H, st, launch_gemm(s.dtype, g, st));
+    return CLEARMOE_OK;
+}
+
+// Pinned host copy of the expert counts (padded backend), one per thread.
+thread_local int32_t* t_host_counts = nullptr;
+
 }  // namespace
 
 extern "C" {
@@ -243,18 +324,9 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
                          const void* P, const void* Q, const void* Wg, const float* bg, void* y,
                          int32_t* idx_out, float* gate_out, void* ws, size_t ws_bytes,
                          hipStream_t stream) {
-    int rc = check_shape(shape, true);
+    int rc = check_layer_args(shape, x, W1, b1, US, Vt, b2, P, Q, Wg, bg, y, idx_out, gate_out);
     if (rc != CLEARMOE_OK) return rc;
     const clearmoe_shape& s = *shape;
-    if (!W1 || !Wg || (s.T > 0 && (!x || !y))) return CLEARMOE_ERR_INVALID_ARG;
-    if (s.r > 0 && (!US || !Vt)) return CLEARMOE_ERR_INVALID_ARG;
-    if (s.q > 0 && (!P || !Q)) return CLEARMOE_ERR_INVALID_ARG;
-    const void* v16[] = {x, W1, US, Vt, P, Q, Wg, y};
-    for (const void* p : v16)
-        if (p && !aligned(p, 16)) return CLEARMOE_ERR_INVALID_ARG;
-    const void* v4[] = {b1, b2, bg, idx_out, gate_out};
-    for (const void* p : v4)
-        if (p && !aligned(p, 4)) return CLEARMOE_ERR_INVALID_ARG;
     const Layout L = layout(s);
     if (!ws || !aligned(ws, kAlign) || ws_bytes < L.total) return CLEARMOE_ERR_WORKSPACE;
     if (s.T == 0) return CLEARMOE_OK;
@@ -287,15 +359,15 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
         return CLEARMOE_OK;
     }
 
-    // 3. z = GELU(x W1^T + b1), token order
-    GemmDesc g = gemm_desc(T, s.H, s.D);
-    g.A = x; g.lda = s.D;
-    g.B = W1; g.ldb = s.D;
-    g.C = z; g.ldc = s.H; g.c_f32 = 0;
-    g.bias = b1; g.gelu = 1;
-    CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
-
     if (s.k == 1) {
+        // 3. z = GELU(x W1^T + b1), token order
+        GemmDesc g = gemm_desc(T, s.H, s.D);
+        g.A = x; g.lda = s.D;
+        g.B = W1; g.ldb = s.D;
+        g.C = z; g.ldc = s.H; g.c_f32 = 0;
+        g.bias = b1; g.gelu = 1;
+        CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
+
         // Top-1: every row p of the expert order is one token, so the shared
         // basis and the residual merge into two grouped products over p:
         //   [t | u](p) = z[perm p] [Vt ; Q_e]^T, the u columns scaled by the gate;
@@ -324,37 +396,93 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
         return CLEARMOE_OK;
     }
 
-    // 4. shared basis: t = z Vt^T ; h_sh = t US^T + b2
-    g = gemm_desc(T, s.r, s.H);
-    g.A = z; g.lda = s.H;
-    g.B = Vt; g.ldb = s.H;
-    g.C = tproj; g.ldc = s.r; g.c_f32 = 0;
-    if (s.r > 0) CLEARMOE_STAGE(CLEARMOE_STAGE_BASIS_T, st, launch_gemm(s.dtype, g, st));
-    g = gemm_desc(T, s.D, s.r);
-    g.A = tproj; g.lda = s.r;
-    g.B = US; g.ldb = s.r;
-    g.C = hsh; g.ldc = s.D; g.c_f32 = 1;
-    g.bias = b2;
-    CLEARMOE_STAGE(CLEARMOE_STAGE_BASIS_H, st, launch_gemm(s.dtype, g, st));
-
-    // 5. residual, grouped by expert: u = gate * (z[perm/k] Q_e^T) ; h_res = u P_e^T
-    g = gemm_desc(A, s.q, s.H);
-    g.A = z; g.lda = s.H; g.a_rows = perm; g.a_div = s.k;
-    g.B = Q; g.ldb = s.H; g.b_seg_stride = static_cast<int64_t>(s.q) * s.H;
-    g.C = u; g.ldc = s.q; g.c_f32 = 0;
-    g.row_scale = gate; g.scale_rows = perm;
-    g.seg_offsets = offsets; g.nseg = s.E;
-    if (s.q > 0) CLEARMOE_STAGE(CLEARMOE_STAGE_RES_U, st, launch_gemm(s.dtype, g, st));
-    g = gemm_desc(A, s.D, s.q);
-    g.A = u; g.lda = s.q;
-    g.B = P; g.ldb = s.q; g.b_seg_stride = static_cast<int64_t>(s.D) * s.q;
-    g.C = hres; g.ldc = s.D; g.c_f32 = 1;
-    g.seg_offsets = offsets; g.nseg = s.E;
-    CLEARMOE_STAGE(CLEARMOE_STAGE_RES_H, st, launch_gemm(s.dtype, g, st));
-
+    // 3. z = GELU(x W1^T + b1); 4. shared basis t = z Vt^T, h_sh = t US^T + b2
+    rc = shared_impl(s, x, W1, b1, US, Vt, b2, z, tproj, hsh, st);
+    if (rc != CLEARMOE_OK) return rc;
+    // 5. residual, grouped by expert (segments = the dispatch offsets)
+    rc = residual_impl(s, A, z, perm, offsets, gate, P, Q, u, hres, st);
+    if (rc != CLEARMOE_OK) return rc;
     // 6. y[t] = h_sh[t] + sum_j h_res[inv[t*k+j]]
     CLEARMOE_STAGE(CLEARMOE_STAGE_COMBINE_RES, st,
-                   launch_combine_residual(s.dtype, hsh, hres, inv, y, T, s.D, s.k, st));
+                   launch_combine_residual(s.dtype, hsh, hres, inv, y, T, s.D, s.k, A, st));
+    return CLEARMOE_OK;
+}
+
+size_t clearmoe_padded_workspace_bytes(const clearmoe_shape* shape) {
+    if (check_shape(shape, true) != CLEARMOE_OK) return 0;
+    return layout(*shape).padded_total;
+}
+
+int clearmoe_ffn_forward_padded(const clearmoe_shape* shape, const void* x, const void* W1,
+                                const float* b1, const void* US, const void* Vt, const float* b2,
+                                const void* P, const void* Q, const void* Wg, const float* bg,
+                                void* y, int32_t* idx_out, float* gate_out, void* ws,
+                                size_t ws_bytes, hipStream_t stream) {
+    int rc = check_layer_args(shape, x, W1, b1, US, Vt, b2, P, Q, Wg, bg, y, idx_out, gate_out);
+    if (rc != CLEARMOE_OK) return rc;
+    const clearmoe_shape& s = *shape;
+    const Layout L = layout(s);
+    if (!ws || !aligned(ws, kAlign) || ws_bytes < L.padded_total) return CLEARMOE_ERR_WORKSPACE;
+    if (s.T == 0) return CLEARMOE_OK;
+
+    hipStream_t st = stream;
+    const int64_t T = s.T, A = T * s.k;
+    int32_t* idx = idx_out ? idx_out : at<int32_t>(ws, L.idx);
+    float* gate = gate_out ? gate_out : at<float>(ws, L.gate);
+    int32_t* counts = at<int32_t>(ws, L.counts);
+    int32_t* offsets = at<int32_t>(ws, L.offsets);
+    int32_t* perm = at<int32_t>(ws, L.perm);
+    int32_t* inv = at<int32_t>(ws, L.inv);
+    int32_t* perm_pad = at<int32_t>(ws, L.perm_pad);
+    int32_t* inv_pad = at<int32_t>(ws, L.inv_pad);
+    int32_t* seg = at<int32_t>(ws, L.seg);
+    float* hsh = at<float>(ws, L.hsh);
+    float* hres_pad = at<float>(ws, L.hres_pad);
+
+    rc = route_impl(s, L, x, Wg, bg, idx, gate, ws, st);
+    if (rc != CLEARMOE_OK) return rc;
+    rc = dispatch_impl(s, L, idx, ws, counts, offsets, perm, inv, nullptr, nullptr, true, st);
+    if (rc != CLEARMOE_OK) return rc;
+    // The batch height is the largest expert count, which the host needs to
+    // size the batched launches: copy the counts out, and overlap the round
+    // trip with the shared stages.
+    if (t_host_counts == nullptr &&
+        hipHostMalloc(reinterpret_cast<void**>(&t_host_counts), 64 * sizeof(int32_t)) !=
+            hipSuccess) {
+        t_host_counts = nullptr;
+        return CLEARMOE_ERR_HIP;
+    }
+    hipEvent_t ready = nullptr;
+    if (hipEventCreateWithFlags(&ready, hipEventDisableTiming) != hipSuccess)
+        return CLEARMOE_ERR_HIP;
+    struct EventGuard {
+        hipEvent_t e;
+        ~EventGuard() { (void)hipEventDestroy(e); }
+    } guard{ready};
+    if (hipMemcpyAsync(t_host_counts, counts, sizeof(int32_t) * s.E, hipMemcpyDeviceToHost, st) !=
+            hipSuccess ||
+        hipEventRecord(ready, st) != hipSuccess)
+        return CLEARMOE_ERR_HIP;
+    rc = shared_impl(s, x, W1, b1, US, Vt, b2, at<void>(ws, L.z), at<void>(ws, L.tproj), hsh, st);
+    if (rc != CLEARMOE_OK) return rc;
+    if (hipEventSynchronize(ready) != hipSuccess) return CLEARMOE_ERR_HIP;
+    int64_t C = 0;
+    for (int e = 0; e < s.E; ++e)
+        if (t_host_counts[e] > C) C = t_host_counts[e];
+    if (C < 1 || C > A) return CLEARMOE_ERR_HIP;   // counts sum to A > 0
+
+    // E sub-batches of C rows each (padding rows gather nothing and are
+    // carried through both products as zero rows)
+    CLEARMOE_STAGE(CLEARMOE_STAGE_PAD_INDEX, st,
+                   launch_pad_index(idx, counts, offsets, perm, inv, A, s.E, C, perm_pad, inv_pad,
+                                    seg, st));
+    const int64_t M = static_cast<int64_t>(s.E) * C;
+    rc = residual_impl(s, M, at<void>(ws, L.z), perm_pad, seg, gate, P, Q, at<void>(ws, L.u_pad),
+                       hres_pad, st);
+    if (rc != CLEARMOE_OK) return rc;
+    CLEARMOE_STAGE(CLEARMOE_STAGE_COMBINE_RES, st,
+                   launch_combine_residual(s.dtype, hsh, hres_pad, inv_pad, y, T, s.D, s.k, M,
+                                           st));
     return CLEARMOE_OK;
 }
 
@@ -392,7 +520,7 @@ const char* clearmoe_stage_name(int stage) {
     static const char* names[CLEARMOE_N_STAGES] = {
         "route", "tile_hist", "scan", "permute", "combine", "fc1_gelu",
         "basis_t", "basis_h", "res_u", "res_h", "combine_res", "dense_fc2", "tu_grouped",
-        "y_grouped", "fused_top1"};
+        "y_grouped", "fused_top1", "pad_index"};
     return (stage >= 0 && stage < CLEARMOE_N_STAGES) ? names[stage] : "?";
 }
 

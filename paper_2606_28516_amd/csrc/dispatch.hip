@@ -318,9 +318,9 @@ __global__ __launch_bounds__(256) void k_combine_residual(const float* __restric
                                                           const float* __restrict__ hres,
                                                           const int32_t* __restrict__ inv,
                                                           T* __restrict__ y, int64_t Tn, int D,
-                                                          int k) {
+                                                          int k, int64_t hres_rows) {
     const int ppr = D / 4;
-    const int64_t n = Tn * ppr, A = Tn * k;
+    const int64_t n = Tn * ppr, A = hres_rows;
     const int64_t base = static_cast<int64_t>(blockIdx.x) * 256 * kCombineU + threadIdx.x;
     float4 a[kCombineU];
 #pragma unroll
@@ -421,16 +421,54 @@ hipError_t launch_combine_gated(int dtype, const void* ye, const int32_t* inv, c
 
 hipError_t launch_combine_residual(int dtype, const float* hsh, const float* hres,
                                    const int32_t* inv, void* y, int64_t T, int D, int k,
-                                   hipStream_t st) {
+                                   int64_t hres_rows, hipStream_t st) {
     const int64_t n = T * (D / 4);
     if (n == 0) return hipSuccess;
     const unsigned blocks = static_cast<unsigned>((n + 256 * kCombineU - 1) / (256 * kCombineU));
     if (dtype == 0)
         k_combine_residual<float><<<blocks, 256, 0, st>>>(hsh, hres, inv, static_cast<float*>(y),
-                                                           T, D, k);
+                                                           T, D, k, hres_rows);
     else
-        k_combine_residual<bf16_bits><<<blocks, 256, 0, st>>>(hsh, hres, inv,
-                                                               static_cast<bf16_bits*>(y), T, D, k);
+        k_combine_residual<bf16_bits><<<blocks, 256, 0, st>>>(
+            hsh, hres, inv, static_cast<bf16_bits*>(y), T, D, k, hres_rows);
+    return hipGetLastError();
+}
+
+// Padded batches: expert e owns rows [e C, e C + C) of the padded order.
+//   perm_pad[e C + i] = perm[offsets[e] + i] for i < counts[e], else -1;
+//   inv_pad[a] = e C + (inv[a] - offsets[e]) with e = idx[a];
+//   seg[e] = e C (e = 0..E).
+__global__ __launch_bounds__(256) void k_pad_index(const int32_t* __restrict__ idx,
+                                                   const int32_t* __restrict__ counts,
+                                                   const int32_t* __restrict__ offsets,
+                                                   const int32_t* __restrict__ perm,
+                                                   const int32_t* __restrict__ inv, int64_t A, int E,
+                                                   int64_t C, int32_t* __restrict__ perm_pad,
+                                                   int32_t* __restrict__ inv_pad,
+                                                   int32_t* __restrict__ seg) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    const int64_t npad = static_cast<int64_t>(E) * C;
+    if (i < npad) {
+        const int e = static_cast<int>(i / C);
+        const int64_t r = i - static_cast<int64_t>(e) * C;
+        perm_pad[i] = r < counts[e] ? perm[offsets[e] + r] : -1;
+    }
+    if (i < A) {
+        const int e = idx[i];
+        inv_pad[i] = (e >= 0 && e < E) ? static_cast<int32_t>(static_cast<int64_t>(e) * C + inv[i] - offsets[e])
+                                       : -1;
+    }
+    if (i <= E) seg[i] = static_cast<int32_t>(i * C);
+}
+
+hipError_t launch_pad_index(const int32_t* idx, const int32_t* counts, const int32_t* offsets,
+                            const int32_t* perm, const int32_t* inv, int64_t A, int E, int64_t C,
+                            int32_t* perm_pad, int32_t* inv_pad, int32_t* seg, hipStream_t st) {
+    int64_t n = static_cast<int64_t>(E) * C;
+    if (A > n) n = A;
+    if (E + 1 > n) n = E + 1;
+    const unsigned blocks = static_cast<unsigned>((n + 255) / 256);
+    k_pad_index<<<blocks, 256, 0, st>>>(idx, counts, offsets, perm, inv, A, E, C, perm_pad, inv_pad, seg);
     return hipGetLastError();
 }
 

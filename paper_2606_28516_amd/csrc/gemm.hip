@@ -163,8 +163,9 @@ __global__ __launch_bounds__(256) void k_gemm(GemmDesc g, int mtiles, int ntiles
         const int64_t m = m_lo + r;
         arow[i] = nullptr;
         if (m < m_hi) {
-            const int64_t src = g.a_rows != nullptr ? static_cast<int64_t>(g.a_rows[m] / g.a_div) : m;
-            arow[i] = A + src * g.lda;
+            // a negative gather index is a padding row: it reads zeros
+            const int64_t src = g.a_rows != nullptr ? static_cast<int64_t>(g.a_rows[m]) : m;
+            if (src >= 0) arow[i] = A + (g.a_rows != nullptr ? src / g.a_div : src) * g.lda;
         }
         achunk[i] = cpos ^ swz(r);
     }
@@ -287,8 +288,11 @@ __global__ __launch_bounds__(256) void k_gemm(GemmDesc g, int mtiles, int ntiles
         for (int v = 0; v < 16; ++v) {
             const int64_t m = m_lo + wm * WTM + i * 32 + 8 * (v >> 2) + 4 * lhalf + (v & 3);
             const bool in = m < m_hi;
-            rs[i][v] = (g.row_scale != nullptr && in) ? g.row_scale[g.scale_rows[m]] : 1.0f;
-            crow[i][v] = !in ? -1 : (g.c_rows != nullptr ? static_cast<int64_t>(g.c_rows[m] / g.c_div) : m);
+            const int32_t sr = (g.row_scale != nullptr && in) ? g.scale_rows[m] : 0;
+            rs[i][v] = g.row_scale == nullptr || !in ? 1.0f : (sr >= 0 ? g.row_scale[sr] : 0.0f);
+            // a negative scatter index is a padding row: it is not stored
+            const int64_t cr = !in ? -1 : (g.c_rows != nullptr ? static_cast<int64_t>(g.c_rows[m]) : m);
+            crow[i][v] = cr < 0 ? -1 : (g.c_rows != nullptr ? cr / g.c_div : cr);
         }
 #pragma unroll
     for (int i = 0; i < TM; ++i) {

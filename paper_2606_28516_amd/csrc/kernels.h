@@ -93,10 +93,16 @@ constexpr int64_t kInlineScanMax = 8192;
 // y[t] = sum_j gate[t,j] ye[inv[t*k+j]]  (ye, y in dtype).
 hipError_t launch_combine_gated(int dtype, const void* ye, const int32_t* inv, const float* gate,
                                 void* y, int64_t T, int D, int k, hipStream_t st);
-// y[t] = hsh[t] + sum_j hres[inv[t*k+j]]  (hsh, hres float32; y in dtype).
+// y[t] = hsh[t] + sum_j hres[inv[t*k+j]]  (hsh, hres float32; y in dtype);
+// hres has hres_rows rows (other positions count as zero rows).
 hipError_t launch_combine_residual(int dtype, const float* hsh, const float* hres,
                                    const int32_t* inv, void* y, int64_t T, int D, int k,
-                                   hipStream_t st);
+                                   int64_t hres_rows, hipStream_t st);
+// Index maps of the padded-batch backend (expert e owns rows [e C, e C + C)):
+// perm_pad [E C] (-1 = padding), inv_pad [A], seg [E + 1] = e C.
+hipError_t launch_pad_index(const int32_t* idx, const int32_t* counts, const int32_t* offsets,
+                            const int32_t* perm, const int32_t* inv, int64_t A, int E, int64_t C,
+                            int32_t* perm_pad, int32_t* inv_pad, int32_t* seg, hipStream_t st);
 
 // NT GEMM  C[crow(m), n] = epi( sum_k A[arow(m), k] B_seg(m)[n, k] ).
 // B may come in two parts: rows n >= n_split from B1 (row n - n_split), or

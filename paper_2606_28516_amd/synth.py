@@ -36,7 +36,7 @@ from typing import Optional, Sequence
 import numpy as np
 
 __all__ = ["LayerConfig", "CONFIGS", "DISPATCH_CONFIG", "make_layer", "make_dispatch",
-           "to_bf16_bits", "bf16_bits_to_f32", "fingerprint"]
+           "to_bf16_bits", "bf16_bits_to_f32", "fingerprint", "imbalance_mixture"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -99,6 +99,18 @@ def _store(a: np.ndarray, dtype: str) -> np.ndarray:
     if dtype == "bf16":
         return to_bf16_bits(a)
     raise ValueError(f"unknown dtype {dtype!r}")
+
+
+def imbalance_mixture(E: int, p: float) -> tuple:
+    """Cluster mixture of the dispatch benchmark's imbalance level p in [0, 1):
+    a share p of the tokens comes from cluster 0 on top of an even spread of
+    the rest, i.e. weights (p + (1 - p) / E, (1 - p) / E, ...).  p = 0 is the
+    balanced load.  (The paper sweeps 0/40/60/80 % imbalance without defining
+    the term; this is the reading the benchmark and tests use.)"""
+    if not 0.0 <= p < 1.0 or E < 1:
+        raise ValueError("imbalance must be in [0, 1) and E >= 1")
+    rest = (1.0 - p) / E
+    return tuple([p + rest] + [rest] * (E - 1))
 
 
 def _unit_rows(g: np.ndarray) -> np.ndarray:

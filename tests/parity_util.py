@@ -21,13 +21,16 @@ def layer_to_device(L):
     return {n: dev(L[n]) for n in ("x", "W1", "b1", "US", "Vt", "b2", "P", "Q", "Wg", "bg")}
 
 
-def gpu_ffn(L, ws=None, with_routing=True):
+def gpu_ffn(L, ws=None, with_routing=True, padded=False):
+    """The whole layer through clearmoe_ffn_forward (or, with padded=True,
+    clearmoe_ffn_forward_padded)."""
     d = layer_to_device(L)
     T, k = L["cfg"].T, L["cfg"].k
     idx = torch.empty((T, k), dtype=torch.int32, device="cuda") if with_routing else None
     gate = torch.empty((T, k), dtype=torch.float32, device="cuda") if with_routing else None
-    y = cm.ffn_forward(d["x"], d["W1"], d["b1"], d["US"], d["Vt"], d["b2"], d["P"], d["Q"],
-                       d["Wg"], d["bg"], k, ws=ws, idx_out=idx, gate_out=gate)
+    fwd = cm.ffn_forward_padded if padded else cm.ffn_forward
+    y = fwd(d["x"], d["W1"], d["b1"], d["US"], d["Vt"], d["b2"], d["P"], d["Q"], d["Wg"],
+            d["bg"], k, ws=ws, idx_out=idx, gate_out=gate)
     torch.cuda.synchronize()
     out = dict(y=oracle.widen(cm.to_stored(y)))
     if with_routing:

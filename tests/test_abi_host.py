@@ -132,3 +132,26 @@ def test_binding_signatures_match_header():
     for name, n in protos.items():
         argtypes = getattr(L, name).argtypes
         assert len(argtypes or []) == n, (name, len(argtypes or []), n)
+
+
+def test_padded_entry_point_workspace_and_rejections():
+    L = cm.lib()
+    s = _shape()
+    n = cm.workspace_bytes(s)
+    npad = cm.padded_workspace_bytes(s)
+    # room for E * T * k padded rows of u (dtype) and h_res (float32) on top
+    # of the grouped workspace
+    E, T, k, D, q = s.E, s.T, s.k, s.D, s.q
+    assert npad >= n + E * T * k * (2 * q + 4 * D)
+    assert cm.padded_workspace_bytes(_shape(k=5)) == 0
+    assert cm.padded_workspace_bytes(_shape(T=2 * s.T)) > npad
+    args = [FAKE] * 13
+    a = list(args)
+    a[1] = None                                                    # NULL W1
+    assert L.clearmoe_ffn_forward_padded(ctypes.byref(s), *a, FAKE, npad, None) == 1
+    assert L.clearmoe_ffn_forward_padded(ctypes.byref(_shape(q=6)), *args, FAKE, npad,
+                                         None) == 1
+    # the grouped workspace is not enough for the padded batch
+    assert L.clearmoe_ffn_forward_padded(ctypes.byref(s), *args, FAKE, n, None) == 3
+    assert L.clearmoe_ffn_forward_padded(ctypes.byref(s), *args, FAKE, npad - 1, None) == 3
+    assert L.clearmoe_ffn_forward_padded(ctypes.byref(s), *args, None, npad, None) == 3

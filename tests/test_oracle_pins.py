@@ -349,3 +349,21 @@ def test_svd_tail_experts_are_scaled_tail():
         R = oracle.widen(L["P"])[e] @ oracle.widen(L["Q"])[e]
         assert np.max(np.abs(R - L["s"][e] * tail)) < 1e-6
     assert np.all(np.abs(L["s"] - 1.0) < 0.2)
+
+
+def test_imbalance_mixture_recipe():
+    """The load-imbalance recipe of the dispatch benchmark: balanced at 0,
+    cluster 0 holding p + (1 - p) / E of the mass at p, and the oracle's
+    routing of a draw follows it (the router rows point at the centres)."""
+    assert synth.imbalance_mixture(4, 0.0) == (0.25, 0.25, 0.25, 0.25)
+    w = synth.imbalance_mixture(4, 0.8)
+    assert abs(sum(w) - 1.0) < 1e-12 and abs(w[0] - 0.85) < 1e-12
+    assert all(abs(v - 0.05) < 1e-12 for v in w[1:])
+    with pytest.raises(ValueError):
+        synth.imbalance_mixture(4, 1.0)
+    cfg = synth.LayerConfig("imb", T=4000, D=32, H=32, E=4, k=1, r=8, q=8, dtype="f32", seed=3,
+                            mixture=w, n_cal=500)
+    L = synth.make_layer(cfg)
+    idx, _, _ = oracle.route(L["x"], L["Wg"], L["bg"], 1)
+    share = np.bincount(idx[:, 0], minlength=4) / 4000.0
+    assert abs(share.max() - 0.85) < 0.05, share
