@@ -23,6 +23,11 @@
  *   residual      Eq. (2) residual term; Algorithm 3 per-expert step, here
  *                 token by token with a mask (the paper's Naive backend style)
  *   output        Algorithm 3 last step, y = h_sh + h_res
+ *   adaptive      Sec. III Phase 4 "Adaptive" router: top-1, escalated to
+ *                 top-2 when the router's confidence is below a threshold
+ *   MLP router    Sec. III Phase 4 "MLP" router (one hidden layer of width
+ *                 d/6; Table C5's 149,400 parameters over six layers): the
+ *                 hidden layer is ref_fc1_gelu applied to the router weights
  *
  * Readings where the paper is silent (router bias, tie-break, gate weighting,
  * stable order, b2 placement, exact-erf GELU, low-rank residual factors) are
@@ -95,15 +100,19 @@ void ref_topk(int64_t T, int E, int k, const double* logits, int32_t* idx, doubl
 /* Dispatch by direct counting.  Assignment a = t*k + j goes to expert idx[a].
  * counts[e] = #{a : idx[a] = e};  offsets[0] = 0, offsets[e+1] = offsets[e] + counts[e];
  * perm lists, expert by expert, the assignments of that expert in ascending a
- * (a stable sort by expert); inv is the inverse of perm.  Returns -1 if an
- * index is outside [0, E), else 0. */
+ * (a stable sort by expert); inv is the inverse of perm.  idx[a] = -1 is an
+ * empty slot (a token the adaptive router left at top-1): it is in no
+ * sub-batch, inv[a] = -1, and perm ends with -1 entries after the
+ * offsets[E] assignments.  Returns -1 if an index is below -1 or >= E, else 0. */
 int ref_dispatch(int64_t T, int E, int k, const int32_t* idx, int32_t* counts,
                  int32_t* offsets, int32_t* perm, int32_t* inv) {
     const int64_t A = T * k;
     for (int e = 0; e < E; ++e) counts[e] = 0;
     for (int64_t a = 0; a < A; ++a) {
-        if (idx[a] < 0 || idx[a] >= E) return -1;
-        counts[idx[a]]++;
+        if (idx[a] < -1 || idx[a] >= E) return -1;
+        if (idx[a] >= 0) counts[idx[a]]++;
+        inv[a] = -1;
+        perm[a] = -1;
     }
     offsets[0] = 0;
     for (int e = 0; e < E; ++e) offsets[e + 1] = offsets[e] + counts[e];
@@ -114,10 +123,49 @@ int ref_dispatch(int64_t T, int E, int k, const int32_t* idx, int32_t* counts,
     return 0;
 }
 
-/* Row copy into expert order: xperm[p, :] = x[perm[p] / k, :]. */
+/* Adaptive router (Sec. III Phase 4): the confidence of a token is its
+ * largest softmax probability over all E logits,
+ * p = 1 / sum_e exp(l_e - l_max).  If p >= tau the token stays top-1
+ * (idx = (best, -1), gate = (1, 0)); otherwise it is escalated to top-2 with
+ * the two selected logits' softmax renormalised, exactly as ref_topk with
+ * k = 2.  idx, gate are [T, 2]. */
+void ref_adaptive_topk(int64_t T, int E, double tau, const double* logits, int32_t* idx,
+                       double* gate) {
+    if (E == 1) {                        /* one expert: always confident */
+        for (int64_t t = 0; t < T; ++t) {
+            idx[t * 2] = 0;
+            idx[t * 2 + 1] = -1;
+            gate[t * 2] = 1.0;
+            gate[t * 2 + 1] = 0.0;
+        }
+        return;
+    }
+    ref_topk(T, E, 2, logits, idx, gate);
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t) {
+        const double* l = logits + t * E;
+        double lmax = l[0];
+        for (int e = 1; e < E; ++e)
+            if (l[e] > lmax) lmax = l[e];
+        double den = 0.0;
+        for (int e = 0; e < E; ++e) den += exp(l[e] - lmax);
+        if (1.0 / den >= tau) {
+            idx[t * 2 + 1] = -1;
+            gate[t * 2] = 1.0;
+            gate[t * 2 + 1] = 0.0;
+        }
+    }
+}
+
+/* Row copy into expert order: xperm[p, :] = x[perm[p] / k, :] (zero rows
+ * for the -1 entries after the assignments). */
 void ref_permute_rows(int64_t T, int D, int k, const double* x, const int32_t* perm, double* xperm) {
-    for (int64_t p = 0; p < T * k; ++p)
-        memcpy(xperm + p * D, x + (int64_t)(perm[p] / k) * D, sizeof(double) * (size_t)D);
+    for (int64_t p = 0; p < T * k; ++p) {
+        if (perm[p] < 0)
+            memset(xperm + p * D, 0, sizeof(double) * (size_t)D);
+        else
+            memcpy(xperm + p * D, x + (int64_t)(perm[p] / k) * D, sizeof(double) * (size_t)D);
+    }
 }
 
 /* z[t,h] = GELU(sum_d x[t,d] W1[h,d] + b1[h])  (b1 may be NULL). */
@@ -166,6 +214,7 @@ void ref_residual(int64_t T, int D, int H, int E, int k, int q, const double* z,
         for (int d = 0; d < D; ++d) hres[t * D + d] = 0.0;
         for (int j = 0; j < k; ++j) {
             const int e = idx[t * k + j];
+            if (e < 0) continue;                      /* empty slot (adaptive top-1) */
             const double g = gate[t * k + j];
             const double* Qe = Q + (int64_t)e * q * H;
             const double* Pe = P + (int64_t)e * D * q;
@@ -216,14 +265,17 @@ int ref_ffn_forward(int64_t T, int D, int H, int E, int k, int r, int q,
 }
 
 /* Inverse-permute combine: y[t,:] = sum_j gate[t,j] * ye[inv[t*k+j], :]
- * (ye in expert order, one row per assignment). */
+ * (ye in expert order, one row per assignment; inv = -1 is an empty slot). */
 void ref_combine(int64_t T, int D, int k, const double* ye, const int32_t* inv,
                  const double* gate, double* y) {
 #pragma omp parallel for schedule(static)
     for (int64_t t = 0; t < T; ++t)
         for (int d = 0; d < D; ++d) {
             double s = 0.0;
-            for (int j = 0; j < k; ++j) s += gate[t * k + j] * ye[(int64_t)inv[t * k + j] * D + d];
+            for (int j = 0; j < k; ++j) {
+                if (inv[t * k + j] < 0) continue;
+                s += gate[t * k + j] * ye[(int64_t)inv[t * k + j] * D + d];
+            }
             y[t * D + d] = s;
         }
 }

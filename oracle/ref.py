@@ -20,7 +20,9 @@ _lib = None
 
 __all__ = ["build", "lib", "widen", "num_threads", "set_num_threads", "gelu", "router_logits",
            "topk", "route", "dispatch", "permute_rows", "fc1_gelu", "shared", "residual",
-           "ffn_forward", "ffn_forward_layer", "combine", "margins"]
+           "ffn_forward", "ffn_forward_layer", "combine", "margins", "adaptive_topk",
+           "round_to_storage", "mlp_router_logits", "route_layer", "ffn_forward_routed",
+           "confidence"]
 
 
 def build(force: bool = True) -> str:
@@ -57,6 +59,7 @@ def lib():
         L.ref_ffn_forward.argtypes = [i64] + [i32] * 6 + [dp] * 10 + [dp, ip, dp, dp]
         L.ref_ffn_forward.restype = i32
         L.ref_combine.argtypes = [i64, i32, i32, dp, ip, dp, dp]
+        L.ref_adaptive_topk.argtypes = [i64, i32, ctypes.c_double, dp, ip, dp]
         _lib = L
     return _lib
 
@@ -111,6 +114,62 @@ def topk(logits, k: int):
     gate = np.empty((T, k))
     lib().ref_topk(T, E, k, _dp(logits), _ip(idx), _dp(gate))
     return idx, gate
+
+
+def adaptive_topk(logits, tau: float):
+    """Adaptive router's choice (Sec. III Phase 4): (idx [T,2], gate [T,2]);
+    slot 1 is -1 (gate 0) for tokens whose confidence is at least tau."""
+    logits = np.ascontiguousarray(logits, dtype=np.float64)
+    T, E = logits.shape
+    idx = np.empty((T, 2), dtype=np.int32)
+    gate = np.empty((T, 2))
+    lib().ref_adaptive_topk(T, E, float(tau), _dp(logits), _ip(idx), _dp(gate))
+    return idx, gate
+
+
+def confidence(logits) -> np.ndarray:
+    """Largest softmax probability of each token (the adaptive router's
+    confidence), in double."""
+    lg = np.asarray(logits, dtype=np.float64)
+    return 1.0 / np.sum(np.exp(lg - lg.max(axis=1, keepdims=True)), axis=1)
+
+
+def round_to_storage(v, dtype: str) -> np.ndarray:
+    """Round exact values once to the storage precision: float32, or bfloat16
+    (8 significant bits, ties to even).  Returns float64."""
+    v = np.asarray(v, dtype=np.float64)
+    if dtype == "f32":
+        return v.astype(np.float32).astype(np.float64)
+    if dtype != "bf16":
+        raise ValueError(dtype)
+    m, e = np.frexp(v)                       # v = m 2^e, 0.5 <= |m| < 1
+    return np.ldexp(np.round(np.ldexp(m, 8)), e - 8)
+
+
+def mlp_router_logits(x, Wh, bh, Wg, bg, dtype: str):
+    """MLP router (Sec. III Phase 4, hidden width h = d/6): the hidden layer
+    hr = GELU(x Wh^T + bh) is rounded to the storage precision (where the
+    kernels keep it), then l = hr Wg^T + bg exactly.  Returns (logits, hr)."""
+    hr = round_to_storage(fc1_gelu(x, Wh, bh), dtype)
+    return router_logits(hr, Wg, bg), hr
+
+
+def route_layer(layer: dict, rows=None):
+    """Routing of a layer dict by its router (linear when the dict has no
+    "router" entry).  Returns (idx, gate, logits)."""
+    x = layer["x"] if rows is None else layer["x"][np.asarray(rows)]
+    rt = layer.get("router") or {"kind": "linear"}
+    k = layer["cfg"].k
+    if rt["kind"] == "mlp":
+        lg, _ = mlp_router_logits(x, rt["Wh"], rt["bh"], layer["Wg"], layer["bg"],
+                                  layer["cfg"].dtype)
+    else:
+        lg = router_logits(x, layer["Wg"], layer["bg"])
+    if rt["kind"] == "adaptive":
+        idx, gate = adaptive_topk(lg, rt["tau"])
+    else:
+        idx, gate = topk(lg, k)
+    return idx, gate, lg
 
 
 def route(x, Wg, bg, k: int):
@@ -193,14 +252,27 @@ def ffn_forward(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int):
     return dict(y=y, idx=idx, gate=gate, logits=logits)
 
 
+def ffn_forward_routed(x, W1, b1, US, Vt, b2, P, Q, idx, gate):
+    """The layer after routing (Eq. 2, Algorithm 3): y = h_sh + h_res with the
+    given idx [T,k] (-1 = empty slot) and gates."""
+    z = fc1_gelu(x, W1, b1)
+    return shared(z, Vt, US, b2) + residual(z, Q, P, idx, gate)
+
+
 def ffn_forward_layer(layer: dict, rows=None):
     """ffn_forward on a layer dict as drawn by the input generator.
 
     ``rows`` (optional index array) evaluates only those tokens: every output
     of the layer depends on its own token alone, so a sample of rows gives the
-    same values as the full run at those rows.
+    same values as the full run at those rows.  A "router" entry (MLP or
+    adaptive) routes through route_layer; without it the linear router runs.
     """
     x = layer["x"] if rows is None else layer["x"][np.asarray(rows)]
+    if layer.get("router") is not None and layer["router"]["kind"] != "linear":
+        idx, gate, lg = route_layer(layer, rows)
+        y = ffn_forward_routed(x, layer["W1"], layer["b1"], layer["US"], layer["Vt"],
+                               layer["b2"], layer["P"], layer["Q"], idx, gate)
+        return dict(y=y, idx=idx, gate=gate, logits=lg)
     return ffn_forward(x, layer["W1"], layer["b1"], layer["US"], layer["Vt"], layer["b2"],
                        layer["P"], layer["Q"], layer["Wg"], layer["bg"], layer["cfg"].k)
 

@@ -36,7 +36,8 @@ from typing import Optional, Sequence
 import numpy as np
 
 __all__ = ["LayerConfig", "CONFIGS", "DISPATCH_CONFIG", "make_layer", "make_dispatch",
-           "to_bf16_bits", "bf16_bits_to_f32", "fingerprint", "imbalance_mixture"]
+           "to_bf16_bits", "bf16_bits_to_f32", "fingerprint", "imbalance_mixture",
+           "with_mlp_router", "with_adaptive_router"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -212,6 +213,44 @@ def make_layer(cfg: LayerConfig, **overrides) -> dict:
         P=_store(P, dt), Q=_store(Q, dt), Wg=_store(Wg, dt), bg=bg.astype(np.float32),
         labels=labels, s=s, W2=W2,
     )
+
+
+def with_mlp_router(layer: dict, h: Optional[int] = None, seed: int = 0) -> dict:
+    """The layer with an MLP router in place of the linear one (Sec. III
+    Phase 4: one hidden layer of width h = d/6).  Stand-in for a router fitted
+    to the cluster labels: the first E hidden units look along the linear
+    router's rows (unit vectors towards the cluster centres), the other h - E
+    are random N(0, 1/d) directions; the output layer reads hidden unit e with
+    weight 2 for expert e plus N(0, 0.05^2) from every unit; biases zero.
+    Adds "router" = {"kind": "mlp", "Wh" [h,D], "bh" [h]} and replaces Wg [E,h]
+    and bg [E]."""
+    cfg = layer["cfg"]
+    D, E, dt = cfg.D, cfg.E, cfg.dtype
+    h = D // 6 if h is None else h
+    if h < E:
+        raise ValueError("the MLP router needs h >= E")
+    rng = np.random.default_rng(seed)
+    lin = layer["Wg"]
+    lin = bf16_bits_to_f32(lin) if lin.dtype == np.uint16 else lin
+    Wh = rng.standard_normal((h, D)) / np.sqrt(D)
+    Wh[:E] = _unit_rows(lin.astype(np.float64))
+    Wo = 0.05 * rng.standard_normal((E, h))
+    Wo[np.arange(E), np.arange(E)] += 2.0
+    out = dict(layer)
+    out["router"] = {"kind": "mlp", "Wh": _store(Wh, dt), "bh": np.zeros(h, np.float32)}
+    out["Wg"] = _store(Wo, dt)
+    out["bg"] = np.zeros(E, np.float32)
+    return out
+
+
+def with_adaptive_router(layer: dict, tau: float) -> dict:
+    """The layer with the adaptive router (Sec. III Phase 4): the linear
+    router's weights, top-1 escalated to top-2 below confidence tau.  The
+    layer gets k = 2 slots per token."""
+    out = dict(layer)
+    out["cfg"] = dataclasses.replace(layer["cfg"], k=2)
+    out["router"] = {"kind": "adaptive", "tau": float(tau)}
+    return out
 
 
 def make_dispatch(T=None, D=None, E=None, k=None, dtype=None, seed=None, zipf_s=None) -> dict:

@@ -367,3 +367,118 @@ def test_imbalance_mixture_recipe():
     idx, _, _ = oracle.route(L["x"], L["Wg"], L["bg"], 1)
     share = np.bincount(idx[:, 0], minlength=4) / 4000.0
     assert abs(share.max() - 0.85) < 0.05, share
+
+
+# ---- router variants (Sec. III Phase 4: MLP and adaptive routers) ----------
+
+def _worked():
+    return json.load(open(os.path.join(GOLDEN, "router_variants_worked.json")))
+
+
+def test_mlp_router_worked_example():
+    """Hand-worked token (normal CDF table values): a transposed Wh, a dropped
+    bias or GELU taken as the identity would all move these logits."""
+    g = _worked()["mlp"]
+    x = np.array([g["x"]], np.float32)
+    Wh, bh = np.array(g["Wh"], np.float32), np.array(g["bh"], np.float32)
+    Wg, bg = np.array(g["Wg"], np.float32), np.array(g["bg"], np.float32)
+    lg, hr = oracle.mlp_router_logits(x, Wh, bh, Wg, bg, "f32")
+    # table values carry 9 decimals; hr is rounded to float32 (2^-24 relative)
+    assert np.allclose(hr[0], g["hidden"], rtol=0, atol=2e-7)
+    assert np.allclose(lg[0], g["logits"], rtol=0, atol=4e-7)
+    idx, _ = oracle.topk(lg, 1)
+    assert idx[0, 0] == g["top1"]
+
+
+def test_mlp_router_params_and_hidden_rounding():
+    g = json.load(open(os.path.join(GOLDEN, "table_c5_router_params.json")))
+    cfg = synth.LayerConfig("c5", T=8, D=g["d"], H=64, E=g["E"], k=1, r=8, q=8, dtype="f32",
+                            seed=0, n_cal=50)
+    M = synth.with_mlp_router(synth.make_layer(cfg))
+    rt = M["router"]
+    per_layer = rt["Wh"].size + rt["bh"].size + M["Wg"].size + M["bg"].size
+    assert per_layer * g["layers"] == g["mlp_params_total"]
+    assert rt["Wh"].shape == (g["mlp_hidden"], g["d"])
+    # bf16 storage rounding of the hidden layer: 8 significant bits, ties to
+    # even, and the same as the input generator's float32 -> bf16 rounding
+    v = np.array([1.0, 1 + 2 ** -8, 1 + 3 * 2 ** -8, -(1 + 2 ** -7 + 5 * 2 ** -10), 3.0e-3,
+                  -7.5e5, 1 + 2 ** -7 + 2 ** -9])
+    r = oracle.round_to_storage(v, "bf16")
+    assert r[1] == 1.0 and r[2] == 1 + 2 ** -6 and r[3] == -(1 + 2 ** -6)
+    assert r[6] == 1 + 2 ** -7
+    assert np.array_equal(r, synth.bf16_bits_to_f32(synth.to_bf16_bits(v.astype(np.float32))))
+
+
+def test_adaptive_router_worked_example_and_limits():
+    g = _worked()["adaptive"]
+    lg = np.array([g["logits"]])
+    assert abs(oracle.confidence(lg)[0] - g["confidence"]) < 1e-9
+    for c in g["cases"]:
+        idx, gate = oracle.adaptive_topk(lg, c["tau"])
+        assert idx[0].tolist() == c["idx"]
+        assert np.allclose(gate[0], c["gate"], atol=1e-9)
+    rng = np.random.default_rng(11)
+    for E in (2, 3, 5, 8):
+        lg = rng.standard_normal((300, E)) * 2.0
+        i1, g1 = oracle.topk(lg, 1)
+        i2, g2 = oracle.topk(lg, 2)
+        # tau <= 1/E: the confidence is never below it, so every token is top-1
+        ia, ga = oracle.adaptive_topk(lg, 1.0 / E)
+        assert np.array_equal(ia[:, 0], i1[:, 0]) and np.all(ia[:, 1] == -1)
+        assert np.all(ga[:, 0] == 1.0) and np.all(ga[:, 1] == 0.0)
+        # tau above 1: every token escalates to the plain top-2
+        ia, ga = oracle.adaptive_topk(lg, 1.5)
+        assert np.array_equal(ia, i2) and np.allclose(ga, g2)
+        if E == 2:
+            # two experts: confidence = sigmoid(|l0 - l1|), so a token escalates
+            # exactly when |l0 - l1| < log(tau / (1 - tau))
+            tau = 0.8
+            ia, _ = oracle.adaptive_topk(lg, tau)
+            esc = np.abs(lg[:, 0] - lg[:, 1]) < math.log(tau / (1 - tau))
+            assert np.array_equal(ia[:, 1] >= 0, esc)
+    ia, ga = oracle.adaptive_topk(np.zeros((3, 1)), 0.99)       # one expert
+    assert np.all(ia[:, 0] == 0) and np.all(ia[:, 1] == -1) and np.all(ga[:, 0] == 1.0)
+
+
+def test_dispatch_with_empty_slots_brute_force():
+    """-1 marks an empty slot: not counted, no row, inv = -1; the rest is the
+    stable sort by expert."""
+    rng = np.random.default_rng(5)
+    for T, E, k in ((1, 2, 2), (7, 3, 2), (40, 5, 2), (25, 4, 3)):
+        idx = rng.integers(-1, E, size=(T, k)).astype(np.int32)
+        counts, offsets, perm, inv = oracle.dispatch(idx, E)
+        flat = idx.ravel()
+        valid = [a for a in range(T * k) if flat[a] >= 0]
+        order = sorted(valid, key=lambda a: (flat[a], a))
+        n = len(order)
+        assert offsets[-1] == n and counts.sum() == n
+        assert perm[:n].tolist() == order and np.all(perm[n:] == -1)
+        for a in range(T * k):
+            assert (inv[a] == -1) == (flat[a] < 0)
+            if flat[a] >= 0:
+                assert perm[inv[a]] == a
+    with pytest.raises(ValueError):
+        oracle.dispatch(np.array([[0, -2]], np.int32), 2)
+
+
+def test_residual_and_layer_with_empty_slots():
+    """An empty slot adds nothing: the same as any expert with gate 0; the
+    adaptive layer equals the top-1 layer on confident tokens and the top-2
+    layer on escalated ones."""
+    cfg = synth.LayerConfig("ad", T=300, D=24, H=40, E=4, k=2, r=8, q=6, dtype="f32", seed=8,
+                            residual="random", n_cal=200)
+    L = synth.make_layer(cfg)
+    A = synth.with_adaptive_router(L, 0.95)
+    ref = oracle.ffn_forward_layer(A)
+    esc = ref["idx"][:, 1] >= 0
+    assert 0 < esc.sum() < cfg.T
+    idx2 = ref["idx"].copy()
+    idx2[~esc, 1] = 3                       # any expert, gate 0
+    z = oracle.fc1_gelu(L["x"], L["W1"], L["b1"])
+    r1 = oracle.residual(z, L["Q"], L["P"], ref["idx"], ref["gate"])
+    r2 = oracle.residual(z, L["Q"], L["P"], idx2, ref["gate"])
+    assert np.array_equal(r1, r2)
+    y1 = oracle.ffn_forward_layer(L, )                       # k = 2 layer
+    y0 = oracle.ffn_forward_layer(dict(L, cfg=synth.dataclasses.replace(cfg, k=1)))
+    assert np.allclose(ref["y"][esc], y1["y"][esc], rtol=0, atol=1e-12)
+    assert np.allclose(ref["y"][~esc], y0["y"][~esc], rtol=0, atol=1e-12)
