@@ -21,7 +21,9 @@ Prints one JSON line.  Besides the contract fields it carries
   imbalance    the dispatch-backend sweep: grouped (clearmoe_ffn_forward)
                against padded batches (clearmoe_ffn_forward_padded) at 0, 40,
                60 and 80 % load imbalance, E = 4, DeiT-Small widths, top-1 and
-               top-2, 1568 and 12608 tokens.
+               top-2, 1568 and 12608 tokens;
+  routers      the same layer with the linear, MLP and adaptive routers
+               (clearmoe_ffn_forward_ex).
 """
 import argparse
 import hashlib
@@ -260,6 +262,7 @@ def main():
         del W2, yd
         out["dispatch"] = bench_dispatch(cm, synth, torch, np, stream, max(10, args.steps // 10))
         out["imbalance"] = bench_imbalance(cm, synth, torch, np, stream, max(20, args.steps // 5))
+        out["routers"] = bench_routers(cm, synth, torch, np, stream, L, max(20, args.steps // 5))
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(L, cfg, args.cpu_seconds)
@@ -386,6 +389,58 @@ def bench_imbalance(cm, synth, torch, np, stream, steps):
             del d, y
     return {"workload": "DeiT-Small widths D=384 H=1536 r=128 q=32 bf16, E=4, seed 5",
             "steps": steps, "points": out}
+
+
+def bench_routers(cm, synth, torch, np, stream, L, steps):
+    """The same DeiT-Small-shaped layer with the paper's three routers
+    (Sec. III Phase 4, Table C5): linear top-1, MLP top-1 (hidden d/6 = 64)
+    and adaptive (linear scores, top-1 escalated to top-2 below the confidence
+    threshold tau = 0.9: a token whose largest softmax probability is below
+    0.9 takes two experts, about 30 % of this workload's tokens).  Per
+    variant: ms per layer call, tokens/s, the router kernel's time and the
+    share of tokens on two experts."""
+    cfg = L["cfg"]
+    d = {n: cm.from_stored(L[n]) for n in ("x", "W1", "b1", "US", "Vt", "b2", "P", "Q")}
+    Lm = synth.with_mlp_router(L, seed=1)
+    keep = {"Wg": cm.from_stored(L["Wg"]), "bg": cm.from_stored(L["bg"]),
+            "Wo": cm.from_stored(Lm["Wg"]), "bo": cm.from_stored(Lm["bg"]),
+            "Wh": cm.from_stored(Lm["router"]["Wh"]), "bh": cm.from_stored(Lm["router"]["bh"])}
+    tau = 0.9
+    variants = [
+        ("linear", cm.make_router(keep["Wg"], keep["bg"]), 1),
+        ("mlp", cm.make_router(keep["Wo"], keep["bo"], keep["Wh"], keep["bh"]), 1),
+        ("adaptive", cm.make_router(keep["Wg"], keep["bg"], adaptive=True, tau=tau), 2),
+    ]
+    out = {"workload": f"{cfg.name} (T={cfg.T} D={cfg.D} H={cfg.H} E={cfg.E} r={cfg.r} "
+                       f"q={cfg.q} bf16)", "mlp_hidden": int(Lm["router"]["Wh"].shape[0]),
+           "adaptive_tau": tau, "steps": steps, "variants": {}}
+    dev = d["x"].device
+    for name, router, k in variants:
+        shape = cm.make_shape(cfg.T, cfg.D, cfg.E, k, cm.BF16, H=cfg.H, r=cfg.r, q=cfg.q)
+        ws = cm.alloc_workspace(shape)
+        y = torch.empty((cfg.T, cfg.D), dtype=d["x"].dtype, device=dev)
+        idx = torch.empty((cfg.T, k), dtype=torch.int32, device=dev)
+
+        def run():
+            cm.ffn_forward_ex(d["x"], d["W1"], d["b1"], d["US"], d["Vt"], d["b2"], d["P"],
+                              d["Q"], router, k, ws=ws, out=y, idx_out=idx)
+        for _ in range(5):
+            run()
+        torch.cuda.synchronize()
+        cm.timing_start(["route"], steps)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            run()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        r_ms, r_n = cm.timing_stop()["route"]
+        ms = e0.elapsed_time(e1) / steps
+        two = float((idx[:, 1] >= 0).float().mean()) if k == 2 else 0.0
+        out["variants"][name] = {"ms": ms, "tokens_per_s": cfg.T / (ms * 1e-3),
+                                 "route_us": r_ms / r_n * 1e3, "share_top2": two}
+        del ws, y, idx
+    return out
 
 
 def cpu_baseline(L, cfg, min_seconds):

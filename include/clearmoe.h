@@ -91,16 +91,64 @@ size_t clearmoe_workspace_bytes(const clearmoe_shape* shape);
 int clearmoe_route(const clearmoe_shape* shape, const void* x, const void* Wg, const float* bg,
                    int32_t* idx, float* gate, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Router of a layer.  Sec. III Phase 4 fits one of three routers to the
+ * cluster labels (Table C5 compares them): Linear, MLP (one hidden layer,
+ * width d/6 there) and Adaptive (top-1, escalated to top-2 when the router is
+ * not confident).  Here the scoring function and the selection rule are
+ * independent fields, so an MLP router can also select adaptively.
+ *   Scores:   hidden == 0: l = x Wg^T + bg, Wg [E, D] (as clearmoe_route);
+ *             hidden  > 0: hr = GELU(x Wh^T + bh) rounded once to dtype,
+ *             l = hr Wg^T + bg, Wh [hidden, D], Wg [E, hidden].
+ *   Choice:   adaptive == 0: the top k = shape->k, gates as clearmoe_route;
+ *             adaptive == 1 (shape->k must be 2, E >= 2): the confidence of a
+ *             token is its largest softmax probability over all E experts,
+ *             p = 1 / sum_e exp(l_e - l_max); p >= tau keeps it at top-1
+ *             (idx = (best, -1), gate = (1, 0): slot 1 is empty), otherwise
+ *             it takes the top 2 with their softmax renormalised.
+ * Weights have element type shape->dtype, biases are float32 (NULL = zero). */
+typedef struct {
+    const void* Wg;        /* output layer [E, D] (linear) or [E, hidden] (MLP) */
+    const float* bg;       /* [E] or NULL */
+    const void* Wh;        /* MLP hidden layer [hidden, D]; ignored if hidden == 0 */
+    const float* bh;       /* MLP hidden bias [hidden] or NULL */
+    int32_t hidden;        /* 0 = linear router; 1..256 = MLP hidden width */
+    int32_t adaptive;      /* 0 = top-k; 1 = adaptive top-1 / top-2 */
+    double tau;            /* adaptive confidence threshold (any finite value) */
+} clearmoe_router;
+
+/* Routing by any router (see clearmoe_router), same outputs and workspace
+ * contract as clearmoe_route: idx [T, k] (-1 marks an adaptive router's empty
+ * slot), gate [T, k], and the per-tile histogram left in ws for a following
+ * clearmoe_dispatch with CLEARMOE_DISPATCH_HIST_IN_WS.  Decisions:
+ *   linear: certified as in clearmoe_route; for adaptive selection a token
+ *     whose confidence is within the float32 rounding bound of tau is also
+ *     recomputed in double, so the threshold is applied to exact logits;
+ *   MLP: both layers run in double (products of stored values are exact),
+ *     GELU uses the double erf and the hidden values are rounded to dtype
+ *     from double in one step; the choice matches exact arithmetic except
+ *     where a hidden value lies within double rounding of a dtype rounding
+ *     boundary or a top-k gap / |log p - log tau| is below double rounding.
+ * Returns CLEARMOE_ERR_INVALID_ARG for a NULL router, hidden outside
+ * [0, 256], adaptive not 0 or 1, adaptive with k != 2 or E < 2, a NaN tau, or
+ * NULL / misaligned weights (Wg, Wh 16-byte aligned; biases 4-byte). */
+int clearmoe_route_ex(const clearmoe_shape* shape, const clearmoe_router* router, const void* x,
+                      int32_t* idx, float* gate, void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Dispatch: expert histogram, exclusive scan and stable permutation (Sec. III
  * "Dispatch Backends", Grouped: tokens sorted by expert into contiguous
  * sub-batches; Algorithm 3 sort step).
- *   idx     [T, k] int32 in, every entry in [0, E).
- *   counts  [E] out; offsets [E+1] out, offsets[0] = 0, offsets[E] = T*k.
+ *   idx     [T, k] int32 in, every entry in [0, E) or -1 (an empty slot, as
+ *           an adaptive router leaves it).
+ *   counts  [E] out; offsets [E+1] out, offsets[0] = 0, offsets[E] = number
+ *           of entries that are not -1 (T*k when there are none).
  *   perm    [T*k] out: perm[p] = a = t*k + j, the assignments of expert 0 in
- *           ascending a, then expert 1, ...  inv [T*k] out: inv[perm[p]] = p.
- *   x [T, D] and xperm [T*k, D] (dtype): if both non-NULL, xperm[p] = x[perm[p]/k].
- * An index outside [0, E) is not detected on the device; it is the caller's
- * contract (clearmoe_route only produces valid ones).  Uses T, D, E, k, dtype. */
+ *           ascending a, then expert 1, ..., then -1 for p >= offsets[E].
+ *   inv     [T*k] out: inv[perm[p]] = p; inv[a] = -1 for an empty slot.
+ *   x [T, D] and xperm [T*k, D] (dtype): if both non-NULL, xperm[p] = x[perm[p]/k]
+ *           for p < offsets[E] (rows after that are not written).
+ * An index outside [-1, E) is not detected on the device; it is the caller's
+ * contract (the routers only produce valid ones); such an entry is treated
+ * as empty.  Uses T, D, E, k, dtype. */
 int clearmoe_dispatch(const clearmoe_shape* shape, const int32_t* idx, void* ws, size_t ws_bytes,
                       int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv,
                       const void* x, void* xperm, unsigned flags, hipStream_t stream);
@@ -108,7 +156,8 @@ int clearmoe_dispatch(const clearmoe_shape* shape, const int32_t* idx, void* ws,
 /* Inverse-permute combine (Algorithm 3 "unshuffle h_res; y <- h_sh + h_res",
  * weighted by the gates):  y[t] = sum_j gate[t, j] * ye[inv[t*k + j]],
  * accumulated in float32 in slot order, stored in dtype.
- *   ye [T*k, D] (dtype, expert order), inv [T*k], gate [T, k], y [T, D] out.
+ *   ye [T*k, D] (dtype, expert order), inv [T*k] (-1: empty slot, adds
+ *   nothing), gate [T, k], y [T, D] out.
  * Uses T, D, k, dtype. */
 int clearmoe_combine(const clearmoe_shape* shape, const void* ye, const int32_t* inv,
                      const float* gate, void* y, hipStream_t stream);
@@ -128,6 +177,17 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
                          const void* P, const void* Q, const void* Wg, const float* bg, void* y,
                          int32_t* idx_out, float* gate_out, void* ws, size_t ws_bytes,
                          hipStream_t stream);
+
+/* The whole layer with any router (see clearmoe_router and
+ * clearmoe_route_ex); the other arguments, layouts, results and workspace are
+ * those of clearmoe_ffn_forward.  Router weights replace Wg / bg.  An empty
+ * slot (adaptive top-1) adds no residual: y = h_sh + h_res of the chosen
+ * expert with gate 1. */
+int clearmoe_ffn_forward_ex(const clearmoe_shape* shape, const clearmoe_router* router,
+                            const void* x, const void* W1, const float* b1, const void* US,
+                            const void* Vt, const float* b2, const void* P, const void* Q,
+                            void* y, int32_t* idx_out, float* gate_out, void* ws,
+                            size_t ws_bytes, hipStream_t stream);
 
 /* Bytes of workspace clearmoe_ffn_forward_padded needs for this shape (room
  * for a padded batch of E * T * k rows); 0 if the shape is invalid. */

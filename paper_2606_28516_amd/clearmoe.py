@@ -18,7 +18,8 @@ __all__ = ["ClearMoEError", "Shape", "lib", "version", "workspace_bytes", "alloc
            "route", "dispatch", "combine", "ffn_forward", "from_stored", "to_stored",
            "DISPATCH_HIST_IN_WS", "F32", "BF16", "SYMBOLS", "N_STAGES", "stage_names",
            "timing_start", "timing_stop", "make_shape", "dense_ffn_forward",
-           "padded_workspace_bytes", "ffn_forward_padded"]
+           "padded_workspace_bytes", "ffn_forward_padded", "Router", "make_router", "route_ex",
+           "ffn_forward_ex"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libclearmoe.so")
@@ -28,7 +29,7 @@ SYMBOLS = ("clearmoe_version", "clearmoe_status_string", "clearmoe_workspace_byt
            "clearmoe_route", "clearmoe_dispatch", "clearmoe_combine", "clearmoe_ffn_forward",
            "clearmoe_dense_ffn_forward", "clearmoe_stage_name", "clearmoe_timing_start",
            "clearmoe_timing_stop", "clearmoe_padded_workspace_bytes",
-           "clearmoe_ffn_forward_padded")
+           "clearmoe_ffn_forward_padded", "clearmoe_route_ex", "clearmoe_ffn_forward_ex")
 N_STAGES = 16
 
 
@@ -38,6 +39,14 @@ class ClearMoEError(RuntimeError):
 
 class Shape(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in ("T", "D", "H", "E", "k", "r", "q", "dtype")]
+
+
+class Router(ctypes.Structure):
+    """clearmoe_router: scores (linear, or an MLP with `hidden` units) and the
+    selection rule (top-k, or adaptive top-1 / top-2 at threshold tau)."""
+    _fields_ = [("Wg", ctypes.c_void_p), ("bg", ctypes.c_void_p), ("Wh", ctypes.c_void_p),
+                ("bh", ctypes.c_void_p), ("hidden", ctypes.c_int32), ("adaptive", ctypes.c_int32),
+                ("tau", ctypes.c_double)]
 
 
 _lib = None
@@ -66,6 +75,11 @@ def lib():
         L.clearmoe_combine.argtypes = [sp, vp, vp, vp, vp, vp]
         L.clearmoe_ffn_forward.restype = ctypes.c_int
         L.clearmoe_ffn_forward.argtypes = [sp] + [vp] * 13 + [vp, sz, vp]
+        rp = ctypes.POINTER(Router)
+        L.clearmoe_route_ex.restype = ctypes.c_int
+        L.clearmoe_route_ex.argtypes = [sp, rp, vp, vp, vp, vp, sz, vp]
+        L.clearmoe_ffn_forward_ex.restype = ctypes.c_int
+        L.clearmoe_ffn_forward_ex.argtypes = [sp, rp] + [vp] * 11 + [vp, sz, vp]
         L.clearmoe_padded_workspace_bytes.restype = sz
         L.clearmoe_padded_workspace_bytes.argtypes = [sp]
         L.clearmoe_ffn_forward_padded.restype = ctypes.c_int
@@ -145,6 +159,27 @@ def route(x, Wg, bg, k: int, ws: Optional[torch.Tensor] = None, stream=None):
     return idx, gate
 
 
+def make_router(Wg, bg=None, Wh=None, bh=None, adaptive: bool = False, tau: float = 0.0):
+    """A Router over device tensors (keep the tensors alive while it is used):
+    linear when Wh is None, else an MLP with Wh.shape[0] hidden units."""
+    p = lambda t: None if t is None else _p(t).value  # noqa: E731
+    return Router(p(Wg), p(bg), p(Wh), p(bh), 0 if Wh is None else int(Wh.shape[0]),
+                  1 if adaptive else 0, float(tau))
+
+
+def route_ex(x, router: Router, E: int, k: int, ws: Optional[torch.Tensor] = None, stream=None):
+    """clearmoe_route_ex: returns (idx [T,k] int32, -1 = empty slot; gate [T,k])."""
+    T, D = x.shape
+    s = make_shape(T, D, E, k, _dt(x))
+    ws = alloc_workspace(s, x.device) if ws is None else ws
+    idx = torch.empty((T, k), dtype=torch.int32, device=x.device)
+    gate = torch.empty((T, k), dtype=torch.float32, device=x.device)
+    rc = lib().clearmoe_route_ex(ctypes.byref(s), ctypes.byref(router), _p(x), _p(idx), _p(gate),
+                                 _p(ws), ws.numel(), _stream(stream))
+    _check(rc, "clearmoe_route_ex")
+    return idx, gate
+
+
 def dispatch(idx, E: int, ws: Optional[torch.Tensor] = None, x=None, D: Optional[int] = None,
              hist_in_ws: bool = False, stream=None):
     """clearmoe_dispatch: returns (counts, offsets, perm, inv, xperm or None)."""
@@ -219,6 +254,25 @@ def ffn_forward_padded(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int,
     backend (blocks the host until dispatch is done).  Returns y [T, D]."""
     return _layer_call("clearmoe_ffn_forward_padded", padded_workspace_bytes, x, W1, b1, US, Vt,
                        b2, P, Q, Wg, bg, k, ws, out, idx_out, gate_out, stream)
+
+
+def ffn_forward_ex(x, W1, b1, US, Vt, b2, P, Q, router: Router, k: int,
+                   ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                   idx_out=None, gate_out=None, stream=None):
+    """clearmoe_ffn_forward_ex: the whole layer with any router.  Returns y."""
+    T, D = x.shape
+    H = W1.shape[0]
+    r = US.shape[1]
+    E, _, q = P.shape
+    s = make_shape(T, D, E, k, _dt(x), H=H, r=r, q=q)
+    ws = alloc_workspace(s, x.device) if ws is None else ws
+    y = torch.empty((T, D), dtype=x.dtype, device=x.device) if out is None else out
+    rc = lib().clearmoe_ffn_forward_ex(ctypes.byref(s), ctypes.byref(router), _p(x), _p(W1),
+                                       _p(b1), _p(US), _p(Vt), _p(b2), _p(P), _p(Q), _p(y),
+                                       _p(idx_out), _p(gate_out), _p(ws), ws.numel(),
+                                       _stream(stream))
+    _check(rc, "clearmoe_ffn_forward_ex")
+    return y
 
 
 def dense_ffn_forward(x, W1, b1, W2, b2, ws: Optional[torch.Tensor] = None,

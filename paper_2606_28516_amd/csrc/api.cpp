@@ -139,11 +139,40 @@ P* at(void* ws, size_t off) {
     return reinterpret_cast<P*>(static_cast<unsigned char*>(ws) + off);
 }
 
-int route_impl(const clearmoe_shape& s, const Layout& L, const void* x, const void* Wg,
-               const float* bg, int32_t* idx, float* gate, void* ws, hipStream_t st) {
+clearmoe_router linear_router(const void* Wg, const float* bg) {
+    clearmoe_router r{};
+    r.Wg = Wg;
+    r.bg = bg;
+    return r;
+}
+
+// Router checks (before any HIP call).
+int check_router(const clearmoe_shape& s, const clearmoe_router* r) {
+    if (r == nullptr || r->Wg == nullptr || !aligned(r->Wg, 16)) return CLEARMOE_ERR_INVALID_ARG;
+    if (r->bg && !aligned(r->bg, 4)) return CLEARMOE_ERR_INVALID_ARG;
+    if (r->hidden < 0 || r->hidden > kMlpHiddenMax) return CLEARMOE_ERR_INVALID_ARG;
+    if (r->hidden > 0 && (r->Wh == nullptr || !aligned(r->Wh, 16) || (r->bh && !aligned(r->bh, 4))))
+        return CLEARMOE_ERR_INVALID_ARG;
+    if (r->adaptive != 0 && r->adaptive != 1) return CLEARMOE_ERR_INVALID_ARG;
+    if (r->adaptive && (s.k != 2 || s.E < 2 || r->tau != r->tau)) return CLEARMOE_ERR_INVALID_ARG;
+    return CLEARMOE_OK;
+}
+
+// Routing and the per-tile histogram (left in the workspace for dispatch).
+int route_impl(const clearmoe_shape& s, const Layout& L, const clearmoe_router& rt, const void* x,
+               int32_t* idx, float* gate, void* ws, hipStream_t st) {
+    int32_t* tc = at<int32_t>(ws, L.tile_counts);
+    if (rt.hidden == 0) {
+        CLEARMOE_STAGE(CLEARMOE_STAGE_ROUTE, st,
+                       launch_route(s.dtype, x, rt.Wg, rt.bg, s.T, s.D, s.E, s.k, rt.adaptive,
+                                    rt.tau, idx, gate, tc, st));
+        return CLEARMOE_OK;
+    }
     CLEARMOE_STAGE(CLEARMOE_STAGE_ROUTE, st,
-                   launch_route(s.dtype, x, Wg, bg, s.T, s.D, s.E, s.k, idx, gate,
-                                at<int32_t>(ws, L.tile_counts), st));
+                   launch_route_mlp(s.dtype, x, rt.Wh, rt.bh, rt.Wg, rt.bg, s.T, s.D, rt.hidden,
+                                    s.E, s.k, rt.adaptive, rt.tau, idx, gate, st));
+    CLEARMOE_STAGE(CLEARMOE_STAGE_TILE_HIST, st,
+                   launch_tile_histogram(idx, s.T, s.E, s.k, tc, st));
     return CLEARMOE_OK;
 }
 
@@ -178,7 +207,7 @@ int check_layer_args(const clearmoe_shape* shape, const void* x, const void* W1,
     int rc = check_shape(shape, true);
     if (rc != CLEARMOE_OK) return rc;
     const clearmoe_shape& s = *shape;
-    if (!W1 || !Wg || (s.T > 0 && (!x || !y))) return CLEARMOE_ERR_INVALID_ARG;
+    if (!W1 || (s.T > 0 && (!x || !y))) return CLEARMOE_ERR_INVALID_ARG;
     if (s.r > 0 && (!US || !Vt)) return CLEARMOE_ERR_INVALID_ARG;
     if (s.q > 0 && (!P || !Q)) return CLEARMOE_ERR_INVALID_ARG;
     const void* v16[] = {x, W1, US, Vt, P, Q, Wg, y};
@@ -244,7 +273,7 @@ thread_local int32_t* t_host_counts = nullptr;
 
 extern "C" {
 
-int clearmoe_version(void) { return (0 << 16) | 1; }
+int clearmoe_version(void) { return (0 << 16) | 2; }
 
 const char* clearmoe_status_string(int status) {
     switch (status) {
@@ -282,7 +311,24 @@ int clearmoe_route(const clearmoe_shape* shape, const void* x, const void* Wg, c
     sl.H = sl.r = sl.q = 0;
     const Layout L = layout(sl);
     if (!ws || !aligned(ws, kAlign) || ws_bytes < L.dispatch_end) return CLEARMOE_ERR_WORKSPACE;
-    return route_impl(s, L, x, Wg, bg, idx, gate, ws, stream);
+    return route_impl(s, L, linear_router(Wg, bg), x, idx, gate, ws, stream);
+}
+
+int clearmoe_route_ex(const clearmoe_shape* shape, const clearmoe_router* router, const void* x,
+                      int32_t* idx, float* gate, void* ws, size_t ws_bytes, hipStream_t stream) {
+    int rc = check_shape(shape, false);
+    if (rc != CLEARMOE_OK) return rc;
+    const clearmoe_shape& s = *shape;
+    rc = check_router(s, router);
+    if (rc != CLEARMOE_OK) return rc;
+    const bool tok = s.T > 0;
+    if (tok && (!x || !idx || !gate)) return CLEARMOE_ERR_INVALID_ARG;
+    if (!aligned(x, 16) || !aligned(idx, 4) || !aligned(gate, 4)) return CLEARMOE_ERR_INVALID_ARG;
+    clearmoe_shape sl = s;
+    sl.H = sl.r = sl.q = 0;
+    const Layout L = layout(sl);
+    if (!ws || !aligned(ws, kAlign) || ws_bytes < L.dispatch_end) return CLEARMOE_ERR_WORKSPACE;
+    return route_impl(s, L, *router, x, idx, gate, ws, stream);
 }
 
 int clearmoe_dispatch(const clearmoe_shape* shape, const int32_t* idx, void* ws, size_t ws_bytes,
@@ -319,14 +365,20 @@ int clearmoe_combine(const clearmoe_shape* shape, const void* ye, const int32_t*
     return CLEARMOE_OK;
 }
 
-int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void* W1,
-                         const float* b1, const void* US, const void* Vt, const float* b2,
-                         const void* P, const void* Q, const void* Wg, const float* bg, void* y,
-                         int32_t* idx_out, float* gate_out, void* ws, size_t ws_bytes,
-                         hipStream_t stream) {
-    int rc = check_layer_args(shape, x, W1, b1, US, Vt, b2, P, Q, Wg, bg, y, idx_out, gate_out);
+}  // extern "C"
+
+namespace {
+
+int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router, const void* x,
+                     const void* W1, const float* b1, const void* US, const void* Vt,
+                     const float* b2, const void* P, const void* Q, void* y, int32_t* idx_out,
+                     float* gate_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+    int rc = check_layer_args(shape, x, W1, b1, US, Vt, b2, P, Q, nullptr, nullptr, y, idx_out,
+                              gate_out);
     if (rc != CLEARMOE_OK) return rc;
     const clearmoe_shape& s = *shape;
+    rc = check_router(s, router);
+    if (rc != CLEARMOE_OK) return rc;
     const Layout L = layout(s);
     if (!ws || !aligned(ws, kAlign) || ws_bytes < L.total) return CLEARMOE_ERR_WORKSPACE;
     if (s.T == 0) return CLEARMOE_OK;
@@ -346,7 +398,7 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
     float* hres = at<float>(ws, L.hres);
 
     // 1. router + top-k + per-tile histogram; 2. scan + stable permutation
-    rc = route_impl(s, L, x, Wg, bg, idx, gate, ws, st);
+    rc = route_impl(s, L, *router, x, idx, gate, ws, st);
     if (rc != CLEARMOE_OK) return rc;
     rc = dispatch_impl(s, L, idx, ws, counts, offsets, perm, inv, nullptr, nullptr, true, st);
     if (rc != CLEARMOE_OK) return rc;
@@ -408,6 +460,29 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
     return CLEARMOE_OK;
 }
 
+}  // namespace
+
+extern "C" {
+
+int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void* W1,
+                         const float* b1, const void* US, const void* Vt, const float* b2,
+                         const void* P, const void* Q, const void* Wg, const float* bg, void* y,
+                         int32_t* idx_out, float* gate_out, void* ws, size_t ws_bytes,
+                         hipStream_t stream) {
+    const clearmoe_router rt = linear_router(Wg, bg);
+    return ffn_forward_impl(shape, &rt, x, W1, b1, US, Vt, b2, P, Q, y, idx_out, gate_out, ws,
+                            ws_bytes, stream);
+}
+
+int clearmoe_ffn_forward_ex(const clearmoe_shape* shape, const clearmoe_router* router,
+                            const void* x, const void* W1, const float* b1, const void* US,
+                            const void* Vt, const float* b2, const void* P, const void* Q,
+                            void* y, int32_t* idx_out, float* gate_out, void* ws,
+                            size_t ws_bytes, hipStream_t stream) {
+    return ffn_forward_impl(shape, router, x, W1, b1, US, Vt, b2, P, Q, y, idx_out, gate_out, ws,
+                            ws_bytes, stream);
+}
+
 size_t clearmoe_padded_workspace_bytes(const clearmoe_shape* shape) {
     if (check_shape(shape, true) != CLEARMOE_OK) return 0;
     return layout(*shape).padded_total;
@@ -421,6 +496,9 @@ int clearmoe_ffn_forward_padded(const clearmoe_shape* shape, const void* x, cons
     int rc = check_layer_args(shape, x, W1, b1, US, Vt, b2, P, Q, Wg, bg, y, idx_out, gate_out);
     if (rc != CLEARMOE_OK) return rc;
     const clearmoe_shape& s = *shape;
+    const clearmoe_router rt = linear_router(Wg, bg);
+    rc = check_router(s, &rt);
+    if (rc != CLEARMOE_OK) return rc;
     const Layout L = layout(s);
     if (!ws || !aligned(ws, kAlign) || ws_bytes < L.padded_total) return CLEARMOE_ERR_WORKSPACE;
     if (s.T == 0) return CLEARMOE_OK;
@@ -439,7 +517,7 @@ int clearmoe_ffn_forward_padded(const clearmoe_shape* shape, const void* x, cons
     float* hsh = at<float>(ws, L.hsh);
     float* hres_pad = at<float>(ws, L.hres_pad);
 
-    rc = route_impl(s, L, x, Wg, bg, idx, gate, ws, st);
+    rc = route_impl(s, L, rt, x, idx, gate, ws, st);
     if (rc != CLEARMOE_OK) return rc;
     rc = dispatch_impl(s, L, idx, ws, counts, offsets, perm, inv, nullptr, nullptr, true, st);
     if (rc != CLEARMOE_OK) return rc;

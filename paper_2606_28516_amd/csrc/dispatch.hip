@@ -142,6 +142,7 @@ __global__ __launch_bounds__(kRouteTile) void k_permute(
     __shared__ int s_run[64];
     __shared__ int s_base[64];
     __shared__ int s_pre[64], s_tot[64];
+    __shared__ int s_total;               // assignments that have an expert
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int64_t A = T * k;
     const int64_t a0 = static_cast<int64_t>(blockIdx.x) * kRouteTile * k;
@@ -174,13 +175,22 @@ __global__ __launch_bounds__(kRouteTile) void k_permute(
                 o += s_tot[e];
             }
             if (blockIdx.x == 0) offsets[E] = o;
+            s_total = o;
         }
         if (tid < E) s_run[tid] = 0;
-    } else if (tid < E) {
-        s_run[tid] = 0;
-        s_base[tid] = offsets[tid] + tb[static_cast<int64_t>(blockIdx.x) * E + tid];
+    } else {
+        if (tid < E) {
+            s_run[tid] = 0;
+            s_base[tid] = offsets[tid] + tb[static_cast<int64_t>(blockIdx.x) * E + tid];
+        }
+        if (tid == 0) s_total = offsets[E];
     }
     __syncthreads();
+    // Empty slots (index -1) are in no sub-batch: perm ends with -1 entries
+    // after the offsets[E] real assignments.
+    for (int64_t i = static_cast<int64_t>(s_total) + static_cast<int64_t>(blockIdx.x) * kRouteTile + tid;
+         i < A; i += static_cast<int64_t>(gridDim.x) * kRouteTile)
+        if (i >= 0) perm[i] = -1;
     for (int c = 0; c < k; ++c) {
         const int al = c * kRouteTile + tid;
         const bool valid = al < na;

@@ -59,7 +59,9 @@ __device__ __forceinline__ float gelu_erf(float v) {
     const float e = __builtin_amdgcn_exp2f(v * v * -0.72134752044448170368f);   // -log2(e) / 2
     const float h = fabsf(v) * (t * hp) * e;
     return fmaxf(v, 0.0f) - h;
-}// ---------------------------------------------------------------------------
+}
+
+// ---------------------------------------------------------------------------
 // Tiling constants shared by host and device code.
 // ---------------------------------------------------------------------------
 constexpr int kRouteTile = 256;      // tokens per routing / dispatch tile (one per thread)
@@ -70,10 +72,19 @@ __host__ __device__ inline int64_t route_tiles(int64_t T) { return (T + kRouteTi
 // Host launchers (return hipError_t of the launch).
 // ---------------------------------------------------------------------------
 // Router logits (float32 MFMA, certified; double recompute of near ties),
-// top-k, gates, per-tile expert histogram (tile_counts may be NULL).
+// top-k (adaptive != 0: top-1 / top-2 by confidence tau, k = 2 slots), gates,
+// per-tile expert histogram (tile_counts may be NULL).
 hipError_t launch_route(int dtype, const void* x, const void* Wg, const float* bg, int64_t T,
-                        int D, int E, int k, int32_t* idx, float* gate, int32_t* tile_counts,
-                        hipStream_t st);
+                        int D, int E, int k, int adaptive, double tau, int32_t* idx, float* gate,
+                        int32_t* tile_counts, hipStream_t st);
+// MLP router: hidden GELU(x Wh^T + bh) of width Hr (1..kMlpHiddenMax) rounded
+// to the storage type, logits hr Wo^T + bo in double; then as launch_route
+// (no histogram).
+hipError_t launch_route_mlp(int dtype, const void* x, const void* Wh, const float* bh,
+                            const void* Wo, const float* bo, int64_t T, int D, int Hr, int E,
+                            int k, int adaptive, double tau, int32_t* idx, float* gate,
+                            hipStream_t st);
+constexpr int kMlpHiddenMax = 256;
 // Per-tile expert histogram of an index array.
 hipError_t launch_tile_histogram(const int32_t* idx, int64_t T, int E, int k,
                                  int32_t* tile_counts, hipStream_t st);
@@ -83,7 +94,8 @@ hipError_t launch_scan(const int32_t* tile_counts, int64_t ntiles, int E, int32_
                        int32_t* counts, int32_t* offsets, hipStream_t st);
 // Stable permutation (and optional row copy x -> xperm).  With tile_counts
 // non-NULL the tile scan is done inline (tile_base unused) and counts/offsets
-// are written; otherwise tile_base/offsets come from launch_scan.
+// are written; otherwise tile_base/offsets come from launch_scan.  An index
+// of -1 is an empty slot: inv = -1, and perm[offsets[E] .. T*k) = -1.
 hipError_t launch_permute(int dtype, const int32_t* idx, const int32_t* tile_base,
                           int32_t* offsets, const int32_t* tile_counts, int32_t* counts,
                           int64_t T, int E, int k, int32_t* perm, int32_t* inv, const void* x,

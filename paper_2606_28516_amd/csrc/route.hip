@@ -100,6 +100,60 @@ __device__ __forceinline__ double topk_gap(const double (&lg)[EP], int E, int k)
     return gap;
 }
 
+// Largest softmax probability of a token over its E logits,
+// 1 / sum_e exp(l_e - l_max): the confidence of the adaptive router.
+template <int EP>
+__device__ __forceinline__ double route_confidence(const double (&lg)[EP], int E) {
+    double lmax = lg[0];
+#pragma unroll
+    for (int e = 1; e < EP; ++e)
+        if (e < E && lg[e] > lmax) lmax = lg[e];
+    double den = 0.0;
+#pragma unroll
+    for (int e = 0; e < EP; ++e)
+        if (e < E) den += exp(lg[e] - lmax);
+    return 1.0 / den;
+}
+
+// Choice of one token from its logits (descending, ties to the lower index):
+// the top k with the softmax of the selected logits renormalised (k = 1:
+// gate 1), or, adaptive (k = 2 slots), top-1 when the confidence reaches tau
+// and top-2 otherwise, the unused second slot being expert -1 with gate 0.
+// Writes idx/gate of token t; returns the bit set of the chosen experts.
+template <int EP>
+__device__ __forceinline__ uint64_t route_select(const double (&lg)[EP], int E, int k,
+                                                 int adaptive, double tau, int64_t t,
+                                                 int32_t* __restrict__ idx,
+                                                 float* __restrict__ gate) {
+    const int kk = (adaptive && route_confidence<EP>(lg, E) >= tau) ? 1 : k;
+    uint64_t mine = 0;
+    double top = 0.0, den = 0.0;
+    for (int j = 0; j < kk; ++j) {
+        double bv;
+        const int best = pick<EP>(lg, E, mine, bv);
+        mine |= 1ull << best;
+        if (j == 0) top = bv;
+        den += exp(bv - top);
+        idx[t * k + j] = best;
+    }
+    if (kk == 1) {
+        gate[t * k] = 1.0f;
+    } else {
+        uint64_t tk = 0;
+        for (int j = 0; j < kk; ++j) {
+            double bv;
+            const int best = pick<EP>(lg, E, tk, bv);
+            tk |= 1ull << best;
+            gate[t * k + j] = static_cast<float>(exp(bv - top) / den);
+        }
+    }
+    for (int j = kk; j < k; ++j) {          // adaptive top-1: empty second slot
+        idx[t * k + j] = -1;
+        gate[t * k + j] = 0.0f;
+    }
+    return mine;
+}
+
 // 16 bytes per lane, global -> LDS at m0 + 16 * lane.  Inline asm, issued
 // before any other load of the wave: every later wait of the wave (the
 // compiler's, in issue order) also covers it.
@@ -117,8 +171,8 @@ typedef __attribute__((address_space(3))) uint32_t route_lds_word;
 template <typename Tin, int EG>
 __global__ __launch_bounds__(kRouteTile) void k_route(
     const Tin* __restrict__ x, const Tin* __restrict__ Wg, const float* __restrict__ bg, int64_t T,
-    int D, int E, int k, int32_t* __restrict__ idx, float* __restrict__ gate,
-    int32_t* __restrict__ tile_counts, int w_lds) {
+    int D, int E, int k, int adaptive, double tau, int32_t* __restrict__ idx,
+    float* __restrict__ gate, int32_t* __restrict__ tile_counts, int w_lds) {
     extern __shared__ __attribute__((aligned(16))) unsigned char s_w[];
     constexpr int EP = 16 * EG;                      // experts padded to MFMA rows
     constexpr int PER16 = Elem<Tin>::per16;
@@ -248,7 +302,13 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
         lg[e] += (bg != nullptr && e < E) ? static_cast<double>(bg[e]) : 0.0;
     // Rounding bound of every logit (S itself rounded up by 1%).
     const double beta = 2.0 * (kPart + 8) * 0x1p-24 * static_cast<double>(smax) * 1.01;
-    const bool certain = topk_gap<EP>(lg, E, k) > 2.0 * beta;
+    bool certain = topk_gap<EP>(lg, E, k) > 2.0 * beta;
+    if (adaptive && certain && tau > 0.0) {
+        // log of the confidence moves by at most 2 beta (l_max and the
+        // log-sum-exp by beta each): decide only outside that band
+        const double lp = log(route_confidence<EP>(lg, E));
+        certain = fabs(lp - log(tau)) > 2.0 * beta + 1e-12;
+    }
 
     // ---- exact recompute in double of the tokens that are not certified
     uint64_t todo = __ballot(valid && !certain);
@@ -324,30 +384,9 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
                 lg[e] = part[e] + ((bg != nullptr && e < E) ? static_cast<double>(bg[e]) : 0.0);
         }
     }
-    // ---- top-k, gates (softmax of the selected logits), outputs
+    // ---- top-k (or adaptive top-1 / top-2), gates, outputs
     uint64_t mine = 0;
-    if (valid) {
-        double top = 0.0, den = 0.0;
-        for (int j = 0; j < k; ++j) {
-            double bv;
-            const int best = pick<EP>(lg, E, mine, bv);
-            mine |= 1ull << best;
-            if (j == 0) top = bv;
-            den += exp(bv - top);
-            idx[t * k + j] = best;
-        }
-        if (k == 1) {
-            gate[t] = 1.0f;
-        } else {
-            uint64_t tk = 0;
-            for (int j = 0; j < k; ++j) {
-                double bv;
-                const int best = pick<EP>(lg, E, tk, bv);
-                tk |= 1ull << best;
-                gate[t * k + j] = static_cast<float>(exp(bv - top) / den);
-            }
-        }
-    }
+    if (valid) mine = route_select<EP>(lg, E, k, adaptive, tau, t, idx, gate);
     if (tile_counts != nullptr) {
         for (int e = 0; e < E; ++e) {
             const uint64_t m = __ballot((mine >> e) & 1ull);
@@ -363,11 +402,183 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
     }
 }
 
+// ---------------------------------------------------------------------------
+// MLP router (Sec. III Phase 4: one hidden layer, width d/6 in the paper):
+//     hr = round_storage(GELU(x Wh^T + bh)),   l = hr Wo^T + bo,
+// then the same top-k / adaptive choice as the linear router.  The hidden
+// layer is rounded to the storage type (where a real deployment keeps it),
+// and that rounding decides the logits to far more than the 1e-6 routing
+// margin, so it must be taken on the exact pre-activation: both products run
+// in double on the f64 MFMA (v_mfma_f64_16x16x4f64, the same 78.6 TFLOP/s as
+// the vector unit, fed by 16-byte loads), GELU uses the double erf, and the
+// rounding to bfloat16 is done straight from double (one rounding, ties to
+// even).  Storage products are exact in double; only the summation order
+// differs from a plain loop.
+//
+// Mapping: a workgroup of 4 waves routes 16 tokens; wave w forms hidden
+// units [16 i, 16 i + 16) for i = w, w + 4, ... (one 16 x 16 f64 MFMA tile
+// each), so a small token count still spreads over many waves.  In a D-chunk
+// of 4 x per16 columns, lane l loads 16 bytes of token row l % 16 and of
+// hidden row 16 i + l % 16 at column chunk l / 16, and feeds element s of
+// them as MFMA k-index l / 16 in sub-step s: A = tokens x k, B = k x hidden
+// units, the same (column, k) pairing on both sides.  Four chunks are loaded
+// before their MFMAs, so a wave waits once per 4 chunks.  The f64 MFMA's
+// result holds D[l / 16 + 4 v][l % 16] in value v of lane l.  The hidden
+// values meet in LDS; wave g < EG then forms logits of experts [16 g, 16 g +
+// 16), and the first 16 lanes of wave 0 take one token each for the choice.
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+constexpr int kMlpTokens = 16;             // tokens per workgroup
+constexpr int kMlpChunks = 4;              // 16-byte chunks in flight per lane
+static_assert(kMlpHiddenMax == 256, "LDS plan of k_route_mlp");
+
+__device__ __forceinline__ double mlp_gelu(double v) {
+    return 0.5 * v * (1.0 + erf(v * 0.70710678118654752440));
+}
+
+// double -> nearest bfloat16 (ties to even), returned as the exact float.
+__device__ __forceinline__ float round_to_bf16(double v) {
+    uint64_t u = static_cast<uint64_t>(__double_as_longlong(v));
+    u += ((uint64_t{1} << 44) - 1) + ((u >> 45) & 1);   // 45 of 52 mantissa bits dropped
+    u &= ~((uint64_t{1} << 45) - 1);
+    return static_cast<float>(__longlong_as_double(static_cast<long long>(u)));
+}
+template <typename Tin> __device__ float round_storage(double v);
+template <> __device__ __forceinline__ float round_storage<bf16_bits>(double v) { return round_to_bf16(v); }
+template <> __device__ __forceinline__ float round_storage<float>(double v) { return static_cast<float>(v); }
+
+// Element s of a 16-byte piece, widened to double (register shifts only: s
+// is a compile-time constant after unrolling).
+template <typename Tin> __device__ double elem_f64(const uint4& v, int s);
+template <>
+__device__ __forceinline__ double elem_f64<bf16_bits>(const uint4& v, int s) {
+    const uint32_t w = s < 2 ? v.x : s < 4 ? v.y : s < 6 ? v.z : v.w;
+    return static_cast<double>(__uint_as_float((s & 1) ? (w & 0xffff0000u) : (w << 16)));
+}
+template <>
+__device__ __forceinline__ double elem_f64<float>(const uint4& v, int s) {
+    const uint32_t w = s == 0 ? v.x : s == 1 ? v.y : s == 2 ? v.z : v.w;
+    return static_cast<double>(__uint_as_float(w));
+}
+
+template <typename Tin, int EG>
+__global__ __launch_bounds__(256) void k_route_mlp(
+    const Tin* __restrict__ x, const Tin* __restrict__ Wh, const float* __restrict__ bh,
+    const Tin* __restrict__ Wo, const float* __restrict__ bo, int64_t T, int D, int Hr, int E,
+    int k, int adaptive, double tau, int32_t* __restrict__ idx, float* __restrict__ gate) {
+    constexpr int EP = 16 * EG;
+    static_assert(EG <= 4, "one wave per 16 experts");
+    constexpr int PER16 = Elem<Tin>::per16;
+    constexpr int KC = 4 * PER16;                   // columns per 16-byte-per-lane chunk
+    __shared__ float s_hr[kMlpTokens][kMlpHiddenMax + 1];   // odd pitch: column reads spread
+    __shared__ double s_lg[kMlpTokens][EP + 1];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int row = lane & 15, grp = lane >> 4;
+    const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kMlpTokens;
+    const uint4* zp = reinterpret_cast<const uint4*>(g_route_zero);
+    const int64_t tr = t0 + row;                    // this lane's A row (token)
+    const Tin* xrow = tr < T ? x + tr * D : nullptr;
+
+    // ---- hidden layer: one 16-unit tile per wave per pass
+    for (int u0 = 16 * w; u0 < Hr; u0 += 64) {
+        // two accumulators (even / odd sub-steps) halve the dependent chain
+        f64x4 acc0 = f64x4{0.0, 0.0, 0.0, 0.0}, acc1 = acc0;
+        const int u = u0 + row;
+        const Tin* wrow = u < Hr ? Wh + static_cast<int64_t>(u) * D : nullptr;
+        for (int c0 = 0; c0 < D; c0 += kMlpChunks * KC) {
+            uint4 xv[kMlpChunks], wv[kMlpChunks];
+#pragma unroll
+            for (int c = 0; c < kMlpChunks; ++c) {
+                // D % PER16 == 0: a chunk is all in or out; out-of-range reads
+                // take a 16-byte zero page (one wide load either way)
+                const int col = c0 + c * KC + grp * PER16;
+                const bool cin = col < D;
+                xv[c] = *((xrow != nullptr && cin) ? reinterpret_cast<const uint4*>(xrow + col) : zp);
+                wv[c] = *((wrow != nullptr && cin) ? reinterpret_cast<const uint4*>(wrow + col) : zp);
+            }
+#pragma unroll
+            for (int c = 0; c < kMlpChunks; ++c)
+#pragma unroll
+                for (int s = 0; s < PER16; s += 2) {
+                    acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(elem_f64<Tin>(xv[c], s),
+                                                                elem_f64<Tin>(wv[c], s), acc0, 0, 0, 0);
+                    acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(elem_f64<Tin>(xv[c], s + 1),
+                                                                elem_f64<Tin>(wv[c], s + 1), acc1, 0, 0, 0);
+                }
+        }
+        const f64x4 acc = acc0 + acc1;
+        // + bias, GELU, one rounding to storage, into LDS (token-major)
+        if (u < Hr) {
+            const double b = bh != nullptr ? static_cast<double>(bh[u]) : 0.0;
+#pragma unroll
+            for (int v = 0; v < 4; ++v)              // result row = token grp + 4 v
+                s_hr[grp + 4 * v][u] = round_storage<Tin>(mlp_gelu(acc[v] + b));
+        }
+    }
+    __syncthreads();
+    // ---- output layer l = hr Wo^T (+ bo below): wave g, experts [16 g, 16 g + 16)
+    if (w < EG) {
+        f64x4 acc = f64x4{0.0, 0.0, 0.0, 0.0};
+        const int e = 16 * w + row;
+        const Tin* orow = e < E ? Wo + static_cast<int64_t>(e) * Hr : nullptr;
+        for (int j0 = 0; j0 < Hr; j0 += 4) {
+            const int j = j0 + grp;
+            const double a = j < Hr ? static_cast<double>(s_hr[row][j]) : 0.0;
+            const double b = (orow != nullptr && j < Hr) ? static_cast<double>(Elem<Tin>::load(orow, j)) : 0.0;
+            acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int v = 0; v < 4; ++v) s_lg[grp + 4 * v][16 * w + row] = acc[v];
+    }
+    __syncthreads();
+    // ---- one token per lane (16 lanes of wave 0): choice, gates, outputs
+    const int64_t t = t0 + lane;
+    if (w == 0 && lane < kMlpTokens && t < T) {
+        double lg[EP];
+#pragma unroll
+        for (int e = 0; e < EP; ++e)
+            lg[e] = s_lg[lane][e] + ((bo != nullptr && e < E) ? static_cast<double>(bo[e]) : 0.0);
+        (void)route_select<EP>(lg, E, k, adaptive, tau, t, idx, gate);
+    }
+}
+
+template <typename Tin>
+static hipError_t route_mlp_dt(const Tin* x, const Tin* Wh, const float* bh, const Tin* Wo,
+                               const float* bo, int64_t T, int D, int Hr, int E, int k,
+                               int adaptive, double tau, int32_t* idx, float* gate,
+                               hipStream_t st) {
+    const int64_t blocks = (T + kMlpTokens - 1) / kMlpTokens;
+    if (blocks == 0) return hipSuccess;
+    const dim3 grid(static_cast<unsigned>(blocks));
+    if (E <= 16)
+        k_route_mlp<Tin, 1><<<grid, 256, 0, st>>>(x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau, idx, gate);
+    else if (E <= 32)
+        k_route_mlp<Tin, 2><<<grid, 256, 0, st>>>(x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau, idx, gate);
+    else
+        k_route_mlp<Tin, 4><<<grid, 256, 0, st>>>(x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau, idx, gate);
+    return hipGetLastError();
+}
+
+hipError_t launch_route_mlp(int dtype, const void* x, const void* Wh, const float* bh,
+                            const void* Wo, const float* bo, int64_t T, int D, int Hr, int E,
+                            int k, int adaptive, double tau, int32_t* idx, float* gate,
+                            hipStream_t st) {
+    if (Hr < 1 || Hr > kMlpHiddenMax) return hipErrorInvalidValue;
+    if (dtype == 0)
+        return route_mlp_dt<float>(static_cast<const float*>(x), static_cast<const float*>(Wh), bh,
+                                   static_cast<const float*>(Wo), bo, T, D, Hr, E, k, adaptive,
+                                   tau, idx, gate, st);
+    return route_mlp_dt<bf16_bits>(static_cast<const bf16_bits*>(x),
+                                   static_cast<const bf16_bits*>(Wh), bh,
+                                   static_cast<const bf16_bits*>(Wo), bo, T, D, Hr, E, k, adaptive,
+                                   tau, idx, gate, st);
+}
+
 constexpr int64_t kRouteWLds = 32 * 1024;
 
 template <typename Tin>
 static hipError_t route_dt(const Tin* x, const Tin* Wg, const float* bg, int64_t T, int D, int E,
-                           int k, int32_t* idx, float* gate, int32_t* tc, hipStream_t st) {
+                           int k, int adaptive, double tau, int32_t* idx, float* gate,
+                           int32_t* tc, hipStream_t st) {
     const int64_t blocks = route_tiles(T);
     if (blocks == 0) return hipSuccess;
     const dim3 grid(static_cast<unsigned>(blocks));
@@ -375,22 +586,25 @@ static hipError_t route_dt(const Tin* x, const Tin* Wg, const float* bg, int64_t
     const int64_t wbytes = static_cast<int64_t>(E) * D * static_cast<int64_t>(sizeof(Tin));
     const int w_lds = wbytes <= kRouteWLds ? static_cast<int>((wbytes + 1023) / 1024 * 1024) : 0;
     if (E <= 16)
-        k_route<Tin, 1><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, idx, gate, tc, w_lds);
+        k_route<Tin, 1><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive, tau,
+                                                             idx, gate, tc, w_lds);
     else if (E <= 32)
-        k_route<Tin, 2><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, idx, gate, tc, w_lds);
+        k_route<Tin, 2><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive, tau,
+                                                             idx, gate, tc, w_lds);
     else
-        k_route<Tin, 4><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, idx, gate, tc, w_lds);
+        k_route<Tin, 4><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive, tau,
+                                                             idx, gate, tc, w_lds);
     return hipGetLastError();
 }
 
 hipError_t launch_route(int dtype, const void* x, const void* Wg, const float* bg, int64_t T,
-                        int D, int E, int k, int32_t* idx, float* gate, int32_t* tile_counts,
-                        hipStream_t st) {
+                        int D, int E, int k, int adaptive, double tau, int32_t* idx, float* gate,
+                        int32_t* tile_counts, hipStream_t st) {
     if (dtype == 0)
         return route_dt<float>(static_cast<const float*>(x), static_cast<const float*>(Wg), bg, T,
-                               D, E, k, idx, gate, tile_counts, st);
+                               D, E, k, adaptive, tau, idx, gate, tile_counts, st);
     return route_dt<bf16_bits>(static_cast<const bf16_bits*>(x), static_cast<const bf16_bits*>(Wg),
-                               bg, T, D, E, k, idx, gate, tile_counts, st);
+                               bg, T, D, E, k, adaptive, tau, idx, gate, tile_counts, st);
 }
 
 }  // namespace clearmoe

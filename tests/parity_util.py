@@ -78,3 +78,46 @@ def check_dispatch(idx_gpu, E, counts, offsets, perm, inv):
     assert np.array_equal(offsets, o)
     assert np.array_equal(perm, p)
     assert np.array_equal(inv, i)
+
+
+def gpu_router(L, d=None):
+    """A cm.Router for a layer dict (linear, or the "router" entry's MLP /
+    adaptive variant) and the device tensors it points at (keep them alive)."""
+    rt = L.get("router") or {"kind": "linear"}
+    keep = {"Wg": dev(L["Wg"]), "bg": dev(L["bg"])}
+    if rt["kind"] == "mlp":
+        keep["Wh"], keep["bh"] = dev(rt["Wh"]), dev(rt["bh"])
+    r = cm.make_router(keep["Wg"], keep["bg"], keep.get("Wh"), keep.get("bh"),
+                       adaptive=rt.get("adaptive", rt["kind"] == "adaptive"),
+                       tau=rt.get("tau", 0.0))
+    return r, keep
+
+
+def gpu_ffn_ex(L):
+    """The whole layer through clearmoe_ffn_forward_ex with the layer's router."""
+    d = layer_to_device(L)
+    T, k = L["cfg"].T, L["cfg"].k
+    r, keep = gpu_router(L)
+    idx = torch.empty((T, k), dtype=torch.int32, device="cuda")
+    gate = torch.empty((T, k), dtype=torch.float32, device="cuda")
+    y = cm.ffn_forward_ex(d["x"], d["W1"], d["b1"], d["US"], d["Vt"], d["b2"], d["P"], d["Q"], r,
+                          k, idx_out=idx, gate_out=gate)
+    torch.cuda.synchronize()
+    del keep
+    return dict(y=oracle.widen(cm.to_stored(y)), idx=idx.cpu().numpy(), gate=gate.cpu().numpy())
+
+
+def rounding_gap(v, dtype):
+    """Distance of each exact value to the nearest rounding midpoint of the
+    storage type, relative to the value's binade (0 = exactly halfway)."""
+    bits = 8 if dtype == "bf16" else 24
+    m, _ = np.frexp(np.asarray(v, dtype=np.float64))
+    frac = np.ldexp(np.abs(m), bits)
+    return np.abs(frac - np.floor(frac) - 0.5) * 2.0 ** -bits
+
+
+def confidence_gap(logits, tau):
+    """|log p - log tau| of the adaptive router's confidence p (inf if tau <= 0)."""
+    if tau <= 0:
+        return np.full(np.asarray(logits).shape[0], np.inf)
+    return np.abs(np.log(oracle.confidence(logits)) - np.log(tau))

@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert cm.version() == 1
+    assert cm.version() == 2
     L = cm.lib()
     assert L.clearmoe_status_string(0) == b"ok"
     assert L.clearmoe_status_string(3).startswith(b"workspace")
@@ -155,3 +155,54 @@ def test_padded_entry_point_workspace_and_rejections():
     assert L.clearmoe_ffn_forward_padded(ctypes.byref(s), *args, FAKE, n, None) == 3
     assert L.clearmoe_ffn_forward_padded(ctypes.byref(s), *args, FAKE, npad - 1, None) == 3
     assert L.clearmoe_ffn_forward_padded(ctypes.byref(s), *args, None, npad, None) == 3
+
+
+def _router(**kw):
+    d = dict(Wg=FAKE.value, bg=None, Wh=None, bh=None, hidden=0, adaptive=0, tau=0.0)
+    d.update(kw)
+    return cm.Router(d["Wg"], d["bg"], d["Wh"], d["bh"], d["hidden"], d["adaptive"], d["tau"])
+
+
+def test_router_descriptor_layout():
+    """The ctypes mirror of clearmoe_router: four pointers, two int32, one
+    double, no padding (48 bytes)."""
+    assert ctypes.sizeof(cm.Router) == 48
+    assert cm.Router.tau.offset == 40 and cm.Router.hidden.offset == 32
+
+
+def test_route_ex_and_ffn_ex_reject_bad_routers_before_launch():
+    L = cm.lib()
+    s = _shape()                                   # E = 4, k = 2
+    n = cm.workspace_bytes(s)
+    ok_args = (FAKE, FAKE, FAKE, FAKE, n, None)    # x, idx, gate, ws, bytes, stream
+
+    def route(r, shape=s):
+        return L.clearmoe_route_ex(ctypes.byref(shape), None if r is None else ctypes.byref(r),
+                                   *ok_args)
+    assert route(None) == 1                                         # no router
+    assert route(_router(Wg=None)) == 1                             # no output layer
+    assert route(_router(Wg=0x10002)) == 1                          # misaligned Wg
+    assert route(_router(hidden=-1)) == 1
+    assert route(_router(hidden=257, Wh=FAKE.value)) == 1           # above the MLP limit
+    assert route(_router(hidden=64)) == 1                           # MLP without Wh
+    assert route(_router(hidden=64, Wh=0x10008)) == 1               # misaligned Wh
+    assert route(_router(hidden=64, Wh=FAKE.value, bh=0x10001)) == 1
+    assert route(_router(adaptive=2)) == 1
+    assert route(_router(adaptive=1, tau=float("nan"))) == 1        # NaN threshold
+    assert route(_router(adaptive=1, tau=0.5), _shape(k=1)) == 1    # adaptive needs k = 2
+    assert route(_router(adaptive=1, tau=0.5), _shape(E=1, k=1)) == 1
+    assert L.clearmoe_route_ex(ctypes.byref(s), ctypes.byref(_router()), FAKE, FAKE, FAKE, FAKE,
+                               8, None) == 3                        # workspace too small
+    args = [FAKE] * 11
+    assert L.clearmoe_ffn_forward_ex(ctypes.byref(s), None, *args, FAKE, n, None) == 1
+    assert L.clearmoe_ffn_forward_ex(ctypes.byref(s), ctypes.byref(_router(hidden=300,
+                                     Wh=FAKE.value)), *args, FAKE, n, None) == 1
+    assert L.clearmoe_ffn_forward_ex(ctypes.byref(_shape(k=1)),
+                                     ctypes.byref(_router(adaptive=1, tau=0.9)), *args, FAKE, n,
+                                     None) == 1
+    a = list(args)
+    a[1] = None                                                     # NULL W1
+    assert L.clearmoe_ffn_forward_ex(ctypes.byref(s), ctypes.byref(_router()), *a, FAKE, n,
+                                     None) == 1
+    assert L.clearmoe_ffn_forward_ex(ctypes.byref(s), ctypes.byref(_router()), *args, FAKE, n - 1,
+                                     None) == 3
