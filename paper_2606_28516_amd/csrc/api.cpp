@@ -36,6 +36,7 @@ Layout layout(const clearmoe_shape& s) {
     Layout L{};
     const int64_t T = s.T, k = s.k, E = s.E;
     const int64_t ntiles = route_tiles(T);
+    const int64_t nhist = E > 0 ? hist_tiles(T, static_cast<int>(E)) : 0;   // 64- or 256-token tiles
     const size_t es = elem_size(s.dtype);
     size_t off = 0;
     auto take = [&](size_t bytes) {
@@ -45,7 +46,7 @@ Layout layout(const clearmoe_shape& s) {
     };
     // The histogram regions come first and depend on T and E only, so route and
     // dispatch calls with different D (or none) agree on where they are.
-    L.tile_counts = take(sizeof(int32_t) * (ntiles * E > 0 ? ntiles * E : 1));
+    L.tile_counts = take(sizeof(int32_t) * (nhist * E > 0 ? nhist * E : 1));
     L.tile_base = take(sizeof(int32_t) * (ntiles * E > 0 ? ntiles * E : 1));
     L.dispatch_end = off;
     L.counts = take(sizeof(int32_t) * E);
@@ -185,7 +186,7 @@ int dispatch_impl(const clearmoe_shape& s, const Layout& L, const int32_t* idx, 
     if (!hist_in_ws)
         CLEARMOE_STAGE(CLEARMOE_STAGE_TILE_HIST, st,
                        launch_tile_histogram(idx, s.T, s.E, s.k, tc, st));
-    if (nt * s.E <= kInlineScanMax) {
+    if (hist_tiles(s.T, s.E) * s.E <= kInlineScanMax) {
         // small histogram: the permutation scans it itself (one launch fewer)
         CLEARMOE_STAGE(CLEARMOE_STAGE_PERMUTE, st,
                        launch_permute(s.dtype, idx, tb, offsets, tc, counts, s.T, s.E, s.k, perm,

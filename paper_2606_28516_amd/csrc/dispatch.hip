@@ -35,21 +35,24 @@ __device__ __forceinline__ int wave_rank(bool ok, int ex, int E, int lane, int w
     return rank;
 }
 
-__global__ __launch_bounds__(kRouteTile) void k_tile_hist(const int32_t* __restrict__ idx,
-                                                          int64_t T, int E, int k,
-                                                          int32_t* __restrict__ tile_counts) {
-    __shared__ int s_wc[kWaves][64];
+// Expert histogram of one tile of TILE tokens (= TILE * k assignments), one
+// workgroup of TILE threads per tile.
+template <int TILE>
+__global__ __launch_bounds__(TILE) void k_tile_hist(const int32_t* __restrict__ idx, int64_t T,
+                                                     int E, int k,
+                                                     int32_t* __restrict__ tile_counts) {
+    constexpr int kW = TILE / 64;
+    __shared__ int s_wc[kW][64];
     __shared__ int s_run[64];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int64_t A = T * k;
-    const int64_t a0 = static_cast<int64_t>(blockIdx.x) * kRouteTile * k;
-    const int64_t na64 = A - a0 < static_cast<int64_t>(kRouteTile) * k ? A - a0
-                                                                         : static_cast<int64_t>(kRouteTile) * k;
+    const int64_t a0 = static_cast<int64_t>(blockIdx.x) * TILE * k;
+    const int64_t na64 = A - a0 < static_cast<int64_t>(TILE) * k ? A - a0 : static_cast<int64_t>(TILE) * k;
     const int na = static_cast<int>(na64);
     if (tid < E) s_run[tid] = 0;
     __syncthreads();
     for (int c = 0; c < k; ++c) {
-        const int al = c * kRouteTile + tid;
+        const int al = c * TILE + tid;
         const int ex = al < na ? idx[a0 + al] : -1;
         const bool ok = ex >= 0 && ex < E;
         (void)wave_rank(ok, ex, E, lane, w, s_wc);
@@ -57,7 +60,7 @@ __global__ __launch_bounds__(kRouteTile) void k_tile_hist(const int32_t* __restr
         if (tid < E) {
             int s = 0;
 #pragma unroll
-            for (int i = 0; i < kWaves; ++i) s += s_wc[i][tid];
+            for (int i = 0; i < kW; ++i) s += s_wc[i][tid];
             s_run[tid] += s;
         }
         __syncthreads();
@@ -126,17 +129,20 @@ __global__ __launch_bounds__(1024) void k_scan(const int32_t* __restrict__ tc, i
     }
 }
 
-// Stable permutation.  Tile bases come either from the scan kernel
-// (tile_base + offsets) or, when tile_counts is given (small histograms), from
-// an inline scan: every workgroup sums the histogram columns itself (LDS
-// integer atomics: exact and order independent) and workgroup 0 publishes
-// counts and offsets.
+// Stable permutation, one workgroup per 256 tokens.  Tile bases come either
+// from the scan kernel (tile_base + offsets, 256-token tiles) or, when
+// tile_counts is given (small histograms), from an inline scan: every
+// workgroup sums the histogram columns itself (LDS integer atomics: exact and
+// order independent; the histogram tiles hold htile tokens, 64 or 256, so a
+// workgroup's tokens start at histogram tile blockIdx * 256 / htile) and
+// workgroup 0 publishes counts and offsets.
 template <typename Tin>
 __global__ __launch_bounds__(kRouteTile) void k_permute(
     const int32_t* __restrict__ idx, const int32_t* __restrict__ tb,
     int32_t* __restrict__ offsets, const int32_t* __restrict__ tile_counts,
     int32_t* __restrict__ counts, int64_t T, int E, int k, int32_t* __restrict__ perm,
-    int32_t* __restrict__ inv, const Tin* __restrict__ x, Tin* __restrict__ xperm, int D) {
+    int32_t* __restrict__ inv, const Tin* __restrict__ x, Tin* __restrict__ xperm, int D,
+    int htile) {
     extern __shared__ int s_p[];          // [256 * k] destination of each assignment
     __shared__ int s_wc[kWaves][64];
     __shared__ int s_run[64];
@@ -155,13 +161,14 @@ __global__ __launch_bounds__(kRouteTile) void k_permute(
             s_tot[tid] = 0;
         }
         __syncthreads();
-        const int64_t nt = route_tiles(T);
+        const int64_t nt = (T + htile - 1) / htile;
+        const int64_t first = static_cast<int64_t>(blockIdx.x) * (kRouteTile / htile);
         for (int64_t i = tid; i < nt * E; i += kRouteTile) {
             const int64_t b = i / E;
             const int e = static_cast<int>(i - b * E);
             const int c = tile_counts[i];
             atomicAdd(&s_tot[e], c);
-            if (b < static_cast<int64_t>(blockIdx.x)) atomicAdd(&s_pre[e], c);
+            if (b < first) atomicAdd(&s_pre[e], c);
         }
         __syncthreads();
         if (tid == 0) {
@@ -377,9 +384,14 @@ __global__ __launch_bounds__(256) void k_combine_residual(const float* __restric
 
 hipError_t launch_tile_histogram(const int32_t* idx, int64_t T, int E, int k,
                                  int32_t* tile_counts, hipStream_t st) {
-    const int64_t nt = route_tiles(T);
+    const int64_t nt = hist_tiles(T, E);
     if (nt == 0) return hipSuccess;
-    k_tile_hist<<<dim3(static_cast<unsigned>(nt)), kRouteTile, 0, st>>>(idx, T, E, k, tile_counts);
+    if (hist_tile(T, E) == kSmallTile)
+        k_tile_hist<kSmallTile><<<dim3(static_cast<unsigned>(nt)), kSmallTile, 0, st>>>(idx, T, E, k,
+                                                                                        tile_counts);
+    else
+        k_tile_hist<kRouteTile><<<dim3(static_cast<unsigned>(nt)), kRouteTile, 0, st>>>(idx, T, E, k,
+                                                                                        tile_counts);
     return hipGetLastError();
 }
 
@@ -403,14 +415,15 @@ hipError_t launch_permute(int dtype, const int32_t* idx, const int32_t* tile_bas
     const int64_t nt = route_tiles(T);
     if (nt == 0) return hipSuccess;
     const size_t shm = sizeof(int) * static_cast<size_t>(kRouteTile) * k;
+    const int htile = hist_tile(T, E);
     if (dtype == 0)
         k_permute<float><<<dim3(static_cast<unsigned>(nt)), kRouteTile, shm, st>>>(
             idx, tile_base, offsets, tile_counts, counts, T, E, k, perm, inv,
-            static_cast<const float*>(x), static_cast<float*>(xperm), D);
+            static_cast<const float*>(x), static_cast<float*>(xperm), D, htile);
     else
         k_permute<bf16_bits><<<dim3(static_cast<unsigned>(nt)), kRouteTile, shm, st>>>(
             idx, tile_base, offsets, tile_counts, counts, T, E, k, perm, inv,
-            static_cast<const bf16_bits*>(x), static_cast<bf16_bits*>(xperm), D);
+            static_cast<const bf16_bits*>(x), static_cast<bf16_bits*>(xperm), D, htile);
     return hipGetLastError();
 }
 

@@ -61,12 +61,44 @@ __device__ __forceinline__ float gelu_erf(float v) {
     return fmaxf(v, 0.0f) - h;
 }
 
+// Raw buffer resources (gfx950): a 16-byte load at an offset outside
+// [0, bytes) returns zeros, so tails need neither branches nor a zero page,
+// and the loads stay in the vector-memory counter (a select between two
+// pointers of different address spaces turns loads into flat ones, which
+// also count against the 4-bit LDS/scalar counter and so stall a wave after
+// 15 outstanding loads).  bytes must be below 2^31.
+constexpr uint32_t kRawOob = 0x80000000u;        // an offset past every resource
+constexpr int kRawWord3 = 0x00020000;            // raw dword access
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* p, int64_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), static_cast<short>(0),
+                                             static_cast<int>(bytes), kRawWord3);
+}
+__device__ __forceinline__ uint4 raw_load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, 0));
+}
+
 // ---------------------------------------------------------------------------
 // Tiling constants shared by host and device code.
 // ---------------------------------------------------------------------------
-constexpr int kRouteTile = 256;      // tokens per routing / dispatch tile (one per thread)
+constexpr int kRouteTile = 256;      // tokens per dispatch tile (permutation workgroup)
+constexpr int kSmallTile = 64;       // tokens per histogram tile for small token counts
+// Largest tile histogram (tiles x experts) scanned inline by the permutation.
+constexpr int64_t kInlineScanMax = 8192;
 
 __host__ __device__ inline int64_t route_tiles(int64_t T) { return (T + kRouteTile - 1) / kRouteTile; }
+// Tokens per histogram tile (the router's workgroup): 64 when there are few
+// tokens (E <= 16 and the 64-token histogram still fits the permutation's
+// inline scan), so that a small token count spreads over four times as many
+// workgroups; otherwise 256.  A function of T and E only: the router and the
+// dispatch agree on it.
+__host__ __device__ inline int hist_tile(int64_t T, int E) {
+    return (E <= 16 && (T + kSmallTile - 1) / kSmallTile * E <= kInlineScanMax) ? kSmallTile : kRouteTile;
+}
+__host__ __device__ inline int64_t hist_tiles(int64_t T, int E) {
+    const int h = hist_tile(T, E);
+    return (T + h - 1) / h;
+}
 
 // ---------------------------------------------------------------------------
 // Host launchers (return hipError_t of the launch).
@@ -85,23 +117,23 @@ hipError_t launch_route_mlp(int dtype, const void* x, const void* Wh, const floa
                             int k, int adaptive, double tau, int32_t* idx, float* gate,
                             hipStream_t st);
 constexpr int kMlpHiddenMax = 256;
-// Per-tile expert histogram of an index array.
+// Per-tile expert histogram of an index array (tiles of hist_tile(T, E) tokens).
 hipError_t launch_tile_histogram(const int32_t* idx, int64_t T, int E, int k,
                                  int32_t* tile_counts, hipStream_t st);
 // Exclusive scan of tile histograms: tile_base[b][e] = sum_{b'<b} tile_counts[b'][e];
 // counts[e] = column sums; offsets[e] = exclusive scan of counts (offsets[E] = total).
 hipError_t launch_scan(const int32_t* tile_counts, int64_t ntiles, int E, int32_t* tile_base,
                        int32_t* counts, int32_t* offsets, hipStream_t st);
-// Stable permutation (and optional row copy x -> xperm).  With tile_counts
-// non-NULL the tile scan is done inline (tile_base unused) and counts/offsets
-// are written; otherwise tile_base/offsets come from launch_scan.  An index
+// Stable permutation (and optional row copy x -> xperm), one workgroup per
+// 256 tokens.  With tile_counts non-NULL the histogram (tiles of
+// hist_tile(T, E) tokens) is scanned inline (tile_base unused) and
+// counts/offsets are written; otherwise tile_base/offsets come from
+// launch_scan over 256-token tiles.  An index
 // of -1 is an empty slot: inv = -1, and perm[offsets[E] .. T*k) = -1.
 hipError_t launch_permute(int dtype, const int32_t* idx, const int32_t* tile_base,
                           int32_t* offsets, const int32_t* tile_counts, int32_t* counts,
                           int64_t T, int E, int k, int32_t* perm, int32_t* inv, const void* x,
                           void* xperm, int D, hipStream_t st);
-// Largest tile histogram (tiles x experts) scanned inline by the permutation.
-constexpr int64_t kInlineScanMax = 8192;
 // y[t] = sum_j gate[t,j] ye[inv[t*k+j]]  (ye, y in dtype).
 hipError_t launch_combine_gated(int dtype, const void* ye, const int32_t* inv, const float* gate,
                                 void* y, int64_t T, int D, int k, hipStream_t st);

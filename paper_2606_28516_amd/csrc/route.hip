@@ -26,6 +26,8 @@
 // and B = 16 token rows, each lane loading 16 contiguous bytes of a token row.
 // The 16 x 16 results go through LDS so that each lane owns one token for the
 // top-k, gates and the ballot histogram.
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace clearmoe {
@@ -66,6 +68,20 @@ template <> struct RouteMfma<float> {
     }
 };
 
+// Element s of a 16-byte piece, widened to double (register shifts only: s
+// is a compile-time constant after unrolling).
+template <typename Tin> __device__ double elem_f64(const uint4& v, int s);
+template <>
+__device__ __forceinline__ double elem_f64<bf16_bits>(const uint4& v, int s) {
+    const uint32_t w = s < 2 ? v.x : s < 4 ? v.y : s < 6 ? v.z : v.w;
+    return static_cast<double>(__uint_as_float((s & 1) ? (w & 0xffff0000u) : (w << 16)));
+}
+template <>
+__device__ __forceinline__ double elem_f64<float>(const uint4& v, int s) {
+    const uint32_t w = s == 0 ? v.x : s == 1 ? v.y : s == 2 ? v.z : v.w;
+    return static_cast<double>(__uint_as_float(w));
+}
+
 // One selection step over lg[0..E): the best expert not in `taken`
 // (logit descending, ties to the lower index: strict '>' while scanning up).
 // The first untaken expert seeds the scan, so NaN logits still give a choice.
@@ -100,6 +116,11 @@ __device__ __forceinline__ double topk_gap(const double (&lg)[EP], int E, int k)
     return gap;
 }
 
+// Double exp as one out-of-line routine: the choice code below calls it from
+// unrolled loops, and a single copy keeps the kernels' code (and so their
+// cold instruction-cache misses) small.
+__device__ __attribute__((noinline)) double exp_ool(double v) { return exp(v); }
+
 // Largest softmax probability of a token over its E logits,
 // 1 / sum_e exp(l_e - l_max): the confidence of the adaptive router.
 template <int EP>
@@ -111,7 +132,7 @@ __device__ __forceinline__ double route_confidence(const double (&lg)[EP], int E
     double den = 0.0;
 #pragma unroll
     for (int e = 0; e < EP; ++e)
-        if (e < E) den += exp(lg[e] - lmax);
+        if (e < E) den += exp_ool(lg[e] - lmax);
     return 1.0 / den;
 }
 
@@ -133,7 +154,7 @@ __device__ __forceinline__ uint64_t route_select(const double (&lg)[EP], int E, 
         const int best = pick<EP>(lg, E, mine, bv);
         mine |= 1ull << best;
         if (j == 0) top = bv;
-        den += exp(bv - top);
+        den += exp_ool(bv - top);
         idx[t * k + j] = best;
     }
     if (kk == 1) {
@@ -144,7 +165,7 @@ __device__ __forceinline__ uint64_t route_select(const double (&lg)[EP], int E, 
             double bv;
             const int best = pick<EP>(lg, E, tk, bv);
             tk |= 1ull << best;
-            gate[t * k + j] = static_cast<float>(exp(bv - top) / den);
+            gate[t * k + j] = static_cast<float>(exp_ool(bv - top) / den);
         }
     }
     for (int j = kk; j < k; ++j) {          // adaptive top-1: empty second slot
@@ -168,8 +189,9 @@ typedef __attribute__((address_space(3))) uint32_t route_lds_word;
 
 // w_lds > 0: the router matrix (E x D, w_lds bytes of dynamic LDS) is copied to
 // LDS for the exact recompute of uncertified tokens.
-template <typename Tin, int EG>
-__global__ __launch_bounds__(kRouteTile) void k_route(
+template <typename Tin, int EG, int NB, int KP>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(EG == 1 ? 2 : 1)))
+void k_route(
     const Tin* __restrict__ x, const Tin* __restrict__ Wg, const float* __restrict__ bg, int64_t T,
     int D, int E, int k, int adaptive, double tau, int32_t* __restrict__ idx,
     float* __restrict__ gate, int32_t* __restrict__ tile_counts, int w_lds) {
@@ -178,19 +200,33 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
     constexpr int PER16 = Elem<Tin>::per16;
     constexpr int KS = RouteMfma<Tin>::kstep;
     constexpr int kPart = RouteMfma<Tin>::kpart;
-    __shared__ double s_l[kRouteTile / 64][64][17];
-    __shared__ float s_s[kRouteTile / 64][64][4 * EG + 1];
-    __shared__ int s_wcnt[kRouteTile / 64][64];
+    constexpr int kWaves = 4;
+    constexpr int kTok = 16 * NB;                    // tokens per wave
+    constexpr int kTile = kWaves * kTok;             // tokens per workgroup = histogram tile
+    static_assert(kTile == kRouteTile || kTile == kSmallTile, "histogram tile sizes");
+    __shared__ double s_l[kWaves][64][17];           // kTok rows; 64 for the recompute's sums
+    __shared__ float s_s[kWaves][kTok][4 * EG + 1];
+    __shared__ int s_wcnt[kWaves][64];
+    __shared__ double s_fb[kWaves][4][EP];           // recomputed logits of a batch
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int col = lane & 15, grp = lane >> 4;
-    const int64_t tw = static_cast<int64_t>(blockIdx.x) * kRouteTile + w * 64;  // wave's first token
+    const int64_t tw = static_cast<int64_t>(blockIdx.x) * kTile + w * kTok;  // wave's first token
+    // this tile's x rows and the router rows as raw buffers (zeros outside)
+    constexpr int esz = static_cast<int>(sizeof(Tin));
+    const int64_t tile0 = static_cast<int64_t>(blockIdx.x) * kTile;
+    const int rows = static_cast<int>(T - tile0 < kTile ? T - tile0 : kTile);
+    const __amdgpu_buffer_rsrc_t rx = raw_rsrc(x + tile0 * D, static_cast<int64_t>(rows) * D * esz);
+    const __amdgpu_buffer_rsrc_t rw = raw_rsrc(Wg, static_cast<int64_t>(E) * D * esz);
+    __shared__ double bgv[EP];                       // router bias, loaded up front (read
+    if (tid < EP)                                    // after the transposes' barriers)
+        bgv[tid] = (bg != nullptr && tid < E) ? static_cast<double>(bg[tid]) : 0.0;
 
     if (w_lds > 0) {                               // router rows -> LDS (read after a barrier)
         const int64_t wbytes = static_cast<int64_t>(E) * D * static_cast<int>(sizeof(Tin));
         const uint32_t base_l =
             static_cast<uint32_t>(reinterpret_cast<uintptr_t>((route_lds_word*)s_w));
-        for (int base = w * 64; base * 16 < w_lds; base += kRouteTile) {
+        for (int base = w * 64; base * 16 < w_lds; base += 64 * kWaves) {
             const int64_t off = static_cast<int64_t>(base + lane) * 16;
             const void* src = off < wbytes ? static_cast<const void*>(
                                                  reinterpret_cast<const unsigned char*>(Wg) + off)
@@ -199,45 +235,40 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
         }
     }
 
-    f32x4 acc[EG][4], aab[EG][4];
-    double lacc[EG][4][4];             // double sums of the float32 partials
+    f32x4 acc[EG][NB], aab[EG][NB];
+    double lacc[EG][NB][4];            // double sums of the float32 partials
 #pragma unroll
     for (int g = 0; g < EG; ++g)
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
+        for (int b = 0; b < NB; ++b)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 acc[g][b][v] = aab[g][b][v] = 0.0f;
                 lacc[g][b][v] = 0.0;
             }
 
-    // Loads of step s (KS columns of d) for the wave's 4 token blocks and the
+    // Loads of step s (KS columns of d) for the wave's NB token blocks and the
     // router rows.  A ring of kPre steps keeps several steps in flight; the loop
     // is branch-free (steps past D and rows past T read a 16-byte zero page),
     // so the compiler's waits stay per round instead of per step.  Every
     // kPart columns the float32 partials move into double.
-    constexpr int kPre = KPRE;
+    constexpr int kPre = KP;
     static_assert((kPre * KS) % kPart == 0 && kPart % KS == 0, "partials align with rounds");
     const int nsteps = (D + KS - 1) / KS;
     const int nround = (nsteps + kPre - 1) / kPre;
-    const uint4* zp = reinterpret_cast<const uint4*>(g_route_zero);
-    uint4 xr[kPre][4], wr[kPre][EG];
-    auto load_step = [&](int s, uint4 (&xv)[4], uint4 (&wv)[EG]) {
+    uint4 xr[kPre][NB], wr[kPre][EG];
+    auto load_step = [&](int s, uint4 (&xv)[NB], uint4 (&wv)[EG]) {
         const int dd = s * KS + grp * PER16;
         const bool din = dd < D;
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
-            const int64_t t = tw + 16 * b + col;
-            const uint4* src = (din && t < T) ? reinterpret_cast<const uint4*>(x + t * D + dd) : zp;
-            xv[b] = *src;
+        for (int b = 0; b < NB; ++b) {
+            const int tr = w * kTok + 16 * b + col;      // row within the tile
+            xv[b] = raw_load16(rx, (din && tr < rows) ? static_cast<uint32_t>((tr * D + dd) * esz) : kRawOob);
         }
 #pragma unroll
         for (int g = 0; g < EG; ++g) {
             const int e = 16 * g + col;
-            const uint4* src = (din && e < E)
-                                   ? reinterpret_cast<const uint4*>(Wg + static_cast<int64_t>(e) * D + dd)
-                                   : zp;
-            wv[g] = *src;
+            wv[g] = raw_load16(rw, (din && e < E) ? static_cast<uint32_t>((e * D + dd) * esz) : kRawOob);
         }
     };
 #pragma unroll
@@ -249,7 +280,7 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
             for (int g = 0; g < EG; ++g) {
                 const uint4 wa = RouteMfma<Tin>::absv(wr[i][g]);
 #pragma unroll
-                for (int b = 0; b < 4; ++b) {
+                for (int b = 0; b < NB; ++b) {
                     RouteMfma<Tin>::step(wr[i][g], xr[i][b], acc[g][b]);
                     RouteMfma<Tin>::step(wa, RouteMfma<Tin>::absv(xr[i][b]), aab[g][b]);
                 }
@@ -259,7 +290,7 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
 #pragma unroll
                 for (int g = 0; g < EG; ++g)
 #pragma unroll
-                    for (int b = 0; b < 4; ++b)
+                    for (int b = 0; b < NB; ++b)
 #pragma unroll
                         for (int v = 0; v < 4; ++v) {
                             lacc[g][b][v] += static_cast<double>(acc[g][b][v]);
@@ -269,20 +300,21 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
         }
     }
     // C of a 16x16 MFMA: lane holds column lane%16 (token), rows 4*(lane/16)+v
-    // (experts).  Through LDS, one 16-expert group at a time, each lane takes
-    // the logits of one token; for S only each lane's maximum over its four
-    // experts is exchanged.
+    // (experts).  Through LDS, one 16-expert group at a time, each of the
+    // wave's first kTok lanes takes the logits of one token; for S only each
+    // lane's maximum over its four experts is exchanged.
     const int64_t t = tw + lane;
-    const bool valid = t < T;
+    const bool valid = lane < kTok && t < T;
+    const int tl = lane < kTok ? lane : kTok - 1;    // lanes past the wave's tokens idle
     double lg[EP];
 #pragma unroll
     for (int g = 0; g < EG; ++g) {
 #pragma unroll
-        for (int b = 0; b < 4; ++b)
+        for (int b = 0; b < NB; ++b)
 #pragma unroll
             for (int v = 0; v < 4; ++v) s_l[w][16 * b + col][4 * grp + v] = lacc[g][b][v];
 #pragma unroll
-        for (int b = 0; b < 4; ++b) {
+        for (int b = 0; b < NB; ++b) {
             float m = 0.0f;
 #pragma unroll
             for (int v = 0; v < 4; ++v)
@@ -291,15 +323,14 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
         }
         __syncthreads();
 #pragma unroll
-        for (int e = 0; e < 16; ++e) lg[16 * g + e] = s_l[w][lane][e];
+        for (int e = 0; e < 16; ++e) lg[16 * g + e] = s_l[w][tl][e];
         __syncthreads();
     }
     float smax = 0.0f;
 #pragma unroll
-    for (int i = 0; i < 4 * EG; ++i) smax = fmaxf(smax, s_s[w][lane][i]);
+    for (int i = 0; i < 4 * EG; ++i) smax = fmaxf(smax, s_s[w][tl][i]);
 #pragma unroll
-    for (int e = 0; e < EP; ++e)
-        lg[e] += (bg != nullptr && e < E) ? static_cast<double>(bg[e]) : 0.0;
+    for (int e = 0; e < EP; ++e) lg[e] += bgv[e];
     // Rounding bound of every logit (S itself rounded up by 1%).
     const double beta = 2.0 * (kPart + 8) * 0x1p-24 * static_cast<double>(smax) * 1.01;
     bool certain = topk_gap<EP>(lg, E, k) > 2.0 * beta;
@@ -310,79 +341,96 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
         certain = fabs(lp - log(tau)) > 2.0 * beta + 1e-12;
     }
 
-    // ---- exact recompute in double of the tokens that are not certified
+    // ---- exact recompute in double of the tokens that are not certified.
+    //      A batch takes nb = 1, 2 or 4 of them (as many as are left, up to
+    //      4); lane group q = lane / G (G = 64 / nb lanes) takes the q-th, lane
+    //      r = lane % G its 16-byte chunks r, r + G, ... (the loads of a pass
+    //      issued first, each x chunk widened once), router rows from LDS when
+    //      they fit; a G-lane butterfly sums each group, and the sums reach the
+    //      owner lane through LDS.  One uncertified token (the usual case)
+    //      thus has the whole wave.  The loops over experts and chunks are
+    //      left rolled: this path is rare and runs from a cold instruction
+    //      cache, so its code is kept small.
     uint64_t todo = __ballot(valid && !certain);
     while (todo != 0ull) {
-        const int owner = __ffsll(static_cast<long long>(todo)) - 1;
-        todo &= todo - 1ull;
-        const int64_t to = tw + owner;
+        const int left = __popcll(todo);
+        const int nb = left >= 4 ? 4 : (left >= 2 ? 2 : 1);
+        const int G = 64 / nb;
+        int myq = -1, src_tok[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            src_tok[q] = -1;
+            if (q < nb) {
+                const int o = __ffsll(static_cast<long long>(todo)) - 1;
+                todo &= todo - 1ull;
+                src_tok[q] = o;
+                if (lane == o) myq = q;
+            }
+        }
+        const int q = lane / G, r = lane - q * G;
+        const int mine_tok = q == 0 ? src_tok[0] : q == 1 ? src_tok[1] : q == 2 ? src_tok[2] : src_tok[3];
+        const int trow = w * kTok + mine_tok;          // row within the tile
+        const int nch = D / PER16;                     // 16-byte chunks of a row
+        // all experts in one pass over the lane's chunks (x loaded and widened
+        // once per chunk), then one butterfly for all of them, so the
+        // experts' shuffles overlap instead of forming E dependent chains
         double part[EP];
 #pragma unroll
         for (int e = 0; e < EP; ++e) part[e] = 0.0;
-        if (w_lds > 0) {
-            // router rows from LDS: only the token's x row comes from memory
-            const Tin* wl = reinterpret_cast<const Tin*>(s_w);
-            constexpr int kU = 8;                      // d = lane + 64 i, per lane per round
-            for (int d0 = 0; d0 < D; d0 += 64 * kU) {
-                float xv[kU];
+#pragma unroll 1
+        for (int c = r; c - r < nch; c += G) {
+            const bool in = mine_tok >= 0 && c < nch;
+            const uint4 xv = raw_load16(rx, in ? static_cast<uint32_t>((trow * D + c * PER16) * esz) : kRawOob);
+            const int cc = c < nch ? c : 0;            // past the row: zero x, any valid W chunk
+            double xd[PER16];
 #pragma unroll
-                for (int i = 0; i < kU; ++i) {
-                    const int d = d0 + lane + 64 * i;
-                    const float xr = Elem<Tin>::load(x, to * D + (d < D ? d : D - 1));
-                    xv[i] = d < D ? xr : 0.0f;
-                }
+            for (int i = 0; i < PER16; ++i) xd[i] = elem_f64<Tin>(xv, i);
 #pragma unroll
-                for (int i = 0; i < kU; ++i) {
-                    const int d = d0 + lane + 64 * i;
-                    const int dc = d < D ? d : D - 1;
+            for (int e = 0; e < EP; ++e) {
+                if (e < E) {                           // uniform
+                    const int64_t at = static_cast<int64_t>(e) * D + cc * PER16;
+                    uint4 wv;
+                    if (w_lds > 0)
+                        wv = *reinterpret_cast<const uint4*>(s_w + at * static_cast<int64_t>(sizeof(Tin)));
+                    else
+                        wv = raw_load16(rw, static_cast<uint32_t>(at * esz));
 #pragma unroll
-                    for (int e = 0; e < EP; ++e) {
-                        const int ec = e < E ? e : E - 1;
-                        part[e] = __builtin_fma(static_cast<double>(xv[i]),
-                                                static_cast<double>(Elem<Tin>::load(wl, ec * D + dc)),
-                                                part[e]);
-                    }
+                    for (int i = 0; i < PER16; ++i)
+                        part[e] = __builtin_fma(xd[i], elem_f64<Tin>(wv, i), part[e]);
                 }
             }
-        } else {
-        constexpr int kFallU = EP <= 16 ? 4 : 1;   // d = lane + 64 i, per lane per round
-        for (int d0 = 0; d0 < D; d0 += 64 * kFallU) {
-            // Branch-free: out-of-range columns / experts load a clamped (valid)
-            // address and are zeroed afterwards, so all loads of a round are in
-            // flight together.
-            float xv[kFallU], wv[kFallU][EP];
+        }
+        // sums over each group's G lanes through LDS (this wave's transpose
+        // rows, free by now): lane (q, e) adds its group's column e
+        double* red = &s_l[w][0][0];                  // [64 lanes][16 experts], pitch 17
 #pragma unroll
-            for (int i = 0; i < kFallU; ++i) {
-                const int d = d0 + lane + 64 * i;
-                const int dc = d < D ? d : D - 1;
-                const float xr = Elem<Tin>::load(x, to * D + dc);
-                xv[i] = d < D ? xr : 0.0f;
+        for (int g = 0; g < EG; ++g) {
 #pragma unroll
-                for (int e = 0; e < EP; ++e) {
-                    const int ec = e < E ? e : E - 1;
-                    wv[i][e] = Elem<Tin>::load(Wg, static_cast<int64_t>(ec) * D + dc);
+            for (int e = 0; e < 16; ++e)
+                if (16 * g + e < E) red[lane * 17 + e] = part[16 * g + e];
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            if (lane < 16 * nb) {
+                const int qq = lane >> 4, e = lane & 15;
+                if (16 * g + e < E) {
+                    double acc = 0.0;
+                    for (int j = 0; j < G; ++j) acc += red[(qq * G + j) * 17 + e];
+                    s_fb[w][qq][16 * g + e] = acc;
                 }
             }
-#pragma unroll
-            for (int i = 0; i < kFallU; ++i)
-#pragma unroll
-                for (int e = 0; e < EP; ++e)
-                    part[e] = __builtin_fma(static_cast<double>(xv[i]), static_cast<double>(wv[i][e]),
-                                            part[e]);
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
         }
-        }
-#pragma unroll
-        for (int e = 0; e < EP; ++e) {
-            if (e < E) {                           // uniform: the loop stays unrolled
-#pragma unroll
-                for (int o = 32; o >= 1; o >>= 1) part[e] += __shfl_xor(part[e], o);
-            }
-        }
-        if (lane == owner) {
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+        if (myq >= 0) {
 #pragma unroll
             for (int e = 0; e < EP; ++e)
-                lg[e] = part[e] + ((bg != nullptr && e < E) ? static_cast<double>(bg[e]) : 0.0);
+                if (e < E) lg[e] = s_fb[w][myq][e] + bgv[e];
         }
+        __builtin_amdgcn_wave_barrier();
     }
     // ---- top-k (or adaptive top-1 / top-2), gates, outputs
     uint64_t mine = 0;
@@ -396,7 +444,7 @@ __global__ __launch_bounds__(kRouteTile) void k_route(
         if (tid < E) {
             int s = 0;
 #pragma unroll
-            for (int i = 0; i < kRouteTile / 64; ++i) s += s_wcnt[i][tid];
+            for (int i = 0; i < kWaves; ++i) s += s_wcnt[i][tid];
             tile_counts[static_cast<int64_t>(blockIdx.x) * E + tid] = s;
         }
     }
@@ -431,7 +479,7 @@ constexpr int kMlpTokens = 16;             // tokens per workgroup
 constexpr int kMlpChunks = 4;              // 16-byte chunks in flight per lane
 static_assert(kMlpHiddenMax == 256, "LDS plan of k_route_mlp");
 
-__device__ __forceinline__ double mlp_gelu(double v) {
+__device__ __attribute__((noinline)) double mlp_gelu(double v) {
     return 0.5 * v * (1.0 + erf(v * 0.70710678118654752440));
 }
 
@@ -445,20 +493,6 @@ __device__ __forceinline__ float round_to_bf16(double v) {
 template <typename Tin> __device__ float round_storage(double v);
 template <> __device__ __forceinline__ float round_storage<bf16_bits>(double v) { return round_to_bf16(v); }
 template <> __device__ __forceinline__ float round_storage<float>(double v) { return static_cast<float>(v); }
-
-// Element s of a 16-byte piece, widened to double (register shifts only: s
-// is a compile-time constant after unrolling).
-template <typename Tin> __device__ double elem_f64(const uint4& v, int s);
-template <>
-__device__ __forceinline__ double elem_f64<bf16_bits>(const uint4& v, int s) {
-    const uint32_t w = s < 2 ? v.x : s < 4 ? v.y : s < 6 ? v.z : v.w;
-    return static_cast<double>(__uint_as_float((s & 1) ? (w & 0xffff0000u) : (w << 16)));
-}
-template <>
-__device__ __forceinline__ double elem_f64<float>(const uint4& v, int s) {
-    const uint32_t w = s == 0 ? v.x : s == 1 ? v.y : s == 2 ? v.z : v.w;
-    return static_cast<double>(__uint_as_float(w));
-}
 
 template <typename Tin, int EG>
 __global__ __launch_bounds__(256) void k_route_mlp(
@@ -474,26 +508,26 @@ __global__ __launch_bounds__(256) void k_route_mlp(
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int row = lane & 15, grp = lane >> 4;
     const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kMlpTokens;
-    const uint4* zp = reinterpret_cast<const uint4*>(g_route_zero);
-    const int64_t tr = t0 + row;                    // this lane's A row (token)
-    const Tin* xrow = tr < T ? x + tr * D : nullptr;
+    constexpr int esz = static_cast<int>(sizeof(Tin));
+    const int rows = static_cast<int>(T - t0 < kMlpTokens ? T - t0 : kMlpTokens);
+    const __amdgpu_buffer_rsrc_t rx = raw_rsrc(x + t0 * D, static_cast<int64_t>(rows) * D * esz);
+    const __amdgpu_buffer_rsrc_t rh = raw_rsrc(Wh, static_cast<int64_t>(Hr) * D * esz);
 
     // ---- hidden layer: one 16-unit tile per wave per pass
     for (int u0 = 16 * w; u0 < Hr; u0 += 64) {
         // two accumulators (even / odd sub-steps) halve the dependent chain
         f64x4 acc0 = f64x4{0.0, 0.0, 0.0, 0.0}, acc1 = acc0;
         const int u = u0 + row;
-        const Tin* wrow = u < Hr ? Wh + static_cast<int64_t>(u) * D : nullptr;
         for (int c0 = 0; c0 < D; c0 += kMlpChunks * KC) {
             uint4 xv[kMlpChunks], wv[kMlpChunks];
 #pragma unroll
             for (int c = 0; c < kMlpChunks; ++c) {
-                // D % PER16 == 0: a chunk is all in or out; out-of-range reads
-                // take a 16-byte zero page (one wide load either way)
+                // D % PER16 == 0: a chunk is all in or out; rows past T or Hr
+                // and columns past D read zeros from the raw buffers
                 const int col = c0 + c * KC + grp * PER16;
                 const bool cin = col < D;
-                xv[c] = *((xrow != nullptr && cin) ? reinterpret_cast<const uint4*>(xrow + col) : zp);
-                wv[c] = *((wrow != nullptr && cin) ? reinterpret_cast<const uint4*>(wrow + col) : zp);
+                xv[c] = raw_load16(rx, (cin && row < rows) ? static_cast<uint32_t>((row * D + col) * esz) : kRawOob);
+                wv[c] = raw_load16(rh, (cin && u < Hr) ? static_cast<uint32_t>((u * D + col) * esz) : kRawOob);
             }
 #pragma unroll
             for (int c = 0; c < kMlpChunks; ++c)
@@ -575,25 +609,30 @@ hipError_t launch_route_mlp(int dtype, const void* x, const void* Wh, const floa
 
 constexpr int64_t kRouteWLds = 32 * 1024;
 
+
 template <typename Tin>
 static hipError_t route_dt(const Tin* x, const Tin* Wg, const float* bg, int64_t T, int D, int E,
                            int k, int adaptive, double tau, int32_t* idx, float* gate,
                            int32_t* tc, hipStream_t st) {
-    const int64_t blocks = route_tiles(T);
+    const int64_t blocks = hist_tiles(T, E);
     if (blocks == 0) return hipSuccess;
     const dim3 grid(static_cast<unsigned>(blocks));
+    const bool small = hist_tile(T, E) == kSmallTile;   // implies E <= 16
     // the router rows go to LDS when they fit in kRouteWLds (whole 1 KB rounds)
     const int64_t wbytes = static_cast<int64_t>(E) * D * static_cast<int64_t>(sizeof(Tin));
     const int w_lds = wbytes <= kRouteWLds ? static_cast<int>((wbytes + 1023) / 1024 * 1024) : 0;
-    if (E <= 16)
-        k_route<Tin, 1><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive, tau,
-                                                             idx, gate, tc, w_lds);
+    if (small)
+        k_route<Tin, 1, 1, 12><<<grid, 256, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive, tau, idx,
+                                                          gate, tc, w_lds);
+    else if (E <= 16)
+        k_route<Tin, 1, 4, KPRE><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive,
+                                                                   tau, idx, gate, tc, w_lds);
     else if (E <= 32)
-        k_route<Tin, 2><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive, tau,
-                                                             idx, gate, tc, w_lds);
+        k_route<Tin, 2, 4, KPRE><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive,
+                                                                   tau, idx, gate, tc, w_lds);
     else
-        k_route<Tin, 4><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive, tau,
-                                                             idx, gate, tc, w_lds);
+        k_route<Tin, 4, 4, KPRE><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive,
+                                                                   tau, idx, gate, tc, w_lds);
     return hipGetLastError();
 }
 
