@@ -22,7 +22,7 @@ size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 // Workspace layout.  Prefix shared by every entry point, then the buffers of
 // the whole-layer forward.
 struct Layout {
-    size_t tile_counts, tile_base;                // route / dispatch
+    size_t tile_counts, tile_base, chunk_tot;     // route / dispatch
     size_t counts, offsets, idx, gate, perm, inv;  // ffn_forward
     size_t z, tproj, hsh, u, hres, tu;
     size_t dispatch_end, total;
@@ -48,6 +48,7 @@ Layout layout(const clearmoe_shape& s) {
     // dispatch calls with different D (or none) agree on where they are.
     L.tile_counts = take(sizeof(int32_t) * (nhist * E > 0 ? nhist * E : 1));
     L.tile_base = take(sizeof(int32_t) * (ntiles * E > 0 ? ntiles * E : 1));
+    L.chunk_tot = take(sizeof(int32_t) * (scan_chunks(ntiles) * E > 0 ? scan_chunks(ntiles) * E : 1));
     L.dispatch_end = off;
     L.counts = take(sizeof(int32_t) * E);
     L.offsets = take(sizeof(int32_t) * (E + 1));
@@ -189,13 +190,14 @@ int dispatch_impl(const clearmoe_shape& s, const Layout& L, const int32_t* idx, 
     if (hist_tiles(s.T, s.E) * s.E <= kInlineScanMax) {
         // small histogram: the permutation scans it itself (one launch fewer)
         CLEARMOE_STAGE(CLEARMOE_STAGE_PERMUTE, st,
-                       launch_permute(s.dtype, idx, tb, offsets, tc, counts, s.T, s.E, s.k, perm,
-                                      inv, x, xperm, s.D, st));
+                       launch_permute(s.dtype, idx, tb, nullptr, offsets, tc, counts, s.T, s.E,
+                                      s.k, perm, inv, x, xperm, s.D, st));
     } else {
-        CLEARMOE_STAGE(CLEARMOE_STAGE_SCAN, st, launch_scan(tc, nt, s.E, tb, counts, offsets, st));
+        int32_t* ct = at<int32_t>(ws, L.chunk_tot);
+        CLEARMOE_STAGE(CLEARMOE_STAGE_SCAN, st, launch_scan(tc, nt, s.E, tb, ct, st));
         CLEARMOE_STAGE(CLEARMOE_STAGE_PERMUTE, st,
-                       launch_permute(s.dtype, idx, tb, offsets, nullptr, counts, s.T, s.E, s.k,
-                                      perm, inv, x, xperm, s.D, st));
+                       launch_permute(s.dtype, idx, tb, ct, offsets, nullptr, counts, s.T, s.E,
+                                      s.k, perm, inv, x, xperm, s.D, st));
     }
     return CLEARMOE_OK;
 }

@@ -68,64 +68,53 @@ __global__ __launch_bounds__(TILE) void k_tile_hist(const int32_t* __restrict__ 
     if (tid < E) tile_counts[static_cast<int64_t>(blockIdx.x) * E + tid] = s_run[tid];
 }
 
-// One workgroup: exclusive scan over tiles of every expert column at once.
-// 1024 tiles per pass, one per thread; a thread holds its tile's histogram
-// (EP >= E registers), the wave scans it with shuffles, wave totals and the
-// running carry of earlier passes live in LDS.
+// Exclusive scan over tiles of every expert column at once, in chunks of
+// kScanChunk tiles: workgroup c scans tiles [c kScanChunk, (c + 1)
+// kScanChunk), one per thread (a thread holds its tile's histogram, EP >= E
+// registers; the wave scans it with shuffles, wave totals meet in LDS), and
+// writes the within-chunk exclusive prefixes tb and the chunk's totals.  The
+// permutation adds the chunk prefixes, so every chunk runs in parallel.
+constexpr int kScanChunk = 256;
+
 template <int EP>
-__global__ __launch_bounds__(1024) void k_scan(const int32_t* __restrict__ tc, int64_t ntiles,
-                                               int E, int32_t* __restrict__ tb,
-                                               int32_t* __restrict__ counts,
-                                               int32_t* __restrict__ offsets) {
-    __shared__ int s_wsum[16][EP];
-    __shared__ int s_carry[EP];
+__global__ __launch_bounds__(kScanChunk) void k_scan(const int32_t* __restrict__ tc, int64_t ntiles,
+                                                     int E, int32_t* __restrict__ tb,
+                                                     int32_t* __restrict__ chunk_tot) {
+    constexpr int kW = kScanChunk / 64;
+    __shared__ int s_wsum[kW][EP];
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    if (tid < EP) s_carry[tid] = 0;
-    __syncthreads();
-    for (int64_t b0 = 0; b0 < ntiles; b0 += 1024) {
-        const int64_t b = b0 + tid;
-        const bool in = b < ntiles;
-        int v[EP], c[EP];
+    const int64_t b = static_cast<int64_t>(blockIdx.x) * kScanChunk + tid;
+    const bool in = b < ntiles;
+    int v[EP], c[EP];
 #pragma unroll
-        for (int e = 0; e < EP; ++e) {
-            c[e] = (in && e < E) ? tc[b * E + e] : 0;
-            v[e] = c[e];
-        }
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-#pragma unroll
-            for (int e = 0; e < EP; ++e) {
-                const int n = __shfl_up(v[e], o);
-                if (lane >= o) v[e] += n;
-            }
-        }
-        if (lane == 63) {
-#pragma unroll
-            for (int e = 0; e < EP; ++e) s_wsum[w][e] = v[e];
-        }
-        __syncthreads();
-#pragma unroll
-        for (int e = 0; e < EP; ++e) {
-            int pre = s_carry[e];
-            for (int i = 0; i < w; ++i) pre += s_wsum[i][e];
-            if (in && e < E) tb[b * E + e] = pre + v[e] - c[e];
-        }
-        __syncthreads();
-        if (tid < EP) {
-            int sum = 0;
-            for (int i = 0; i < 16; ++i) sum += s_wsum[i][tid];
-            s_carry[tid] += sum;
-        }
-        __syncthreads();
+    for (int e = 0; e < EP; ++e) {
+        c[e] = (in && e < E) ? tc[b * E + e] : 0;
+        v[e] = c[e];
     }
-    if (tid == 0) {
-        int o = 0;
-        for (int e = 0; e < E; ++e) {
-            counts[e] = s_carry[e];
-            offsets[e] = o;
-            o += s_carry[e];
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+#pragma unroll
+        for (int e = 0; e < EP; ++e) {
+            const int n = __shfl_up(v[e], o);
+            if (lane >= o) v[e] += n;
         }
-        offsets[E] = o;
+    }
+    if (lane == 63) {
+#pragma unroll
+        for (int e = 0; e < EP; ++e) s_wsum[w][e] = v[e];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < EP; ++e) {
+        int pre = 0;
+        for (int i = 0; i < w; ++i) pre += s_wsum[i][e];
+        if (in && e < E) tb[b * E + e] = pre + v[e] - c[e];
+    }
+    if (tid < E) {
+        int sum = 0;
+#pragma unroll
+        for (int i = 0; i < kW; ++i) sum += s_wsum[i][tid];
+        chunk_tot[static_cast<int64_t>(blockIdx.x) * E + tid] = sum;
     }
 }
 
@@ -142,7 +131,7 @@ __global__ __launch_bounds__(kRouteTile) void k_permute(
     int32_t* __restrict__ offsets, const int32_t* __restrict__ tile_counts,
     int32_t* __restrict__ counts, int64_t T, int E, int k, int32_t* __restrict__ perm,
     int32_t* __restrict__ inv, const Tin* __restrict__ x, Tin* __restrict__ xperm, int D,
-    int htile) {
+    int htile, const int32_t* __restrict__ chunk_tot) {
     extern __shared__ int s_p[];          // [256 * k] destination of each assignment
     __shared__ int s_wc[kWaves][64];
     __shared__ int s_run[64];
@@ -163,12 +152,20 @@ __global__ __launch_bounds__(kRouteTile) void k_permute(
         __syncthreads();
         const int64_t nt = (T + htile - 1) / htile;
         const int64_t first = static_cast<int64_t>(blockIdx.x) * (kRouteTile / htile);
-        for (int64_t i = tid; i < nt * E; i += kRouteTile) {
-            const int64_t b = i / E;
-            const int e = static_cast<int>(i - b * E);
-            const int c = tile_counts[i];
-            atomicAdd(&s_tot[e], c);
-            if (b < first) atomicAdd(&s_pre[e], c);
+        // thread tid sums, for expert tid % E, the tiles tid / E + G i in
+        // registers (coalesced reads), then adds its two sums into LDS: one
+        // atomic per thread instead of one per histogram entry
+        const int G = kRouteTile / E;                  // threads per expert
+        if (tid < G * E) {
+            const int e = tid % E;
+            int tot = 0, pre = 0;
+            for (int64_t b = tid / E; b < nt; b += G) {
+                const int c = tile_counts[b * E + e];
+                tot += c;
+                pre += b < first ? c : 0;
+            }
+            atomicAdd(&s_tot[e], tot);
+            atomicAdd(&s_pre[e], pre);
         }
         __syncthreads();
         if (tid == 0) {
@@ -186,11 +183,42 @@ __global__ __launch_bounds__(kRouteTile) void k_permute(
         }
         if (tid < E) s_run[tid] = 0;
     } else {
+        // tile bases from the chunked scan: earlier chunks' totals plus the
+        // prefix within this tile's chunk; offsets from the grand totals
         if (tid < E) {
-            s_run[tid] = 0;
-            s_base[tid] = offsets[tid] + tb[static_cast<int64_t>(blockIdx.x) * E + tid];
+            s_pre[tid] = 0;
+            s_tot[tid] = 0;
         }
-        if (tid == 0) s_total = offsets[E];
+        __syncthreads();
+        const int64_t nchunks = (route_tiles(T) + kScanChunk - 1) / kScanChunk;
+        const int64_t mychunk = static_cast<int64_t>(blockIdx.x) / kScanChunk;
+        const int G = kRouteTile / E;
+        if (tid < G * E) {
+            const int e = tid % E;
+            int tot = 0, pre = 0;
+            for (int64_t c = tid / E; c < nchunks; c += G) {
+                const int v = chunk_tot[c * E + e];
+                tot += v;
+                pre += c < mychunk ? v : 0;
+            }
+            atomicAdd(&s_tot[e], tot);
+            atomicAdd(&s_pre[e], pre);
+        }
+        __syncthreads();
+        if (tid == 0) {
+            int o = 0;
+            for (int e = 0; e < E; ++e) {
+                s_base[e] = o + s_pre[e] + tb[static_cast<int64_t>(blockIdx.x) * E + e];
+                if (blockIdx.x == 0) {
+                    counts[e] = s_tot[e];
+                    offsets[e] = o;
+                }
+                o += s_tot[e];
+            }
+            if (blockIdx.x == 0) offsets[E] = o;
+            s_total = o;
+        }
+        if (tid < E) s_run[tid] = 0;
     }
     __syncthreads();
     // Empty slots (index -1) are in no sub-batch: perm ends with -1 entries
@@ -395,23 +423,27 @@ hipError_t launch_tile_histogram(const int32_t* idx, int64_t T, int E, int k,
     return hipGetLastError();
 }
 
+int64_t scan_chunks(int64_t ntiles) { return (ntiles + kScanChunk - 1) / kScanChunk; }
+
 hipError_t launch_scan(const int32_t* tile_counts, int64_t ntiles, int E, int32_t* tile_base,
-                       int32_t* counts, int32_t* offsets, hipStream_t st) {
+                       int32_t* chunk_tot, hipStream_t st) {
+    const dim3 grid(static_cast<unsigned>(scan_chunks(ntiles)));
+    if (ntiles == 0) return hipSuccess;
     if (E <= 8)
-        k_scan<8><<<1, 1024, 0, st>>>(tile_counts, ntiles, E, tile_base, counts, offsets);
+        k_scan<8><<<grid, kScanChunk, 0, st>>>(tile_counts, ntiles, E, tile_base, chunk_tot);
     else if (E <= 16)
-        k_scan<16><<<1, 1024, 0, st>>>(tile_counts, ntiles, E, tile_base, counts, offsets);
+        k_scan<16><<<grid, kScanChunk, 0, st>>>(tile_counts, ntiles, E, tile_base, chunk_tot);
     else if (E <= 32)
-        k_scan<32><<<1, 1024, 0, st>>>(tile_counts, ntiles, E, tile_base, counts, offsets);
+        k_scan<32><<<grid, kScanChunk, 0, st>>>(tile_counts, ntiles, E, tile_base, chunk_tot);
     else
-        k_scan<64><<<1, 1024, 0, st>>>(tile_counts, ntiles, E, tile_base, counts, offsets);
+        k_scan<64><<<grid, kScanChunk, 0, st>>>(tile_counts, ntiles, E, tile_base, chunk_tot);
     return hipGetLastError();
 }
 
 hipError_t launch_permute(int dtype, const int32_t* idx, const int32_t* tile_base,
-                          int32_t* offsets, const int32_t* tile_counts, int32_t* counts,
-                          int64_t T, int E, int k, int32_t* perm, int32_t* inv, const void* x,
-                          void* xperm, int D, hipStream_t st) {
+                          const int32_t* chunk_tot, int32_t* offsets, const int32_t* tile_counts,
+                          int32_t* counts, int64_t T, int E, int k, int32_t* perm, int32_t* inv,
+                          const void* x, void* xperm, int D, hipStream_t st) {
     const int64_t nt = route_tiles(T);
     if (nt == 0) return hipSuccess;
     const size_t shm = sizeof(int) * static_cast<size_t>(kRouteTile) * k;
@@ -419,11 +451,11 @@ hipError_t launch_permute(int dtype, const int32_t* idx, const int32_t* tile_bas
     if (dtype == 0)
         k_permute<float><<<dim3(static_cast<unsigned>(nt)), kRouteTile, shm, st>>>(
             idx, tile_base, offsets, tile_counts, counts, T, E, k, perm, inv,
-            static_cast<const float*>(x), static_cast<float*>(xperm), D, htile);
+            static_cast<const float*>(x), static_cast<float*>(xperm), D, htile, chunk_tot);
     else
         k_permute<bf16_bits><<<dim3(static_cast<unsigned>(nt)), kRouteTile, shm, st>>>(
             idx, tile_base, offsets, tile_counts, counts, T, E, k, perm, inv,
-            static_cast<const bf16_bits*>(x), static_cast<bf16_bits*>(xperm), D, htile);
+            static_cast<const bf16_bits*>(x), static_cast<bf16_bits*>(xperm), D, htile, chunk_tot);
     return hipGetLastError();
 }
 

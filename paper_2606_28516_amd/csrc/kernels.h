@@ -120,20 +120,24 @@ constexpr int kMlpHiddenMax = 256;
 // Per-tile expert histogram of an index array (tiles of hist_tile(T, E) tokens).
 hipError_t launch_tile_histogram(const int32_t* idx, int64_t T, int E, int k,
                                  int32_t* tile_counts, hipStream_t st);
-// Exclusive scan of tile histograms: tile_base[b][e] = sum_{b'<b} tile_counts[b'][e];
-// counts[e] = column sums; offsets[e] = exclusive scan of counts (offsets[E] = total).
+// Chunked exclusive scan of 256-token tile histograms: for tile b in chunk
+// c = b / 256, tile_base[b][e] = sum of tile_counts[b'][e] over the earlier
+// tiles b' of chunk c, and chunk_tot[c][e] = the chunk's column sums
+// (scan_chunks(ntiles) chunks, all scanned in parallel).
+int64_t scan_chunks(int64_t ntiles);
 hipError_t launch_scan(const int32_t* tile_counts, int64_t ntiles, int E, int32_t* tile_base,
-                       int32_t* counts, int32_t* offsets, hipStream_t st);
+                       int32_t* chunk_tot, hipStream_t st);
 // Stable permutation (and optional row copy x -> xperm), one workgroup per
 // 256 tokens.  With tile_counts non-NULL the histogram (tiles of
 // hist_tile(T, E) tokens) is scanned inline (tile_base unused) and
 // counts/offsets are written; otherwise tile_base/offsets come from
-// launch_scan over 256-token tiles.  An index
-// of -1 is an empty slot: inv = -1, and perm[offsets[E] .. T*k) = -1.
+// launch_scan over 256-token tiles (tile bases within a chunk, plus the
+// chunk totals, from which the permutation forms counts and offsets).  An
+// index of -1 is an empty slot: inv = -1, and perm[offsets[E] .. T*k) = -1.
 hipError_t launch_permute(int dtype, const int32_t* idx, const int32_t* tile_base,
-                          int32_t* offsets, const int32_t* tile_counts, int32_t* counts,
-                          int64_t T, int E, int k, int32_t* perm, int32_t* inv, const void* x,
-                          void* xperm, int D, hipStream_t st);
+                          const int32_t* chunk_tot, int32_t* offsets, const int32_t* tile_counts,
+                          int32_t* counts, int64_t T, int E, int k, int32_t* perm, int32_t* inv,
+                          const void* x, void* xperm, int D, hipStream_t st);
 // y[t] = sum_j gate[t,j] ye[inv[t*k+j]]  (ye, y in dtype).
 hipError_t launch_combine_gated(int dtype, const void* ye, const int32_t* inv, const float* gate,
                                 void* y, int64_t T, int D, int k, hipStream_t st);

@@ -97,6 +97,21 @@ def test_dispatch_edge_cases():
                        perm.cpu().numpy(), inv.cpu().numpy())
 
 
+@pytest.mark.parametrize("T,E,k", [(256 * 549, 64, 2), (256 * 1030 + 17, 16, 3)])
+def test_dispatch_chunked_scan(T, E, k):
+    """Histograms too large for the permutation's inline scan go through the
+    chunked scan (256 tiles per chunk, the chunk prefixes added by the
+    permutation): several chunks and a ragged last one, bit-exact against the
+    oracle, with empty slots mixed in."""
+    rng = np.random.default_rng(T)
+    idx_np = np.stack([rng.choice(E, size=k, replace=False) for _ in range(T)]).astype(np.int32)
+    idx_np[rng.random((T, k)) < 0.1] = -1
+    counts, offsets, perm, inv, _ = cm.dispatch(torch.from_numpy(idx_np).cuda(), E, D=8)
+    torch.cuda.synchronize()
+    check_dispatch(idx_np, E, counts.cpu().numpy(), offsets.cpu().numpy(), perm.cpu().numpy(),
+                   inv.cpu().numpy())
+
+
 @pytest.mark.parametrize("dt,k", [("bf16", 1), ("bf16", 2), ("f32", 3)])
 def test_combine_against_oracle(dt, k):
     T, D, E = 513, 136 if dt == "bf16" else 100, 6
