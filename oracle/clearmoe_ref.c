@@ -28,6 +28,8 @@
  *   MLP router    Sec. III Phase 4 "MLP" router (one hidden layer of width
  *                 d/6; Table C5's 149,400 parameters over six layers): the
  *                 hidden layer is ref_fc1_gelu applied to the router weights
+ *   class tokens  Table C6: excluded from expert dispatch, run on the dense
+ *                 path (ref_fc1_gelu, then ref_dense_fc2 with the original fc2)
  *
  * Readings where the paper is silent (router bias, tie-break, gate weighting,
  * stable order, b2 placement, exact-erf GELU, low-rank residual factors) are
@@ -199,6 +201,21 @@ void ref_shared(int64_t T, int D, int H, int r, const double* z, const double* V
         }
         free(tv);
     }
+}
+
+/* Dense fc2 of the unexpertised FFN: out[t,d] = sum_h z[t,h] W2[d,h] + b2[d]
+ * (b2 may be NULL).  The class tokens' path: Table C6 excludes the class
+ * token from expert dispatch and runs it on the dense path, the original
+ * fc1 + GELU + fc2 (Table III, D0). */
+void ref_dense_fc2(int64_t T, int D, int H, const double* z, const double* W2, const double* b2,
+                   double* out) {
+#pragma omp parallel for schedule(static)
+    for (int64_t t = 0; t < T; ++t)
+        for (int d = 0; d < D; ++d) {
+            double s = 0.0;
+            for (int h = 0; h < H; ++h) s += z[t * H + h] * W2[(int64_t)d * H + h];
+            out[t * D + d] = s + (b2 ? b2[d] : 0.0);
+        }
 }
 
 /* Residual experts, token by token (no permutation):

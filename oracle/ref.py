@@ -22,7 +22,7 @@ __all__ = ["build", "lib", "widen", "num_threads", "set_num_threads", "gelu", "r
            "topk", "route", "dispatch", "permute_rows", "fc1_gelu", "shared", "residual",
            "ffn_forward", "ffn_forward_layer", "combine", "margins", "adaptive_topk",
            "round_to_storage", "mlp_router_logits", "route_layer", "ffn_forward_routed",
-           "confidence"]
+           "confidence", "dense_fc2", "class_tokens"]
 
 
 def build(force: bool = True) -> str:
@@ -60,6 +60,7 @@ def lib():
         L.ref_ffn_forward.restype = i32
         L.ref_combine.argtypes = [i64, i32, i32, dp, ip, dp, dp]
         L.ref_adaptive_topk.argtypes = [i64, i32, ctypes.c_double, dp, ip, dp]
+        L.ref_dense_fc2.argtypes = [i64, i32, i32, dp, dp, dp, dp]
         _lib = L
     return _lib
 
@@ -220,6 +221,26 @@ def shared(z, Vt, US, b2=None) -> np.ndarray:
     return out
 
 
+def dense_fc2(z, W2, b2=None) -> np.ndarray:
+    """z W2^T + b2: fc2 of the unexpertised FFN (the class tokens' dense path)."""
+    z, W2, b2 = _f64(z), _f64(W2), _f64(b2)
+    T, H = z.shape
+    D = W2.shape[0]
+    out = np.empty((T, D))
+    lib().ref_dense_fc2(T, D, H, _dp(z), _dp(W2), _dp(b2), _dp(out))
+    return out
+
+
+def class_tokens(tokens, stride: int) -> np.ndarray:
+    """Mask of the class tokens among the given token indices: one per image of
+    `stride` tokens, the first (Table C6: 197 tokens per image, the class token
+    excluded from dispatch).  stride <= 0: none."""
+    tokens = np.asarray(tokens)
+    if stride <= 0:
+        return np.zeros(tokens.shape, dtype=bool)
+    return tokens % stride == 0
+
+
 def residual(z, Q, P, idx, gate) -> np.ndarray:
     z, Q, P = _f64(z), _f64(Q), _f64(P)
     idx = np.ascontiguousarray(idx, dtype=np.int32)
@@ -266,8 +287,24 @@ def ffn_forward_layer(layer: dict, rows=None):
     of the layer depends on its own token alone, so a sample of rows gives the
     same values as the full run at those rows.  A "router" entry (MLP or
     adaptive) routes through route_layer; without it the linear router runs.
+    A "dense_stride" entry s > 0 makes every token t with t % s == 0 a class
+    token (Table C6): it takes no expert slot (idx -1, gate 0) and its output
+    is the dense FFN's, GELU(x W1^T + b1) W2^T + b2 with the layer's "W2".
     """
     x = layer["x"] if rows is None else layer["x"][np.asarray(rows)]
+    stride = int(layer.get("dense_stride") or 0)
+    if stride > 0:
+        # class tokens: no expert slot, and the dense FFN's output (Table C6)
+        tok = np.arange(layer["x"].shape[0]) if rows is None else np.asarray(rows)
+        cls = class_tokens(tok, stride)
+        idx, gate, lg = route_layer(layer, rows)
+        idx[cls] = -1
+        gate[cls] = 0.0
+        z = fc1_gelu(x, layer["W1"], layer["b1"])
+        y = shared(z, layer["Vt"], layer["US"], layer["b2"]) + residual(z, layer["Q"], layer["P"],
+                                                                        idx, gate)
+        y[cls] = dense_fc2(z[cls], layer["W2"], layer["b2"])
+        return dict(y=y, idx=idx, gate=gate, logits=lg, cls=cls)
     if layer.get("router") is not None and layer["router"]["kind"] != "linear":
         idx, gate, lg = route_layer(layer, rows)
         y = ffn_forward_routed(x, layer["W1"], layer["b1"], layer["US"], layer["Vt"],

@@ -37,7 +37,7 @@ import numpy as np
 
 __all__ = ["LayerConfig", "CONFIGS", "DISPATCH_CONFIG", "make_layer", "make_dispatch",
            "to_bf16_bits", "bf16_bits_to_f32", "fingerprint", "imbalance_mixture",
-           "with_mlp_router", "with_adaptive_router"]
+           "with_mlp_router", "with_adaptive_router", "with_class_tokens"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -250,6 +250,18 @@ def with_adaptive_router(layer: dict, tau: float) -> dict:
     out = dict(layer)
     out["cfg"] = dataclasses.replace(layer["cfg"], k=2)
     out["router"] = {"kind": "adaptive", "tau": float(tau)}
+    return out
+
+
+def with_class_tokens(layer: dict, stride: int = 197) -> dict:
+    """The layer with one class token per image of `stride` tokens (token t
+    with t % stride == 0; DeiT / ViT put it first): Table C6 excludes it from
+    expert dispatch and runs it on the dense path, the original fc1 + GELU +
+    fc2.  Adds "dense_stride" and stores "W2" in the storage precision (the
+    dense path's fc2 weight as the kernels receive it)."""
+    out = dict(layer)
+    out["dense_stride"] = int(stride)
+    out["W2"] = _store(layer["W2"], layer["cfg"].dtype)
     return out
 
 

@@ -482,3 +482,54 @@ def test_residual_and_layer_with_empty_slots():
     y0 = oracle.ffn_forward_layer(dict(L, cfg=synth.dataclasses.replace(cfg, k=1)))
     assert np.allclose(ref["y"][esc], y1["y"][esc], rtol=0, atol=1e-12)
     assert np.allclose(ref["y"][~esc], y0["y"][~esc], rtol=0, atol=1e-12)
+
+
+# ---- class tokens (Table C6: excluded from dispatch, dense path) -----------
+def test_class_tokens_take_the_dense_ffn():
+    """With one class token per image of 13 tokens, the class rows equal the
+    textbook dense FFN with the original fc2, take no expert slot, and leave
+    every other row exactly as the layer without class tokens computes it."""
+    L = _with_biases(_small(E=5, k=2, T=91, residual="random"))
+    C = synth.with_class_tokens(L, stride=13)
+    out = oracle.ffn_forward_layer(C)
+    cls = np.arange(91) % 13 == 0
+    assert np.array_equal(out["cls"], cls) and cls.sum() == 7
+    assert np.all(out["idx"][cls] == -1) and np.all(out["gate"][cls] == 0.0)
+    want = _dense(C["x"][cls], C["W1"], C["b1"], oracle.widen(C["W2"]), C["b2"])
+    assert np.max(np.abs(out["y"][cls] - want)) < 1e-12
+    base = oracle.ffn_forward_layer(L)
+    assert np.array_equal(out["idx"][~cls], base["idx"][~cls])
+    assert np.max(np.abs(out["y"][~cls] - base["y"][~cls])) < 1e-13
+    # the class rows really differ from the expert path (the residual is low rank)
+    assert np.max(np.abs(out["y"][cls] - base["y"][cls])) > 1e-4
+    # dispatch counts only the routed tokens
+    counts, offsets, _, _ = oracle.dispatch(out["idx"], 5)
+    assert counts.sum() == (91 - 7) * 2 and offsets[-1] == (91 - 7) * 2
+
+
+def test_class_tokens_with_full_residual_agree_with_experts():
+    """D3 (q = D - r, every s_e = 1): the expert path reconstructs fc2
+    exactly, so class and routed tokens alike give the dense FFN."""
+    D, H, r = 18, 30, 7
+    L = _with_biases(_small(E=3, k=1, T=40, D=D, H=H, r=r, q=D - r, residual="svd_tail"))
+    U, S, Vh = np.linalg.svd(L["W2"], full_matrices=False)
+    L["US"], L["Vt"] = U[:, :r] * S[:r], Vh[:r]
+    L["P"] = np.broadcast_to(U[:, r:] * S[r:], (3, D, D - r)).copy()
+    L["Q"] = np.broadcast_to(Vh[r:], (3, D - r, H)).copy()
+    C = synth.with_class_tokens(L, stride=10)
+    C["W2"] = L["W2"]                                   # float64 here: exact reconstruction
+    out = oracle.ffn_forward_layer(C)
+    want = _dense(L["x"], L["W1"], L["b1"], L["W2"], L["b2"])
+    assert out["cls"].sum() == 4
+    assert np.max(np.abs(out["y"] - want)) < 1e-12
+
+
+def test_class_tokens_on_a_row_sample_use_global_positions():
+    """A sample of rows is classified by its global token index."""
+    L = _with_biases(_small(E=4, k=1, T=60))
+    C = synth.with_class_tokens(L, stride=20)
+    rows = np.array([0, 1, 20, 39, 40, 59])
+    part = oracle.ffn_forward_layer(C, rows=rows)
+    full = oracle.ffn_forward_layer(C)
+    assert np.array_equal(part["cls"], [True, False, True, False, True, False])
+    assert np.max(np.abs(part["y"] - full["y"][rows])) < 1e-13
