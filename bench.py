@@ -23,7 +23,9 @@ Prints one JSON line.  Besides the contract fields it carries
                60 and 80 % load imbalance, E = 4, DeiT-Small widths, top-1 and
                top-2, 1568 and 12608 tokens;
   routers      the same layer with the linear, MLP and adaptive routers
-               (clearmoe_ffn_forward_ex).
+               (clearmoe_ffn_forward_ex);
+  ffn_stack    the FFN part of a 12-block DeiT-Small forward with 6 CLEAR-MoE
+               layers (class tokens on the dense path) against 12 dense ones.
 """
 import argparse
 import hashlib
@@ -263,6 +265,7 @@ def main():
         out["dispatch"] = bench_dispatch(cm, synth, torch, np, stream, max(10, args.steps // 10))
         out["imbalance"] = bench_imbalance(cm, synth, torch, np, stream, max(20, args.steps // 5))
         out["routers"] = bench_routers(cm, synth, torch, np, stream, L, max(20, args.steps // 5))
+        out["ffn_stack"] = bench_stack(cm, synth, torch, np, stream, L, max(20, args.steps // 10))
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(L, cfg, args.cpu_seconds)
@@ -441,6 +444,53 @@ def bench_routers(cm, synth, torch, np, stream, L, steps):
                                  "route_us": r_ms / r_n * 1e3, "share_top2": two}
         del ws, y, idx
     return out
+
+
+def bench_stack(cm, synth, torch, np, stream, L, steps):
+    """The FFN part of a DeiT-Small forward: 12 blocks, of which the 6 with the
+    best layer scores are CLEAR-MoE (Sec. III Phase 2 keeps the top L/2) and
+    the others stay dense, with each image's class token on the dense path in
+    the CLEAR-MoE layers (Table C6).  Every layer runs on the same resident
+    12608-token input with the same weights (timing only; attention, layer
+    norms and residual adds are not part of this path).  Compared with 12
+    dense FFN layers through the same kernels: the FFN-only analogue of the
+    paper's model-level CLEAR-MoE / dense latency ratio (Table III)."""
+    cfg = L["cfg"]
+    C = synth.with_class_tokens(L, stride=197)
+    d = {n: cm.from_stored(C[n]) for n in ("x", "W1", "b1", "US", "Vt", "b2", "P", "Q", "Wg",
+                                          "bg", "W2")}
+    router = cm.make_router(d["Wg"], d["bg"], dense_stride=197, W2=d["W2"])
+    shape = cm.make_shape(cfg.T, cfg.D, cfg.E, cfg.k, cm.BF16, H=cfg.H, r=cfg.r, q=cfg.q)
+    ws = cm.alloc_workspace(shape)
+    y = torch.empty_like(d["x"])
+    moe_layers = 6
+
+    def moe():
+        cm.ffn_forward_ex(d["x"], d["W1"], d["b1"], d["US"], d["Vt"], d["b2"], d["P"], d["Q"],
+                          router, cfg.k, ws=ws, out=y)
+
+    def dense():
+        cm.dense_ffn_forward(d["x"], d["W1"], d["b1"], d["W2"], d["b2"], ws=ws, out=y)
+
+    def timed(fn_list):
+        for f in fn_list:
+            f()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(steps):
+            for f in fn_list:
+                f()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
+    mixed = timed([moe] * moe_layers + [dense] * (12 - moe_layers))
+    all_dense = timed([dense] * 12)
+    return {"workload": f"12 FFN layers at {cfg.name} (T={cfg.T}), {moe_layers} CLEAR-MoE "
+                        f"(class tokens on the dense path) + {12 - moe_layers} dense",
+            "ms": mixed, "tokens_per_s": cfg.T / (mixed * 1e-3), "dense_ms": all_dense,
+            "moe_over_dense_time": mixed / all_dense, "steps": steps}
 
 
 def cpu_baseline(L, cfg, min_seconds):

@@ -105,14 +105,23 @@ int clearmoe_route(const clearmoe_shape* shape, const void* x, const void* Wg, c
  *             p = 1 / sum_e exp(l_e - l_max); p >= tau keeps it at top-1
  *             (idx = (best, -1), gate = (1, 0): slot 1 is empty), otherwise
  *             it takes the top 2 with their softmax renormalised.
+ *   Class tokens (Table C6 excludes the class token of each image from
+ *   expert dispatch and runs it on the dense path): with dense_stride s > 0
+ *   every token t with t % s == 0 gets no expert (all k slots -1, gate 0);
+ *   clearmoe_ffn_forward_ex gives it the unexpertised FFN's output,
+ *   GELU(x W1^T + b1) W2^T + b2.
  * Weights have element type shape->dtype, biases are float32 (NULL = zero). */
 typedef struct {
     const void* Wg;        /* output layer [E, D] (linear) or [E, hidden] (MLP) */
     const float* bg;       /* [E] or NULL */
     const void* Wh;        /* MLP hidden layer [hidden, D]; ignored if hidden == 0 */
     const float* bh;       /* MLP hidden bias [hidden] or NULL */
+    const void* W2;        /* dense fc2 [D, H] of the class tokens' path; NULL
+                              when dense_stride == 0 (unused by route_ex) */
     int32_t hidden;        /* 0 = linear router; 1..256 = MLP hidden width */
     int32_t adaptive;      /* 0 = top-k; 1 = adaptive top-1 / top-2 */
+    int32_t dense_stride;  /* s > 0: token t with t % s == 0 is a class token */
+    int32_t reserved;      /* must be 0 */
     double tau;            /* adaptive confidence threshold (any finite value) */
 } clearmoe_router;
 
@@ -129,8 +138,10 @@ typedef struct {
  *     where a hidden value lies within double rounding of a dtype rounding
  *     boundary or a top-k gap / |log p - log tau| is below double rounding.
  * Returns CLEARMOE_ERR_INVALID_ARG for a NULL router, hidden outside
- * [0, 256], adaptive not 0 or 1, adaptive with k != 2 or E < 2, a NaN tau, or
- * NULL / misaligned weights (Wg, Wh 16-byte aligned; biases 4-byte). */
+ * [0, 256], adaptive not 0 or 1, adaptive with k != 2 or E < 2, a NaN tau,
+ * a negative dense_stride, reserved != 0, or NULL / misaligned weights (Wg,
+ * Wh, W2 16-byte aligned; biases 4-byte; W2 required by
+ * clearmoe_ffn_forward_ex when dense_stride > 0). */
 int clearmoe_route_ex(const clearmoe_shape* shape, const clearmoe_router* router, const void* x,
                       int32_t* idx, float* gate, void* ws, size_t ws_bytes, hipStream_t stream);
 
@@ -182,7 +193,9 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
  * clearmoe_route_ex); the other arguments, layouts, results and workspace are
  * those of clearmoe_ffn_forward.  Router weights replace Wg / bg.  An empty
  * slot (adaptive top-1) adds no residual: y = h_sh + h_res of the chosen
- * expert with gate 1. */
+ * expert with gate 1.  A class token (dense_stride) gets
+ * y = GELU(x W1^T + b1) W2^T + b2 instead, from two extra products over the
+ * ceil(T / dense_stride) class rows. */
 int clearmoe_ffn_forward_ex(const clearmoe_shape* shape, const clearmoe_router* router,
                             const void* x, const void* W1, const float* b1, const void* US,
                             const void* Vt, const float* b2, const void* P, const void* Q,

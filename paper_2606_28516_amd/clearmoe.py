@@ -45,8 +45,9 @@ class Router(ctypes.Structure):
     """clearmoe_router: scores (linear, or an MLP with `hidden` units) and the
     selection rule (top-k, or adaptive top-1 / top-2 at threshold tau)."""
     _fields_ = [("Wg", ctypes.c_void_p), ("bg", ctypes.c_void_p), ("Wh", ctypes.c_void_p),
-                ("bh", ctypes.c_void_p), ("hidden", ctypes.c_int32), ("adaptive", ctypes.c_int32),
-                ("tau", ctypes.c_double)]
+                ("bh", ctypes.c_void_p), ("W2", ctypes.c_void_p), ("hidden", ctypes.c_int32),
+                ("adaptive", ctypes.c_int32), ("dense_stride", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("tau", ctypes.c_double)]
 
 
 _lib = None
@@ -159,12 +160,15 @@ def route(x, Wg, bg, k: int, ws: Optional[torch.Tensor] = None, stream=None):
     return idx, gate
 
 
-def make_router(Wg, bg=None, Wh=None, bh=None, adaptive: bool = False, tau: float = 0.0):
+def make_router(Wg, bg=None, Wh=None, bh=None, adaptive: bool = False, tau: float = 0.0,
+                dense_stride: int = 0, W2=None):
     """A Router over device tensors (keep the tensors alive while it is used):
-    linear when Wh is None, else an MLP with Wh.shape[0] hidden units."""
+    linear when Wh is None, else an MLP with Wh.shape[0] hidden units; with
+    dense_stride > 0, token t with t % dense_stride == 0 is a class token
+    (dense path, fc2 weight W2)."""
     p = lambda t: None if t is None else _p(t).value  # noqa: E731
-    return Router(p(Wg), p(bg), p(Wh), p(bh), 0 if Wh is None else int(Wh.shape[0]),
-                  1 if adaptive else 0, float(tau))
+    return Router(p(Wg), p(bg), p(Wh), p(bh), p(W2), 0 if Wh is None else int(Wh.shape[0]),
+                  1 if adaptive else 0, int(dense_stride), 0, float(tau))
 
 
 def route_ex(x, router: Router, E: int, k: int, ws: Optional[torch.Tensor] = None, stream=None):

@@ -157,6 +157,8 @@ int check_router(const clearmoe_shape& s, const clearmoe_router* r) {
         return CLEARMOE_ERR_INVALID_ARG;
     if (r->adaptive != 0 && r->adaptive != 1) return CLEARMOE_ERR_INVALID_ARG;
     if (r->adaptive && (s.k != 2 || s.E < 2 || r->tau != r->tau)) return CLEARMOE_ERR_INVALID_ARG;
+    if (r->dense_stride < 0 || r->reserved != 0) return CLEARMOE_ERR_INVALID_ARG;
+    if (r->W2 && !aligned(r->W2, 16)) return CLEARMOE_ERR_INVALID_ARG;
     return CLEARMOE_OK;
 }
 
@@ -167,12 +169,13 @@ int route_impl(const clearmoe_shape& s, const Layout& L, const clearmoe_router& 
     if (rt.hidden == 0) {
         CLEARMOE_STAGE(CLEARMOE_STAGE_ROUTE, st,
                        launch_route(s.dtype, x, rt.Wg, rt.bg, s.T, s.D, s.E, s.k, rt.adaptive,
-                                    rt.tau, idx, gate, tc, st));
+                                    rt.tau, rt.dense_stride, idx, gate, tc, st));
         return CLEARMOE_OK;
     }
     CLEARMOE_STAGE(CLEARMOE_STAGE_ROUTE, st,
                    launch_route_mlp(s.dtype, x, rt.Wh, rt.bh, rt.Wg, rt.bg, s.T, s.D, rt.hidden,
-                                    s.E, s.k, rt.adaptive, rt.tau, idx, gate, st));
+                                    s.E, s.k, rt.adaptive, rt.tau, rt.dense_stride, idx, gate,
+                                    st));
     CLEARMOE_STAGE(CLEARMOE_STAGE_TILE_HIST, st,
                    launch_tile_histogram(idx, s.T, s.E, s.k, tc, st));
     return CLEARMOE_OK;
@@ -271,6 +274,37 @@ int residual_impl(const clearmoe_shape& s, int64_t M, const void* z, const int32
 
 // Pinned host copy of the expert counts (padded backend), one per thread.
 thread_local int32_t* t_host_counts = nullptr;
+
+// A side stream per device (default priority, created on first use and kept
+// until the process ends) on which work that does not depend on the routing
+// runs beside it: fork = an event recorded on the caller's stream that the
+// side stream waits for; join = an event recorded on the side stream that
+// the caller's stream waits for, so the call's work stays ordered on the
+// caller's stream as a whole.  One call forks and joins under g_side_mu.
+struct SideStream {
+    hipStream_t s = nullptr;
+    hipEvent_t fork = nullptr, join = nullptr;
+};
+std::mutex g_side_mu;
+std::vector<SideStream> g_side;
+
+int side_stream(SideStream** out) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return CLEARMOE_ERR_HIP;
+    if (static_cast<size_t>(dev) >= g_side.size()) g_side.resize(static_cast<size_t>(dev) + 1);
+    SideStream& ss = g_side[static_cast<size_t>(dev)];
+    if (ss.s == nullptr) {
+        if (hipStreamCreateWithFlags(&ss.s, hipStreamNonBlocking) != hipSuccess) {
+            ss.s = nullptr;
+            return CLEARMOE_ERR_HIP;
+        }
+        if (hipEventCreateWithFlags(&ss.fork, hipEventDisableTiming) != hipSuccess ||
+            hipEventCreateWithFlags(&ss.join, hipEventDisableTiming) != hipSuccess)
+            return CLEARMOE_ERR_HIP;
+    }
+    *out = &ss;
+    return CLEARMOE_OK;
+}
 
 }  // namespace
 
@@ -372,6 +406,37 @@ int clearmoe_combine(const clearmoe_shape* shape, const void* ye, const int32_t*
 
 namespace {
 
+// Class tokens (every dense_stride-th token, from token 0) on the dense path:
+// y[c] = GELU(x[c] W1^T + b1) W2^T + b2 over the ceil(T / dense_stride) class
+// rows, which the strided leading dimensions pick out of x and y.  With
+// z_all the token-order z of the whole layer is already there (its class
+// rows are read with a stride); otherwise fc1 + GELU runs on the class rows
+// into the workspace's z region first.
+int class_tokens_impl(const clearmoe_shape& s, const clearmoe_router& rt, const void* x,
+                      const void* W1, const float* b1, const float* b2, void* z, bool z_all,
+                      void* y, hipStream_t st) {
+    const int64_t sd = rt.dense_stride;
+    const int64_t ncls = (s.T + sd - 1) / sd;
+    int64_t zld = s.H;
+    if (z_all) {
+        zld = static_cast<int64_t>(s.H) * sd;
+    } else {
+        GemmDesc g = gemm_desc(ncls, s.H, s.D);
+        g.A = x; g.lda = static_cast<int64_t>(s.D) * sd;
+        g.B = W1; g.ldb = s.D;
+        g.C = z; g.ldc = s.H; g.c_f32 = 0;
+        g.bias = b1; g.gelu = 1;
+        CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
+    }
+    GemmDesc g = gemm_desc(ncls, s.D, s.H);
+    g.A = z; g.lda = zld;
+    g.B = rt.W2; g.ldb = s.H;
+    g.C = y; g.ldc = static_cast<int64_t>(s.D) * sd; g.c_f32 = 0;
+    g.bias = b2;
+    CLEARMOE_STAGE(CLEARMOE_STAGE_DENSE_FC2, st, launch_gemm(s.dtype, g, st));
+    return CLEARMOE_OK;
+}
+
 int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router, const void* x,
                      const void* W1, const float* b1, const void* US, const void* Vt,
                      const float* b2, const void* P, const void* Q, void* y, int32_t* idx_out,
@@ -382,12 +447,15 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
     const clearmoe_shape& s = *shape;
     rc = check_router(s, router);
     if (rc != CLEARMOE_OK) return rc;
+    if (router->dense_stride > 0 && router->W2 == nullptr) return CLEARMOE_ERR_INVALID_ARG;
     const Layout L = layout(s);
     if (!ws || !aligned(ws, kAlign) || ws_bytes < L.total) return CLEARMOE_ERR_WORKSPACE;
     if (s.T == 0) return CLEARMOE_OK;
 
     hipStream_t st = stream;
     const int64_t T = s.T, A = T * s.k;
+    const bool cls = router->dense_stride > 0;
+    const bool fused = s.k == 1 && s.dtype == CLEARMOE_BF16 && fused_top1_supported(s.D, s.H, s.r, s.q);
     int32_t* idx = idx_out ? idx_out : at<int32_t>(ws, L.idx);
     float* gate = gate_out ? gate_out : at<float>(ws, L.gate);
     int32_t* counts = at<int32_t>(ws, L.counts);
@@ -400,6 +468,33 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
     void* u = at<void>(ws, L.u);
     float* hres = at<float>(ws, L.hres);
 
+    // With the fused top-1 kernel the class tokens' dense path needs only x:
+    // it runs on the side stream beside routing, dispatch and the fused
+    // kernel (which leave compute units idle), into the workspace's z region
+    // (unused by the fused path).
+    std::unique_lock<std::mutex> side_lock;
+    SideStream* side = nullptr;
+    // whatever happens below, the caller's stream waits for the side work
+    struct JoinGuard {
+        hipStream_t st;
+        SideStream** side;
+        bool done = false;
+        ~JoinGuard() {
+            if (!done && *side != nullptr) (void)hipStreamWaitEvent(st, (*side)->join, 0);
+        }
+    } join_guard{st, &side};
+    if (cls && fused) {
+        side_lock = std::unique_lock<std::mutex>(g_side_mu);
+        rc = side_stream(&side);
+        if (rc != CLEARMOE_OK) return rc;
+        if (hipEventRecord(side->fork, st) != hipSuccess ||
+            hipStreamWaitEvent(side->s, side->fork, 0) != hipSuccess)
+            return CLEARMOE_ERR_HIP;
+        rc = class_tokens_impl(s, *router, x, W1, b1, b2, z, false, y, side->s);
+        if (rc != CLEARMOE_OK) return rc;
+        if (hipEventRecord(side->join, side->s) != hipSuccess) return CLEARMOE_ERR_HIP;
+    }
+
     // 1. router + top-k + per-tile histogram; 2. scan + stable permutation
     rc = route_impl(s, L, *router, x, idx, gate, ws, st);
     if (rc != CLEARMOE_OK) return rc;
@@ -407,10 +502,16 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
     if (rc != CLEARMOE_OK) return rc;
 
     // Top-1 in bf16: fc1 + GELU, [t|u] and y in one kernel (z stays on chip).
-    if (s.k == 1 && s.dtype == CLEARMOE_BF16 && fused_top1_supported(s.D, s.H, s.r, s.q)) {
+    if (fused) {
         CLEARMOE_STAGE(CLEARMOE_STAGE_FUSED_TOP1, st,
                        launch_fused_top1(x, W1, b1, US, Vt, b2, P, Q, perm, offsets, gate, y, T,
                                          s.D, s.H, s.E, s.r, s.q, st));
+        // join: the class rows of y (written on the side stream) are complete
+        // before anything later on the caller's stream
+        if (side != nullptr) {
+            join_guard.done = true;
+            if (hipStreamWaitEvent(st, side->join, 0) != hipSuccess) return CLEARMOE_ERR_HIP;
+        }
         return CLEARMOE_OK;
     }
 
@@ -448,6 +549,7 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
         g.bias = b2;
         g.seg_offsets = offsets; g.nseg = s.E;
         CLEARMOE_STAGE(CLEARMOE_STAGE_Y, st, launch_gemm(s.dtype, g, st));
+        if (cls) return class_tokens_impl(s, *router, x, W1, b1, b2, z, true, y, st);
         return CLEARMOE_OK;
     }
 
@@ -460,6 +562,8 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
     // 6. y[t] = h_sh[t] + sum_j h_res[inv[t*k+j]]
     CLEARMOE_STAGE(CLEARMOE_STAGE_COMBINE_RES, st,
                    launch_combine_residual(s.dtype, hsh, hres, inv, y, T, s.D, s.k, A, st));
+    // 7. class tokens: the dense FFN's output replaces theirs
+    if (cls) return class_tokens_impl(s, *router, x, W1, b1, b2, z, true, y, st);
     return CLEARMOE_OK;
 }
 

@@ -193,7 +193,7 @@ template <typename Tin, int EG, int NB, int KP>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(EG == 1 ? 2 : 1)))
 void k_route(
     const Tin* __restrict__ x, const Tin* __restrict__ Wg, const float* __restrict__ bg, int64_t T,
-    int D, int E, int k, int adaptive, double tau, int32_t* __restrict__ idx,
+    int D, int E, int k, int adaptive, double tau, int dense_stride, int32_t* __restrict__ idx,
     float* __restrict__ gate, int32_t* __restrict__ tile_counts, int w_lds) {
     extern __shared__ __attribute__((aligned(16))) unsigned char s_w[];
     constexpr int EP = 16 * EG;                      // experts padded to MFMA rows
@@ -247,46 +247,61 @@ void k_route(
                 lacc[g][b][v] = 0.0;
             }
 
-    // Loads of step s (KS columns of d) for the wave's NB token blocks and the
-    // router rows.  A ring of kPre steps keeps several steps in flight; the loop
-    // is branch-free (steps past D and rows past T read a 16-byte zero page),
-    // so the compiler's waits stay per round instead of per step.  Every
-    // kPart columns the float32 partials move into double.
+    // Loads of MFMA k-steps (KS columns of d each) for the wave's NB token
+    // blocks and the router rows, two k-steps per ring step: the two 16-byte
+    // loads a lane makes from one row cover the two 64-byte halves of a
+    // 128-byte line and are issued back to back.  A ring of kPre / 2 ring
+    // steps keeps several in flight; the loop is branch-free (columns past D
+    // and rows past the tile read zeros from the raw buffers), so the
+    // compiler's waits stay per round instead of per step.  Every kPart
+    // columns the float32 partials move into double.
     constexpr int kPre = KP;
-    static_assert((kPre * KS) % kPart == 0 && kPart % KS == 0, "partials align with rounds");
+    static_assert(kPre % 2 == 0 && (kPre * KS) % kPart == 0 && (2 * KS) % kPart == 0,
+                  "partials align with ring steps");
     const int nsteps = (D + KS - 1) / KS;
-    const int nround = (nsteps + kPre - 1) / kPre;
-    uint4 xr[kPre][NB], wr[kPre][EG];
-    auto load_step = [&](int s, uint4 (&xv)[NB], uint4 (&wv)[EG]) {
-        const int dd = s * KS + grp * PER16;
-        const bool din = dd < D;
+    constexpr int kP = kPre / 2;
+    uint4 xr[kP][NB][2], wr[kP][EG][2];
+    auto load_step = [&](int s, uint4 (&xv)[NB][2], uint4 (&wv)[EG][2]) {
 #pragma unroll
-        for (int b = 0; b < NB; ++b) {
-            const int tr = w * kTok + 16 * b + col;      // row within the tile
-            xv[b] = raw_load16(rx, (din && tr < rows) ? static_cast<uint32_t>((tr * D + dd) * esz) : kRawOob);
+        for (int h = 0; h < 2; ++h) {
+            const int dd = (2 * s + h) * KS + grp * PER16;
+            const bool din = dd < D;
+#pragma unroll
+            for (int b = 0; b < NB; ++b) {
+                const int tr = w * kTok + 16 * b + col;
+                xv[b][h] = raw_load16(rx, (din && tr < rows) ? static_cast<uint32_t>((tr * D + dd) * esz) : kRawOob);
+            }
         }
 #pragma unroll
-        for (int g = 0; g < EG; ++g) {
-            const int e = 16 * g + col;
-            wv[g] = raw_load16(rw, (din && e < E) ? static_cast<uint32_t>((e * D + dd) * esz) : kRawOob);
-        }
-    };
-#pragma unroll
-    for (int i = 0; i < kPre; ++i) load_step(i, xr[i], wr[i]);
-    for (int o = 0; o < nround; ++o) {
-#pragma unroll
-        for (int i = 0; i < kPre; ++i) {
+        for (int h = 0; h < 2; ++h) {
+            const int dd = (2 * s + h) * KS + grp * PER16;
+            const bool din = dd < D;
 #pragma unroll
             for (int g = 0; g < EG; ++g) {
-                const uint4 wa = RouteMfma<Tin>::absv(wr[i][g]);
+                const int e = 16 * g + col;
+                wv[g][h] = raw_load16(rw, (din && e < E) ? static_cast<uint32_t>((e * D + dd) * esz) : kRawOob);
+            }
+        }
+    };
+    const int nround2 = (nsteps + 2 * kP - 1) / (2 * kP);
+#pragma unroll
+    for (int i = 0; i < kP; ++i) load_step(i, xr[i], wr[i]);
+    for (int o = 0; o < nround2; ++o) {
+#pragma unroll
+        for (int i = 0; i < kP; ++i) {
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+            for (int g = 0; g < EG; ++g) {
+                const uint4 wa = RouteMfma<Tin>::absv(wr[i][g][h]);
 #pragma unroll
                 for (int b = 0; b < NB; ++b) {
-                    RouteMfma<Tin>::step(wr[i][g], xr[i][b], acc[g][b]);
-                    RouteMfma<Tin>::step(wa, RouteMfma<Tin>::absv(xr[i][b]), aab[g][b]);
+                    RouteMfma<Tin>::step(wr[i][g][h], xr[i][b][h], acc[g][b]);
+                    RouteMfma<Tin>::step(wa, RouteMfma<Tin>::absv(xr[i][b][h]), aab[g][b]);
                 }
             }
-            load_step((o + 1) * kPre + i, xr[i], wr[i]);   // past the end: zero page
-            if (((i + 1) * KS) % kPart == 0) {
+            load_step((o + 1) * kP + i, xr[i], wr[i]);
+            if (((i + 1) * 2 * KS) % kPart == 0) {
 #pragma unroll
                 for (int g = 0; g < EG; ++g)
 #pragma unroll
@@ -304,7 +319,9 @@ void k_route(
     // wave's first kTok lanes takes the logits of one token; for S only each
     // lane's maximum over its four experts is exchanged.
     const int64_t t = tw + lane;
-    const bool valid = lane < kTok && t < T;
+    // a class token (dense path) takes no expert: no choice to certify
+    const bool cls = dense_stride > 0 && t % dense_stride == 0;
+    const bool valid = lane < kTok && t < T && !cls;
     const int tl = lane < kTok ? lane : kTok - 1;    // lanes past the wave's tokens idle
     double lg[EP];
 #pragma unroll
@@ -435,6 +452,12 @@ void k_route(
     // ---- top-k (or adaptive top-1 / top-2), gates, outputs
     uint64_t mine = 0;
     if (valid) mine = route_select<EP>(lg, E, k, adaptive, tau, t, idx, gate);
+    if (cls && lane < kTok && t < T) {
+        for (int j = 0; j < k; ++j) {
+            idx[t * k + j] = -1;
+            gate[t * k + j] = 0.0f;
+        }
+    }
     if (tile_counts != nullptr) {
         for (int e = 0; e < E; ++e) {
             const uint64_t m = __ballot((mine >> e) & 1ull);
@@ -498,7 +521,8 @@ template <typename Tin, int EG>
 __global__ __launch_bounds__(256) void k_route_mlp(
     const Tin* __restrict__ x, const Tin* __restrict__ Wh, const float* __restrict__ bh,
     const Tin* __restrict__ Wo, const float* __restrict__ bo, int64_t T, int D, int Hr, int E,
-    int k, int adaptive, double tau, int32_t* __restrict__ idx, float* __restrict__ gate) {
+    int k, int adaptive, double tau, int dense_stride, int32_t* __restrict__ idx,
+    float* __restrict__ gate) {
     constexpr int EP = 16 * EG;
     static_assert(EG <= 4, "one wave per 16 experts");
     constexpr int PER16 = Elem<Tin>::per16;
@@ -567,44 +591,54 @@ __global__ __launch_bounds__(256) void k_route_mlp(
     // ---- one token per lane (16 lanes of wave 0): choice, gates, outputs
     const int64_t t = t0 + lane;
     if (w == 0 && lane < kMlpTokens && t < T) {
-        double lg[EP];
+        if (dense_stride > 0 && t % dense_stride == 0) {       // class token: no expert
+            for (int j = 0; j < k; ++j) {
+                idx[t * k + j] = -1;
+                gate[t * k + j] = 0.0f;
+            }
+        } else {
+            double lg[EP];
 #pragma unroll
-        for (int e = 0; e < EP; ++e)
-            lg[e] = s_lg[lane][e] + ((bo != nullptr && e < E) ? static_cast<double>(bo[e]) : 0.0);
-        (void)route_select<EP>(lg, E, k, adaptive, tau, t, idx, gate);
+            for (int e = 0; e < EP; ++e)
+                lg[e] = s_lg[lane][e] + ((bo != nullptr && e < E) ? static_cast<double>(bo[e]) : 0.0);
+            (void)route_select<EP>(lg, E, k, adaptive, tau, t, idx, gate);
+        }
     }
 }
 
 template <typename Tin>
 static hipError_t route_mlp_dt(const Tin* x, const Tin* Wh, const float* bh, const Tin* Wo,
                                const float* bo, int64_t T, int D, int Hr, int E, int k,
-                               int adaptive, double tau, int32_t* idx, float* gate,
-                               hipStream_t st) {
+                               int adaptive, double tau, int dense_stride, int32_t* idx,
+                               float* gate, hipStream_t st) {
     const int64_t blocks = (T + kMlpTokens - 1) / kMlpTokens;
     if (blocks == 0) return hipSuccess;
     const dim3 grid(static_cast<unsigned>(blocks));
     if (E <= 16)
-        k_route_mlp<Tin, 1><<<grid, 256, 0, st>>>(x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau, idx, gate);
+        k_route_mlp<Tin, 1><<<grid, 256, 0, st>>>(x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau,
+                                                    dense_stride, idx, gate);
     else if (E <= 32)
-        k_route_mlp<Tin, 2><<<grid, 256, 0, st>>>(x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau, idx, gate);
+        k_route_mlp<Tin, 2><<<grid, 256, 0, st>>>(x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau,
+                                                    dense_stride, idx, gate);
     else
-        k_route_mlp<Tin, 4><<<grid, 256, 0, st>>>(x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau, idx, gate);
+        k_route_mlp<Tin, 4><<<grid, 256, 0, st>>>(x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau,
+                                                    dense_stride, idx, gate);
     return hipGetLastError();
 }
 
 hipError_t launch_route_mlp(int dtype, const void* x, const void* Wh, const float* bh,
                             const void* Wo, const float* bo, int64_t T, int D, int Hr, int E,
-                            int k, int adaptive, double tau, int32_t* idx, float* gate,
-                            hipStream_t st) {
+                            int k, int adaptive, double tau, int dense_stride, int32_t* idx,
+                            float* gate, hipStream_t st) {
     if (Hr < 1 || Hr > kMlpHiddenMax) return hipErrorInvalidValue;
     if (dtype == 0)
         return route_mlp_dt<float>(static_cast<const float*>(x), static_cast<const float*>(Wh), bh,
                                    static_cast<const float*>(Wo), bo, T, D, Hr, E, k, adaptive,
-                                   tau, idx, gate, st);
+                                   tau, dense_stride, idx, gate, st);
     return route_mlp_dt<bf16_bits>(static_cast<const bf16_bits*>(x),
                                    static_cast<const bf16_bits*>(Wh), bh,
                                    static_cast<const bf16_bits*>(Wo), bo, T, D, Hr, E, k, adaptive,
-                                   tau, idx, gate, st);
+                                   tau, dense_stride, idx, gate, st);
 }
 
 constexpr int64_t kRouteWLds = 32 * 1024;
@@ -612,8 +646,8 @@ constexpr int64_t kRouteWLds = 32 * 1024;
 
 template <typename Tin>
 static hipError_t route_dt(const Tin* x, const Tin* Wg, const float* bg, int64_t T, int D, int E,
-                           int k, int adaptive, double tau, int32_t* idx, float* gate,
-                           int32_t* tc, hipStream_t st) {
+                           int k, int adaptive, double tau, int dense_stride, int32_t* idx,
+                           float* gate, int32_t* tc, hipStream_t st) {
     const int64_t blocks = hist_tiles(T, E);
     if (blocks == 0) return hipSuccess;
     const dim3 grid(static_cast<unsigned>(blocks));
@@ -622,28 +656,32 @@ static hipError_t route_dt(const Tin* x, const Tin* Wg, const float* bg, int64_t
     const int64_t wbytes = static_cast<int64_t>(E) * D * static_cast<int64_t>(sizeof(Tin));
     const int w_lds = wbytes <= kRouteWLds ? static_cast<int>((wbytes + 1023) / 1024 * 1024) : 0;
     if (small)
-        k_route<Tin, 1, 1, 12><<<grid, 256, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive, tau, idx,
-                                                          gate, tc, w_lds);
+        k_route<Tin, 1, 1, 12><<<grid, 256, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive, tau,
+                                                          dense_stride, idx, gate, tc, w_lds);
     else if (E <= 16)
         k_route<Tin, 1, 4, KPRE><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive,
-                                                                   tau, idx, gate, tc, w_lds);
+                                                                   tau, dense_stride, idx, gate, tc,
+                                                                   w_lds);
     else if (E <= 32)
         k_route<Tin, 2, 4, KPRE><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive,
-                                                                   tau, idx, gate, tc, w_lds);
+                                                                   tau, dense_stride, idx, gate, tc,
+                                                                   w_lds);
     else
         k_route<Tin, 4, 4, KPRE><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive,
-                                                                   tau, idx, gate, tc, w_lds);
+                                                                   tau, dense_stride, idx, gate, tc,
+                                                                   w_lds);
     return hipGetLastError();
 }
 
 hipError_t launch_route(int dtype, const void* x, const void* Wg, const float* bg, int64_t T,
-                        int D, int E, int k, int adaptive, double tau, int32_t* idx, float* gate,
-                        int32_t* tile_counts, hipStream_t st) {
+                        int D, int E, int k, int adaptive, double tau, int dense_stride,
+                        int32_t* idx, float* gate, int32_t* tile_counts, hipStream_t st) {
     if (dtype == 0)
         return route_dt<float>(static_cast<const float*>(x), static_cast<const float*>(Wg), bg, T,
-                               D, E, k, adaptive, tau, idx, gate, tile_counts, st);
+                               D, E, k, adaptive, tau, dense_stride, idx, gate, tile_counts, st);
     return route_dt<bf16_bits>(static_cast<const bf16_bits*>(x), static_cast<const bf16_bits*>(Wg),
-                               bg, T, D, E, k, adaptive, tau, idx, gate, tile_counts, st);
+                               bg, T, D, E, k, adaptive, tau, dense_stride, idx, gate, tile_counts,
+                               st);
 }
 
 }  // namespace clearmoe

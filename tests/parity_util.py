@@ -87,9 +87,12 @@ def gpu_router(L, d=None):
     keep = {"Wg": dev(L["Wg"]), "bg": dev(L["bg"])}
     if rt["kind"] == "mlp":
         keep["Wh"], keep["bh"] = dev(rt["Wh"]), dev(rt["bh"])
+    stride = int(L.get("dense_stride") or 0)
+    if stride > 0:
+        keep["W2"] = dev(L["W2"])
     r = cm.make_router(keep["Wg"], keep["bg"], keep.get("Wh"), keep.get("bh"),
                        adaptive=rt.get("adaptive", rt["kind"] == "adaptive"),
-                       tau=rt.get("tau", 0.0))
+                       tau=rt.get("tau", 0.0), dense_stride=stride, W2=keep.get("W2"))
     return r, keep
 
 

@@ -158,16 +158,19 @@ def test_padded_entry_point_workspace_and_rejections():
 
 
 def _router(**kw):
-    d = dict(Wg=FAKE.value, bg=None, Wh=None, bh=None, hidden=0, adaptive=0, tau=0.0)
+    d = dict(Wg=FAKE.value, bg=None, Wh=None, bh=None, W2=None, hidden=0, adaptive=0,
+             dense_stride=0, reserved=0, tau=0.0)
     d.update(kw)
-    return cm.Router(d["Wg"], d["bg"], d["Wh"], d["bh"], d["hidden"], d["adaptive"], d["tau"])
+    return cm.Router(d["Wg"], d["bg"], d["Wh"], d["bh"], d["W2"], d["hidden"], d["adaptive"],
+                     d["dense_stride"], d["reserved"], d["tau"])
 
 
 def test_router_descriptor_layout():
-    """The ctypes mirror of clearmoe_router: four pointers, two int32, one
-    double, no padding (48 bytes)."""
-    assert ctypes.sizeof(cm.Router) == 48
-    assert cm.Router.tau.offset == 40 and cm.Router.hidden.offset == 32
+    """The ctypes mirror of clearmoe_router: five pointers, four int32, one
+    double, no padding (64 bytes)."""
+    assert ctypes.sizeof(cm.Router) == 64
+    assert cm.Router.hidden.offset == 40 and cm.Router.dense_stride.offset == 48
+    assert cm.Router.tau.offset == 56
 
 
 def test_route_ex_and_ffn_ex_reject_bad_routers_before_launch():
@@ -191,6 +194,9 @@ def test_route_ex_and_ffn_ex_reject_bad_routers_before_launch():
     assert route(_router(adaptive=1, tau=float("nan"))) == 1        # NaN threshold
     assert route(_router(adaptive=1, tau=0.5), _shape(k=1)) == 1    # adaptive needs k = 2
     assert route(_router(adaptive=1, tau=0.5), _shape(E=1, k=1)) == 1
+    assert route(_router(dense_stride=-1)) == 1
+    assert route(_router(reserved=1)) == 1
+    assert route(_router(dense_stride=197, W2=0x10004)) == 1        # misaligned W2
     assert L.clearmoe_route_ex(ctypes.byref(s), ctypes.byref(_router()), FAKE, FAKE, FAKE, FAKE,
                                8, None) == 3                        # workspace too small
     args = [FAKE] * 11
@@ -204,5 +210,8 @@ def test_route_ex_and_ffn_ex_reject_bad_routers_before_launch():
     a[1] = None                                                     # NULL W1
     assert L.clearmoe_ffn_forward_ex(ctypes.byref(s), ctypes.byref(_router()), *a, FAKE, n,
                                      None) == 1
+    # class tokens need the dense fc2 weight
+    assert L.clearmoe_ffn_forward_ex(ctypes.byref(s), ctypes.byref(_router(dense_stride=197)),
+                                     *args, FAKE, n, None) == 1
     assert L.clearmoe_ffn_forward_ex(ctypes.byref(s), ctypes.byref(_router()), *args, FAKE, n - 1,
                                      None) == 3
