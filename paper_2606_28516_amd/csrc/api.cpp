@@ -496,16 +496,23 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
     }
 
     // 1. router + top-k + per-tile histogram; 2. scan + stable permutation
+    // (the fused top-1 kernel does the latter itself from the histogram
+    // when it is small enough for one workgroup's scan)
     rc = route_impl(s, L, *router, x, idx, gate, ws, st);
     if (rc != CLEARMOE_OK) return rc;
-    rc = dispatch_impl(s, L, idx, ws, counts, offsets, perm, inv, nullptr, nullptr, true, st);
-    if (rc != CLEARMOE_OK) return rc;
+    const bool own_dispatch = fused && hist_tiles(T, s.E) * s.E <= kInlineScanMax;
+    if (!own_dispatch) {
+        rc = dispatch_impl(s, L, idx, ws, counts, offsets, perm, inv, nullptr, nullptr, true, st);
+        if (rc != CLEARMOE_OK) return rc;
+    }
 
     // Top-1 in bf16: fc1 + GELU, [t|u] and y in one kernel (z stays on chip).
     if (fused) {
+        const int32_t* tc = own_dispatch ? at<int32_t>(ws, L.tile_counts) : nullptr;
         CLEARMOE_STAGE(CLEARMOE_STAGE_FUSED_TOP1, st,
-                       launch_fused_top1(x, W1, b1, US, Vt, b2, P, Q, perm, offsets, gate, y, T,
-                                         s.D, s.H, s.E, s.r, s.q, st));
+                       launch_fused_top1(x, W1, b1, US, Vt, b2, P, Q, perm, offsets,
+                                         own_dispatch ? idx : nullptr, tc, gate, y, T, s.D, s.H,
+                                         s.E, s.r, s.q, st));
         // join: the class rows of y (written on the side stream) are complete
         // before anything later on the caller's stream
         if (side != nullptr) {

@@ -166,6 +166,9 @@ struct FusedArgs {
     const bf16_bits* Q;
     const int32_t* perm;
     const int32_t* offsets;
+    const int32_t* idx;          // [T] expert of each token (k = 1), with tile_counts:
+    const int32_t* tile_counts;  //   the router's histogram [nh][E] of htile-token tiles;
+    int htile, nh;               //   non-NULL: the workgroup finds its rows' tokens itself
     const float* gate;
     bf16_bits* y;
     int64_t T;
@@ -228,6 +231,31 @@ void k_fused_top1(FusedArgs a) {
     // ---- tile -> (expert e, rows [m_lo, m_hi)), XCD-major order
     const int tile = (blockIdx.x % kFXcds) * a.per_xcd + blockIdx.x / kFXcds;
     if (tile >= a.tiles_bound) return;
+    const bool own_dispatch = a.tile_counts != nullptr;
+    __shared__ int s_off[65];                   // expert offsets (own dispatch)
+    __shared__ int s_nlist;
+    if (own_dispatch) {
+        // Expert totals from the router's histogram (staged in the x region,
+        // free until the gather): thread tid sums expert tid % E over tiles
+        // tid / E + G i, then one LDS atomic; thread 0 scans them.
+        int* s_h = reinterpret_cast<int*>(smem + a.x_off);
+        const int nhE = a.nh * a.E;
+        for (int i = tid; i < nhE; i += 256) s_h[i] = a.tile_counts[i];
+        if (tid <= a.E) s_off[tid] = 0;
+        if (tid == 0) s_nlist = 0;
+        __syncthreads();
+        const int G = 256 / a.E;
+        if (tid < G * a.E) {
+            const int ee = tid % a.E;
+            int c = 0;
+            for (int b = tid / a.E; b < a.nh; b += G) c += s_h[b * a.E + ee];
+            atomicAdd(&s_off[ee + 1], c);
+        }
+        __syncthreads();
+        if (tid == 0)
+            for (int ee = 0; ee < a.E; ++ee) s_off[ee + 1] += s_off[ee];
+        __syncthreads();
+    }
     int e = -1;
     int64_t m_lo = 0, m_hi = 0;
     {
@@ -236,7 +264,8 @@ void k_fused_top1(FusedArgs a) {
         for (int s = 0; s < a.E; ++s) {
             // offsets are clamped to [0, T]: bad offsets cannot send a
             // workgroup outside the buffers
-            int64_t lo = a.offsets[s], hi = a.offsets[s + 1];
+            int64_t lo = own_dispatch ? s_off[s] : a.offsets[s];
+            int64_t hi = own_dispatch ? s_off[s + 1] : a.offsets[s + 1];
             lo = lo < 0 ? 0 : (lo > M ? M : lo);
             hi = hi < lo ? lo : (hi > M ? M : hi);
             const int64_t nt = (hi - lo + kFRows - 1) / kFRows;
@@ -253,7 +282,80 @@ void k_fused_top1(FusedArgs a) {
     const int rows = static_cast<int>(m_hi - m_lo);
     const int D = a.D, H = a.H, r = a.r, rq = a.r + a.q;
 
-    if (tid < kFRows) {
+    if (own_dispatch) {
+        // The tokens of ranks [rlo, rhi) of expert e in the stable order (by
+        // token index).  A block scan over the histogram column of e gives
+        // every tile's first rank; the tiles that hold ranks of the range (at
+        // most 64: each holds at least one) go to a list, and the waves scan
+        // their idx with ballots, each rank's token landing in s_tok.
+        const int* s_h = reinterpret_cast<const int*>(smem + a.x_off);
+        int2* s_list = reinterpret_cast<int2*>(smem + a.x_off) + (a.nh * a.E + 1) / 2;
+        __shared__ int s_wsum[4];
+        const int rlo = static_cast<int>(m_lo) - s_off[e], rhi = static_cast<int>(m_hi) - s_off[e];
+        const int per = (a.nh + 255) / 256;
+        const int b0 = tid * per, b1 = b0 + per < a.nh ? b0 + per : a.nh;
+        int mine = 0;
+        for (int b = b0; b < b1; ++b) mine += s_h[b * a.E + e];
+        int incl = mine;                        // inclusive scan over the block
+#pragma unroll
+        for (int o = 1; o < 64; o <<= 1) {
+            const int n = __shfl_up(incl, o);
+            if (lane >= o) incl += n;
+        }
+        if (lane == 63) s_wsum[wave] = incl;
+        if (tid < kFRows) s_tok[tid] = -1;
+        __syncthreads();
+        int pre = incl - mine;
+        for (int i = 0; i < wave; ++i) pre += s_wsum[i];
+        for (int b = b0; b < b1; ++b) {
+            const int c = s_h[b * a.E + e];
+            if (c > 0 && pre < rhi && pre + c > rlo) {
+                const int at = atomicAdd(&s_nlist, 1);
+                if (at < kFRows) s_list[at] = make_int2(b, pre);
+            }
+            pre += c;
+        }
+        __syncthreads();
+        const int nlist = s_nlist < kFRows ? s_nlist : kFRows;
+        const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+        // a wave's 64-token chunks of its listed tiles, up to 8 loads in
+        // flight before the ballots use them
+        const int cpt = a.htile / 64;                  // chunks per tile
+        for (int li0 = wave; li0 < nlist; li0 += 4 * (8 / cpt)) {
+            int exv[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int li = li0 + 4 * (j / cpt);
+                const int c0 = 64 * (j % cpt);
+                exv[j] = -1;
+                if (li < nlist && j < 8 / cpt * cpt) {
+                    const int64_t t = static_cast<int64_t>(s_list[li].x) * a.htile + c0 + lane;
+                    if (t < a.T) exv[j] = a.idx[t];
+                }
+            }
+            int run = 0;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const int li = li0 + 4 * (j / cpt);
+                if (li >= nlist || j >= 8 / cpt * cpt) break;   // uniform
+                const int c0 = 64 * (j % cpt);
+                if (c0 == 0) run = s_list[li].y;
+                const uint64_t m = __ballot(exv[j] == e);
+                const int rank = run + __popcll(m & below);
+                const int64_t t = static_cast<int64_t>(s_list[li].x) * a.htile + c0 + lane;
+                if (exv[j] == e && rank >= rlo && rank < rhi) s_tok[rank - rlo] = static_cast<int32_t>(t);
+                run += __popcll(m);
+            }
+        }
+        __syncthreads();
+        // top-1 gates are exactly 1 (the softmax of one selected logit)
+        if (tid < kFRows) {
+            const int32_t t = s_tok[tid];
+            const bool ok = tid < rows && t >= 0 && t < a.T;
+            s_gate[tid] = ok ? 1.0f : 0.0f;
+            if (!ok) s_tok[tid] = -1;
+        }
+    } else if (tid < kFRows) {
         int32_t tok = -1;
         float g = 0.0f;
         if (tid < rows) {
@@ -735,9 +837,9 @@ bool fused_top1_supported(int D, int H, int r, int q) {
 
 hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, const void* US,
                              const void* Vt, const float* b2, const void* P, const void* Q,
-                             const int32_t* perm, const int32_t* offsets, const float* gate,
-                             void* y, int64_t T, int D, int H, int E, int r, int q,
-                             hipStream_t st) {
+                             const int32_t* perm, const int32_t* offsets, const int32_t* idx,
+                             const int32_t* tile_counts, const float* gate, void* y, int64_t T,
+                             int D, int H, int E, int r, int q, hipStream_t st) {
     if (!fused_top1_supported(D, H, r, q)) return hipErrorInvalidValue;
     if (T == 0) return hipSuccess;
     FusedArgs a{};
@@ -751,6 +853,13 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
     a.Q = static_cast<const bf16_bits*>(Q);
     a.perm = perm;
     a.offsets = offsets;
+    a.idx = idx;
+    a.tile_counts = tile_counts;
+    a.htile = hist_tile(T, E);
+    a.nh = static_cast<int>(hist_tiles(T, E));
+    if (tile_counts != nullptr &&
+        (idx == nullptr || static_cast<int64_t>(a.nh) * E > kInlineScanMax || E > 64))
+        return hipErrorInvalidValue;
     a.gate = gate;
     a.y = static_cast<bf16_bits*>(y);
     a.T = T;

@@ -201,16 +201,19 @@ hipError_t launch_gemm(int dtype, const GemmDesc& g, hipStream_t st);
 
 // Fused top-1 layer in bfloat16: y[perm p] = [t|u](p) [US | P_e]^T + b2 with
 // [t|u](p) = GELU(x[perm p] W1^T + b1) [Vt ; Q_e]^T (u columns times the gate),
-// every intermediate on chip.  Needs the expert order (perm, offsets) of a
-// top-1 routing.  Shapes outside fused_top1_supported use the GEMM path.
+// every intermediate on chip.  Needs the expert order of a top-1 routing:
+// either (perm, offsets) from the dispatch, or (tile_counts non-NULL) the
+// router's tile histogram and idx, from which each workgroup finds its rows'
+// tokens itself (histograms of at most kInlineScanMax entries).  Shapes
+// outside fused_top1_supported use the GEMM path.
 constexpr int kFusedMaxD = 768;      // x rows of a 64-row tile live in LDS ...
 constexpr int kFusedMaxH = 8192;     // ... beside b1
 constexpr int kFusedMaxRQ = 160;     // [t|u] accumulators live in registers
 bool fused_top1_supported(int D, int H, int r, int q);
 hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, const void* US,
                              const void* Vt, const float* b2, const void* P, const void* Q,
-                             const int32_t* perm, const int32_t* offsets, const float* gate,
-                             void* y, int64_t T, int D, int H, int E, int r, int q,
-                             hipStream_t st);
+                             const int32_t* perm, const int32_t* offsets, const int32_t* idx,
+                             const int32_t* tile_counts, const float* gate, void* y, int64_t T,
+                             int D, int H, int E, int r, int q, hipStream_t st);
 
 }  // namespace clearmoe
