@@ -40,6 +40,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 PROFILE_DIR = os.path.join(ROOT, "profiles")
+TIME_EVERY = 8
 
 
 def parse():
@@ -59,11 +60,24 @@ def parse():
     return ap.parse_args()
 
 
-def source_digest():
-    """Hash of the HIP sources: counters taken on other code are not reported."""
+KERNEL_SOURCES = {
+    "route": ["route.hip"], "tile_hist": ["dispatch.hip"], "scan": ["dispatch.hip"],
+    "permute": ["dispatch.hip"], "combine": ["dispatch.hip"], "combine_res": ["dispatch.hip"],
+    "fused_top1": ["fused.hip"],
+}
+
+
+def source_digest(kernel=None):
+    """Hash of the HIP sources a kernel is built from (its own file and the shared
+    header; GEMM stages: gemm.hip), or of all of them: counters taken on other
+    code are not reported."""
     h = hashlib.sha256()
     cdir = os.path.join(ROOT, "paper_2606_28516_amd", "csrc")
-    for name in sorted(os.listdir(cdir)):
+    if kernel is None:
+        names = sorted(os.listdir(cdir))
+    else:
+        names = sorted(KERNEL_SOURCES.get(kernel, ["gemm.hip"]) + ["kernels.h"])
+    for name in names:
         with open(os.path.join(cdir, name), "rb") as f:
             h.update(name.encode())
             h.update(f.read())
@@ -88,10 +102,11 @@ def stage_work(stage, cfg, b):
         "dense_fc2": (2 * T * D * H, T * H * b + D * H * b + T * D * b),
         "tu_grouped": (2 * A * (r + q) * H, A * H * b + (r + E * q) * H * b + A * (r + q) * b),
         "y_grouped": (2 * A * D * (r + q), A * (r + q) * b + D * (r + E * q) * b + T * D * b),
-        # x in, y out; W1, [Vt;Q_e] and [US|P_e] once each; b1, b2, perm and gate
+        # x in, y out; W1, [Vt;Q_e] and [US|P_e] once each; b1, b2; the expert
+        # index of every token and the router's tile histogram
         "fused_top1": (2 * T * (D * H + H * (r + q) + (r + q) * D),
                        2 * T * D * b + H * D * b + 2 * (r + E * q) * (H + D) * b // 2
-                       + (H + D) * 4 + T * 8),
+                       + (H + D) * 4 + T * 4 + 4 * E * ((T + 63) // 64 if E <= 16 else (T + 255) // 256)),
     }
     return w.get(stage, (0, 0))
 
@@ -173,8 +188,10 @@ def main():
     stages = {s: ms / n for s, (ms, n) in per.items()}
     dominant = max(stages, key=stages.get)
 
-    # Timed region: exactly K steps; events recorded around the dominant kernel only.
-    cm.timing_start([dominant], args.steps)
+    # Timed region: exactly K steps.  One launch of the dominant kernel in
+    # TIME_EVERY is dispatched with start/end events (a timed dispatch costs
+    # the step a few microseconds, so timing all of them would slow the step).
+    cm.timing_start([dominant], args.steps, every=TIME_EVERY)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -190,7 +207,7 @@ def main():
 
     flops, byts = stage_work(dominant, cfg, b)
     dom_avg_s = dom_ms / dom_n * 1e-3
-    digest = source_digest()
+    digest = source_digest(dominant)
     if flops > 0:
         roof = dict(bound="mfma", achieved=flops / dom_avg_s / 1e12,
                     peak=MFMA_PEAK_TFLOPS[cfg.dtype], unit="TFLOP/s")
@@ -200,6 +217,7 @@ def main():
     roof["traffic"] = load_traffic(dominant, args.workload, digest)
     roof["kernel"] = dominant
     roof["avg_launch_us"] = dom_avg_s * 1e6
+    roof["timed_launches"] = dom_n
     roof["algorithmic_per_launch"] = flops if flops > 0 else byts
 
     out = {
@@ -221,7 +239,7 @@ def main():
         "layer_tflops": layer_flops(cfg) / (ms_step * 1e-3) / 1e12,
         "stages_us": {s: v * 1e3 for s, v in sorted(stages.items(), key=lambda kv: -kv[1])},
         "wall_s": wall,
-        "source_digest": digest,
+        "source_digest": source_digest(),
     }
 
     if not args.no_extras:
@@ -310,16 +328,19 @@ def bench_dispatch(cm, synth, torch, np, stream, steps):
     for _ in range(3):
         run()
     torch.cuda.synchronize()
-    names = cm.stage_names()
-    cm.timing_start(names, steps * len(names))
+    # untimed steps for the step time, then timed ones for the per-kernel times
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)
     for _ in range(steps):
         run()
     e1.record(stream)
     torch.cuda.synchronize()
-    per = cm.timing_stop()
     ms = e0.elapsed_time(e1) / steps
+    names = cm.stage_names()
+    cm.timing_start(names, steps * len(names))
+    for _ in range(steps):
+        run()
+    per = cm.timing_stop()
     A = T * k
     b = 2
     # x read, xperm written and read, y written, idx/gate/perm/inv written, inv/gate read
@@ -430,15 +451,17 @@ def bench_routers(cm, synth, torch, np, stream, L, steps):
         for _ in range(5):
             run()
         torch.cuda.synchronize()
-        cm.timing_start(["route"], steps)
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for _ in range(steps):
             run()
         e1.record(stream)
         torch.cuda.synchronize()
-        r_ms, r_n = cm.timing_stop()["route"]
         ms = e0.elapsed_time(e1) / steps
+        cm.timing_start(["route"], steps)
+        for _ in range(steps):
+            run()
+        r_ms, r_n = cm.timing_stop()["route"]
         two = float((idx[:, 1] >= 0).float().mean()) if k == 2 else 0.0
         out["variants"][name] = {"ms": ms, "tokens_per_s": cfg.T / (ms * 1e-3),
                                  "route_us": r_ms / r_n * 1e3, "share_top2": two}

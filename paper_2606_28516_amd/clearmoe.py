@@ -28,7 +28,7 @@ DISPATCH_HIST_IN_WS = 1
 SYMBOLS = ("clearmoe_version", "clearmoe_status_string", "clearmoe_workspace_bytes",
            "clearmoe_route", "clearmoe_dispatch", "clearmoe_combine", "clearmoe_ffn_forward",
            "clearmoe_dense_ffn_forward", "clearmoe_stage_name", "clearmoe_timing_start",
-           "clearmoe_timing_stop", "clearmoe_padded_workspace_bytes",
+           "clearmoe_timing_start_sampled", "clearmoe_timing_stop", "clearmoe_padded_workspace_bytes",
            "clearmoe_ffn_forward_padded", "clearmoe_route_ex", "clearmoe_ffn_forward_ex")
 N_STAGES = 16
 
@@ -91,6 +91,8 @@ def lib():
         L.clearmoe_stage_name.argtypes = [ctypes.c_int]
         L.clearmoe_timing_start.restype = ctypes.c_int
         L.clearmoe_timing_start.argtypes = [u32, ctypes.c_int]
+        L.clearmoe_timing_start_sampled.restype = ctypes.c_int
+        L.clearmoe_timing_start_sampled.argtypes = [u32, ctypes.c_int, ctypes.c_int]
         L.clearmoe_timing_stop.restype = ctypes.c_int
         L.clearmoe_timing_stop.argtypes = [ctypes.POINTER(ctypes.c_double),
                                            ctypes.POINTER(ctypes.c_int32)]
@@ -297,13 +299,15 @@ def stage_names():
     return [lib().clearmoe_stage_name(i).decode() for i in range(N_STAGES)]
 
 
-def timing_start(stages, max_records: int) -> None:
-    """Time every launch of the named stages (at most max_records launches)."""
+def timing_start(stages, max_records: int, every: int = 1) -> None:
+    """Time every every-th launch of the named stages (at most max_records
+    timed launches)."""
     names = stage_names()
     mask = 0
     for s in stages:
         mask |= 1 << names.index(s)
-    _check(lib().clearmoe_timing_start(mask, int(max_records)), "clearmoe_timing_start")
+    _check(lib().clearmoe_timing_start_sampled(mask, int(max_records), int(every)),
+           "clearmoe_timing_start_sampled")
 
 
 def timing_stop() -> dict:

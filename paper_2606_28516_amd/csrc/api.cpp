@@ -12,6 +12,11 @@
 
 using namespace clearmoe;
 
+LaunchTiming& clearmoe::launch_timing() {
+    thread_local LaunchTiming t;
+    return t;
+}
+
 namespace {
 
 constexpr size_t kAlign = 256;
@@ -101,6 +106,8 @@ struct StageTimer {
     bool on = false;
     unsigned mask = 0;
     int used = 0;
+    int every = 1;     // time launches 0, every, 2 every, ... of the selected stages
+    int64_t seen = 0;  // selected launches since timing started
     std::vector<hipEvent_t> ev;   // 2 per record
     std::vector<int> stage;
 };
@@ -109,22 +116,29 @@ std::mutex g_timer_mu;
 
 class StageScope {
   public:
-    StageScope(int stage, hipStream_t st) : st_(st) {
+    StageScope(int stage, hipStream_t st) {
+        (void)st;
         if (!g_timer.on || !((g_timer.mask >> stage) & 1u)) return;
         std::lock_guard<std::mutex> lk(g_timer_mu);
+        if (g_timer.seen++ % g_timer.every != 0) return;
         if (g_timer.used >= static_cast<int>(g_timer.stage.size())) return;
         slot_ = g_timer.used++;
         g_timer.stage[slot_] = stage;
-        (void)hipEventRecord(g_timer.ev[2 * slot_], st_);
+        launch_timing() = LaunchTiming{g_timer.ev[2 * slot_], g_timer.ev[2 * slot_ + 1]};
     }
     ~StageScope() {
-        if (slot_ >= 0) (void)hipEventRecord(g_timer.ev[2 * slot_ + 1], st_);
+        if (slot_ < 0) return;
+        LaunchTiming& t = launch_timing();
+        if (t.start == g_timer.ev[2 * slot_]) {   // no kernel took the events
+            t = LaunchTiming{};
+            std::lock_guard<std::mutex> lk(g_timer_mu);
+            g_timer.stage[slot_] = -1;
+        }
     }
     StageScope(const StageScope&) = delete;
     StageScope& operator=(const StageScope&) = delete;
 
   private:
-    hipStream_t st_;
     int slot_ = -1;
 };
 
@@ -717,8 +731,12 @@ const char* clearmoe_stage_name(int stage) {
 }
 
 int clearmoe_timing_start(unsigned stage_mask, int max_records) {
+    return clearmoe_timing_start_sampled(stage_mask, max_records, 1);
+}
+
+int clearmoe_timing_start_sampled(unsigned stage_mask, int max_records, int every) {
     std::lock_guard<std::mutex> lk(g_timer_mu);
-    if (g_timer.on || max_records < 1) return CLEARMOE_ERR_INVALID_ARG;
+    if (g_timer.on || max_records < 1 || every < 1) return CLEARMOE_ERR_INVALID_ARG;
     g_timer.ev.assign(2 * static_cast<size_t>(max_records), nullptr);
     g_timer.stage.assign(static_cast<size_t>(max_records), -1);
     for (auto& e : g_timer.ev) {
@@ -732,6 +750,8 @@ int clearmoe_timing_start(unsigned stage_mask, int max_records) {
     }
     g_timer.mask = stage_mask;
     g_timer.used = 0;
+    g_timer.every = every;
+    g_timer.seen = 0;
     g_timer.on = true;
     return CLEARMOE_OK;
 }
@@ -743,6 +763,7 @@ int clearmoe_timing_stop(double* ms, int32_t* launches) {
     int32_t cnt[CLEARMOE_N_STAGES] = {};
     int rc = CLEARMOE_OK;
     for (int i = 0; i < g_timer.used; ++i) {
+        if (g_timer.stage[i] < 0) continue;   // the stage launched no kernel
         float t = 0.0f;
         if (hipEventSynchronize(g_timer.ev[2 * i + 1]) != hipSuccess ||
             hipEventElapsedTime(&t, g_timer.ev[2 * i], g_timer.ev[2 * i + 1]) != hipSuccess) {

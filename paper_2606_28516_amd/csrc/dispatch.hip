@@ -415,10 +415,10 @@ hipError_t launch_tile_histogram(const int32_t* idx, int64_t T, int E, int k,
     const int64_t nt = hist_tiles(T, E);
     if (nt == 0) return hipSuccess;
     if (hist_tile(T, E) == kSmallTile)
-        k_tile_hist<kSmallTile><<<dim3(static_cast<unsigned>(nt)), kSmallTile, 0, st>>>(idx, T, E, k,
+        launch_kernel(k_tile_hist<kSmallTile>, dim3(static_cast<unsigned>(nt)), kSmallTile, 0, st, idx, T, E, k,
                                                                                         tile_counts);
     else
-        k_tile_hist<kRouteTile><<<dim3(static_cast<unsigned>(nt)), kRouteTile, 0, st>>>(idx, T, E, k,
+        launch_kernel(k_tile_hist<kRouteTile>, dim3(static_cast<unsigned>(nt)), kRouteTile, 0, st, idx, T, E, k,
                                                                                         tile_counts);
     return hipGetLastError();
 }
@@ -430,13 +430,13 @@ hipError_t launch_scan(const int32_t* tile_counts, int64_t ntiles, int E, int32_
     const dim3 grid(static_cast<unsigned>(scan_chunks(ntiles)));
     if (ntiles == 0) return hipSuccess;
     if (E <= 8)
-        k_scan<8><<<grid, kScanChunk, 0, st>>>(tile_counts, ntiles, E, tile_base, chunk_tot);
+        launch_kernel(k_scan<8>, grid, kScanChunk, 0, st, tile_counts, ntiles, E, tile_base, chunk_tot);
     else if (E <= 16)
-        k_scan<16><<<grid, kScanChunk, 0, st>>>(tile_counts, ntiles, E, tile_base, chunk_tot);
+        launch_kernel(k_scan<16>, grid, kScanChunk, 0, st, tile_counts, ntiles, E, tile_base, chunk_tot);
     else if (E <= 32)
-        k_scan<32><<<grid, kScanChunk, 0, st>>>(tile_counts, ntiles, E, tile_base, chunk_tot);
+        launch_kernel(k_scan<32>, grid, kScanChunk, 0, st, tile_counts, ntiles, E, tile_base, chunk_tot);
     else
-        k_scan<64><<<grid, kScanChunk, 0, st>>>(tile_counts, ntiles, E, tile_base, chunk_tot);
+        launch_kernel(k_scan<64>, grid, kScanChunk, 0, st, tile_counts, ntiles, E, tile_base, chunk_tot);
     return hipGetLastError();
 }
 
@@ -449,11 +449,11 @@ hipError_t launch_permute(int dtype, const int32_t* idx, const int32_t* tile_bas
     const size_t shm = sizeof(int) * static_cast<size_t>(kRouteTile) * k;
     const int htile = hist_tile(T, E);
     if (dtype == 0)
-        k_permute<float><<<dim3(static_cast<unsigned>(nt)), kRouteTile, shm, st>>>(
+        launch_kernel(k_permute<float>, dim3(static_cast<unsigned>(nt)), kRouteTile, shm, st,
             idx, tile_base, offsets, tile_counts, counts, T, E, k, perm, inv,
             static_cast<const float*>(x), static_cast<float*>(xperm), D, htile, chunk_tot);
     else
-        k_permute<bf16_bits><<<dim3(static_cast<unsigned>(nt)), kRouteTile, shm, st>>>(
+        launch_kernel(k_permute<bf16_bits>, dim3(static_cast<unsigned>(nt)), kRouteTile, shm, st,
             idx, tile_base, offsets, tile_counts, counts, T, E, k, perm, inv,
             static_cast<const bf16_bits*>(x), static_cast<bf16_bits*>(xperm), D, htile, chunk_tot);
     return hipGetLastError();
@@ -466,10 +466,10 @@ hipError_t launch_combine_gated(int dtype, const void* ye, const int32_t* inv, c
     if (n == 0) return hipSuccess;
     const unsigned blocks = static_cast<unsigned>((n + 256 * kCombineU - 1) / (256 * kCombineU));
     if (dtype == 0)
-        k_combine_gated<float><<<blocks, 256, 0, st>>>(static_cast<const float*>(ye), inv, gate,
+        launch_kernel(k_combine_gated<float>, blocks, 256, 0, st, static_cast<const float*>(ye), inv, gate,
                                                         static_cast<float*>(y), T, D, k);
     else
-        k_combine_gated<bf16_bits><<<blocks, 256, 0, st>>>(
+        launch_kernel(k_combine_gated<bf16_bits>, blocks, 256, 0, st,
             static_cast<const bf16_bits*>(ye), inv, gate, static_cast<bf16_bits*>(y), T, D, k);
     return hipGetLastError();
 }
@@ -481,10 +481,10 @@ hipError_t launch_combine_residual(int dtype, const float* hsh, const float* hre
     if (n == 0) return hipSuccess;
     const unsigned blocks = static_cast<unsigned>((n + 256 * kCombineU - 1) / (256 * kCombineU));
     if (dtype == 0)
-        k_combine_residual<float><<<blocks, 256, 0, st>>>(hsh, hres, inv, static_cast<float*>(y),
+        launch_kernel(k_combine_residual<float>, blocks, 256, 0, st, hsh, hres, inv, static_cast<float*>(y),
                                                            T, D, k, hres_rows);
     else
-        k_combine_residual<bf16_bits><<<blocks, 256, 0, st>>>(
+        launch_kernel(k_combine_residual<bf16_bits>, blocks, 256, 0, st,
             hsh, hres, inv, static_cast<bf16_bits*>(y), T, D, k, hres_rows);
     return hipGetLastError();
 }
@@ -523,7 +523,7 @@ hipError_t launch_pad_index(const int32_t* idx, const int32_t* counts, const int
     if (A > n) n = A;
     if (E + 1 > n) n = E + 1;
     const unsigned blocks = static_cast<unsigned>((n + 255) / 256);
-    k_pad_index<<<blocks, 256, 0, st>>>(idx, counts, offsets, perm, inv, A, E, C, perm_pad, inv_pad, seg);
+    launch_kernel(k_pad_index, blocks, 256, 0, st, idx, counts, offsets, perm, inv, A, E, C, perm_pad, inv_pad, seg);
     return hipGetLastError();
 }
 

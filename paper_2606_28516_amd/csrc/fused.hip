@@ -776,7 +776,7 @@ hipError_t fused_cfg(const FusedArgs& a, size_t lds, int grid, hipStream_t st) {
             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
         if (err != hipSuccess) return err;
     }
-    k_fused_top1<NFT, KG><<<dim3(static_cast<unsigned>(grid)), 256, lds, st>>>(a);
+    launch_kernel(k_fused_top1<NFT, KG>, dim3(static_cast<unsigned>(grid)), 256, lds, st, a);
     return hipGetLastError();
 }
 

@@ -324,7 +324,7 @@ static hipError_t gemm_cfg(const GemmDesc& g, hipStream_t st) {
     if (tiles == 0) return hipSuccess;
     const int64_t per_xcd = (tiles + kXcds - 1) / kXcds;
     const int64_t grid = per_xcd * kXcds;
-    k_gemm<Tin, BM, BN, WM, WN, NS><<<dim3(static_cast<unsigned>(grid)), 256, 0, st>>>(
+    launch_kernel(k_gemm<Tin, BM, BN, WM, WN, NS>, dim3(static_cast<unsigned>(grid)), 256, 0, st,
         g, static_cast<int>(mt), static_cast<int>(nt), static_cast<int>(per_xcd));
     return hipGetLastError();
 }

@@ -1,10 +1,35 @@
 // Internal declarations of the CLEAR-MoE HIP kernels (gfx950) and their host
 // launchers.  Nothing here is part of the public C ABI (include/clearmoe.h).
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace clearmoe {
+
+// ---------------------------------------------------------------------------
+// Kernel launches.  Every kernel goes through launch_kernel, so that a timed
+// stage can have its kernel's own start and end written into two events by
+// the dispatch itself (hipExtLaunchKernel): no marker packets join the
+// stream, and the timed step runs as an untimed one does.
+// ---------------------------------------------------------------------------
+struct LaunchTiming {
+    hipEvent_t start = nullptr, stop = nullptr;   // both set, or both null
+};
+// The calling thread's pending timing (defined with the stage timer).
+LaunchTiming& launch_timing();
+
+// Launch on st; the first launch after a timed stage opens takes its events.
+// Errors are left for the caller's hipGetLastError.
+template <typename... KArgs, typename... Args>
+void launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t lds, hipStream_t st,
+                   Args... args) {
+    LaunchTiming& t = launch_timing();
+    const LaunchTiming use = t;
+    t = LaunchTiming{};
+    hipExtLaunchKernelGGL(kernel, grid, block, static_cast<std::uint32_t>(lds), st, use.start,
+                          use.stop, 0u, static_cast<KArgs>(args)...);
+}
 
 // ---------------------------------------------------------------------------
 // Element types.  bfloat16 is carried as raw 16-bit patterns in memory.

@@ -615,13 +615,13 @@ static hipError_t route_mlp_dt(const Tin* x, const Tin* Wh, const float* bh, con
     if (blocks == 0) return hipSuccess;
     const dim3 grid(static_cast<unsigned>(blocks));
     if (E <= 16)
-        k_route_mlp<Tin, 1><<<grid, 256, 0, st>>>(x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau,
+        launch_kernel(k_route_mlp<Tin, 1>, grid, 256, 0, st, x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau,
                                                     dense_stride, idx, gate);
     else if (E <= 32)
-        k_route_mlp<Tin, 2><<<grid, 256, 0, st>>>(x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau,
+        launch_kernel(k_route_mlp<Tin, 2>, grid, 256, 0, st, x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau,
                                                     dense_stride, idx, gate);
     else
-        k_route_mlp<Tin, 4><<<grid, 256, 0, st>>>(x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau,
+        launch_kernel(k_route_mlp<Tin, 4>, grid, 256, 0, st, x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau,
                                                     dense_stride, idx, gate);
     return hipGetLastError();
 }
@@ -656,18 +656,18 @@ static hipError_t route_dt(const Tin* x, const Tin* Wg, const float* bg, int64_t
     const int64_t wbytes = static_cast<int64_t>(E) * D * static_cast<int64_t>(sizeof(Tin));
     const int w_lds = wbytes <= kRouteWLds ? static_cast<int>((wbytes + 1023) / 1024 * 1024) : 0;
     if (small)
-        k_route<Tin, 1, 1, 12><<<grid, 256, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive, tau,
+        launch_kernel(k_route<Tin, 1, 1, 12>, grid, 256, w_lds, st, x, Wg, bg, T, D, E, k, adaptive, tau,
                                                           dense_stride, idx, gate, tc, w_lds);
     else if (E <= 16)
-        k_route<Tin, 1, 4, KPRE><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive,
+        launch_kernel(k_route<Tin, 1, 4, KPRE>, grid, kRouteTile, w_lds, st, x, Wg, bg, T, D, E, k, adaptive,
                                                                    tau, dense_stride, idx, gate, tc,
                                                                    w_lds);
     else if (E <= 32)
-        k_route<Tin, 2, 4, KPRE><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive,
+        launch_kernel(k_route<Tin, 2, 4, KPRE>, grid, kRouteTile, w_lds, st, x, Wg, bg, T, D, E, k, adaptive,
                                                                    tau, dense_stride, idx, gate, tc,
                                                                    w_lds);
     else
-        k_route<Tin, 4, 4, KPRE><<<grid, kRouteTile, w_lds, st>>>(x, Wg, bg, T, D, E, k, adaptive,
+        launch_kernel(k_route<Tin, 4, 4, KPRE>, grid, kRouteTile, w_lds, st, x, Wg, bg, T, D, E, k, adaptive,
                                                                    tau, dense_stride, idx, gate, tc,
                                                                    w_lds);
     return hipGetLastError();

@@ -41,6 +41,15 @@ def test_version_and_status_strings():
     assert L.clearmoe_status_string(99) == b"unknown status"
 
 
+def test_timing_start_rejects_bad_arguments_before_creating_events():
+    L = cm.lib()
+    assert L.clearmoe_timing_start_sampled(1, 4, 0) == 1      # every < 1
+    assert L.clearmoe_timing_start_sampled(1, 0, 2) == 1      # max_records < 1
+    assert L.clearmoe_timing_start(1, 0) == 1
+    # nothing was started: stopping reports that timing is off
+    assert L.clearmoe_timing_stop(None, None) == 1
+
+
 def _shape(**kw):
     d = dict(T=100, D=64, H=128, E=4, k=2, r=16, q=8, dtype=cm.BF16)
     d.update(kw)

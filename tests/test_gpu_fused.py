@@ -69,6 +69,19 @@ def test_fused_top1_against_oracle(T, D, H, E, r, q):
     assert np.all(np.isfinite(g["y"]))
 
 
+def test_sampled_timing_times_every_nth_launch():
+    L = _layer(300, 128, 256, 4, 64, 16, seed=6)
+    gpu_ffn(L)
+    cm.timing_start(["fused_top1"], max_records=16, every=3)
+    try:
+        for _ in range(7):
+            gpu_ffn(L)
+    finally:
+        t = cm.timing_stop()
+    ms, n = t["fused_top1"]
+    assert n == 3 and ms > 0, t                 # launches 0, 3 and 6
+
+
 def test_fused_stage_replaces_the_gemm_chain():
     L = _layer(300, 128, 256, 4, 64, 16, seed=5)
     launched = _stages_of(L)
