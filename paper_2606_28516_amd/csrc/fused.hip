@@ -264,8 +264,10 @@ void k_fused_top1(FusedArgs a) {
         for (int s = 0; s < a.E; ++s) {
             // offsets are clamped to [0, T]: bad offsets cannot send a
             // workgroup outside the buffers
-            int64_t lo = own_dispatch ? s_off[s] : a.offsets[s];
-            int64_t hi = own_dispatch ? s_off[s + 1] : a.offsets[s + 1];
+            // read as uniform values (the same for every lane), so that e
+            // and the expert's buffer descriptors below live in scalar registers
+            int64_t lo = __builtin_amdgcn_readfirstlane(own_dispatch ? s_off[s] : a.offsets[s]);
+            int64_t hi = __builtin_amdgcn_readfirstlane(own_dispatch ? s_off[s + 1] : a.offsets[s + 1]);
             lo = lo < 0 ? 0 : (lo > M ? M : lo);
             hi = hi < lo ? lo : (hi > M ? M : hi);
             const int64_t nt = (hi - lo + kFRows - 1) / kFRows;
