@@ -109,6 +109,20 @@ __device__ __forceinline__ void dma16_buf(const i32x4& d, uint32_t off, uint32_t
                  : "memory", "m0");
 }
 
+// 16 bytes per lane, buffer -> registers (zeros outside the buffer).  Inline
+// asm like the DMA: the compiler does not count it, so its own waits never
+// drain the W1 stages issued after it.  The caller waits with vm_wait and
+// then passes the registers through reg_ready before any use.
+// The zero scalar offset sits in a register (not the inline constant), which
+// also tells these loads apart from the compiler's in the kernel's ISA.
+__device__ __forceinline__ u32x4 bload16_asm(const i32x4& d, uint32_t off, int zero) {
+    u32x4 v;
+    asm volatile("buffer_load_dwordx4 %0, %1, %2, %3 offen" : "=v"(v) : "v"(off), "s"(d), "s"(zero));
+    return v;
+}
+// After the wait that covers an asm load: uses of v stay below this point.
+__device__ __forceinline__ void reg_ready(u32x4& v) { asm volatile("" : "+v"(v)); }
+
 // One W1 ring stage: 8 loads of 16 bytes per lane, buffer -> LDS at
 // base + 1024 i + 16 * lane (zeros for an offset outside the buffer).  Inline
 // asm: the compiler does not count these loads; the kernel waits for them
@@ -439,6 +453,12 @@ void k_fused_top1(FusedArgs a) {
     }
     lds_barrier();
 
+    // [Vt;Q_e] are loaded by asm (d_*) when the step loop is unrolled (KG > 0),
+    // else by compiler-visible loads (r_*): a loop-carried asm result could be
+    // copied by the compiler before it lands.
+    const int soff0 = __builtin_amdgcn_readfirstlane(static_cast<int>(a.T >> 62));   // 0
+    const i32x4 d_vt = dma_desc(a.Vt, static_cast<int64_t>(r) * H * 2);
+    const i32x4 d_qe = dma_desc(a.Q + static_cast<int64_t>(e) * a.q * H, static_cast<int64_t>(a.q) * H * 2);
     const __amdgpu_buffer_rsrc_t r_vt = buf(a.Vt, static_cast<int64_t>(r) * H * 2);
     const __amdgpu_buffer_rsrc_t r_qe =
         buf(a.Q + static_cast<int64_t>(e) * a.q * H, static_cast<int64_t>(a.q) * H * 2);
@@ -476,7 +496,11 @@ void k_fused_top1(FusedArgs a) {
             for (int jj = 0; jj < 2; ++jj) {
                 const int j = j0 + jj;
                 const int hid = hb + 16 * j + 8 * lh;
-                vq[f][j] = bload16(tile_vt ? r_vt : r_qe, (live & (hid < H)) ? rowb + 2u * hid : kOob);
+                const uint32_t off = (live & (hid < H)) ? rowb + 2u * hid : kOob;
+                if constexpr (KG > 0)
+                    vq[f][j] = bload16_asm(tile_vt ? d_vt : d_qe, off, soff0);
+                else
+                    vq[f][j] = bload16(tile_vt ? r_vt : r_qe, off);
             }
         }
     };
@@ -530,7 +554,7 @@ void k_fused_top1(FusedArgs a) {
     auto block = [&](int k, auto p2_tag) {
         constexpr bool p2 = decltype(p2_tag)::value;
         const int hb = (k * 4 + wave) * kFHid;
-        if constexpr (p2) {
+        if constexpr (p2 && KG == 0) {
             // the compiler's wait for vq goes here, before this block's DMA
 #pragma unroll
             for (int f = 0; f < NFT; ++f)
@@ -567,6 +591,16 @@ void k_fused_top1(FusedArgs a) {
                 case 1: vm_wait<16 + 2 * NFT>(); break;
                 default: vm_wait<16 + 4 * NFT>(); break;
             }
+            if constexpr (p2 && KG > 0) {
+                // this wait covers stage n, issued in step 5 of the previous
+                // block after that block's [Vt;Q_e] loads: vq has landed
+                if (g == 1) {
+#pragma unroll
+                    for (int f = 0; f < NFT; ++f)
+#pragma unroll
+                        for (int j = 0; j < 4; ++j) reg_ready(vq[f][j]);
+                }
+            }
             step(n, g);
             if constexpr (p2) {
                 if (g >= 1 && g <= 4) phase2_run(g - 1, zo_prev);
@@ -593,7 +627,14 @@ void k_fused_top1(FusedArgs a) {
     if (n_iter > 0) {
         block(0, std::false_type{});
         for (int k = 1; k < n_iter; ++k) block(k, std::true_type{});
-        // drain: GELU + phase 2 of the last slice
+        // drain: GELU + phase 2 of the last slice, once its [Vt;Q_e] landed
+        if constexpr (KG > 0) {
+            vm_wait<0>();
+#pragma unroll
+            for (int f = 0; f < NFT; ++f)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) reg_ready(vq[f][j]);
+        }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             u32x4 zo[2];
