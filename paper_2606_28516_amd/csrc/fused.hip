@@ -48,7 +48,7 @@ constexpr int kFHid = 64;       // hidden units per wave per step
 constexpr int kFXcds = 8;
 constexpr int kNS = 3;                  // W1 ring stages per wave
 constexpr int kStageBytes = 64 * 128;   // 64 W1 rows x 64 inputs (bf16)
-constexpr int kCt = 3;                  // y column tiles per wave and pass
+constexpr int kCt = 3;                  // y column tiles per wave (4 kCt tiles cover D)
 
 __device__ __attribute__((aligned(16))) const uint32_t g_fused_zero[4] = {0u, 0u, 0u, 0u};
 
@@ -190,7 +190,6 @@ struct FusedArgs {
     int xch;        // LDS pitch of an x row, 16-byte chunks (odd, >= 8 * kgroups)
     int kgroups;    // ceil(D / 64) rounded up to even, at least 6
     int hpad;       // H rounded up to 4 waves x 64
-    int redp;       // LDS pitch (floats) of a token's [t|u] partial sums
     int tuch;       // LDS pitch of a bf16 [t|u] row, 16-byte chunks (odd)
     int yp;         // LDS pitch (elements) of a bf16 y row
     int b2_off;     // byte offset of b2 (after b1)
@@ -644,42 +643,44 @@ void k_fused_top1(FusedArgs a) {
     }
     vm_wait<0>();
 
-    // [US | P_e] operands of this wave's first pass of output columns, loaded
-    // now so that their latency hides behind the reduction (whose barriers
-    // therefore leave vector-memory loads alone)
-    const __amdgpu_buffer_rsrc_t r_us = buf(a.US, static_cast<int64_t>(D) * r * 2);
-    const __amdgpu_buffer_rsrc_t r_pe =
-        buf(a.P + static_cast<int64_t>(e) * D * a.q, static_cast<int64_t>(D) * a.q * 2);
-    const int rqp = (rq + 15) & ~15;
-    const int nks = rqp / 16;
+    // [US | P_e] operands of this wave's output columns (tiles wave + 4 c; the
+    // host admits D <= 128 kCt, so one pass covers every column), issued now
+    // by asm so that they stay here and their latency hides behind the
+    // reduction.  A k step is all US columns or all P_e columns (r is a
+    // multiple of 16); columns past r + q and rows past D read zeros.
+    const i32x4 d_us = dma_desc(a.US, static_cast<int64_t>(D) * r * 2);
+    const i32x4 d_pe = dma_desc(a.P + static_cast<int64_t>(e) * D * a.q, static_cast<int64_t>(D) * a.q * 2);
     u32x4 bw[kCt][2 * NFT];
-    auto load_bw = [&](int ct0) {
 #pragma unroll
-        for (int c = 0; c < kCt; ++c) {
-            const int n = 32 * (ct0 + 4 * c) + lrow;
+    for (int c = 0; c < kCt; ++c) {
+        const int n = 32 * (wave + 4 * c) + lrow;
 #pragma unroll
-            for (int ks = 0; ks < 2 * NFT; ++ks) {
-                // r is a multiple of 16: a k step is all US columns or all P_e columns
-                const int k = 16 * ks + 8 * lh;
-                const bool step_us = 16 * ks < r;
-                const uint32_t off = step_us ? static_cast<uint32_t>(n * r + k) * 2
-                                             : static_cast<uint32_t>(n * a.q + k - r) * 2;
-                bw[c][ks] = bload16(step_us ? r_us : r_pe,
-                                    ((ks < nks) & (n < D) & (k < rq)) ? off : kOob);
-            }
+        for (int ks = 0; ks < 2 * NFT; ++ks) {
+            const int k = 16 * ks + 8 * lh;
+            const bool step_us = 16 * ks < r;
+            const uint32_t off = step_us ? static_cast<uint32_t>(n * r + k) * 2
+                                         : static_cast<uint32_t>(n * a.q + k - r) * 2;
+            bw[c][ks] = bload16_asm(step_us ? d_us : d_pe, ((n < D) & (k < rq)) ? off : kOob, soff0);
         }
-    };
-    load_bw(wave);
+    }
 
-    // ---- sum the four waves' [t|u]^T partials: (w0 + w2) + (w1 + w3).  Areas
-    //      hold [token][feature] floats (pitch redp); lane (token 32b + lrow)
-    //      holds features 32f + 8g + 4 lh + [0, 4) of v-group g: 16-byte moves.
+    // ---- sum the four waves' [t|u]^T partials, in two rounds of feature
+    //      tiles ([0, kRa) and [kRa, NFT)).  Each wave stores its partial
+    //      tiles as [token][feature] floats (16-byte moves; pitch 32 n + 4
+    //      floats puts 16 tokens' moves in 16 different bank groups), then
+    //      sums 16 tokens of all four as (w0 + w2) + (w1 + w3) (fixed order,
+    //      deterministic), gates the u features, rounds to bf16 and writes
+    //      the token's row of tul.
+    constexpr int kRa = (NFT + 1) / 2;
     lds_barrier();                                     // x and the rings no longer read
-    float* area0 = reinterpret_cast<float*>(smem + a.epi_off);
-    float* area1 = area0 + kFRows * a.redp;
-    auto put = [&](float* area) {
+    float* areas = reinterpret_cast<float*>(smem + a.epi_off);
+    bf16_bits* tul = reinterpret_cast<bf16_bits*>(smem + a.tu_off);
+    auto round = [&](auto f0_tag, auto nt_tag) {
+        constexpr int f0 = decltype(f0_tag)::value, nt = decltype(nt_tag)::value;
+        constexpr int rp = 32 * nt + 4;
+        float* mine = areas + wave * (kFRows * rp);
 #pragma unroll
-        for (int f = 0; f < NFT; ++f)
+        for (int f = f0; f < f0 + nt; ++f)
 #pragma unroll
             for (int b = 0; b < 2; ++b)
 #pragma unroll
@@ -687,68 +688,45 @@ void k_fused_top1(FusedArgs a) {
                     float4 v;
                     v.x = tu[f][b][4 * g]; v.y = tu[f][b][4 * g + 1];
                     v.z = tu[f][b][4 * g + 2]; v.w = tu[f][b][4 * g + 3];
-                    *reinterpret_cast<float4*>(area + (32 * b + lrow) * a.redp + 32 * f + 8 * g + 4 * lh) = v;
+                    *reinterpret_cast<float4*>(mine + (32 * b + lrow) * rp + 32 * (f - f0) + 8 * g + 4 * lh) = v;
                 }
-    };
-    // one feature tile at a time (its 8 reads issued together): bounded registers
-    auto add = [&](const float* area) {
+        lds_barrier();
+        // lane: token 16 wave + (lane & 15), 4-feature chunks (lane >> 4) + 4 i
+        const int t = 16 * wave + (lane & 15);
+        const float gt = s_gate[t];
 #pragma unroll
-        for (int f = 0; f < NFT; ++f) {
-            float4 o[2][4];
+        for (int i = 0; i < 2 * nt; ++i) {
+            const int c4 = (lane >> 4) + 4 * i;
+            float4 o[4];
 #pragma unroll
-            for (int b = 0; b < 2; ++b)
-#pragma unroll
-                for (int g = 0; g < 4; ++g)
-                    o[b][g] = *reinterpret_cast<const float4*>(
-                        area + (32 * b + lrow) * a.redp + 32 * f + 8 * g + 4 * lh);
-#pragma unroll
-            for (int b = 0; b < 2; ++b)
-#pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    tu[f][b][4 * g] += o[b][g].x;
-                    tu[f][b][4 * g + 1] += o[b][g].y;
-                    tu[f][b][4 * g + 2] += o[b][g].z;
-                    tu[f][b][4 * g + 3] += o[b][g].w;
-                }
+            for (int w = 0; w < 4; ++w)
+                o[w] = *reinterpret_cast<const float4*>(areas + w * (kFRows * rp) + t * rp + 4 * c4);
+            const int feat = 32 * f0 + 4 * c4;
+            const float sc = feat < r ? 1.0f : gt;
+            uint2 wv;
+            wv.x = pack_bf16x2(((o[0].x + o[2].x) + (o[1].x + o[3].x)) * sc,
+                               ((o[0].y + o[2].y) + (o[1].y + o[3].y)) * sc);
+            wv.y = pack_bf16x2(((o[0].z + o[2].z) + (o[1].z + o[3].z)) * sc,
+                               ((o[0].w + o[2].w) + (o[1].w + o[3].w)) * sc);
+            *reinterpret_cast<uint2*>(tul + t * a.tuch * 8 + feat) = wv;
         }
+        lds_barrier();
     };
-    if (wave >= 2) put(wave == 2 ? area0 : area1);
-    lds_barrier();
-    if (wave < 2) add(wave == 0 ? area0 : area1);
-    lds_barrier();
-    if (wave == 1) put(area0);
-    lds_barrier();
-    bf16_bits* tul = reinterpret_cast<bf16_bits*>(smem + a.tu_off);
-    if (wave == 0) {
-        add(area0);
-        // gate the u features (r is a multiple of 32: whole tiles), round to
-        // bf16, tul[token][feature]
-#pragma unroll
-        for (int b = 0; b < 2; ++b) {
-            const float gt = s_gate[32 * b + lrow];
-#pragma unroll
-            for (int f = 0; f < NFT; ++f) {
-                const float sc = 32 * f < r ? 1.0f : gt;
-#pragma unroll
-                for (int g = 0; g < 4; ++g) {
-                    uint2 w;
-                    w.x = pack_bf16x2(tu[f][b][4 * g] * sc, tu[f][b][4 * g + 1] * sc);
-                    w.y = pack_bf16x2(tu[f][b][4 * g + 2] * sc, tu[f][b][4 * g + 3] * sc);
-                    *reinterpret_cast<uint2*>(tul + (32 * b + lrow) * a.tuch * 8 + 32 * f + 8 * g +
-                                              4 * lh) = w;
-                }
-            }
-        }
-    }
-    lds_barrier();
+    round(std::integral_constant<int, 0>{}, std::integral_constant<int, kRa>{});
+    if constexpr (NFT > kRa)
+        round(std::integral_constant<int, kRa>{}, std::integral_constant<int, NFT - kRa>{});
 
-    // ---- y = [t|u] [US | P_e]^T + b2 into LDS rows (the sums' area, free
-    //      now), kCt column tiles of 32 per pass with every operand load
-    //      issued before any store
+    // ---- y = [t|u] [US | P_e]^T + b2 into LDS rows (over the sums' area,
+    //      free now): y^T[n][token] = [US|P_e][n][k] [t|u]^T[k][token]; the
+    //      lane holds, for token 32 b + lrow, columns 32 ct + 8 g + 4 lh + [0, 4)
+    //      of v-group g.  Features past r + q are zeros on both sides.
+    vm_wait<0>();
+#pragma unroll
+    for (int c = 0; c < kCt; ++c)
+#pragma unroll
+        for (int ks = 0; ks < 2 * NFT; ++ks) reg_ready(bw[c][ks]);
     bf16_bits* yl = reinterpret_cast<bf16_bits*>(smem + a.epi_off);
-    const int nct = (D + 31) / 32;
-    for (int ct0 = wave; ct0 < nct; ct0 += 4 * kCt) {
-        if (ct0 != wave) load_bw(ct0);               // the first pass was prefetched
+    {
         f32x16 ay[kCt][2];
 #pragma unroll
         for (int c = 0; c < kCt; ++c)
@@ -756,23 +734,19 @@ void k_fused_top1(FusedArgs a) {
             for (int b = 0; b < 2; ++b)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) ay[c][b][v] = 0.0f;
-        // y^T[n][token] = [US|P_e][n][k] [t|u]^T[k][token]: the lane holds, for
-        // token 32 b + lrow, features 32 ct + 8 g + 4 lh + [0, 4) of v-group g
 #pragma unroll
         for (int ks = 0; ks < 2 * NFT; ++ks) {
-            if (ks < nks) {
 #pragma unroll
-                for (int b = 0; b < 2; ++b) {
-                    const u32x4 tv = *reinterpret_cast<const u32x4*>(
-                        tul + ((32 * b + lrow) * a.tuch + 2 * ks + lh) * 8);
+            for (int b = 0; b < 2; ++b) {
+                const u32x4 tv = *reinterpret_cast<const u32x4*>(
+                    tul + ((32 * b + lrow) * a.tuch + 2 * ks + lh) * 8);
 #pragma unroll
-                    for (int c = 0; c < kCt; ++c) ay[c][b] = mfma(bw[c][ks], tv, ay[c][b]);
-                }
+                for (int c = 0; c < kCt; ++c) ay[c][b] = mfma(bw[c][ks], tv, ay[c][b]);
             }
         }
 #pragma unroll
         for (int c = 0; c < kCt; ++c) {
-            const int ct = ct0 + 4 * c;
+            const int ct = wave + 4 * c;
 #pragma unroll
             for (int g = 0; g < 4; ++g) {
                 const int n0 = 32 * ct + 8 * g + 4 * lh;
@@ -837,11 +811,11 @@ constexpr size_t kLdsBytes = 160 * 1024;   // gfx950 LDS per workgroup
 constexpr size_t kStaticLds = 1024;        // s_tok, s_gate (aligned)
 
 // LDS plan: [b1 | b2 | x rows | 4 W1 rings] while the hidden loop runs, then
-// [b1 | b2 | two fp32 [t|u] partial-sum areas, later the bf16 y rows | bf16
-// [t|u] rows] (aliasing x and the rings).
+// [b1 | b2 | the four waves' fp32 [t|u] partial sums of one reduction round,
+// later the bf16 y rows | bf16 [t|u] rows] (aliasing x and the rings).
 struct FusedLds {
     size_t b1, b2, x, ring, areas, yrows, epi_off, tu_off, total;
-    int xch, redp, tuch, yp;
+    int xch, tuch, yp;
 };
 FusedLds fused_lds(int D, int H, int r, int q) {
     FusedLds L{};
@@ -849,9 +823,6 @@ FusedLds fused_lds(int D, int H, int r, int q) {
     const int hpad = (H + 4 * kFHid - 1) / (4 * kFHid) * (4 * kFHid);
     const int nft = (r + q + 31) / 32;
     L.xch = odd_at_least(8 * kgroups);
-    // a token's 32 NFT sums, padded so that 16 tokens' 16-byte moves hit 16
-    // different bank groups (pitch = 9 groups mod 16)
-    L.redp = 32 * nft + 4;
     L.tuch = odd_at_least(4 * nft);
     L.yp = D + 8;
     L.b1 = static_cast<size_t>(hpad) * 4;                    // a multiple of 1 KB
@@ -859,7 +830,9 @@ FusedLds fused_lds(int D, int H, int r, int q) {
     // the x copy issues whole 64-lane rounds of slots: round its region up
     L.x = ((static_cast<size_t>(kFRows) * L.xch + 63) / 64) * 64 * 16;
     L.ring = static_cast<size_t>(4) * kNS * kStageBytes;
-    L.areas = static_cast<size_t>(2) * kFRows * L.redp * 4;
+    // the four waves' partial sums of the larger reduction round
+    // ((nft + 1) / 2 feature tiles, pitch 32 n + 4 floats per token)
+    L.areas = static_cast<size_t>(4) * kFRows * (32 * ((nft + 1) / 2) + 4) * 4;
     L.yrows = static_cast<size_t>(kFRows) * L.yp * 2;
     L.epi_off = L.b1 + L.b2;                                 // past b2, which phase C reads
     L.tu_off = L.epi_off + ((L.areas > L.yrows ? L.areas : L.yrows) + 15) / 16 * 16;
@@ -875,6 +848,7 @@ bool fused_top1_supported(int D, int H, int r, int q) {
     if (!(D >= 8 && D <= kFusedMaxD && H >= 8 && H <= kFusedMaxH && r % 32 == 0 && r + q > 0 &&
           r + q <= kFusedMaxRQ))
         return false;
+    if (D > 128 * kCt) return false;               // one pass of y column tiles
     return fused_lds(D, H, r, q).total <= kLdsBytes - kStaticLds;
 }
 
@@ -916,7 +890,6 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
     const int nft = (r + q + 31) / 32;
     const FusedLds L = fused_lds(D, H, r, q);
     a.xch = L.xch;
-    a.redp = L.redp;
     a.tuch = L.tuch;
     a.yp = L.yp;
     a.b2_off = static_cast<int>(L.b1);
