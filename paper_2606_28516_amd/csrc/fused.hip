@@ -228,6 +228,19 @@ __device__ __forceinline__ void lds_barrier() {
     __builtin_amdgcn_s_barrier();
 }
 
+// Inclusive prefix sum over the 64 lanes of a wave by DPP: shifts by 1, 2, 4
+// and 8 lanes within rows of 16 (lanes without a source add 0), then lane 15
+// of each row into the next row and lane 31 into rows 2 and 3.
+__device__ __forceinline__ int wave_incl_scan(int v) {
+    v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);   // row_shr:1
+    v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);   // row_shr:2
+    v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);   // row_shr:4
+    v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);   // row_shr:8
+    v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);   // row_bcast:15
+    v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);   // row_bcast:31
+    return v;
+}
+
 // NFT = 32-row tiles of [t|u] features (r + q <= 32 NFT).  KG > 0 fixes the
 // number of 64-wide input groups at compile time (straight-line phase 1).
 template <int NFT, int KG>
@@ -244,8 +257,59 @@ void k_fused_top1(FusedArgs a) {
     // ---- tile -> (expert e, rows [m_lo, m_hi)), XCD-major order
     const int tile = (blockIdx.x % kFXcds) * a.per_xcd + blockIdx.x / kFXcds;
     if (tile >= a.tiles_bound) return;
+    const int D = a.D, H = a.H, r = a.r, rq = a.r + a.q;
+
+    float* s_b1 = reinterpret_cast<float*>(smem);
+    const float* s_b2 = reinterpret_cast<const float*>(smem + a.b2_off);
+    const unsigned char* xs = smem + a.x_off;
+    unsigned char* ringp = smem + a.ring_off + wave * (kNS * kStageBytes);
+    const uint32_t ring = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_word*)ringp));
+    const int kgroups = KG > 0 ? KG : a.kgroups;
+    const int n_iter = wave * kFHid < H ? (H - wave * kFHid + 4 * kFHid - 1) / (4 * kFHid) : 0;
+    const i32x4 d_w1 = dma_desc(a.W1, static_cast<int64_t>(H) * D * 2);
+
+    // DMA of W1 ring stage n = slice it, input group g into slot n % kNS: ring
+    // row 32q + s holds W1 row hb + hid_of_slot(q, s), and its 16-byte chunk c
+    // (inputs 64g + 8c .. + 8) sits at slot c ^ swz(row).
+    auto dma_stage = [&](int n) {
+        const int it = n / kgroups, g = n - it * kgroups;
+        const int hb = (it * 4 + wave) * kFHid;
+        const uint32_t m0 = ring + static_cast<uint32_t>(n % kNS) * kStageBytes;
+        uint32_t off[8];
+#pragma unroll
+        for (int ins = 0; ins < 8; ++ins) {
+            const int row = 8 * ins + (lane >> 3);
+            const int c = (lane & 7) ^ swz(row);
+            const int hid = hb + hid_of_slot(row >> 5, row & 31);
+            const int k = 64 * g + 8 * c;
+            off[ins] = ((hid < H) & (k < D)) ? static_cast<uint32_t>(hid * D + k) * 2u : kOob;
+        }
+        // the slot's previous stage must have been read by this wave
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+        dma_stage8(d_w1, __builtin_amdgcn_readfirstlane(m0), off);
+    };
+
+    // ---- b1, b2 and the first two W1 stages -> LDS by DMA, issued before the
+    //      tile's tokens are known (they do not depend on them); early exits
+    //      below wait for them first
+    {
+        const uint32_t lb = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_word*)smem));
+        const i32x4 d_b1 = dma_desc(a.b1, a.b1 != nullptr ? static_cast<int64_t>(H) * 4 : 0);
+        const i32x4 d_b2 = dma_desc(a.b2, a.b2 != nullptr ? static_cast<int64_t>(D) * 4 : 0);
+        for (int base = wave * 64; base < a.hpad / 4; base += 256)    // zeros past H
+            dma16_buf(d_b1, static_cast<uint32_t>(base + lane) * 16u,
+                      __builtin_amdgcn_readfirstlane(lb + base * 16));
+        for (int base = wave * 64; base < a.b2_chunks; base += 256)   // zeros past D
+            dma16_buf(d_b2, static_cast<uint32_t>(base + lane) * 16u,
+                      __builtin_amdgcn_readfirstlane(lb + a.b2_off + base * 16));
+    }
+    if (n_iter > 0) {
+        dma_stage(0);
+        dma_stage(1);
+    }
+
     const bool own_dispatch = a.tile_counts != nullptr;
-    __shared__ int s_off[65];                   // expert offsets (own dispatch)
+    __shared__ int s_off[64];                   // expert totals (own dispatch)
     __shared__ int s_nlist;
     if (own_dispatch) {
         // Expert totals from the router's histogram (staged in the x region,
@@ -254,7 +318,7 @@ void k_fused_top1(FusedArgs a) {
         int* s_h = reinterpret_cast<int*>(smem + a.x_off);
         const int nhE = a.nh * a.E;
         for (int i = tid; i < nhE; i += 256) s_h[i] = a.tile_counts[i];
-        if (tid <= a.E) s_off[tid] = 0;
+        if (tid < a.E) s_off[tid] = 0;
         if (tid == 0) s_nlist = 0;
         __syncthreads();
         const int G = 256 / a.E;
@@ -262,16 +326,35 @@ void k_fused_top1(FusedArgs a) {
             const int ee = tid % a.E;
             int c = 0;
             for (int b = tid / a.E; b < a.nh; b += G) c += s_h[b * a.E + ee];
-            atomicAdd(&s_off[ee + 1], c);
+            atomicAdd(&s_off[ee], c);
         }
-        __syncthreads();
-        if (tid == 0)
-            for (int ee = 0; ee < a.E; ++ee) s_off[ee + 1] += s_off[ee];
         __syncthreads();
     }
     int e = -1;
     int64_t m_lo = 0, m_hi = 0;
-    {
+    int e_lo = 0;                               // first row of expert e
+    if (own_dispatch) {
+        // every wave alike: lane s < E holds expert s's total; prefix sums
+        // over the lanes give its rows and its tiles, and the first lane
+        // whose tiles end past this tile is the expert
+        const int M = static_cast<int>(a.T);
+        int tot = lane < a.E ? s_off[lane] : 0;
+        tot = tot < 0 ? 0 : (tot > M ? M : tot);
+        int hi = wave_incl_scan(tot);
+        hi = hi > M ? M : hi;
+        const int lo = (hi - tot) > M ? M : (hi - tot);
+        const int nt = (hi - lo + kFRows - 1) / kFRows;
+        const int tend = wave_incl_scan(nt);
+        const uint64_t hit = __ballot(lane < a.E && tile < tend);
+        if (hit != 0) {
+            e = __builtin_ctzll(hit);
+            e_lo = __builtin_amdgcn_readlane(lo, e);
+            const int e_hi = __builtin_amdgcn_readlane(hi, e);
+            const int t0 = __builtin_amdgcn_readlane(tend - nt, e);
+            m_lo = e_lo + static_cast<int64_t>(tile - t0) * kFRows;
+            m_hi = m_lo + kFRows < e_hi ? m_lo + kFRows : e_hi;
+        }
+    } else {
         const int64_t M = a.T;
         int64_t before = 0;
         for (int s = 0; s < a.E; ++s) {
@@ -279,8 +362,8 @@ void k_fused_top1(FusedArgs a) {
             // workgroup outside the buffers
             // read as uniform values (the same for every lane), so that e
             // and the expert's buffer descriptors below live in scalar registers
-            int64_t lo = __builtin_amdgcn_readfirstlane(own_dispatch ? s_off[s] : a.offsets[s]);
-            int64_t hi = __builtin_amdgcn_readfirstlane(own_dispatch ? s_off[s + 1] : a.offsets[s + 1]);
+            int64_t lo = __builtin_amdgcn_readfirstlane(a.offsets[s]);
+            int64_t hi = __builtin_amdgcn_readfirstlane(a.offsets[s + 1]);
             lo = lo < 0 ? 0 : (lo > M ? M : lo);
             hi = hi < lo ? lo : (hi > M ? M : hi);
             const int64_t nt = (hi - lo + kFRows - 1) / kFRows;
@@ -293,9 +376,11 @@ void k_fused_top1(FusedArgs a) {
             before += nt;
         }
     }
-    if (e < 0) return;                          // uniform over the workgroup
+    if (e < 0) {                                // uniform over the workgroup
+        vm_wait<0>();
+        return;
+    }
     const int rows = static_cast<int>(m_hi - m_lo);
-    const int D = a.D, H = a.H, r = a.r, rq = a.r + a.q;
 
     if (own_dispatch) {
         // The tokens of ranks [rlo, rhi) of expert e in the stable order (by
@@ -306,17 +391,12 @@ void k_fused_top1(FusedArgs a) {
         const int* s_h = reinterpret_cast<const int*>(smem + a.x_off);
         int2* s_list = reinterpret_cast<int2*>(smem + a.x_off) + (a.nh * a.E + 1) / 2;
         __shared__ int s_wsum[4];
-        const int rlo = static_cast<int>(m_lo) - s_off[e], rhi = static_cast<int>(m_hi) - s_off[e];
+        const int rlo = static_cast<int>(m_lo) - e_lo, rhi = static_cast<int>(m_hi) - e_lo;
         const int per = (a.nh + 255) / 256;
         const int b0 = tid * per, b1 = b0 + per < a.nh ? b0 + per : a.nh;
         int mine = 0;
         for (int b = b0; b < b1; ++b) mine += s_h[b * a.E + e];
-        int incl = mine;                        // inclusive scan over the block
-#pragma unroll
-        for (int o = 1; o < 64; o <<= 1) {
-            const int n = __shfl_up(incl, o);
-            if (lane >= o) incl += n;
-        }
+        const int incl = wave_incl_scan(mine);  // inclusive scan over the block
         if (lane == 63) s_wsum[wave] = incl;
         if (tid < kFRows) s_tok[tid] = -1;
         __syncthreads();
@@ -385,49 +465,6 @@ void k_fused_top1(FusedArgs a) {
     }
     __syncthreads();
 
-    float* s_b1 = reinterpret_cast<float*>(smem);
-    const float* s_b2 = reinterpret_cast<const float*>(smem + a.b2_off);
-    const unsigned char* xs = smem + a.x_off;
-    unsigned char* ringp = smem + a.ring_off + wave * (kNS * kStageBytes);
-    const uint32_t ring = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_word*)ringp));
-    const int kgroups = KG > 0 ? KG : a.kgroups;
-    const int n_iter = wave * kFHid < H ? (H - wave * kFHid + 4 * kFHid - 1) / (4 * kFHid) : 0;
-    const i32x4 d_w1 = dma_desc(a.W1, static_cast<int64_t>(H) * D * 2);
-
-    // DMA of W1 ring stage n = slice it, input group g into slot n % kNS: ring
-    // row 32q + s holds W1 row hb + hid_of_slot(q, s), and its 16-byte chunk c
-    // (inputs 64g + 8c .. + 8) sits at slot c ^ swz(row).
-    auto dma_stage = [&](int n) {
-        const int it = n / kgroups, g = n - it * kgroups;
-        const int hb = (it * 4 + wave) * kFHid;
-        const uint32_t m0 = ring + static_cast<uint32_t>(n % kNS) * kStageBytes;
-        uint32_t off[8];
-#pragma unroll
-        for (int ins = 0; ins < 8; ++ins) {
-            const int row = 8 * ins + (lane >> 3);
-            const int c = (lane & 7) ^ swz(row);
-            const int hid = hb + hid_of_slot(row >> 5, row & 31);
-            const int k = 64 * g + 8 * c;
-            off[ins] = ((hid < H) & (k < D)) ? static_cast<uint32_t>(hid * D + k) * 2u : kOob;
-        }
-        // the slot's previous stage must have been read by this wave
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-        dma_stage8(d_w1, __builtin_amdgcn_readfirstlane(m0), off);
-    };
-
-    // ---- prologue: b1, b2 and the gathered x rows -> LDS, the first two W1
-    //      stages; all by DMA, one wait
-    {
-        const uint32_t lb = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_word*)smem));
-        const i32x4 d_b1 = dma_desc(a.b1, a.b1 != nullptr ? static_cast<int64_t>(H) * 4 : 0);
-        const i32x4 d_b2 = dma_desc(a.b2, a.b2 != nullptr ? static_cast<int64_t>(D) * 4 : 0);
-        for (int base = wave * 64; base < a.hpad / 4; base += 256)    // zeros past H
-            dma16_buf(d_b1, static_cast<uint32_t>(base + lane) * 16u,
-                      __builtin_amdgcn_readfirstlane(lb + base * 16));
-        for (int base = wave * 64; base < a.b2_chunks; base += 256)   // zeros past D
-            dma16_buf(d_b2, static_cast<uint32_t>(base + lane) * 16u,
-                      __builtin_amdgcn_readfirstlane(lb + a.b2_off + base * 16));
-    }
     {
         const uint32_t xl = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_word*)xs));
         const int dch = D / 8;
@@ -443,13 +480,7 @@ void k_fused_top1(FusedArgs a) {
             lds_dma16(src, __builtin_amdgcn_readfirstlane(xl + base * 16));
         }
     }
-    if (n_iter > 0) {
-        dma_stage(0);
-        dma_stage(1);
-        vm_wait<16>();                                 // all but the two W1 stages
-    } else {
-        vm_wait<0>();
-    }
+    vm_wait<0>();                                      // b1, b2, x and the first stages
     lds_barrier();
 
     // [Vt;Q_e] are loaded by asm (d_*) when the step loop is unrolled (KG > 0),
