@@ -33,7 +33,10 @@ FUSED_LAYERS = [
     (300, 192, 136, 4, 0, 24),       # r = 0 (residual only), odd input-group count, idle waves
     (250, 96, 8, 3, 0, 8),           # H = 8: one partial slice in wave 0 only (r, q <= H)
     (411, 256, 512, 6, 128, 32),     # rq = 160, NFT = 5, D = 256 (runtime input-group count)
-    (129, 768, 3072, 4, 128, 32),    # widest D: x rows + b1 beyond 64 KB of LDS
+    (129, 384, 3072, 4, 128, 32),    # widest fused D, H = 3072: x rows + b1 beyond 64 KB of LDS
+    (129, 768, 3072, 4, 128, 32),    # D > 384: the GEMM chain takes the layer
+    (20000, 128, 256, 20, 64, 16),   # E > 16: 79 router tiles, the in-kernel scans cross rows and waves
+    (5000, 64, 128, 64, 32, 8),      # E = 64, the most experts: expert totals over a whole wave
 ]
 
 
@@ -98,6 +101,21 @@ def test_fused_stage_replaces_the_gemm_chain():
         ref = oracle.ffn_forward_layer(L)
         tie = assert_routing(g["idx"], ref["logits"], 1)
         assert frob_rel(g["y"][~tie], ref["y"][~tie]) <= BF16_FROB_REGRESS
+
+
+@pytest.mark.parametrize("T,D,H,E,r,q", [(20000, 128, 256, 20, 64, 16), (5000, 64, 128, 64, 32, 8),
+                                          (12608, 128, 256, 16, 64, 16)])
+def test_fused_kernel_dispatches_in_its_prologue(T, D, H, E, r, q):
+    # router histogram small enough for the kernel's own dispatch: no
+    # permute launch, and the fused kernel's result still matches the oracle
+    # (the E = 16 case has 197 router tiles of 64 tokens, the others 256)
+    L = _layer(T, D, H, E, r, q, seed=T + E)
+    launched = _stages_of(L)
+    assert launched.get("fused_top1") == 1 and "permute" not in launched, launched
+    g = gpu_ffn(L)
+    ref = oracle.ffn_forward_layer(L)
+    tie = assert_routing(g["idx"], ref["logits"], 1)
+    assert frob_rel(g["y"][~tie], ref["y"][~tie]) <= BF16_FROB_REGRESS
 
 
 @pytest.mark.parametrize("mode", ["one_expert", "empty_experts"])
