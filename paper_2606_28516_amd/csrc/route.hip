@@ -154,7 +154,7 @@ __device__ __forceinline__ uint64_t route_select(const double (&lg)[EP], int E, 
         const int best = pick<EP>(lg, E, mine, bv);
         mine |= 1ull << best;
         if (j == 0) top = bv;
-        den += exp_ool(bv - top);
+        if (kk > 1) den += exp_ool(bv - top);         // one expert: its gate is 1
         idx[t * k + j] = best;
     }
     if (kk == 1) {
@@ -219,7 +219,7 @@ void k_route(
     const __amdgpu_buffer_rsrc_t rx = raw_rsrc(x + tile0 * D, static_cast<int64_t>(rows) * D * esz);
     const __amdgpu_buffer_rsrc_t rw = raw_rsrc(Wg, static_cast<int64_t>(E) * D * esz);
     __shared__ double bgv[EP];                       // router bias, loaded up front (read
-    if (tid < EP)                                    // after the transposes' barriers)
+    if (tid < EP)                                    // after the barrier past the transposes)
         bgv[tid] = (bg != nullptr && tid < E) ? static_cast<double>(bg[tid]) : 0.0;
 
     if (w_lds > 0) {                               // router rows -> LDS (read after a barrier)
@@ -338,11 +338,19 @@ void k_route(
                 if (16 * g + 4 * grp + v < E) m = fmaxf(m, aab[g][b][v]);
             s_s[w][16 * b + col][4 * g + grp] = m;
         }
-        __syncthreads();
+        // s_l[w] and s_s[w] are this wave's own rows: a wave-level barrier
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 #pragma unroll
         for (int e = 0; e < 16; ++e) lg[16 * g + e] = s_l[w][tl][e];
-        __syncthreads();
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
+    // the bias (written by the first threads) and the router rows in LDS
+    // (every wave's copy has landed: its later loads have) are read below
+    __syncthreads();
     float smax = 0.0f;
 #pragma unroll
     for (int i = 0; i < 4 * EG; ++i) smax = fmaxf(smax, s_s[w][tl][i]);
