@@ -264,52 +264,54 @@ __global__ __launch_bounds__(256) void k_gemm(GemmDesc g, int mtiles, int ntiles
                     const int r = wn * WTN + j * 32 + lrow;
                     fb[j] = *reinterpret_cast<const uint4*>(sb + r * kStageBytes + ((c ^ swz(r)) << 4));
                 }
+                // B first: tile (i, j) accumulates C^T (see the epilogue)
 #pragma unroll
                 for (int i = 0; i < TM; ++i)
 #pragma unroll
-                    for (int j = 0; j < TN; ++j) Mfma<Tin>::step(fa[i], fb[j], acc[i][j]);
+                    for (int j = 0; j < TN; ++j) Mfma<Tin>::step(fb[j], fa[i], acc[i][j]);
             }
         }
     }
 
-    // ---- epilogue: D[v] of a 32x32 tile sits at row 8*(v/4) + 4*(lane/32) + v%4,
-    //      column lane%32.  Bias and row scales are fetched once, up front.
-    float bias_j[TN];
-#pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int n = n0 + wn * WTN + j * 32 + lrow;
-        bias_j[j] = (g.bias != nullptr && n < g.N) ? g.bias[n] : 0.0f;
-    }
-    float rs[TM][16];
-    int64_t crow[TM][16];
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int64_t m = m_lo + wm * WTM + i * 32 + 8 * (v >> 2) + 4 * lhalf + (v & 3);
-            const bool in = m < m_hi;
-            const int32_t sr = (g.row_scale != nullptr && in) ? g.scale_rows[m] : 0;
-            rs[i][v] = g.row_scale == nullptr || !in ? 1.0f : (sr >= 0 ? g.row_scale[sr] : 0.0f);
-            // a negative scatter index is a padding row: it is not stored
-            const int64_t cr = !in ? -1 : (g.c_rows != nullptr ? static_cast<int64_t>(g.c_rows[m]) : m);
-            crow[i][v] = cr < 0 ? -1 : (g.c_rows != nullptr ? cr / g.c_div : cr);
-        }
+    // ---- epilogue.  The MFMAs took B as the first operand, so tile (i, j)
+    //      holds C^T: lane l owns row m = .. + i*32 + l%32, and its value v is
+    //      column n = .. + j*32 + 8*(v/4) + 4*(l/32) + v%4 -- four consecutive
+    //      columns per v-group, written as one 8-byte (bf16) or 16-byte
+    //      (float32) store at a row address formed once per tile row.  N is
+    //      a multiple of 4 (the shape checks), so a group is all in or all out.
 #pragma unroll
     for (int i = 0; i < TM; ++i) {
+        const int64_t m = m_lo + wm * WTM + i * 32 + lrow;
+        if (m >= m_hi) continue;
+        const int32_t sr = g.row_scale != nullptr ? g.scale_rows[m] : 0;
+        const float rs = g.row_scale == nullptr ? 1.0f : (sr >= 0 ? g.row_scale[sr] : 0.0f);
+        // a negative scatter index is a padding row: it is not stored
+        const int64_t cr = g.c_rows != nullptr ? static_cast<int64_t>(g.c_rows[m]) : m;
+        if (cr < 0) continue;
+        const int64_t cm = g.c_rows != nullptr ? cr / g.c_div : cr;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int64_t cm = crow[i][v];
-            if (cm < 0) continue;
+        for (int j = 0; j < TN; ++j) {
 #pragma unroll
-            for (int j = 0; j < TN; ++j) {
-                const int n = n0 + wn * WTN + j * 32 + lrow;
+            for (int q4 = 0; q4 < 4; ++q4) {
+                const int n = n0 + wn * WTN + j * 32 + 8 * q4 + 4 * lhalf;
                 if (n >= g.N) continue;
-                float val = acc[i][j][v] * (n >= g.scale_col0 ? rs[i][v] : 1.0f) + bias_j[j];
-                if (g.gelu) val = gelu_erf(val);
-                if (g.c_f32)
-                    static_cast<float*>(g.C)[cm * g.ldc + n] = val;
-                else
-                    static_cast<Tin*>(g.C)[cm * g.ldc + n] = Elem<Tin>::from_f32(val);
+                float bb[4] = {0.0f, 0.0f, 0.0f, 0.0f};   // the bias is only 4-byte aligned
+                if (g.bias != nullptr) {
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) bb[t] = g.bias[n + t];
+                }
+                float val[4];
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    val[t] = acc[i][j][4 * q4 + t] * (n + t >= g.scale_col0 ? rs : 1.0f) + bb[t];
+                    if (g.gelu) val[t] = gelu_erf(val[t]);
+                }
+                if (g.c_f32) {
+                    *reinterpret_cast<float4*>(static_cast<float*>(g.C) + cm * g.ldc + n) =
+                        make_float4(val[0], val[1], val[2], val[3]);
+                } else {
+                    Elem<Tin>::store4(static_cast<Tin*>(g.C) + cm * g.ldc + n, val);
+                }
             }
         }
     }

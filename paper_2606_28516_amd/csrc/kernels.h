@@ -52,18 +52,38 @@ __device__ __forceinline__ bf16_bits f32_to_bf16(float f) {
     return static_cast<bf16_bits>(u >> 16);
 }
 
+// Two floats -> two bf16 by the hardware conversion (round to nearest even),
+// packed in 32 bits, first value in the low half.
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack2_bf16(float a, float b) {
+    const f32x2_t v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
+}
+
 template <typename T> struct Elem;
 template <> struct Elem<float> {
     static constexpr int per16 = 4;                 // elements per 16-byte piece
     __device__ static float load(const float* p, int64_t i) { return p[i]; }
     __device__ static float to_f32(float v) { return v; }
     __device__ static float from_f32(float v) { return v; }
+    // four consecutive elements (16-byte aligned)
+    __device__ static void store4(float* p, const float (&v)[4]) {
+        *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+    }
 };
 template <> struct Elem<bf16_bits> {
     static constexpr int per16 = 8;
     __device__ static float load(const bf16_bits* p, int64_t i) { return bf16_to_f32(p[i]); }
     __device__ static float to_f32(bf16_bits v) { return bf16_to_f32(v); }
     __device__ static bf16_bits from_f32(float v) { return f32_to_bf16(v); }
+    // four consecutive elements (8-byte aligned)
+    __device__ static void store4(bf16_bits* p, const float (&v)[4]) {
+        uint2 w;
+        w.x = pack2_bf16(v[0], v[1]);
+        w.y = pack2_bf16(v[2], v[3]);
+        *reinterpret_cast<uint2*>(p) = w;
+    }
 };
 
 // Exact-erf GELU, v Phi(v) = 0.5 v (1 + erf(v / sqrt 2)), in float32.
