@@ -24,6 +24,8 @@ Prints one JSON line.  Besides the contract fields it carries
                top-2, 1568 and 12608 tokens;
   routers      the same layer with the linear, MLP and adaptive routers
                (clearmoe_ffn_forward_ex);
+  deit_base    the DeiT-Base-shaped top-2 layer (50432 tokens, D = 768) through
+               the GEMM chain, with each product's rate against the bf16 peak;
   ffn_stack    the FFN part of a 12-block DeiT-Small forward with 6 CLEAR-MoE
                layers (class tokens on the dense path) against 12 dense ones.
 """
@@ -41,6 +43,9 @@ HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 PROFILE_DIR = os.path.join(ROOT, "profiles")
 TIME_EVERY = 8
+# stages whose kernels are matrix products (the router's flops are not its bound)
+MFMA_STAGES = ("fc1_gelu", "basis_t", "basis_h", "res_u", "res_h", "tu_grouped", "y_grouped",
+               "dense_fc2", "fused_top1")
 
 
 def parse():
@@ -284,6 +289,7 @@ def main():
         out["imbalance"] = bench_imbalance(cm, synth, torch, np, stream, max(20, args.steps // 5))
         out["routers"] = bench_routers(cm, synth, torch, np, stream, L, max(20, args.steps // 5))
         out["ffn_stack"] = bench_stack(cm, synth, torch, np, stream, L, max(20, args.steps // 10))
+        out["deit_base"] = bench_layer(cm, synth, torch, np, stream, "C3", 20)
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(L, cfg, args.cpu_seconds)
@@ -467,6 +473,54 @@ def bench_routers(cm, synth, torch, np, stream, L, steps):
                                  "route_us": r_ms / r_n * 1e3, "share_top2": two}
         del ws, y, idx
     return out
+
+
+def bench_layer(cm, synth, torch, np, stream, workload, steps):
+    """One layer of another configuration: step time from an untimed pass,
+    then every stage timed in a second pass; MFMA rate of each product."""
+    cfg = synth.CONFIGS[workload]
+    L = synth.make_layer(cfg)
+    d = {n: cm.from_stored(L[n]) for n in ("x", "W1", "b1", "US", "Vt", "b2", "P", "Q", "Wg", "bg")}
+    shape = cm.make_shape(cfg.T, cfg.D, cfg.E, cfg.k, cm.F32 if cfg.dtype == "f32" else cm.BF16,
+                          H=cfg.H, r=cfg.r, q=cfg.q)
+    ws = cm.alloc_workspace(shape)
+    y = torch.empty_like(d["x"])
+
+    def step():
+        cm.ffn_forward(d["x"], d["W1"], d["b1"], d["US"], d["Vt"], d["b2"], d["P"], d["Q"],
+                       d["Wg"], d["bg"], cfg.k, ws=ws, out=y)
+
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    names = cm.stage_names()
+    cm.timing_start(names, steps * len(names))
+    for _ in range(steps):
+        step()
+    per = cm.timing_stop()
+    b = 4 if cfg.dtype == "f32" else 2
+    peak = MFMA_PEAK_TFLOPS[cfg.dtype]
+    stages = {}
+    for s_, (t_ms, n) in sorted(per.items(), key=lambda kv: -kv[1][0]):
+        us = t_ms / n * 1e3
+        flops = stage_work(s_, cfg, b)[0] if s_ in MFMA_STAGES else 0
+        e = {"us": us}
+        if flops:
+            e["tflops"] = flops / (us * 1e-6) / 1e12
+            e["mfma_frac"] = e["tflops"] / peak
+        stages[s_] = e
+    del ws, y, d
+    return {"workload": f"{cfg.name} (T={cfg.T} D={cfg.D} H={cfg.H} E={cfg.E} k={cfg.k} "
+                        f"r={cfg.r} q={cfg.q} {cfg.dtype})",
+            "ms": ms, "tokens_per_s": cfg.T / (ms * 1e-3),
+            "layer_tflops": layer_flops(cfg) / (ms * 1e-3) / 1e12, "stages": stages, "steps": steps}
 
 
 def bench_stack(cm, synth, torch, np, stream, L, steps):
