@@ -243,7 +243,7 @@ int clearmoe_dense_ffn_forward(const clearmoe_shape* shape, const void* x, const
  * (hipExtLaunchKernel) that the dispatch itself stamps at the kernel's start
  * and end, so the elapsed time is the kernel's own and no marker packet joins
  * the stream.  A timed dispatch still costs the step a few microseconds
- * (about 5 us measured on MI355X at 12608 x 384 tokens), so a benchmark times
+ * (about 5 us measured on MI355X at 12608 tokens of width 384), so a benchmark times
  * a sample of the launches.  Off by default: then the entry points behave
  * exactly as documented. */
 enum {
