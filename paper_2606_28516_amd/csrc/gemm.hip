@@ -6,7 +6,7 @@
 // contiguous expert sub-batch, here with no host round trip for the sizes).
 //
 // Mapping
-//   * 256 threads = 4 waves in a WM x WN grid; a wave owns a (BM/WM) x (BN/WN)
+//   * 4 or 8 waves in a WM x WN grid; a wave owns a (BM/WM) x (BN/WN)
 //     block of 32x32 MFMA tiles with float32 accumulators;
 //   * bf16: v_mfma_f32_32x32x16_bf16, a lane feeds 8 consecutive k of one row
 //     (A) / one column (B); f32: v_mfma_f32_32x32x2f32, a lane holds 4
@@ -83,15 +83,16 @@ template <> struct Mfma<float> {
 };
 
 template <typename Tin, int BM, int BN, int WM, int WN, int NS>
-__global__ __launch_bounds__(256) void k_gemm(GemmDesc g, int mtiles, int ntiles, int per_xcd) {
-    static_assert(WM * WN == 4, "4 waves");
+__global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, int ntiles, int per_xcd) {
+    constexpr int NW = WM * WN;                     // waves: 4 (one per SIMD) or 8 (two)
+    static_assert(NW == 4 || NW == 8, "4 or 8 waves");
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 32, TN = WTN / 32;
     static_assert(TM >= 1 && TN >= 1, "wave tile at least 32x32");
-    static_assert(BM % 32 == 0 && BN % 32 == 0, "8-row load groups per wave");
+    static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "8-row load groups per wave");
     constexpr int PER16 = Elem<Tin>::per16;
     constexpr int BK = kStageBytes / static_cast<int>(sizeof(Tin));
-    constexpr int AL = BM / 32, BL = BN / 32;       // load instructions per wave per stage
+    constexpr int AL = BM / (8 * NW), BL = BN / (8 * NW);   // load instructions per wave per stage
     constexpr int LPS = AL + BL;
     static_assert(LPS * (NS - 1) < 64, "vmcnt range");
     constexpr int STAGE_A = BM * kStageBytes, STAGE_B = BN * kStageBytes;
@@ -326,17 +327,23 @@ static hipError_t gemm_cfg(const GemmDesc& g, hipStream_t st) {
     if (tiles == 0) return hipSuccess;
     const int64_t per_xcd = (tiles + kXcds - 1) / kXcds;
     const int64_t grid = per_xcd * kXcds;
-    launch_kernel(k_gemm<Tin, BM, BN, WM, WN, NS>, dim3(static_cast<unsigned>(grid)), 256, 0, st,
+    launch_kernel(k_gemm<Tin, BM, BN, WM, WN, NS>, dim3(static_cast<unsigned>(grid)), 64 * WM * WN, 0, st,
         g, static_cast<int>(mt), static_cast<int>(nt), static_cast<int>(per_xcd));
     return hipGetLastError();
 }
 
 // Tile choice by shape (measured on MI355X at the layer's sizes): with few
 // 128x128 tiles the GEMM is latency bound, so 64-row tiles (more workgroups
-// per CU) win; long-K skinny products want 64x64 with four stages in flight.
+// per CU) win; long-K skinny products want 64x64 with four stages in flight;
+// large products (a thousand 256x256 tiles or more, e.g. fc1 of a 50432-token
+// DeiT-Base layer) take 256x256 tiles over 8 waves, two per SIMD (half the
+// operand bytes per flop of 128x128, and one wave's waits overlap the other's
+// MFMAs).
 template <typename Tin>
 static hipError_t gemm_dt(const GemmDesc& g, hipStream_t st) {
     const int64_t mt128 = (g.M + 127) / 128;
+    if (g.N >= 1024 && ((g.M + 255) / 256) * ((g.N + 255) / 256) >= 1024)
+        return gemm_cfg<Tin, 256, 256, 4, 2, 2>(g, st);
     if (g.N <= 32) return gemm_cfg<Tin, 128, 32, 4, 1, 3>(g, st);
     if (g.N <= 64) return gemm_cfg<Tin, 128, 64, 4, 1, 3>(g, st);
     if (g.N <= 128 && g.K >= 1024) return gemm_cfg<Tin, 64, 64, 2, 2, 4>(g, st);

@@ -300,3 +300,31 @@ def test_dense_comparator(name):
         assert max_rel(got, ref["y"]) <= F32_MAXREL
     else:
         assert frob_rel(got, ref["y"]) <= BF16_FROB_REGRESS
+
+
+@pytest.mark.parametrize("dt", ["bf16", "f32"])
+def test_large_fc1_tiles_with_ragged_edges(dt):
+    """fc1 of this layer (M = T = 52517, N = H = 1032, K = D = 72) has
+    206 x 5 = 1030 tiles of 256 x 256, which selects the product's 8-wave
+    large-tile configuration; the last row tile holds 37 rows, the last
+    column tile 8 columns, and K ends inside its second 128-byte stage.
+    Top-2, so the layer runs the GEMM chain.  Routing on every token, values
+    on a sample of rows."""
+    cfg = synth.LayerConfig("bigtile", T=52517, D=72, H=1032, E=4, k=2, r=32, q=8, dtype=dt,
+                            seed=11, residual="random", n_cal=2000)
+    L = synth.make_layer(cfg)
+    rng = np.random.default_rng(12)
+    L["b1"] = (0.1 * rng.standard_normal(cfg.H)).astype(np.float32)
+    g = gpu_ffn(L)
+    _, _, lg = oracle.route(L["x"], L["Wg"], L["bg"], cfg.k)
+    tie = assert_routing(g["idx"], lg, cfg.k)
+    rows = _sample_rows(cfg.T, 512, 13)
+    rows = np.unique(np.concatenate([rows, np.arange(cfg.T - 40, cfg.T)]))   # the last row tile
+    rows = rows[~tie[rows]]
+    ref = oracle.ffn_forward_layer(L, rows=rows)
+    if dt == "f32":
+        e = max_rel(g["y"][rows], ref["y"])
+        assert e <= F32_MAXREL, e
+    else:
+        e = frob_rel(g["y"][rows], ref["y"])
+        assert e <= BF16_FROB_REGRESS, e
