@@ -147,6 +147,20 @@ __device__ __forceinline__ uint64_t route_select(const double (&lg)[EP], int E, 
                                                  int32_t* __restrict__ idx,
                                                  float* __restrict__ gate) {
     const int kk = (adaptive && route_confidence<EP>(lg, E) >= tau) ? 1 : k;
+    if (kk == 2) {
+        // two experts: gates 1 / (1 + e1) and e1 / (1 + e1), e1 = exp(l1 - l0)
+        // (the general loop's arithmetic: exp(0) = 1 exactly), one exp
+        double v0, v1;
+        const int b0 = pick<EP>(lg, E, 0ull, v0);
+        const int b1 = pick<EP>(lg, E, 1ull << b0, v1);
+        const double e1 = exp_ool(v1 - v0);
+        const double den = 1.0 + e1;
+        idx[t * k] = b0;
+        idx[t * k + 1] = b1;
+        gate[t * k] = static_cast<float>(1.0 / den);
+        gate[t * k + 1] = static_cast<float>(e1 / den);   // kk == 2 only when k == 2
+        return (1ull << b0) | (1ull << b1);
+    }
     uint64_t mine = 0;
     double top = 0.0, den = 0.0;
     for (int j = 0; j < kk; ++j) {
