@@ -260,11 +260,12 @@ __global__ __launch_bounds__(kRouteTile) void k_permute(
         __syncthreads();
     }
     if (xperm != nullptr) {
-        // Row copy: 16-byte pieces, four per thread per round (all loads issued
-        // before the stores); the destination rows are written once and read
-        // later by another kernel, so the stores bypass the caches.
+        // Row copy: 16-byte pieces, eight per thread per round (all loads
+        // issued before the stores; measured against 4 and 16 at 2^20 tokens);
+        // the destination rows are written once and read later by another
+        // kernel, so the stores bypass the caches.
         constexpr int PER16 = Elem<Tin>::per16;
-        constexpr int U = 4;
+        constexpr int U = 8;
         const int ppr = D / PER16;                      // 16-byte pieces per row
         const int npairs = na * ppr;
         for (int base = 0; base < npairs; base += U * kRouteTile) {
