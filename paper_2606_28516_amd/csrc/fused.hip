@@ -880,6 +880,7 @@ bool fused_top1_supported(int D, int H, int r, int q) {
           r + q <= kFusedMaxRQ))
         return false;
     if (D > 128 * kCt) return false;               // one pass of y column tiles
+    if (fused_kgroups(D) != 6) return false;      // the instantiated input-group count
     return fused_lds(D, H, r, q).total <= kLdsBytes - kStaticLds;
 }
 
@@ -935,12 +936,13 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
     a.per_xcd = static_cast<int>((tiles + kFXcds - 1) / kFXcds);
     const int grid = a.per_xcd * kFXcds;
     switch (nft) {
-        case 1: return fused_cfg<1, 0>(a, lds, grid, st);
-        case 2: return fused_cfg<2, 0>(a, lds, grid, st);
-        case 3: return fused_cfg<3, 0>(a, lds, grid, st);
-        case 4: return fused_cfg<4, 0>(a, lds, grid, st);
-        default: return a.kgroups == 6 ? fused_cfg<5, 6>(a, lds, grid, st)
-                                       : fused_cfg<5, 0>(a, lds, grid, st);
+        // the supported shapes (D <= 384) have six input groups: the step loop
+        // is unrolled at compile time for every feature-tile count
+        case 1: return fused_cfg<1, 6>(a, lds, grid, st);
+        case 2: return fused_cfg<2, 6>(a, lds, grid, st);
+        case 3: return fused_cfg<3, 6>(a, lds, grid, st);
+        case 4: return fused_cfg<4, 6>(a, lds, grid, st);
+        default: return fused_cfg<5, 6>(a, lds, grid, st);
     }
 }
 

@@ -32,7 +32,7 @@ FUSED_LAYERS = [
     (517, 200, 200, 5, 96, 24),      # D, H off the 64 / 256 grids, NFT = 4
     (300, 192, 136, 4, 0, 24),       # r = 0 (residual only), odd input-group count, idle waves
     (250, 96, 8, 3, 0, 8),           # H = 8: one partial slice in wave 0 only (r, q <= H)
-    (411, 256, 512, 6, 128, 32),     # rq = 160, NFT = 5, D = 256 (runtime input-group count)
+    (411, 256, 512, 6, 128, 32),     # rq = 160, NFT = 5, D = 256 (two input groups of zeros)
     (129, 384, 3072, 4, 128, 32),    # widest fused D, H = 3072: x rows + b1 beyond 64 KB of LDS
     (129, 768, 3072, 4, 128, 32),    # D > 384: the GEMM chain takes the layer
     (20000, 128, 256, 20, 64, 16),   # E > 16: 79 router tiles, the in-kernel scans cross rows and waves
