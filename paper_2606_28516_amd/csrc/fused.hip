@@ -49,6 +49,7 @@ constexpr int kFXcds = 8;
 constexpr int kNS = 3;                  // W1 ring stages per wave
 constexpr int kStageBytes = 64 * 128;   // 64 W1 rows x 64 inputs (bf16)
 constexpr int kCt = 3;                  // y column tiles per wave (4 kCt tiles cover D)
+constexpr int kFGroups = 6;             // 64-wide input groups (D <= 384)
 
 __device__ __attribute__((aligned(16))) const uint32_t g_fused_zero[4] = {0u, 0u, 0u, 0u};
 
@@ -67,15 +68,6 @@ __device__ __forceinline__ void lds_dma16(const void* gptr, uint32_t lds_addr) {
 // zero, so tails and absent rows need no pointer selects and no branches.
 constexpr uint32_t kOob = 0x80000000u;          // an offset past every buffer here
 constexpr int kBufWord3 = 0x00020000;           // raw dword access (CDNA)
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buf(const void* p, int64_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), static_cast<short>(0),
-                                             static_cast<int>(bytes), kBufWord3);
-}
-__device__ __forceinline__ u32x4 bload16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
-    return __builtin_bit_cast(u32x4,
-                              __builtin_amdgcn_raw_buffer_load_b128(r, static_cast<int>(off), 0, 0));
-}
 
 // Two floats -> two bf16 (hardware round to nearest even), packed in 32 bits.
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
@@ -188,7 +180,6 @@ struct FusedArgs {
     int64_t T;
     int D, H, E, r, q;
     int xch;        // LDS pitch of an x row, 16-byte chunks (odd, >= 8 * kgroups)
-    int kgroups;    // ceil(D / 64) rounded up to even, at least 6
     int hpad;       // H rounded up to 4 waves x 64
     int tuch;       // LDS pitch of a bf16 [t|u] row, 16-byte chunks (odd)
     int yp;         // LDS pitch (elements) of a bf16 y row
@@ -241,9 +232,10 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
     return v;
 }
 
-// NFT = 32-row tiles of [t|u] features (r + q <= 32 NFT).  KG > 0 fixes the
-// number of 64-wide input groups at compile time (straight-line phase 1).
-template <int NFT, int KG>
+// NFT = 32-row tiles of [t|u] features (r + q <= 32 NFT).  The number of
+// 64-wide input groups is kFGroups (D <= 384, padded groups read zeros), so
+// phase 1 is straight-line code.
+template <int NFT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_fused_top1(FusedArgs a) {
     extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
@@ -264,7 +256,7 @@ void k_fused_top1(FusedArgs a) {
     const unsigned char* xs = smem + a.x_off;
     unsigned char* ringp = smem + a.ring_off + wave * (kNS * kStageBytes);
     const uint32_t ring = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_word*)ringp));
-    const int kgroups = KG > 0 ? KG : a.kgroups;
+    constexpr int kgroups = kFGroups;
     const int n_iter = wave * kFHid < H ? (H - wave * kFHid + 4 * kFHid - 1) / (4 * kFHid) : 0;
     const i32x4 d_w1 = dma_desc(a.W1, static_cast<int64_t>(H) * D * 2);
 
@@ -483,15 +475,13 @@ void k_fused_top1(FusedArgs a) {
     vm_wait<0>();                                      // b1, b2, x and the first stages
     lds_barrier();
 
-    // [Vt;Q_e] are loaded by asm (d_*) when the step loop is unrolled (KG > 0),
-    // else by compiler-visible loads (r_*): a loop-carried asm result could be
-    // copied by the compiler before it lands.
+    // [Vt;Q_e] are loaded by asm, like the W1 stages, so that the compiler's
+    // own waits never drain the stages issued after them; the wave's explicit
+    // waits cover them (the step loop is straight-line, so no loop-carried
+    // copy of a register can be read before its load lands).
     const int soff0 = __builtin_amdgcn_readfirstlane(static_cast<int>(a.T >> 62));   // 0
     const i32x4 d_vt = dma_desc(a.Vt, static_cast<int64_t>(r) * H * 2);
     const i32x4 d_qe = dma_desc(a.Q + static_cast<int64_t>(e) * a.q * H, static_cast<int64_t>(a.q) * H * 2);
-    const __amdgpu_buffer_rsrc_t r_vt = buf(a.Vt, static_cast<int64_t>(r) * H * 2);
-    const __amdgpu_buffer_rsrc_t r_qe =
-        buf(a.Q + static_cast<int64_t>(e) * a.q * H, static_cast<int64_t>(a.q) * H * 2);
     // LDS byte offsets of this lane's x chunks for token blocks 0 and 1
     const int xoff0 = (lrow * a.xch + 4 * lh) * 16;
     const int xoff1 = xoff0 + 32 * a.xch * 16;
@@ -527,10 +517,7 @@ void k_fused_top1(FusedArgs a) {
                 const int j = j0 + jj;
                 const int hid = hb + 16 * j + 8 * lh;
                 const uint32_t off = (live & (hid < H)) ? rowb + 2u * hid : kOob;
-                if constexpr (KG > 0)
-                    vq[f][j] = bload16_asm(tile_vt ? d_vt : d_qe, off, soff0);
-                else
-                    vq[f][j] = bload16(tile_vt ? r_vt : r_qe, off);
+                vq[f][j] = bload16_asm(tile_vt ? d_vt : d_qe, off, soff0);
             }
         }
     };
@@ -584,13 +571,6 @@ void k_fused_top1(FusedArgs a) {
     auto block = [&](int k, auto p2_tag) {
         constexpr bool p2 = decltype(p2_tag)::value;
         const int hb = (k * 4 + wave) * kFHid;
-        if constexpr (p2 && KG == 0) {
-            // the compiler's wait for vq goes here, before this block's DMA
-#pragma unroll
-            for (int f = 0; f < NFT; ++f)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) asm volatile("" : : "v"(vq[f][j]));
-        }
         // z^T accumulators start at b1 (lane's value v of tile qq is hidden
         // unit hb + 32 qq + 16 (v/8) + 8 lh + v%8; the LDS copy of b1 is zero
         // past H)
@@ -621,7 +601,7 @@ void k_fused_top1(FusedArgs a) {
                 case 1: vm_wait<16 + 2 * NFT>(); break;
                 default: vm_wait<16 + 4 * NFT>(); break;
             }
-            if constexpr (p2 && KG > 0) {
+            if constexpr (p2) {
                 // this wait covers stage n, issued in step 5 of the previous
                 // block after that block's [Vt;Q_e] loads: vq has landed
                 if (g == 1) {
@@ -658,13 +638,11 @@ void k_fused_top1(FusedArgs a) {
         block(0, std::false_type{});
         for (int k = 1; k < n_iter; ++k) block(k, std::true_type{});
         // drain: GELU + phase 2 of the last slice, once its [Vt;Q_e] landed
-        if constexpr (KG > 0) {
-            vm_wait<0>();
+        vm_wait<0>();
 #pragma unroll
-            for (int f = 0; f < NFT; ++f)
+        for (int f = 0; f < NFT; ++f)
 #pragma unroll
-                for (int j = 0; j < 4; ++j) reg_ready(vq[f][j]);
-        }
+            for (int j = 0; j < 4; ++j) reg_ready(vq[f][j]);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             u32x4 zo[2];
@@ -816,15 +794,15 @@ void k_fused_top1(FusedArgs a) {
     }
 }
 
-template <int NFT, int KG>
+template <int NFT>
 hipError_t fused_cfg(const FusedArgs& a, size_t lds, int grid, hipStream_t st) {
     if (lds > 65536) {
         const hipError_t err = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&k_fused_top1<NFT, KG>),
+            reinterpret_cast<const void*>(&k_fused_top1<NFT>),
             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
         if (err != hipSuccess) return err;
     }
-    launch_kernel(k_fused_top1<NFT, KG>, dim3(static_cast<unsigned>(grid)), 256, lds, st, a);
+    launch_kernel(k_fused_top1<NFT>, dim3(static_cast<unsigned>(grid)), 256, lds, st, a);
     return hipGetLastError();
 }
 
@@ -880,7 +858,7 @@ bool fused_top1_supported(int D, int H, int r, int q) {
           r + q <= kFusedMaxRQ))
         return false;
     if (D > 128 * kCt) return false;               // one pass of y column tiles
-    if (fused_kgroups(D) != 6) return false;      // the instantiated input-group count
+    if (fused_kgroups(D) != kFGroups) return false;   // the compiled input-group count
     return fused_lds(D, H, r, q).total <= kLdsBytes - kStaticLds;
 }
 
@@ -917,7 +895,6 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
     a.E = E;
     a.r = r;
     a.q = q;
-    a.kgroups = fused_kgroups(D);
     a.hpad = (H + 4 * kFHid - 1) / (4 * kFHid) * (4 * kFHid);
     const int nft = (r + q + 31) / 32;
     const FusedLds L = fused_lds(D, H, r, q);
@@ -936,13 +913,11 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
     a.per_xcd = static_cast<int>((tiles + kFXcds - 1) / kFXcds);
     const int grid = a.per_xcd * kFXcds;
     switch (nft) {
-        // the supported shapes (D <= 384) have six input groups: the step loop
-        // is unrolled at compile time for every feature-tile count
-        case 1: return fused_cfg<1, 6>(a, lds, grid, st);
-        case 2: return fused_cfg<2, 6>(a, lds, grid, st);
-        case 3: return fused_cfg<3, 6>(a, lds, grid, st);
-        case 4: return fused_cfg<4, 6>(a, lds, grid, st);
-        default: return fused_cfg<5, 6>(a, lds, grid, st);
+        case 1: return fused_cfg<1>(a, lds, grid, st);
+        case 2: return fused_cfg<2>(a, lds, grid, st);
+        case 3: return fused_cfg<3>(a, lds, grid, st);
+        case 4: return fused_cfg<4>(a, lds, grid, st);
+        default: return fused_cfg<5>(a, lds, grid, st);
     }
 }
 
