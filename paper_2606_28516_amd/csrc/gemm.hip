@@ -346,7 +346,9 @@ static hipError_t gemm_dt(const GemmDesc& g, hipStream_t st) {
         return gemm_cfg<Tin, 256, 256, 4, 2, 2>(g, st);
     if (g.N <= 32) return gemm_cfg<Tin, 128, 32, 4, 1, 3>(g, st);
     if (g.N <= 64) return gemm_cfg<Tin, 128, 64, 4, 1, 3>(g, st);
-    if (g.N <= 128 && g.K >= 1024) return gemm_cfg<Tin, 64, 64, 2, 2, 4>(g, st);
+    // long k rows (2 KB or more: a float32 stage holds half the k of a bf16 one)
+    const int64_t kbytes = static_cast<int64_t>(g.K) * static_cast<int64_t>(sizeof(Tin));
+    if (g.N <= 128 && kbytes >= 2048) return gemm_cfg<Tin, 64, 64, 2, 2, 4>(g, st);
     if (mt128 * ((g.N + 127) / 128) < 2048) return gemm_cfg<Tin, 64, 128, 2, 2, 2>(g, st);
     return gemm_cfg<Tin, 128, 128, 2, 2, 2>(g, st);
 }
