@@ -26,6 +26,8 @@ Prints one JSON line.  Besides the contract fields it carries
                (clearmoe_ffn_forward_ex);
   deit_base    the DeiT-Base-shaped top-2 layer (50432 tokens, D = 768) through
                the GEMM chain, with each product's rate against the bf16 peak;
+  deit_tiny    the DeiT-Tiny-shaped fp32 layer (1576 tokens, D = 192);
+  expert_sweep the DeiT-Small shape for E = 2, 4, 6, 8 beside the dense FFN;
   ffn_stack    the FFN part of a 12-block DeiT-Small forward with 6 CLEAR-MoE
                layers (class tokens on the dense path) against 12 dense ones.
 """
@@ -290,6 +292,18 @@ def main():
         out["routers"] = bench_routers(cm, synth, torch, np, stream, L, max(20, args.steps // 5))
         out["ffn_stack"] = bench_stack(cm, synth, torch, np, stream, L, max(20, args.steps // 10))
         out["deit_base"] = bench_layer(cm, synth, torch, np, stream, "C3", 20)
+        out["deit_tiny"] = bench_layer(cm, synth, torch, np, stream, "C1", 100)
+        dense_ms = out["dense"]["ms_per_step"]
+        sweep = {}
+        for e in (2, 4, 6, 8):
+            r = bench_layer(cm, synth, torch, np, stream, f"C5-E{e}", 100)
+            sweep[f"E{e}"] = {"ms": r["ms"], "tokens_per_s": r["tokens_per_s"],
+                              "moe_over_dense_time": r["ms"] / dense_ms,
+                              "stages_us": {k: v["us"] for k, v in r["stages"].items()}}
+        out["expert_sweep"] = {"workload": "DeiT-Small shape (12608 tokens, D = 384, H = 1536, r = 128, "
+                                           "q = 32, bf16, top-1) for E in {2, 4, 6, 8}, uniform "
+                                           "clusters, seed 4; dense = the dense comparator above",
+                               "points": sweep}
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(L, cfg, args.cpu_seconds)
