@@ -29,7 +29,7 @@ size_t up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 struct Layout {
     size_t tile_counts, tile_base, chunk_tot;     // route / dispatch
     size_t counts, offsets, idx, gate, perm, inv;  // ffn_forward
-    size_t z, tproj, hsh, u, hres, tu;
+    size_t z, tproj, hsh, u, hres, tu, fpart, fcount;
     size_t dispatch_end, total;
     // padded-batch backend only (after total): capacity E * T * k rows
     size_t perm_pad, inv_pad, seg, u_pad, hres_pad, padded_total;
@@ -67,6 +67,12 @@ Layout layout(const clearmoe_shape& s) {
     L.u = take(es * T * k * s.q);
     L.hres = take(sizeof(float) * T * k * s.D);
     L.tu = take(es * T * k * (s.r + s.q));
+    // fused top-1 of a small batch: float32 [t|u] partials of the hidden
+    // split and the per-tile arrival counters
+    const bool fused = k == 1 && s.dtype == CLEARMOE_BF16 && fused_top1_supported(s.D, s.H, s.r, s.q);
+    const size_t fpart = fused && T > 0 ? fused_part_bytes(T, static_cast<int>(E), s.H, s.r, s.q) : 0;
+    L.fpart = take(fpart > 0 ? fpart : 1);
+    L.fcount = take(sizeof(int32_t) * (fpart > 0 ? T / 64 + E + 1 : 1));
     L.total = off;
     // A padded batch holds E sub-batches of the largest expert count, which
     // can be every assignment: room for E * T * k rows.
@@ -526,7 +532,8 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
         CLEARMOE_STAGE(CLEARMOE_STAGE_FUSED_TOP1, st,
                        launch_fused_top1(x, W1, b1, US, Vt, b2, P, Q, perm, offsets,
                                          own_dispatch ? idx : nullptr, tc, gate, y, T, s.D, s.H,
-                                         s.E, s.r, s.q, st));
+                                         s.E, s.r, s.q, at<float>(ws, L.fpart),
+                                         at<int32_t>(ws, L.fcount), st));
         // join: the class rows of y (written on the side stream) are complete
         // before anything later on the caller's stream
         if (side != nullptr) {

@@ -46,6 +46,7 @@ namespace {
 constexpr int kFRows = 64;      // rows (tokens) per workgroup
 constexpr int kFHid = 64;       // hidden units per wave per step
 constexpr int kFXcds = 8;
+constexpr int kFMaxSplit = 8;   // workgroups per tile of a small batch (hidden split)
 constexpr int kNS = 3;                  // W1 ring stages per wave
 constexpr int kStageBytes = 64 * 128;   // 64 W1 rows x 64 inputs (bf16)
 constexpr int kCt = 3;                  // y column tiles per wave (4 kCt tiles cover D)
@@ -191,6 +192,9 @@ struct FusedArgs {
     int tu_off;     // byte offset of the bf16 [t|u] rows (after the sums / y rows)
     int tiles_bound;
     int per_xcd;
+    int split;            // S >= 1 workgroups per tile, each on every S-th hidden slice group
+    float* part;          // S > 1: [tiles][S][64][32 NFT] float32 partial [t|u] sums
+    int32_t* counters;    // S > 1: [tiles] arrivals, zero before the launch
 };
 
 // [Vt;Q_e] halves (issued in steps 4 and 5 of every block, before that step's
@@ -235,7 +239,7 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
 // NFT = 32-row tiles of [t|u] features (r + q <= 32 NFT).  The number of
 // 64-wide input groups is kFGroups (D <= 384, padded groups read zeros), so
 // phase 1 is straight-line code.
-template <int NFT>
+template <int NFT, bool SPLIT>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1)))
 void k_fused_top1(FusedArgs a) {
     extern __shared__ __attribute__((aligned(1024))) unsigned char smem[];
@@ -247,7 +251,8 @@ void k_fused_top1(FusedArgs a) {
     const int lrow = lane & 31, lh = lane >> 5;
 
     // ---- tile -> (expert e, rows [m_lo, m_hi)), XCD-major order
-    const int tile = (blockIdx.x % kFXcds) * a.per_xcd + blockIdx.x / kFXcds;
+    const int wg = (blockIdx.x % kFXcds) * a.per_xcd + blockIdx.x / kFXcds;
+    const int tile = SPLIT ? wg / a.split : wg, part = SPLIT ? wg - tile * a.split : 0;
     if (tile >= a.tiles_bound) return;
     const int D = a.D, H = a.H, r = a.r, rq = a.r + a.q;
 
@@ -257,7 +262,9 @@ void k_fused_top1(FusedArgs a) {
     unsigned char* ringp = smem + a.ring_off + wave * (kNS * kStageBytes);
     const uint32_t ring = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_word*)ringp));
     constexpr int kgroups = kFGroups;
-    const int n_iter = wave * kFHid < H ? (H - wave * kFHid + 4 * kFHid - 1) / (4 * kFHid) : 0;
+    // hidden slices of this wave: slot, slot + 4 S, ... (slot = 4 part + wave)
+    const int slot = SPLIT ? 4 * part + wave : wave, nslot = SPLIT ? 4 * a.split : 4;
+    const int n_iter = slot * kFHid < H ? (H - slot * kFHid + nslot * kFHid - 1) / (nslot * kFHid) : 0;
     const i32x4 d_w1 = dma_desc(a.W1, static_cast<int64_t>(H) * D * 2);
 
     // DMA of W1 ring stage n = slice it, input group g into slot n % kNS: ring
@@ -265,7 +272,7 @@ void k_fused_top1(FusedArgs a) {
     // (inputs 64g + 8c .. + 8) sits at slot c ^ swz(row).
     auto dma_stage = [&](int n) {
         const int it = n / kgroups, g = n - it * kgroups;
-        const int hb = (it * 4 + wave) * kFHid;
+        const int hb = (it * nslot + slot) * kFHid;
         const uint32_t m0 = ring + static_cast<uint32_t>(n % kNS) * kStageBytes;
         uint32_t off[8];
 #pragma unroll
@@ -570,7 +577,7 @@ void k_fused_top1(FusedArgs a) {
     // block, where the scheduler can interleave them.
     auto block = [&](int k, auto p2_tag) {
         constexpr bool p2 = decltype(p2_tag)::value;
-        const int hb = (k * 4 + wave) * kFHid;
+        const int hb = (k * nslot + slot) * kFHid;
         // z^T accumulators start at b1 (lane's value v of tile qq is hidden
         // unit hb + 32 qq + 16 (v/8) + 8 lh + v%8; the LDS copy of b1 is zero
         // past H)
@@ -684,6 +691,16 @@ void k_fused_top1(FusedArgs a) {
     lds_barrier();                                     // x and the rings no longer read
     float* areas = reinterpret_cast<float*>(smem + a.epi_off);
     bf16_bits* tul = reinterpret_cast<bf16_bits*>(smem + a.tu_off);
+    // hidden split (S > 1): a part's four-wave sums go to its slot of the
+    // partial buffer instead (float32, [tile][part][token][32 NFT]), written
+    // and read with device-scope (sc1) accesses: they miss the CU's L1 and are
+    // coherent across the XCDs' L2s, as relaxed device-scope atomics are
+    constexpr bool split = SPLIT;
+    constexpr int kFP = 32 * NFT;
+    constexpr int kDevScope = 16;    // cache-policy bits: sc1
+    const __amdgpu_buffer_rsrc_t tpart = __builtin_amdgcn_make_buffer_rsrc(
+        split ? a.part + static_cast<int64_t>(tile) * a.split * kFRows * kFP : nullptr, 0,
+        split ? a.split * kFRows * kFP * 4 : 0, kBufWord3);
     auto round = [&](auto f0_tag, auto nt_tag) {
         constexpr int f0 = decltype(f0_tag)::value, nt = decltype(nt_tag)::value;
         constexpr int rp = 32 * nt + 4;
@@ -711,19 +728,74 @@ void k_fused_top1(FusedArgs a) {
             for (int w = 0; w < 4; ++w)
                 o[w] = *reinterpret_cast<const float4*>(areas + w * (kFRows * rp) + t * rp + 4 * c4);
             const int feat = 32 * f0 + 4 * c4;
-            const float sc = feat < r ? 1.0f : gt;
-            uint2 wv;
-            wv.x = pack_bf16x2(((o[0].x + o[2].x) + (o[1].x + o[3].x)) * sc,
-                               ((o[0].y + o[2].y) + (o[1].y + o[3].y)) * sc);
-            wv.y = pack_bf16x2(((o[0].z + o[2].z) + (o[1].z + o[3].z)) * sc,
-                               ((o[0].w + o[2].w) + (o[1].w + o[3].w)) * sc);
-            *reinterpret_cast<uint2*>(tul + t * a.tuch * 8 + feat) = wv;
+            float4 sum;
+            sum.x = (o[0].x + o[2].x) + (o[1].x + o[3].x);
+            sum.y = (o[0].y + o[2].y) + (o[1].y + o[3].y);
+            sum.z = (o[0].z + o[2].z) + (o[1].z + o[3].z);
+            sum.w = (o[0].w + o[2].w) + (o[1].w + o[3].w);
+            if constexpr (split) {
+                f32x4 v = {sum.x, sum.y, sum.z, sum.w};
+                __builtin_amdgcn_raw_buffer_store_b128(v, tpart, ((part * kFRows + t) * kFP + feat) * 4,
+                                                       0, kDevScope);
+            } else {
+                const float sc = feat < r ? 1.0f : gt;
+                uint2 wv;
+                wv.x = pack_bf16x2(sum.x * sc, sum.y * sc);
+                wv.y = pack_bf16x2(sum.z * sc, sum.w * sc);
+                *reinterpret_cast<uint2*>(tul + t * a.tuch * 8 + feat) = wv;
+            }
         }
         lds_barrier();
     };
     round(std::integral_constant<int, 0>{}, std::integral_constant<int, kRa>{});
     if constexpr (NFT > kRa)
         round(std::integral_constant<int, kRa>{}, std::integral_constant<int, NFT - kRa>{});
+    if constexpr (split) {
+        // publish this part's sums: its stores have completed at device scope
+        // before the tile's arrival counter is bumped; the last part of the
+        // tile to arrive loads all S only after it has seen the count, and
+        // sums them in part order (deterministic whatever the arrival order),
+        // gates the u features, rounds to bf16 and finishes the tile.  (An
+        // agent-scope fence here is an L2 write-back and invalidate on each
+        // XCD: 15-35 % slower at 1568-6304 tokens.)
+        __shared__ int s_last;
+        vm_wait<0>();
+        __syncthreads();
+        if (tid == 0)
+            s_last = __hip_atomic_fetch_add(a.counters + tile, 1, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT) == a.split - 1;
+        __syncthreads();
+        if (!s_last) {
+            vm_wait<0>();                              // the [US|P_e] loads above
+            return;
+        }
+        const int S = a.split;
+        for (int item = tid; item < kFRows * (kFP / 4); item += 256) {
+            const int t = item / (kFP / 4), c4 = item - t * (kFP / 4);
+            f32x4 v[kFMaxSplit];
+#pragma unroll
+            for (int pp = 0; pp < kFMaxSplit; ++pp)
+                if (pp < S)
+                    v[pp] = __builtin_amdgcn_raw_buffer_load_b128(
+                        tpart, ((pp * kFRows + t) * kFP + 4 * c4) * 4, 0, kDevScope);
+            f32x4 sum = v[0];
+#pragma unroll
+            for (int pp = 1; pp < kFMaxSplit; ++pp)
+                if (pp < S) {
+                    sum.x += v[pp].x;
+                    sum.y += v[pp].y;
+                    sum.z += v[pp].z;
+                    sum.w += v[pp].w;
+                }
+            const int feat = 4 * c4;
+            const float sc = feat < r ? 1.0f : s_gate[t];
+            uint2 wv;
+            wv.x = pack_bf16x2(sum.x * sc, sum.y * sc);
+            wv.y = pack_bf16x2(sum.z * sc, sum.w * sc);
+            *reinterpret_cast<uint2*>(tul + t * a.tuch * 8 + feat) = wv;
+        }
+        lds_barrier();
+    }
 
     // ---- y = [t|u] [US | P_e]^T + b2 into LDS rows (over the sums' area,
     //      free now): y^T[n][token] = [US|P_e][n][k] [t|u]^T[k][token]; the
@@ -794,15 +866,15 @@ void k_fused_top1(FusedArgs a) {
     }
 }
 
-template <int NFT>
+template <int NFT, bool SPLIT>
 hipError_t fused_cfg(const FusedArgs& a, size_t lds, int grid, hipStream_t st) {
     if (lds > 65536) {
         const hipError_t err = hipFuncSetAttribute(
-            reinterpret_cast<const void*>(&k_fused_top1<NFT>),
+            reinterpret_cast<const void*>(&k_fused_top1<NFT, SPLIT>),
             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
         if (err != hipSuccess) return err;
     }
-    launch_kernel(k_fused_top1<NFT>, dim3(static_cast<unsigned>(grid)), 256, lds, st, a);
+    launch_kernel(k_fused_top1<NFT, SPLIT>, dim3(static_cast<unsigned>(grid)), 256, lds, st, a);
     return hipGetLastError();
 }
 
@@ -853,6 +925,29 @@ FusedLds fused_lds(int D, int H, int r, int q) {
 
 }  // namespace
 
+// Arrival counters of the hidden split start at zero in every launch (a fill
+// kernel, so that the launch sequence records no memset).
+__global__ void k_zero_counters(int32_t* c, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) c[i] = 0;
+}
+
+int fused_split(int64_t T, int E, int H) {
+    const int64_t tiles = (T + kFRows - 1) / kFRows + E;
+    const int64_t groups = (H + 4 * kFHid - 1) / (4 * kFHid);   // four-slice groups
+    int64_t s = kFMaxSplit;
+    if (256 / tiles < s) s = 256 / tiles;
+    if (groups < s) s = groups;
+    return s < 2 ? 1 : static_cast<int>(s);
+}
+
+size_t fused_part_bytes(int64_t T, int E, int H, int r, int q) {
+    const int s = fused_split(T, E, H);
+    if (s < 2) return 0;
+    const int64_t tiles = (T + kFRows - 1) / kFRows + E;
+    return static_cast<size_t>(tiles) * s * kFRows * (32 * ((r + q + 31) / 32)) * sizeof(float);
+}
+
 bool fused_top1_supported(int D, int H, int r, int q) {
     if (!(D >= 8 && D <= kFusedMaxD && H >= 8 && H <= kFusedMaxH && r % 32 == 0 && r + q > 0 &&
           r + q <= kFusedMaxRQ))
@@ -866,9 +961,12 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
                              const void* Vt, const float* b2, const void* P, const void* Q,
                              const int32_t* perm, const int32_t* offsets, const int32_t* idx,
                              const int32_t* tile_counts, const float* gate, void* y, int64_t T,
-                             int D, int H, int E, int r, int q, hipStream_t st) {
+                             int D, int H, int E, int r, int q, float* part, int32_t* counters,
+                             hipStream_t st) {
     if (!fused_top1_supported(D, H, r, q)) return hipErrorInvalidValue;
     if (T == 0) return hipSuccess;
+    const int split = fused_split(T, E, H);
+    if (split > 1 && (part == nullptr || counters == nullptr)) return hipErrorInvalidValue;
     FusedArgs a{};
     a.x = static_cast<const bf16_bits*>(x);
     a.W1 = static_cast<const bf16_bits*>(W1);
@@ -910,14 +1008,33 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
     const size_t lds = L.total;
     const int64_t tiles = (T + kFRows - 1) / kFRows + E;
     a.tiles_bound = static_cast<int>(tiles);
-    a.per_xcd = static_cast<int>((tiles + kFXcds - 1) / kFXcds);
+    a.split = split;
+    a.part = part;
+    a.counters = counters;
+    // XCD-major workgroup order; a tile's S parts stay within one XCD (and
+    // its L2), per_xcd being a multiple of S
+    int per_xcd = static_cast<int>((tiles * split + kFXcds - 1) / kFXcds);
+    per_xcd = (per_xcd + split - 1) / split * split;
+    a.per_xcd = per_xcd;
     const int grid = a.per_xcd * kFXcds;
+    if (split > 1) {
+        // the fill kernel must not take the timing events meant for the
+        // fused launch
+        LaunchTiming& lt = launch_timing();
+        const LaunchTiming keep = lt;
+        lt = LaunchTiming{};
+        launch_kernel(k_zero_counters, dim3((a.tiles_bound + 255) / 256), 256, 0, st, counters,
+                      a.tiles_bound);
+        lt = keep;
+        const hipError_t err = hipGetLastError();
+        if (err != hipSuccess) return err;
+    }
     switch (nft) {
-        case 1: return fused_cfg<1>(a, lds, grid, st);
-        case 2: return fused_cfg<2>(a, lds, grid, st);
-        case 3: return fused_cfg<3>(a, lds, grid, st);
-        case 4: return fused_cfg<4>(a, lds, grid, st);
-        default: return fused_cfg<5>(a, lds, grid, st);
+        case 1: return split > 1 ? fused_cfg<1, true>(a, lds, grid, st) : fused_cfg<1, false>(a, lds, grid, st);
+        case 2: return split > 1 ? fused_cfg<2, true>(a, lds, grid, st) : fused_cfg<2, false>(a, lds, grid, st);
+        case 3: return split > 1 ? fused_cfg<3, true>(a, lds, grid, st) : fused_cfg<3, false>(a, lds, grid, st);
+        case 4: return split > 1 ? fused_cfg<4, true>(a, lds, grid, st) : fused_cfg<4, false>(a, lds, grid, st);
+        default: return split > 1 ? fused_cfg<5, true>(a, lds, grid, st) : fused_cfg<5, false>(a, lds, grid, st);
     }
 }
 

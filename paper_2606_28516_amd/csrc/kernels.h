@@ -259,6 +259,13 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
                              const void* Vt, const float* b2, const void* P, const void* Q,
                              const int32_t* perm, const int32_t* offsets, const int32_t* idx,
                              const int32_t* tile_counts, const float* gate, void* y, int64_t T,
-                             int D, int H, int E, int r, int q, hipStream_t st);
+                             int D, int H, int E, int r, int q, float* part, int32_t* counters,
+                             hipStream_t st);
+// Small batches (fewer 64-row tiles than CUs) split each tile's hidden units
+// over fused_split(T, E, H) workgroups; the launch then needs part
+// (fused_part_bytes) and counters (T / 64 + E + 1 int32) of workspace, else
+// both may be NULL.
+int fused_split(int64_t T, int E, int H);
+size_t fused_part_bytes(int64_t T, int E, int H, int r, int q);
 
 }  // namespace clearmoe

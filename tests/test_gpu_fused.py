@@ -5,7 +5,8 @@ Shapes sweep the kernel's edges: token counts that leave ragged 64-row tiles
 in every expert segment, widths D that are not multiples of 64 (padded input
 groups), hidden widths H that are not multiples of the 4 x 64 round (waves with
 partial or no slices), every count of 32-row [t|u] tiles (1 to 5), q = 0,
-r = 0, and the widest D (x rows beyond 64 KB of LDS).  The GELU test isolates
+r = 0, the widest D (x rows beyond 64 KB of LDS), and small batches whose
+tiles split their hidden units over 2 to 8 workgroups.  The GELU test isolates
 the activation (W1, Vt and US identities) and checks it against the exact erf
 form to the bound of the published approximation the kernels use.
 """
@@ -37,6 +38,13 @@ FUSED_LAYERS = [
     (129, 768, 3072, 4, 128, 32),    # D > 384: the GEMM chain takes the layer
     (20000, 128, 256, 20, 64, 16),   # E > 16: 79 router tiles, the in-kernel scans cross rows and waves
     (5000, 64, 128, 64, 32, 8),      # E = 64, the most experts: expert totals over a whole wave
+    # small batches: each tile's hidden units split over S workgroups
+    (300, 128, 1024, 4, 32, 0),      # S = 4, NFT = 1
+    (200, 192, 768, 3, 64, 0),       # S = 3, NFT = 2
+    (150, 64, 2048, 2, 64, 32),      # S = 8, NFT = 3
+    (260, 200, 1000, 5, 96, 24),     # S = 4, NFT = 4, the last slot partial
+    (1, 64, 2048, 2, 32, 8),         # S = 8, one token: one tile with rows, two empty
+    (1568, 384, 1536, 8, 128, 32),   # S = 6: eight images of DeiT-S tokens
 ]
 
 
@@ -133,8 +141,11 @@ def test_fused_skewed_routing(mode):
     assert frob_rel(g["y"], ref["y"]) <= BF16_FROB_REGRESS
 
 
-def test_fused_deterministic():
-    L = _layer(1000, 384, 1536, 8, 128, 32, seed=21)
+@pytest.mark.parametrize("T", [1000, 12608])
+def test_fused_deterministic(T):
+    # T = 1000: hidden split (partials summed in part order whatever the
+    # order the parts finish in); T = 12608: one workgroup per tile
+    L = _layer(T, 384, 1536, 8, 128, 32, seed=21)
     a, b = gpu_ffn(L), gpu_ffn(L)
     assert np.array_equal(a["y"], b["y"])
 
