@@ -27,11 +27,14 @@ Prints one JSON line.  Besides the contract fields it carries
   deit_base    the DeiT-Base-shaped top-2 layer (50432 tokens, D = 768) through
                the GEMM chain, with each product's rate against the bf16 peak;
   deit_tiny    the DeiT-Tiny-shaped fp32 layer (1576 tokens, D = 192);
+  small_batch  the DeiT-Small layer at 1 and 8 images (197 and 1576 tokens),
+               where the fused kernel splits each tile's hidden units;
   expert_sweep the DeiT-Small shape for E = 2, 4, 6, 8 beside the dense FFN;
   ffn_stack    the FFN part of a 12-block DeiT-Small forward with 6 CLEAR-MoE
                layers (class tokens on the dense path) against 12 dense ones.
 """
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -293,6 +296,12 @@ def main():
         out["ffn_stack"] = bench_stack(cm, synth, torch, np, stream, L, max(20, args.steps // 10))
         out["deit_base"] = bench_layer(cm, synth, torch, np, stream, "C3", 20)
         out["deit_tiny"] = bench_layer(cm, synth, torch, np, stream, "C1", 100)
+        small = {}
+        for n_img in (1, 8):
+            c = dataclasses.replace(synth.CONFIGS["C2"], name=f"C2-widths-{n_img}-images",
+                                    T=197 * n_img)
+            small[f"images{n_img}"] = bench_layer(cm, synth, torch, np, stream, None, 200, cfg=c)
+        out["small_batch"] = small
         dense_ms = out["dense"]["ms_per_step"]
         sweep = {}
         for e in (2, 4, 6, 8):
@@ -489,10 +498,11 @@ def bench_routers(cm, synth, torch, np, stream, L, steps):
     return out
 
 
-def bench_layer(cm, synth, torch, np, stream, workload, steps):
-    """One layer of another configuration: step time from an untimed pass,
-    then every stage timed in a second pass; MFMA rate of each product."""
-    cfg = synth.CONFIGS[workload]
+def bench_layer(cm, synth, torch, np, stream, workload, steps, cfg=None):
+    """One layer of another configuration (a named workload, or cfg): step
+    time from an untimed pass, then every stage timed in a second pass; MFMA
+    rate of each product."""
+    cfg = cfg if cfg is not None else synth.CONFIGS[workload]
     L = synth.make_layer(cfg)
     d = {n: cm.from_stored(L[n]) for n in ("x", "W1", "b1", "US", "Vt", "b2", "P", "Q", "Wg", "bg")}
     shape = cm.make_shape(cfg.T, cfg.D, cfg.E, cfg.k, cm.F32 if cfg.dtype == "f32" else cm.BF16,
