@@ -73,7 +73,7 @@ def parse():
 KERNEL_SOURCES = {
     "route": ["route.hip"], "tile_hist": ["dispatch.hip"], "scan": ["dispatch.hip"],
     "permute": ["dispatch.hip"], "combine": ["dispatch.hip"], "combine_res": ["dispatch.hip"],
-    "fused_top1": ["fused.hip"],
+    "fused_top1": ["fused_kernel.h", "fused.hip", "fused_split.hip"],
 }
 
 
