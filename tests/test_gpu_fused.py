@@ -150,6 +150,22 @@ def test_fused_deterministic(T):
     assert np.array_equal(a["y"], b["y"])
 
 
+def test_fused_split_reuses_a_dirty_workspace():
+    # the split's arrival counters and partials live in the caller's
+    # workspace: filled with 0xFF first, then reused by three calls (each
+    # leaves its counters at S), every result the same and at the oracle
+    L = _layer(700, 384, 1536, 8, 128, 32, seed=23)
+    shape = cm.make_shape(700, 384, 8, 1, cm.BF16, H=1536, r=128, q=32)
+    ws = cm.alloc_workspace(shape)
+    ws.fill_(255)
+    outs = [gpu_ffn(L, ws=ws)["y"] for _ in range(3)]
+    for o in outs[1:]:
+        assert np.array_equal(o, outs[0])
+    ref = oracle.ffn_forward_layer(L)
+    tie = assert_routing(gpu_ffn(L, ws=ws)["idx"], ref["logits"], 1)
+    assert frob_rel(outs[0][~tie], ref["y"][~tie]) <= BF16_FROB_REGRESS
+
+
 def _gelu_exact(v):
     return np.array([0.5 * t * (1.0 + math.erf(t / math.sqrt(2.0))) for t in v.ravel()]).reshape(
         v.shape)
