@@ -67,12 +67,20 @@ Layout layout(const clearmoe_shape& s) {
     L.u = take(es * T * k * s.q);
     L.hres = take(sizeof(float) * T * k * s.D);
     L.tu = take(es * T * k * (s.r + s.q));
-    // fused top-1 of a small batch: float32 [t|u] partials of the hidden
-    // split and the per-tile arrival counters
+    // float32 partials and per-tile arrival counters: of the fused top-1
+    // kernel's hidden split (small batches), or else, on the top-1 GEMM
+    // chain, of the [t|u] product's split K
     const bool fused = k == 1 && s.dtype == CLEARMOE_BF16 && fused_top1_supported(s.D, s.H, s.r, s.q);
-    const size_t fpart = fused && T > 0 ? fused_part_bytes(T, static_cast<int>(E), s.H, s.r, s.q) : 0;
+    size_t fpart = 0, fcount = 0;
+    if (fused && T > 0) {
+        fpart = fused_part_bytes(T, static_cast<int>(E), s.H, s.r, s.q);
+        fcount = fpart > 0 ? static_cast<size_t>(T / 64 + E + 1) : 0;
+    } else if (k == 1 && T > 0) {
+        fpart = kGemmKsplitBytes;
+        fcount = kGemmKsplitTiles;
+    }
     L.fpart = take(fpart > 0 ? fpart : 1);
-    L.fcount = take(sizeof(int32_t) * (fpart > 0 ? T / 64 + E + 1 : 1));
+    L.fcount = take(sizeof(int32_t) * (fcount > 0 ? fcount : 1));
     L.total = off;
     // A padded batch holds E sub-batches of the largest expert count, which
     // can be every assignment: room for E * T * k rows.
@@ -566,6 +574,7 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
         g.C = tu; g.ldc = rq; g.c_f32 = 0;
         g.row_scale = gate; g.scale_rows = perm; g.scale_col0 = s.r;
         g.seg_offsets = offsets; g.nseg = s.E;
+        g.ks_part = at<float>(ws, L.fpart); g.ks_count = at<int32_t>(ws, L.fcount);
         if (rq > 0) CLEARMOE_STAGE(CLEARMOE_STAGE_TU, st, launch_gemm(s.dtype, g, st));
         g = gemm_desc(A, s.D, rq);
         g.A = tu; g.lda = rq;

@@ -83,7 +83,8 @@ template <> struct Mfma<float> {
 };
 
 template <typename Tin, int BM, int BN, int WM, int WN, int NS>
-__global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, int ntiles, int per_xcd) {
+__global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, int ntiles, int per_xcd,
+                                                       int ksplit) {
     constexpr int NW = WM * WN;                     // waves: 4 (one per SIMD) or 8 (two)
     static_assert(NW == 4 || NW == 8, "4 or 8 waves");
     constexpr int WTM = BM / WM, WTN = BN / WN;
@@ -108,8 +109,12 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, i
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
 
-    // ---- tile of this workgroup (XCD-major order)
-    const int tile = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    // ---- tile of this workgroup (XCD-major order); with split K, S
+    //      consecutive workgroups (one XCD) share a tile, part kp taking its
+    //      share of the k stages
+    const int wg = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    const int S = g.ks_part != nullptr ? ksplit : 1;
+    const int tile = wg / S, kp = wg - tile * S;
     if (tile >= mtiles * ntiles) return;
     const int mt = tile / ntiles, nt = tile % ntiles;
     int64_t m_lo, m_hi;
@@ -186,6 +191,11 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, i
         bchunk[i] = cpos ^ swz(r);
     }
 
+    // k stages of this part: [kb0, kb0 + nk)
+    const int nk_all = (g.K + BK - 1) / BK;
+    const int kb0 = static_cast<int>(static_cast<int64_t>(kp) * nk_all / S);
+    const int nk = static_cast<int>(static_cast<int64_t>(kp + 1) * nk_all / S) - kb0;
+
     auto stage = [&](int b) -> unsigned char* {
         return b == 0 ? st0 : b == 1 ? st1 : b == 2 ? st2 : st3;
     };
@@ -194,7 +204,7 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, i
     auto issue = [&](int kt, int b) {
         const uint32_t base = __builtin_amdgcn_readfirstlane(
             static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_u32*)(stage(b)))));
-        const int kbase = kt * BK;
+        const int kbase = (kb0 + kt) * BK;
 #pragma unroll
         for (int i = 0; i < AL; ++i) {
             const int kk = kbase + achunk[i] * PER16;
@@ -226,7 +236,6 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, i
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.0f;
 
-    const int nk = (g.K + BK - 1) / BK;
 #pragma unroll
     for (int s = 0; s < NS - 1; ++s)
         if (s < nk) issue(s, s);
@@ -274,6 +283,54 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, i
         }
     }
 
+    // ---- split K: each part stores its accumulators (float32, 16 per lane
+    //      and tile contiguous) with device-scope accesses, waits for them,
+    //      and counts itself in; the last part of the tile to arrive sums the
+    //      S parts in part order (the same bits whichever part is last) and
+    //      runs the epilogue.  The parts of a tile share an XCD.
+    if (S > 1) {
+        constexpr int kDevScope = 16;   // cache-policy bits: sc1
+        constexpr int kTiles = TM * TN;
+        const __amdgpu_buffer_rsrc_t rp = raw_rsrc(
+            g.ks_part + static_cast<int64_t>(tile) * S * BM * BN, static_cast<int64_t>(S) * BM * BN * 4);
+        auto off = [&](int pp, int i, int j, int q) {
+            return static_cast<int>(((((pp * NW + wave) * kTiles + i * TN + j) * 64 + lane) * 4 + q) * 16);
+        };
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const f32x4 v = {acc[i][j][4 * q], acc[i][j][4 * q + 1], acc[i][j][4 * q + 2],
+                                     acc[i][j][4 * q + 3]};
+                    __builtin_amdgcn_raw_buffer_store_b128(v, rp, off(kp, i, j, q), 0, kDevScope);
+                }
+        wait_vmcnt<0>();
+        __syncthreads();
+        __shared__ int s_last;
+        if (tid == 0)
+            s_last = __hip_atomic_fetch_add(g.ks_count + tile, 1, __ATOMIC_RELAXED,
+                                            __HIP_MEMORY_SCOPE_AGENT) == S - 1;
+        __syncthreads();
+        if (!s_last) return;
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    f32x4 sum = __builtin_amdgcn_raw_buffer_load_b128(rp, off(0, i, j, q), 0, kDevScope);
+                    for (int pp = 1; pp < S; ++pp) {
+                        const f32x4 v = __builtin_amdgcn_raw_buffer_load_b128(rp, off(pp, i, j, q), 0,
+                                                                               kDevScope);
+                        sum += v;
+                    }
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) acc[i][j][4 * q + t] = sum[t];
+                }
+    }
+
     // ---- epilogue.  The MFMAs took B as the first operand, so tile (i, j)
     //      holds C^T: lane l owns row m = .. + i*32 + l%32, and its value v is
     //      column n = .. + j*32 + 8*(v/4) + 4*(l/32) + v%4 -- four consecutive
@@ -318,6 +375,21 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, i
     }
 }
 
+__global__ void k_zero_tiles(int32_t* c, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) c[i] = 0;
+}
+
+// Split K (S parts of every tile's k stages) when the tiles alone would leave
+// most CUs idle and every part still has four stages or more.
+int gemm_ksplit(int64_t tiles, int nk) {
+    if (tiles >= kGemmKsplitTiles || nk < 8) return 1;
+    int64_t s = 8;
+    if (256 / tiles < s) s = 256 / tiles;
+    if (nk / 4 < s) s = nk / 4;
+    return s < 2 ? 1 : static_cast<int>(s);
+}
+
 template <typename Tin, int BM, int BN, int WM, int WN, int NS>
 static hipError_t gemm_cfg(const GemmDesc& g, hipStream_t st) {
     int64_t mt = (g.M + BM - 1) / BM;
@@ -325,10 +397,30 @@ static hipError_t gemm_cfg(const GemmDesc& g, hipStream_t st) {
     const int64_t nt = (g.N + BN - 1) / BN;
     const int64_t tiles = mt * nt;
     if (tiles == 0) return hipSuccess;
-    const int64_t per_xcd = (tiles + kXcds - 1) / kXcds;
+    constexpr int BK = kStageBytes / static_cast<int>(sizeof(Tin));
+    // tiles x S <= 256 parts of BM x BN floats each fit kGemmKsplitBytes up
+    // to 64 x 128 tiles (larger ones never have so few tiles here)
+    int S = 1;
+    if (g.ks_part != nullptr && g.ks_count != nullptr && BM * BN <= 64 * 128)
+        S = gemm_ksplit(tiles, (g.K + BK - 1) / BK);
+    GemmDesc d = g;
+    if (S == 1) d.ks_part = nullptr;
+    int64_t per_xcd = (tiles * S + kXcds - 1) / kXcds;
+    per_xcd = (per_xcd + S - 1) / S * S;             // a tile's parts on one XCD
     const int64_t grid = per_xcd * kXcds;
+    if (S > 1) {
+        // the fill kernel must not take the timing events meant for the GEMM
+        LaunchTiming& lt = launch_timing();
+        const LaunchTiming keep = lt;
+        lt = LaunchTiming{};
+        launch_kernel(k_zero_tiles, dim3(1), kGemmKsplitTiles, 0, st, d.ks_count,
+                      static_cast<int>(tiles));
+        lt = keep;
+        const hipError_t err = hipGetLastError();
+        if (err != hipSuccess) return err;
+    }
     launch_kernel(k_gemm<Tin, BM, BN, WM, WN, NS>, dim3(static_cast<unsigned>(grid)), 64 * WM * WN, 0, st,
-        g, static_cast<int>(mt), static_cast<int>(nt), static_cast<int>(per_xcd));
+        d, static_cast<int>(mt), static_cast<int>(nt), static_cast<int>(per_xcd), S);
     return hipGetLastError();
 }
 

@@ -229,7 +229,14 @@ struct GemmDesc {
     int N, K;
     const int32_t* seg_offsets;  // optional [nseg+1] on the device: grouped GEMM
     int nseg;
+    // optional split K for products with few tiles and long K (see
+    // gemm_ksplit): float32 partial tiles (kGemmKsplitBytes) and per-tile
+    // arrival counters (kGemmKsplitTiles int32) of workspace
+    float* ks_part;
+    int32_t* ks_count;
 };
+constexpr size_t kGemmKsplitBytes = static_cast<size_t>(256) * 64 * 128 * 4;
+constexpr int kGemmKsplitTiles = 128;
 // A GemmDesc with the neutral defaults for the optional fields.
 inline GemmDesc gemm_desc(int64_t M, int N, int K) {
     GemmDesc g{};

@@ -1,0 +1,45 @@
+"""GPU parity of the top-1 GEMM chain's [t|u] product when it splits K.
+
+With few tiles and a long K (the DeiT-Tiny float32 layer: 58 tiles of 64x64,
+24 k stages), the grouped [t|u] product runs as S parts per tile whose float32
+partial tiles go to the workspace; the last part to arrive sums them in part
+order.  Checked against the fp64 oracle in float32 and bfloat16 (r off the
+fused kernel's 32-grid, so the GEMM chain runs), and bit for bit across calls
+that reuse one workspace filled with 0xFF first.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_28516_amd import clearmoe as cm
+from paper_2606_28516_amd import synth
+from tests.parity_util import (BF16_FROB_REGRESS, F32_MAXREL, assert_routing, frob_rel, gpu_ffn,
+                               max_rel)
+
+pytestmark = pytest.mark.gpu
+
+SPLIT_LAYERS = [
+    # dt, T, D, H, E, r, q
+    ("f32", 1576, 192, 768, 4, 64, 16),     # DeiT-Tiny widths: S = 4
+    ("f32", 70, 64, 2048, 3, 32, 8),        # 4 tiles of 128x64, 64 k stages: S = 8
+    ("bf16", 300, 128, 1024, 4, 48, 16),    # r % 32 != 0: GEMM chain, 7 tiles, S = 4
+]
+
+
+@pytest.mark.parametrize("dt,T,D,H,E,r,q", SPLIT_LAYERS)
+def test_split_k_tu_product(dt, T, D, H, E, r, q):
+    cfg = synth.LayerConfig("splitk", T=T, D=D, H=H, E=E, k=1, r=r, q=q, dtype=dt, seed=T + H,
+                            residual="random", n_cal=2000)
+    L = synth.make_layer(cfg)
+    shape = cm.make_shape(T, D, E, 1, cm.F32 if dt == "f32" else cm.BF16, H=H, r=r, q=q)
+    ws = cm.alloc_workspace(shape)
+    ws.fill_(255)
+    outs = [gpu_ffn(L, ws=ws) for _ in range(3)]
+    for o in outs[1:]:
+        assert np.array_equal(o["y"], outs[0]["y"])
+    ref = oracle.ffn_forward_layer(L)
+    tie = assert_routing(outs[0]["idx"], ref["logits"], 1)
+    if dt == "f32":
+        assert max_rel(outs[0]["y"][~tie], ref["y"][~tie]) <= F32_MAXREL
+    else:
+        assert frob_rel(outs[0]["y"][~tie], ref["y"][~tie]) <= BF16_FROB_REGRESS
