@@ -232,7 +232,9 @@ int clearmoe_ffn_forward_padded(const clearmoe_shape* shape, const void* x, cons
  * paper's dense rows time (Table III, D0), run through the same GEMM kernels.
  *   x [T, D]; W1 [H, D], b1 [H]; W2 [D, H], b2 [D]; y [T, D] out (dtype).
  * Uses T, D, H, dtype (E, k, r, q must still be valid); the workspace of
- * clearmoe_workspace_bytes(shape) suffices. */
+ * clearmoe_workspace_bytes(shape) suffices, and so does that of a CLEAR-MoE
+ * layer with the same T, D, H and dtype (only the fc1 activations are kept
+ * there). */
 int clearmoe_dense_ffn_forward(const clearmoe_shape* shape, const void* x, const void* W1,
                                const float* b1, const void* W2, const float* b2, void* y,
                                void* ws, size_t ws_bytes, hipStream_t stream);

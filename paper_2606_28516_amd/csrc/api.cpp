@@ -719,8 +719,11 @@ int clearmoe_dense_ffn_forward(const clearmoe_shape* shape, const void* x, const
     for (const void* p : v16)
         if (p && !aligned(p, 16)) return CLEARMOE_ERR_INVALID_ARG;
     if ((b1 && !aligned(b1, 4)) || (b2 && !aligned(b2, 4))) return CLEARMOE_ERR_INVALID_ARG;
+    // only z is used: a workspace sized for a CLEAR-MoE layer of the same
+    // T, D, H serves as well
     const Layout L = layout(s);
-    if (!ws || !aligned(ws, kAlign) || ws_bytes < L.total) return CLEARMOE_ERR_WORKSPACE;
+    const size_t need = L.z + elem_size(s.dtype) * static_cast<size_t>(s.T) * static_cast<size_t>(s.H);
+    if (!ws || !aligned(ws, kAlign) || ws_bytes < need) return CLEARMOE_ERR_WORKSPACE;
     if (s.T == 0) return CLEARMOE_OK;
     void* z = at<void>(ws, L.z);
     GemmDesc g = gemm_desc(s.T, s.H, s.D);

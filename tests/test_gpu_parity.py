@@ -288,7 +288,12 @@ def test_dense_comparator(name):
     rng = np.random.default_rng(2)
     b1 = (0.1 * rng.standard_normal(cfg.H)).astype(np.float32)
     b2 = (0.1 * rng.standard_normal(cfg.D)).astype(np.float32)
-    y = cm.dense_ffn_forward(dev(L["x"]), dev(L["W1"]), dev(b1), dev(W2), dev(b2))
+    # the workspace of the CLEAR-MoE layer of the same shape serves the dense
+    # FFN too (the benchmark's dense comparator reuses it)
+    ws = cm.alloc_workspace(cm.make_shape(cfg.T, cfg.D, cfg.E, cfg.k,
+                                          cm.F32 if cfg.dtype == "f32" else cm.BF16,
+                                          H=cfg.H, r=cfg.r, q=cfg.q))
+    y = cm.dense_ffn_forward(dev(L["x"]), dev(L["W1"]), dev(b1), dev(W2), dev(b2), ws=ws)
     torch.cuda.synchronize()
     rows = _sample_rows(cfg.T, 256, 6)
     D = cfg.D
