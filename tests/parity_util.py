@@ -11,6 +11,20 @@ MARGIN = 1e-6          # tokens whose top-k logit margin is below this may route
 F32_MAXREL = 1e-4      # fp32 mode: max|y - y_ref| / max|y_ref|
 BF16_FROB = 2e-2       # bf16 mode: ||y - y_ref||_F / ||y_ref||_F
 BF16_FROB_REGRESS = 1e-2   # internal regression bar for bf16 (expected error ~3e-3)
+# Per-element bars (every element, beside the normwise ones above).  float32:
+# |y - y_ref| <= F32_ELEM * (|y_ref| + rms(y_ref)); the float32 path's errors
+# are ~2e-7 of that scale (accumulation order, the erf approximation).
+# bfloat16: |y - y_ref| <= 2^-8 |y_ref| + BF16_ELEM_RMS * rms(y_ref): the
+# output rounding is at most 2^-9 |y_ref|, and the roundings of z, t and u to
+# bfloat16 add an absolute error that scales with the size of the sums, i.e.
+# with rms(y_ref) (at most 0.021 rms(y_ref) when those roundings are replayed
+# in double on 2000 rows of the DeiT-Small and DeiT-Base layers).
+F32_ELEM = 1e-5
+BF16_ELEM_REL = 2.0 ** -8
+BF16_ELEM_RMS = 0.05
+# Tokens excluded as near ties may be at most this share of a test's tokens
+# (and at most one token when there are fewer than 1000).
+EXCL_MAX = 1e-3
 
 
 def dev(a):
@@ -44,16 +58,42 @@ def frob_rel(y, ref):
     return float(np.linalg.norm(y - ref) / den) if den > 0 else float(np.linalg.norm(y))
 
 
+def assert_elementwise(y, ref, dtype):
+    """Every element within the per-element bar of its storage type."""
+    y, ref = np.asarray(y), np.asarray(ref)
+    if ref.size == 0:
+        return
+    rms = float(np.sqrt(np.mean(ref * ref)))
+    err = np.abs(y - ref)
+    if dtype == "f32":
+        bound = F32_ELEM * (np.abs(ref) + rms)
+    else:
+        bound = BF16_ELEM_REL * np.abs(ref) + BF16_ELEM_RMS * rms
+    worst = np.unravel_index(np.argmax(err - bound), err.shape)
+    assert np.all(err <= bound), (f"element {worst}: |err| {err[worst]:.3e} > bound "
+                                  f"{bound[worst]:.3e} (rms {rms:.3e})")
+
+
 def max_rel(y, ref):
     den = np.max(np.abs(ref)) if ref.size else 0.0
     return float(np.max(np.abs(y - ref)) / den) if den > 0 else float(np.max(np.abs(y), initial=0))
 
 
+def bound_excluded(mask, what="near-tie"):
+    """Print how many tokens a comparison leaves out and bound their share: at
+    most EXCL_MAX of the tokens (one token below 1000 tokens)."""
+    mask = np.asarray(mask, dtype=bool)
+    n, N = int(mask.sum()), int(mask.size)
+    print(f"excluded {what} tokens: {n} of {N} ({n / max(N, 1):.2e})")
+    assert n <= max(1, int(EXCL_MAX * N)), f"{n} of {N} tokens excluded ({what})"
+    return mask
+
+
 def assert_routing(idx_gpu, logits_ref, k):
     """idx bit-exact wherever the oracle's margin >= MARGIN.  Returns the mask of
-    tokens that are allowed to differ (near ties)."""
+    tokens that are allowed to differ (near ties), whose share is bounded."""
     idx_ref, _ = oracle.topk(logits_ref, k)
-    tie = oracle.margins(logits_ref, k) < MARGIN
+    tie = bound_excluded(oracle.margins(logits_ref, k) < MARGIN)
     bad = np.any(idx_gpu != idx_ref, axis=1) & ~tie
     assert not bad.any(), f"{bad.sum()} tokens routed differently (first {np.nonzero(bad)[0][:5]})"
     return tie

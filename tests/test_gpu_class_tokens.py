@@ -11,7 +11,7 @@ import oracle
 from paper_2606_28516_amd import clearmoe as cm
 from paper_2606_28516_amd import synth
 
-from parity_util import (BF16_FROB_REGRESS, F32_MAXREL, MARGIN, check_dispatch, confidence_gap,
+from parity_util import (bound_excluded, BF16_FROB_REGRESS, F32_MAXREL, MARGIN, check_dispatch, confidence_gap,
                          dev, frob_rel, gpu_ffn_ex, gpu_router, max_rel)
 
 pytestmark = pytest.mark.gpu
@@ -61,7 +61,7 @@ def test_class_tokens_layer(dt, T, D, H, E, k, r, q, stride):
     g = gpu_ffn_ex(C)
     ref = oracle.ffn_forward_layer(C)
     assert ref["cls"].sum() == (T + stride - 1) // stride
-    excl = oracle.margins(ref["logits"], k) < MARGIN
+    excl = bound_excluded(oracle.margins(ref["logits"], k) < MARGIN)
     _check_layer(C, g, ref, excl, dt)
 
 
@@ -84,7 +84,7 @@ def test_class_tokens_route_and_dispatch():
     assert np.all(idx_h[cls] == -1) and np.all(gate_h[cls] == 0.0)
     lg = oracle.router_logits(L["x"], L["Wg"], L["bg"])
     want, _ = oracle.topk(lg, 2)
-    ok = ~cls & (oracle.margins(lg, 2) >= MARGIN)
+    ok = ~cls & ~bound_excluded(oracle.margins(lg, 2) < MARGIN)
     assert np.array_equal(idx_h[ok], want[ok])
     check_dispatch(idx_h, 8, counts.cpu().numpy(), offsets.cpu().numpy(), perm.cpu().numpy(),
                    inv.cpu().numpy())
@@ -100,12 +100,12 @@ def test_class_tokens_with_adaptive_and_mlp_routers():
     A = synth.with_class_tokens(synth.with_adaptive_router(L, tau), stride=100)
     g = gpu_ffn_ex(A)
     ref = oracle.ffn_forward_layer(A)
-    excl = (oracle.margins(lg, 2) < MARGIN) | (confidence_gap(lg, tau) < 1e-9)
+    excl = bound_excluded((oracle.margins(lg, 2) < MARGIN) | (confidence_gap(lg, tau) < 1e-9))
     _check_layer(A, g, ref, excl, "bf16")
     M = synth.with_class_tokens(synth.with_mlp_router(L, h=16, seed=2), stride=60)
     g = gpu_ffn_ex(M)
     ref = oracle.ffn_forward_layer(M)
-    excl = oracle.margins(ref["logits"], 1) < MARGIN
+    excl = bound_excluded(oracle.margins(ref["logits"], 1) < MARGIN)
     _check_layer(M, g, ref, excl, "bf16")
 
 
@@ -124,7 +124,7 @@ def test_class_tokens_at_deit_small():
     lg = oracle.router_logits(C["x"], C["Wg"], C["bg"])
     cls = np.arange(T) % 197 == 0
     assert np.all(g["idx"][cls] == -1)
-    ok = ~cls & (oracle.margins(lg, 1) >= MARGIN)
+    ok = ~cls & ~bound_excluded(oracle.margins(lg, 1) < MARGIN)
     assert np.array_equal(g["idx"][ok, 0], oracle.topk(lg, 1)[0][ok, 0])
     rows = np.unique(np.concatenate([np.nonzero(cls)[0], _sample_rows(T, 192, 4)]))
     rows = rows[cls[rows] | ok[rows]]

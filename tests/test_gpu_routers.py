@@ -20,7 +20,7 @@ import oracle
 from paper_2606_28516_amd import clearmoe as cm
 from paper_2606_28516_amd import synth
 
-from parity_util import (BF16_FROB_REGRESS, F32_MAXREL, MARGIN, check_dispatch, confidence_gap,
+from parity_util import (bound_excluded, BF16_FROB_REGRESS, F32_MAXREL, MARGIN, check_dispatch, confidence_gap,
                          dev, frob_rel, gpu_ffn_ex, gpu_router, max_rel, rounding_gap)
 
 pytestmark = pytest.mark.gpu
@@ -88,7 +88,7 @@ def test_adaptive_linear_router(dt, T, D, E, qt):
     L["router"] = {"kind": "adaptive", "tau": tau}
     idx, gate, counts, offsets, perm, inv, xperm = _route_gpu(L, 2)
     idx_ref, gate_ref = oracle.adaptive_topk(lg, tau)
-    excl = (oracle.margins(lg, 2) < MARGIN) | (confidence_gap(lg, tau) < CONF_GAP)
+    excl = bound_excluded((oracle.margins(lg, 2) < MARGIN) | (confidence_gap(lg, tau) < CONF_GAP))
     _compare_choice(idx, gate, idx_ref, gate_ref, excl)
     if T > 100:                                    # both outcomes are exercised
         assert 0 < (idx[:, 1] == -1).sum() < T
@@ -107,12 +107,12 @@ def test_adaptive_threshold_limits(tau, top1):
     if top1:
         assert np.all(idx[:, 1] == -1) and np.all(gate[:, 0] == 1.0)
         i1, _ = oracle.topk(lg, 1)
-        ok = oracle.margins(lg, 1) >= MARGIN
+        ok = ~bound_excluded(oracle.margins(lg, 1) < MARGIN)
         assert np.array_equal(idx[ok, 0], i1[ok, 0])
         assert offsets[-1] == 333 and np.all(perm[333:] == -1)
     else:
         i2, g2 = oracle.topk(lg, 2)
-        ok = oracle.margins(lg, 2) >= MARGIN
+        ok = ~bound_excluded(oracle.margins(lg, 2) < MARGIN)
         assert np.array_equal(idx[ok], i2[ok])
         assert np.all(np.abs(gate[ok] - g2[ok]) <= 2e-5)
         assert offsets[-1] == 666
@@ -175,7 +175,7 @@ def test_mlp_router(dt, T, D, E, k, hidden):
     lg, near = _mlp_ref(L, dt)
     idx, gate, counts, offsets, perm, inv, xperm = _route_gpu(L, k)
     idx_ref, gate_ref = oracle.topk(lg, k)
-    excl = near | (oracle.margins(lg, k) < MARGIN)
+    excl = bound_excluded(near | (oracle.margins(lg, k) < MARGIN))
     assert excl.mean() < 0.01
     ok = ~excl
     assert np.array_equal(idx[ok], idx_ref[ok])
@@ -194,7 +194,7 @@ def test_mlp_router_hidden_rounding_matters():
                                  L["Wg"], L["bg"])
     assert np.max(np.abs(exact - lg)) > 1e-4                   # the rounding moves logits
     idx, *_ = _route_gpu(L, 1)
-    ok = ~near & (oracle.margins(lg, 1) >= MARGIN)
+    ok = ~near & ~bound_excluded(oracle.margins(lg, 1) < MARGIN)
     assert np.array_equal(idx[ok, 0], oracle.topk(lg, 1)[0][ok, 0])
 
 
@@ -207,7 +207,7 @@ def test_mlp_router_adaptive(qt):
     L["router"]["tau"] = tau
     idx, gate, counts, offsets, perm, inv, xperm = _route_gpu(L, 2)
     idx_ref, gate_ref = oracle.adaptive_topk(lg, tau)
-    excl = near | (oracle.margins(lg, 2) < MARGIN) | (confidence_gap(lg, tau) < CONF_GAP)
+    excl = bound_excluded(near | (oracle.margins(lg, 2) < MARGIN) | (confidence_gap(lg, tau) < CONF_GAP))
     _compare_choice(idx, gate, idx_ref, gate_ref, excl)
     assert 0 < (idx[:, 1] == -1).sum() < 700
     _check_dispatch_and_rows(L, 2, idx, counts, offsets, perm, inv, xperm)
@@ -270,12 +270,12 @@ def test_ffn_forward_ex_small(kind, dt, T, D, H, E, r, q, k, res):
     if kind == "mlp":
         L = synth.with_mlp_router(L, h=max(16, D // 6), seed=3)
         lg, near = _mlp_ref(L, dt)
-        excl = near | (oracle.margins(lg, k) < MARGIN)
+        excl = bound_excluded(near | (oracle.margins(lg, k) < MARGIN))
     else:
         lg = oracle.router_logits(L["x"], L["Wg"], L["bg"])
         tau = float(np.quantile(oracle.confidence(lg), 0.5))
         L = synth.with_adaptive_router(L, tau)
-        excl = (oracle.margins(lg, 2) < MARGIN) | (confidence_gap(lg, tau) < CONF_GAP)
+        excl = bound_excluded((oracle.margins(lg, 2) < MARGIN) | (confidence_gap(lg, tau) < CONF_GAP))
     g = gpu_ffn_ex(L)
     ref = oracle.ffn_forward_layer(L)
     ok = ~excl
@@ -301,7 +301,7 @@ def test_adaptive_layer_isolates_residual():
     L = synth.with_adaptive_router(L, tau)
     g = gpu_ffn_ex(L)
     ref = oracle.ffn_forward_layer(L)
-    ok = (oracle.margins(lg, 2) >= MARGIN) & (confidence_gap(lg, tau) >= CONF_GAP)
+    ok = ~bound_excluded((oracle.margins(lg, 2) < MARGIN) | (confidence_gap(lg, tau) < CONF_GAP))
     assert np.array_equal(g["idx"][ok], ref["idx"][ok])
     assert max_rel(g["y"][ok], ref["y"][ok]) <= F32_MAXREL
 
@@ -322,13 +322,13 @@ def test_router_variants_at_deit_small(kind):
         L = synth.with_mlp_router(L, seed=1)
         lg, near = _mlp_ref(L, "bf16")
         k = 1
-        excl = near | (oracle.margins(lg, 1) < MARGIN)
+        excl = bound_excluded(near | (oracle.margins(lg, 1) < MARGIN))
     else:
         lg = oracle.router_logits(L["x"], L["Wg"], L["bg"])
         tau = float(np.quantile(oracle.confidence(lg), 0.25))
         L = synth.with_adaptive_router(L, tau)
         k = 2
-        excl = (oracle.margins(lg, 2) < MARGIN) | (confidence_gap(lg, tau) < CONF_GAP)
+        excl = bound_excluded((oracle.margins(lg, 2) < MARGIN) | (confidence_gap(lg, tau) < CONF_GAP))
     g = gpu_ffn_ex(L)
     idx_ref, _ = (oracle.topk(lg, 1) if kind == "mlp"
                   else oracle.adaptive_topk(lg, L["router"]["tau"]))

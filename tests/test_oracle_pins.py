@@ -117,6 +117,64 @@ def test_topk_brute_force_with_ties(E, k):
         assert tuple(idx[t]) == _brute_topk(list(logits[t]), k)
 
 
+def test_margins_hand_computed():
+    """The decision margin that decides which tokens a routing comparison may
+    leave out (Algorithm 3's argmax, extended to the top-k order): the
+    smallest gap between neighbours among the sorted top min(k + 1, E)
+    logits.  Values worked by hand, with ties, k = 1..3, E = 1 and E = k."""
+    inf = float("inf")
+    cases = [
+        # logits, k, margin
+        ([3.0, 1.0, 2.0], 1, 1.0),            # 3 | 2: one gap
+        ([3.0, 1.0, 2.0], 2, 1.0),            # 3, 2 | 1: gaps 1, 1
+        ([5.0, 5.0, 0.0], 1, 0.0),            # tie for the top slot
+        ([5.0, 5.0, 0.0], 2, 0.0),            # tie decides the slot order only
+        ([0.0, 5.0, 5.0, 9.0], 1, 4.0),       # tie below the selection boundary
+        ([0.0, 4.0, 4.5, 1.0], 1, 0.5),
+        ([0.0, 4.0, 4.5, 1.0], 2, 0.5),       # gaps 0.5, 3
+        ([0.0, 4.0, 4.5, 1.0], 3, 0.5),       # gaps 0.5, 3, 1
+        ([1.0, 2.0, 4.0, 10.0], 1, 6.0),      # descending order: 10 | 4
+        ([1.0, 2.0, 4.0, 10.0], 2, 2.0),      # 10, 4 | 2: gaps 6, 2
+        ([1.0, 2.0, 4.0, 10.0], 3, 1.0),      # 10, 4, 2 | 1: gaps 6, 2, 1
+        ([-1.0, -3.0, -2.0], 1, 1.0),         # negative logits
+        ([7.0], 1, inf),                      # E = 1: nothing to decide
+        ([1.0, 5.0, 2.0], 3, 1.0),            # E = k: slot-order gaps 3, 1 only
+        ([4.0, 4.0], 2, 0.0),                 # E = k with a tie
+        ([4.0, 3.0], 2, 1.0),
+    ]
+    for lg, k, want in cases:
+        got = oracle.margins(np.array([lg]), k)
+        assert got.shape == (1,) and got[0] == want, (lg, k, got, want)
+    # several tokens at once, one margin per row
+    lg = np.array([[3.0, 1.0, 2.0], [5.0, 5.0, 0.0], [0.0, 0.25, 9.0]])
+    assert oracle.margins(lg, 1).tolist() == [1.0, 0.0, 8.75]
+
+
+@pytest.mark.parametrize("E,k", [(2, 1), (4, 1), (5, 2), (6, 3), (4, 4), (8, 2)])
+def test_margins_bound_the_top_k_decision(E, k):
+    """What the margin means: moving every logit by less than half the margin
+    never changes the ordered top-k (brute force), and some move of just over
+    half the margin does (the two logits at the smallest gap swap)."""
+    rng = np.random.default_rng(100 * E + k)
+    lg = rng.standard_normal((40, E))
+    m = oracle.margins(lg, k)
+    for t in range(lg.shape[0]):
+        base = _brute_topk(list(lg[t]), k)
+        for _ in range(20):
+            d = rng.uniform(-1.0, 1.0, E) * (0.499 * m[t])
+            assert _brute_topk(list(lg[t] + d), k) == base
+        # close the smallest gap among the decided positions
+        order = sorted(range(E), key=lambda e: (-lg[t, e], e))
+        span = min(k, E - 1)
+        gaps = [lg[t, order[j]] - lg[t, order[j + 1]] for j in range(span)]
+        j = int(np.argmin(gaps))
+        assert gaps[j] == m[t]
+        d = np.zeros(E)
+        d[order[j]] -= 0.51 * m[t]
+        d[order[j + 1]] += 0.51 * m[t]
+        assert _brute_topk(list(lg[t] + d), k) != base
+
+
 def test_gates_closed_forms():
     lg = np.array([[0.5, 2.0, -1.0, 2.0], [3.0, 1.0, 0.0, -4.0], [1.0, 1.0, 1.0, 1.0]])
     idx, g1 = oracle.topk(lg, 1)
