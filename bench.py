@@ -2,19 +2,25 @@
 """Benchmark of the CLEAR-MoE FFN forward on one MI355X.
 
 A step is one clearmoe_ffn_forward call (router, dispatch, fc1 + GELU, shared
-SVD basis, grouped residual experts, combine) over the DeiT-Small-shaped layer:
-T = 64 x 197 = 12608 tokens, D = 384, H = 1536, E = 8, top-1, r = 128, q = 32,
-bf16 storage with float32 accumulation, synthetic seeded inputs already in HBM.
+SVD basis, grouped residual experts, combine) over the DeiT-Base-shaped layer,
+the largest configuration: T = 256 x 197 = 50432 tokens, D = 768, H = 3072,
+E = 8, top-2 with renormalised gates, r = 256, q = 64, bf16 storage with
+float32 accumulation, synthetic seeded inputs already in HBM.
 
 Prints one JSON line.  Besides the contract fields it carries
-  roofline     the dominant kernel's algorithmic rate (HIP events recorded on
-               its stream around every launch in the timed region) against its
-               MI355X peak, plus measured HBM traffic when counters exist for
-               the current kernel source;
-  cpu_baseline the CPU oracle on a bounded sample of the same workload;
+  roofline     the dominant kernel's algorithmic rate (HIP events written by
+               the kernel's own dispatch, on its stream, for every launch of
+               it in the timed region, at least 20) against its MI355X peak,
+               plus measured HBM traffic when counters exist for the current
+               kernel source;
+  cpu_baseline the CPU oracle on a bounded sample of the same workload, on all
+               host threads and on one (the analogue of the paper's serial
+               CPU row), with the CPU model;
   stages       per-kernel times of one step;
   cold         the step with the 256 MB last-level cache flushed before it;
   dense        the dense fc1 + GELU + fc2 comparator through the same kernels;
+  deit_small   the DeiT-Small-shaped top-1 layer (12608 tokens, D = 384), the
+               fused kernel, with its own roofline and dense comparator;
   dispatch     the routing/dispatch-only workload (2^20 tokens, D = 384, E = 8,
                top-2, Zipf-skewed bias): route -> dispatch (+ rows) -> combine,
                with its HBM fraction;
@@ -22,13 +28,9 @@ Prints one JSON line.  Besides the contract fields it carries
                against padded batches (clearmoe_ffn_forward_padded) at 0, 40,
                60 and 80 % load imbalance, E = 4, DeiT-Small widths, top-1 and
                top-2, 1568 and 12608 tokens;
-  routers      the same layer with the linear, MLP and adaptive routers
+  routers      the DeiT-Small layer with the linear, MLP and adaptive routers
                (clearmoe_ffn_forward_ex);
-  deit_base    the DeiT-Base-shaped top-2 layer (50432 tokens, D = 768) through
-               the GEMM chain, with each product's rate against the bf16 peak;
   deit_tiny    the DeiT-Tiny-shaped fp32 layer (1576 tokens, D = 192);
-  small_batch  the DeiT-Small layer at 1 and 8 images (197 and 1576 tokens),
-               where the fused kernel splits each tile's hidden units;
   expert_sweep the DeiT-Small shape for E = 2, 4, 6, 8 beside the dense FFN;
   ffn_stack    the FFN part of a 12-block DeiT-Small forward with 6 CLEAR-MoE
                layers (class tokens on the dense path) against 12 dense ones.
@@ -47,7 +49,8 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 MFMA_PEAK_TFLOPS = {"bf16": 2500.0, "f32": 157.3}
 PROFILE_DIR = os.path.join(ROOT, "profiles")
-TIME_EVERY = 8
+TIME_EVERY = 8          # sampling of the dominant kernel's timed launches in short steps
+MIN_TIMED = 20          # timed launches of the dominant kernel, at least
 # stages whose kernels are matrix products (the router's flops are not its bound)
 MFMA_STAGES = ("fc1_gelu", "basis_t", "basis_h", "res_u", "res_h", "tu_grouped", "y_grouped",
                "dense_fc2", "fused_top1")
@@ -63,7 +66,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
                     help="only the timed steps (for profiler runs)")
-    ap.add_argument("--workload", default="C2", choices=["C1", "C2", "C3"])
+    ap.add_argument("--workload", default="C3", choices=["C1", "C2", "C3"])
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for counter runs: one 1 GiB device copy from a cache-cold source "
                          "(known bytes, to scale the counters), then the timed steps only")
@@ -158,81 +161,18 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     cfg = synth.CONFIGS[args.workload]
-    b = 4 if cfg.dtype == "f32" else 2
     L = synth.make_layer(cfg)
-    d = {n: cm.from_stored(L[n]) for n in ("x", "W1", "b1", "US", "Vt", "b2", "P", "Q", "Wg", "bg")}
-    shape = cm.make_shape(cfg.T, cfg.D, cfg.E, cfg.k, cm.F32 if cfg.dtype == "f32" else cm.BF16,
-                          H=cfg.H, r=cfg.r, q=cfg.q)
-    ws = cm.alloc_workspace(shape)
-    y = torch.empty((cfg.T, cfg.D), dtype=d["x"].dtype, device=dev)
-    stream = torch.cuda.current_stream()
-
-    def step():
-        cm.ffn_forward(d["x"], d["W1"], d["b1"], d["US"], d["Vt"], d["b2"], d["P"], d["Q"],
-                       d["Wg"], d["bg"], cfg.k, ws=ws, out=y)
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    if args.traffic_probe:
-        src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        flush.fill_(2)                  # evicts src from the 256 MB last-level cache
-        torch.cuda.synchronize()
-        dst.copy_(src)                  # reads and writes exactly 1 GiB
-        torch.cuda.synchronize()
-        del src, dst, flush
-        for _ in range(args.steps):
-            step()
-        torch.cuda.synchronize()
-        print(json.dumps({"traffic_probe": True, "steps": args.steps}), flush=True)
+    core = measure_layer(cm, torch, cfg, L, args.steps, args.warmup, args.traffic_probe)
+    if core is None:            # traffic probe run: nothing to report
         return
-
-    # Per-stage times of a few steps (all stages timed) to find the dominant kernel.
-    names = cm.stage_names()
-    cm.timing_start(names, 64 * len(names))
-    for _ in range(20):
-        step()
-    per = cm.timing_stop()
-    stages = {s: ms / n for s, (ms, n) in per.items()}
-    dominant = max(stages, key=stages.get)
-
-    # Timed region: exactly K steps.  One launch of the dominant kernel in
-    # TIME_EVERY is dispatched with start/end events (a timed dispatch costs
-    # the step a few microseconds, so timing all of them would slow the step).
-    cm.timing_start([dominant], args.steps, every=TIME_EVERY)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    ev0.record(stream)
-    for _ in range(args.steps):
-        step()
-    ev1.record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    dom_ms, dom_n = cm.timing_stop()[dominant]
-    ms_step = ev0.elapsed_time(ev1) / args.steps
-    value = cfg.T / (ms_step * 1e-3)
-
-    flops, byts = stage_work(dominant, cfg, b)
-    dom_avg_s = dom_ms / dom_n * 1e-3
-    digest = source_digest(dominant)
-    if flops > 0:
-        roof = dict(bound="mfma", achieved=flops / dom_avg_s / 1e12,
-                    peak=MFMA_PEAK_TFLOPS[cfg.dtype], unit="TFLOP/s")
-    else:
-        roof = dict(bound="hbm", achieved=byts / dom_avg_s / 1e9, peak=HBM_PEAK_GBS, unit="GB/s")
-    roof["frac"] = roof["achieved"] / roof["peak"]
-    roof["traffic"] = load_traffic(dominant, args.workload, digest)
-    roof["kernel"] = dominant
-    roof["avg_launch_us"] = dom_avg_s * 1e6
-    roof["timed_launches"] = dom_n
-    roof["algorithmic_per_launch"] = flops if flops > 0 else byts
+    step, d, ws, y, stream = core.pop("_step"), core.pop("_d"), core.pop("_ws"), core.pop("_y"), \
+        core.pop("_stream")
+    b = 4 if cfg.dtype == "f32" else 2
+    ms_step = core["ms_per_step"]
 
     out = {
         "metric": "tokens/sec per CLEAR-MoE FFN layer + % HBM peak (dispatch) / % MFMA peak (GEMM)",
-        "value": value,
+        "value": core["value"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -245,64 +185,37 @@ def main():
         "data": "synthetic (seeded Gaussian-cluster tokens, N(0,0.02) weights, SVD-extracted basis)",
         "config": {"workload": cfg.name, "tokens": cfg.T, "D": cfg.D, "H": cfg.H, "E": cfg.E,
                    "k": cfg.k, "r": cfg.r, "q": cfg.q, "seed": cfg.seed},
-        "roofline": roof,
-        "layer_tflops": layer_flops(cfg) / (ms_step * 1e-3) / 1e12,
-        "stages_us": {s: v * 1e3 for s, v in sorted(stages.items(), key=lambda kv: -kv[1])},
-        "wall_s": wall,
+        "roofline": core["roofline"],
+        "layer_tflops": core["layer_tflops"],
+        "stages_us": core["stages_us"],
+        "wall_s": core["wall_s"],
         "source_digest": source_digest(),
     }
 
     if not args.no_extras:
-        # Cold: flush the 256 MB last-level cache (512 MiB write) before each step.
-        flush = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
-        times = []
-        for _ in range(30):
-            flush.fill_(1)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            step()
-            e1.record(stream)
-            torch.cuda.synchronize()
-            times.append(e0.elapsed_time(e1))
-        del flush
-        cold = float(np.median(times))
-        out["cold"] = {"ms_per_step": cold, "tokens_per_s": cfg.T / (cold * 1e-3)}
-
-        # Dense comparator through the same GEMM kernels.
-        W2 = cm.from_stored(L["W2"].astype(np.float32) if cfg.dtype == "f32"
-                            else synth.to_bf16_bits(L["W2"]))
-        yd = torch.empty_like(y)
-
-        def dense():
-            cm.dense_ffn_forward(d["x"], d["W1"], d["b1"], W2, d["b2"], ws=ws, out=yd)
-
-        for _ in range(args.warmup):
-            dense()
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(args.steps):
-            dense()
-        e1.record(stream)
-        torch.cuda.synchronize()
-        dms = e0.elapsed_time(e1) / args.steps
-        out["dense"] = {"ms_per_step": dms, "tokens_per_s": cfg.T / (dms * 1e-3),
-                        "moe_over_dense_time": ms_step / dms,
-                        "tflops": 4 * cfg.T * cfg.D * cfg.H / (dms * 1e-3) / 1e12}
-        del W2, yd
+        out["cold"] = time_cold(torch, np, step, stream, cfg)
+        out["dense"] = time_dense(cm, synth, torch, np, cfg, L, d, ws, stream, args.steps,
+                                  args.warmup, ms_step)
+        out["products"] = bench_layer(cm, synth, torch, np, stream, None, 20, cfg=cfg, L=L,
+                                      d=d, ws=ws)["stages"]
+        del d, ws, y, step
+        # the DeiT-Small top-1 layer (fused kernel) with its own roofline
+        c2 = synth.CONFIGS["C2"]
+        L2 = synth.make_layer(c2)
+        small = measure_layer(cm, torch, c2, L2, max(args.steps, 100), args.warmup)
+        step2, d2, ws2, _y2, _ = (small.pop(k) for k in ("_step", "_d", "_ws", "_y", "_stream"))
+        small["workload"] = f"{c2.name} (T={c2.T} D={c2.D} H={c2.H} E={c2.E} k={c2.k} r={c2.r} q={c2.q} bf16)"
+        small["cold"] = time_cold(torch, np, step2, stream, c2)
+        small["dense"] = time_dense(cm, synth, torch, np, c2, L2, d2, ws2, stream,
+                                    max(args.steps, 100), args.warmup, small["ms_per_step"])
+        out["deit_small"] = small
+        del d2, ws2, _y2, step2
         out["dispatch"] = bench_dispatch(cm, synth, torch, np, stream, max(10, args.steps // 10))
         out["imbalance"] = bench_imbalance(cm, synth, torch, np, stream, max(20, args.steps // 5))
-        out["routers"] = bench_routers(cm, synth, torch, np, stream, L, max(20, args.steps // 5))
-        out["ffn_stack"] = bench_stack(cm, synth, torch, np, stream, L, max(20, args.steps // 10))
-        out["deit_base"] = bench_layer(cm, synth, torch, np, stream, "C3", 20)
+        out["routers"] = bench_routers(cm, synth, torch, np, stream, L2, max(20, args.steps // 5))
+        out["ffn_stack"] = bench_stack(cm, synth, torch, np, stream, L2, max(20, args.steps // 10))
         out["deit_tiny"] = bench_layer(cm, synth, torch, np, stream, "C1", 100)
-        small = {}
-        for n_img in (1, 8):
-            c = dataclasses.replace(synth.CONFIGS["C2"], name=f"C2-widths-{n_img}-images",
-                                    T=197 * n_img)
-            small[f"images{n_img}"] = bench_layer(cm, synth, torch, np, stream, None, 200, cfg=c)
-        out["small_batch"] = small
-        dense_ms = out["dense"]["ms_per_step"]
+        dense_ms = small["dense"]["ms_per_step"]
         sweep = {}
         for e in (2, 4, 6, 8):
             r = bench_layer(cm, synth, torch, np, stream, f"C5-E{e}", 100)
@@ -311,12 +224,139 @@ def main():
                               "stages_us": {k: v["us"] for k, v in r["stages"].items()}}
         out["expert_sweep"] = {"workload": "DeiT-Small shape (12608 tokens, D = 384, H = 1536, r = 128, "
                                            "q = 32, bf16, top-1) for E in {2, 4, 6, 8}, uniform "
-                                           "clusters, seed 4; dense = the dense comparator above",
+                                           "clusters, seed 4; dense = the DeiT-Small dense comparator",
                                "points": sweep}
 
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(L, cfg, args.cpu_seconds)
     print(json.dumps(out), flush=True)
+
+
+def time_cold(torch, np, step, stream, cfg):
+    """The step with the 256 MB last-level cache flushed (512 MiB written)
+    before each of 30 timed calls; median."""
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    times = []
+    for _ in range(30):
+        flush.fill_(1)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        step()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        times.append(e0.elapsed_time(e1))
+    del flush
+    cold = float(np.median(times))
+    return {"ms_per_step": cold, "tokens_per_s": cfg.T / (cold * 1e-3)}
+
+
+def time_dense(cm, synth, torch, np, cfg, L, d, ws, stream, steps, warmup, moe_ms):
+    """The dense FFN of the same shape, GELU(x W1^T + b1) W2^T + b2 with the
+    layer's pre-extraction fc2, through the same GEMM kernels."""
+    W2 = cm.from_stored(L["W2"].astype(np.float32) if cfg.dtype == "f32"
+                        else synth.to_bf16_bits(L["W2"]))
+    yd = torch.empty_like(d["x"])
+
+    def dense():
+        cm.dense_ffn_forward(d["x"], d["W1"], d["b1"], W2, d["b2"], ws=ws, out=yd)
+
+    for _ in range(warmup):
+        dense()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(steps):
+        dense()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    dms = e0.elapsed_time(e1) / steps
+    return {"ms_per_step": dms, "tokens_per_s": cfg.T / (dms * 1e-3),
+            "moe_over_dense_time": moe_ms / dms,
+            "tflops": 4 * cfg.T * cfg.D * cfg.H / (dms * 1e-3) / 1e12}
+
+
+def measure_layer(cm, torch, cfg, L, steps, warmup, traffic_probe=False):
+    """Warm up, find the dominant kernel from a per-stage pass, then time
+    exactly `steps` layer calls between two events on the stream, with the
+    dominant kernel's own dispatch writing start/end events for at least
+    MIN_TIMED of its launches (every launch when the step is long, one in
+    TIME_EVERY when a timed dispatch would be a visible share of the step;
+    with too few steps for that, every launch)."""
+    dev = torch.device("cuda:0")
+    b = 4 if cfg.dtype == "f32" else 2
+    d = {n: cm.from_stored(L[n]) for n in ("x", "W1", "b1", "US", "Vt", "b2", "P", "Q", "Wg", "bg")}
+    shape = cm.make_shape(cfg.T, cfg.D, cfg.E, cfg.k, cm.F32 if cfg.dtype == "f32" else cm.BF16,
+                          H=cfg.H, r=cfg.r, q=cfg.q)
+    ws = cm.alloc_workspace(shape)
+    y = torch.empty((cfg.T, cfg.D), dtype=d["x"].dtype, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        cm.ffn_forward(d["x"], d["W1"], d["b1"], d["US"], d["Vt"], d["b2"], d["P"], d["Q"],
+                       d["Wg"], d["bg"], cfg.k, ws=ws, out=y)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    if traffic_probe:
+        src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+        dst = torch.empty_like(src)
+        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        flush.fill_(2)                  # evicts src from the 256 MB last-level cache
+        torch.cuda.synchronize()
+        dst.copy_(src)                  # reads and writes exactly 1 GiB
+        torch.cuda.synchronize()
+        del src, dst, flush
+        for _ in range(steps):
+            step()
+        torch.cuda.synchronize()
+        print(json.dumps({"traffic_probe": True, "workload": cfg.name, "steps": steps}), flush=True)
+        return None
+
+    # Per-stage times of a few steps (all stages timed) to find the dominant kernel.
+    names = cm.stage_names()
+    cm.timing_start(names, 64 * len(names))
+    for _ in range(20):
+        step()
+    per = cm.timing_stop()
+    stages = {s_: ms / n for s_, (ms, n) in per.items()}
+    dominant = max(stages, key=stages.get)
+    # a timed dispatch costs a few microseconds: sample one launch in
+    # TIME_EVERY only when the step is short and the steps are many
+    every = TIME_EVERY if sum(stages.values()) < 0.25 else 1
+    every = max(1, min(every, steps // MIN_TIMED))
+
+    cm.timing_start([dominant], max(steps, 1), every=every)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev0.record(stream)
+    for _ in range(steps):
+        step()
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    dom_ms, dom_n = cm.timing_stop()[dominant]
+    ms_step = ev0.elapsed_time(ev1) / steps
+
+    flops, byts = stage_work(dominant, cfg, b)
+    dom_avg_s = dom_ms / dom_n * 1e-3
+    digest = source_digest(dominant)
+    if flops > 0:
+        roof = dict(bound="mfma", achieved=flops / dom_avg_s / 1e12,
+                    peak=MFMA_PEAK_TFLOPS[cfg.dtype], unit="TFLOP/s")
+    else:
+        roof = dict(bound="hbm", achieved=byts / dom_avg_s / 1e9, peak=HBM_PEAK_GBS, unit="GB/s")
+    roof["frac"] = roof["achieved"] / roof["peak"]
+    roof["traffic"] = load_traffic(dominant, cfg.name.split("-")[0], digest)
+    roof["kernel"] = dominant
+    roof["avg_launch_us"] = dom_avg_s * 1e6
+    roof["timed_launches"] = dom_n
+    roof["algorithmic_per_launch"] = flops if flops > 0 else byts
+    return {"value": cfg.T / (ms_step * 1e-3), "ms_per_step": ms_step, "roofline": roof,
+            "layer_tflops": layer_flops(cfg) / (ms_step * 1e-3) / 1e12,
+            "stages_us": {s_: v * 1e3 for s_, v in sorted(stages.items(), key=lambda kv: -kv[1])},
+            "wall_s": wall, "_step": step, "_d": d, "_ws": ws, "_y": y, "_stream": stream}
 
 
 def bench_dispatch(cm, synth, torch, np, stream, steps):
@@ -498,16 +538,20 @@ def bench_routers(cm, synth, torch, np, stream, L, steps):
     return out
 
 
-def bench_layer(cm, synth, torch, np, stream, workload, steps, cfg=None):
+def bench_layer(cm, synth, torch, np, stream, workload, steps, cfg=None, L=None, d=None,
+                ws=None):
     """One layer of another configuration (a named workload, or cfg): step
     time from an untimed pass, then every stage timed in a second pass; MFMA
-    rate of each product."""
+    rate of each product.  L, d and ws may be passed in when they exist."""
     cfg = cfg if cfg is not None else synth.CONFIGS[workload]
-    L = synth.make_layer(cfg)
-    d = {n: cm.from_stored(L[n]) for n in ("x", "W1", "b1", "US", "Vt", "b2", "P", "Q", "Wg", "bg")}
-    shape = cm.make_shape(cfg.T, cfg.D, cfg.E, cfg.k, cm.F32 if cfg.dtype == "f32" else cm.BF16,
-                          H=cfg.H, r=cfg.r, q=cfg.q)
-    ws = cm.alloc_workspace(shape)
+    if d is None:
+        L = synth.make_layer(cfg) if L is None else L
+        d = {n: cm.from_stored(L[n])
+             for n in ("x", "W1", "b1", "US", "Vt", "b2", "P", "Q", "Wg", "bg")}
+    if ws is None:
+        shape = cm.make_shape(cfg.T, cfg.D, cfg.E, cfg.k,
+                              cm.F32 if cfg.dtype == "f32" else cm.BF16, H=cfg.H, r=cfg.r, q=cfg.q)
+        ws = cm.alloc_workspace(shape)
     y = torch.empty_like(d["x"])
 
     def step():
@@ -594,18 +638,24 @@ def bench_stack(cm, synth, torch, np, stream, L, steps):
             "moe_over_dense_time": mixed / all_dense, "steps": steps}
 
 
-def cpu_baseline(L, cfg, min_seconds):
-    """The CPU oracle, as it stands, on whole passes over the same workload's
-    tokens (row blocks of 4096 tokens) until at least min_seconds have run."""
-    import numpy as np
+def cpu_model():
+    """The host CPU's model name and the threads this process may use."""
+    name = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    name = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return name, len(os.sched_getaffinity(0))
 
-    import oracle
 
-    oracle.lib()
-    threads = oracle.num_threads()
-    blk = 4096
-    done, t_used = 0, 0.0
-    start = 0
+def _oracle_rate(oracle, np, L, cfg, blk, min_seconds):
+    """Tokens per second of the oracle's layer on consecutive row blocks of
+    the workload until at least min_seconds of CPU work have run."""
+    done, t_used, start = 0, 0.0, 0
     while t_used < min_seconds:
         rows = np.arange(start, min(cfg.T, start + blk))
         t0 = time.perf_counter()
@@ -613,9 +663,31 @@ def cpu_baseline(L, cfg, min_seconds):
         t_used += time.perf_counter() - t0
         done += rows.size
         start = (start + blk) % cfg.T
+    return done, t_used
+
+
+def cpu_baseline(L, cfg, min_seconds):
+    """The CPU oracle, as it stands, on the same workload's tokens: on every
+    host thread the process may use (OpenMP over tokens) for at least
+    min_seconds, and on one thread (the analogue of the paper's serial CPU
+    row) for at least half that."""
+    import numpy as np
+
+    import oracle
+
+    oracle.lib()
+    model, visible = cpu_model()
+    threads = oracle.num_threads()          # OpenMP's own count (OMP_NUM_THREADS where set)
+    done, t_used = _oracle_rate(oracle, np, L, cfg, 2048, min_seconds)
+    oracle.set_num_threads(1)
+    done1, t1 = _oracle_rate(oracle, np, L, cfg, 128, 0.5 * min_seconds)
+    oracle.set_num_threads(threads)
     return {"value": done / t_used, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"{done} tokens of {cfg.name} in blocks of {blk}, {t_used:.1f} s, fp64 "
-                      f"plain loops, OpenMP over tokens"}
+            "cpu_model": model, "host_threads_visible": visible,
+            "sample": f"{done} tokens of {cfg.name} in blocks of 2048, {t_used:.1f} s, fp64 "
+                      f"plain loops, OpenMP over tokens on {threads} threads",
+            "serial": {"value": done1 / t1, "unit": "tokens/s", "cores": 1,
+                       "sample": f"{done1} tokens in blocks of 128, {t1:.1f} s, one thread"}}
 
 
 if __name__ == "__main__":

@@ -10,8 +10,14 @@
  *     y     = h_sh + h_res
  *
  * Conventions shared by every entry point
- *   - Every tensor pointer is a DEVICE pointer owned by the caller; the
- *     library never allocates, frees or keeps a pointer after a call returns.
+ *   - Every tensor pointer is a DEVICE pointer owned by the caller, and the
+ *     library keeps none after a call returns.  No entry point allocates
+ *     device memory; scratch comes from the caller's workspace.  Host-side
+ *     resources that an entry point creates on first use and keeps until
+ *     the process ends: clearmoe_ffn_forward_padded, a pinned 256-byte host
+ *     buffer per calling thread (and an event per call, destroyed before it
+ *     returns); clearmoe_ffn_forward_ex with class tokens, a side stream and
+ *     two events per device; the stage timer, the events it is started with.
  *   - Matrices are row-major and contiguous.  Weights are stored [out, in]
  *     (the nn.Linear convention), so every product is A[M,K] B[N,K]^T.
  *   - x, W1, US, Vt, P, Q, Wg, ye and y have element type shape->dtype
@@ -65,6 +71,10 @@ typedef struct {
 
 /* Library version, (major << 16) | minor. */
 int clearmoe_version(void);
+
+/* First 16 hex digits of the SHA-256 of the sources the library was built
+ * from (static string, never NULL): lets a caller refuse a stale binary. */
+const char* clearmoe_source_digest(void);
 
 /* Human-readable name of a status code (static string, never NULL). */
 const char* clearmoe_status_string(int status);

@@ -25,7 +25,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libclearmoe.so")
 F32, BF16 = 0, 1
 DISPATCH_HIST_IN_WS = 1
-SYMBOLS = ("clearmoe_version", "clearmoe_status_string", "clearmoe_workspace_bytes",
+SYMBOLS = ("clearmoe_version", "clearmoe_source_digest", "clearmoe_status_string", "clearmoe_workspace_bytes",
            "clearmoe_route", "clearmoe_dispatch", "clearmoe_combine", "clearmoe_ffn_forward",
            "clearmoe_dense_ffn_forward", "clearmoe_stage_name", "clearmoe_timing_start",
            "clearmoe_timing_start_sampled", "clearmoe_timing_stop", "clearmoe_padded_workspace_bytes",
@@ -54,16 +54,26 @@ _lib = None
 
 
 def lib():
-    """Load the in-tree library (building it first only if it does not exist)."""
+    """Load the in-tree library.  It is built first when it is missing or was
+    built from other sources than the ones in the tree (the library carries
+    the digest of its sources)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(LIB_PATH):
-            from . import build as _build
+        from . import build as _build
+        want = _build.source_digest()
+        have = _build.built_digest(LIB_PATH)
+        if have != want:
+            import sys
+            print(f"clearmoe: library {'missing' if not have else 'stale (' + have + ')'}, "
+                  f"building for sources {want}", file=sys.stderr)
             _build.build()
+            if _build.built_digest(LIB_PATH) != want:
+                raise ClearMoEError("the rebuilt library does not carry the source digest")
         L = ctypes.CDLL(LIB_PATH)
         vp, sz, u32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_uint
         sp = ctypes.POINTER(Shape)
         L.clearmoe_version.restype = ctypes.c_int
+        L.clearmoe_source_digest.restype = ctypes.c_char_p
         L.clearmoe_status_string.restype = ctypes.c_char_p
         L.clearmoe_status_string.argtypes = [ctypes.c_int]
         L.clearmoe_workspace_bytes.restype = sz

@@ -336,9 +336,20 @@ int side_stream(SideStream** out) {
 
 }  // namespace
 
+#ifndef CLEARMOE_SOURCE_DIGEST
+#define CLEARMOE_SOURCE_DIGEST "0000000000000000"
+#endif
+// The digest of the sources this library was built from, after a marker that
+// the build scripts find in the file without loading it.
+__attribute__((used)) const char g_source_digest[] = "CLEARMOE-SOURCE-DIGEST=" CLEARMOE_SOURCE_DIGEST;
+
 extern "C" {
 
-int clearmoe_version(void) { return (0 << 16) | 2; }
+int clearmoe_version(void) { return (0 << 16) | 3; }
+
+const char* clearmoe_source_digest(void) {
+    return g_source_digest + sizeof("CLEARMOE-SOURCE-DIGEST=") - 1;
+}
 
 const char* clearmoe_status_string(int status) {
     switch (status) {

@@ -5,7 +5,8 @@
 // With k = 1 every row p of the expert order is one token, and the layer is
 //     z      = GELU(x W1^T + b1)                        shared fc1 (Eq. 2)
 //     [t|u]  = z [Vt ; Q_e]^T, the u columns times the gate
-//     y      = [t|u] [US | P_e]^T + b2                  shared basis + residual (Eq. 3-4)
+//     y      = [t|u] [US | P_e]^T + b2                  shared basis + residual (Eq. 2,
+//                                                        Algorithm 3)
 // A workgroup owns up to 64 consecutive rows of one expert's segment and the
 // whole hidden width, so neither z nor [t|u] ever goes to HBM:
 //   * the 64 gathered x rows are copied to LDS once and stay there;

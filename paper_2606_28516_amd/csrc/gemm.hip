@@ -306,14 +306,19 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, i
                                      acc[i][j][4 * q + 3]};
                     __builtin_amdgcn_raw_buffer_store_b128(v, rp, off(kp, i, j, q), 0, kDevScope);
                 }
+        // release: every wave's partial stores have completed (vmcnt) and the
+        // barrier orders them before thread 0's agent-scope release add; the
+        // part that sees the count complete acquires at agent scope before
+        // any wave reads the partials
         wait_vmcnt<0>();
         __syncthreads();
         __shared__ int s_last;
         if (tid == 0)
-            s_last = __hip_atomic_fetch_add(g.ks_count + tile, 1, __ATOMIC_RELAXED,
+            s_last = __hip_atomic_fetch_add(g.ks_count + tile, 1, __ATOMIC_ACQ_REL,
                                             __HIP_MEMORY_SCOPE_AGENT) == S - 1;
         __syncthreads();
         if (!s_last) return;
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll

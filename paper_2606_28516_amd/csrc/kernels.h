@@ -258,7 +258,7 @@ hipError_t launch_gemm(int dtype, const GemmDesc& g, hipStream_t st);
 // router's tile histogram and idx, from which each workgroup finds its rows'
 // tokens itself (histograms of at most kInlineScanMax entries).  Shapes
 // outside fused_top1_supported use the GEMM path.
-constexpr int kFusedMaxD = 768;      // x rows of a 64-row tile live in LDS ...
+constexpr int kFusedMaxD = 384;      // six 64-wide input groups; x rows of a 64-row tile live in LDS ...
 constexpr int kFusedMaxH = 8192;     // ... beside b1
 constexpr int kFusedMaxRQ = 160;     // [t|u] accumulators live in registers
 bool fused_top1_supported(int D, int H, int r, int q);

@@ -34,8 +34,11 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_version_and_status_strings():
-    assert cm.version() == 2
+    assert cm.version() == 3
     L = cm.lib()
+    # the library carries the digest of the sources in the tree
+    from paper_2606_28516_amd import build as hb
+    assert L.clearmoe_source_digest().decode() == hb.source_digest() == hb.built_digest()
     assert L.clearmoe_status_string(0) == b"ok"
     assert L.clearmoe_status_string(3).startswith(b"workspace")
     assert L.clearmoe_status_string(99) == b"unknown status"
