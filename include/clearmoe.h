@@ -52,7 +52,9 @@ typedef enum {
     CLEARMOE_ERR_INVALID_ARG = 1,   /* bad shape, NULL or misaligned pointer */
     CLEARMOE_ERR_UNSUPPORTED = 2,   /* valid but not handled (e.g. dtype) */
     CLEARMOE_ERR_WORKSPACE = 3,     /* ws NULL or smaller than required */
-    CLEARMOE_ERR_HIP = 4            /* a kernel launch failed */
+    CLEARMOE_ERR_HIP = 4,           /* a kernel launch failed */
+    CLEARMOE_ERR_TOO_LARGE = 5      /* clearmoe_ffn_forward_noalloc: the shape
+                                       needs more than its fixed scratch */
 } clearmoe_status;
 
 typedef enum { CLEARMOE_F32 = 0, CLEARMOE_BF16 = 1 } clearmoe_dtype;
@@ -198,6 +200,31 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
                          const void* P, const void* Q, const void* Wg, const float* bg, void* y,
                          int32_t* idx_out, float* gate_out, void* ws, size_t ws_bytes,
                          hipStream_t stream);
+
+/* Scratch held by the library for clearmoe_ffn_forward_noalloc, per device. */
+#define CLEARMOE_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* clearmoe_ffn_forward without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments (minus ws / ws_bytes),
+ * kernels and results as clearmoe_ffn_forward; it calls no hipMalloc, hipFree
+ * or allocating routine.  Scratch comes from one fixed device array of
+ * CLEARMOE_NOALLOC_SCRATCH_BYTES (64 MiB) that the library holds on each
+ * device it runs on until the process ends; its address is looked up once per
+ * device, on the first call with that device current.  Only the regions the
+ * layer's path touches are placed there, packed: every top-1 bfloat16 layer
+ * the fused kernel takes needs well under 1 MiB plus its small-batch split
+ * partials; the GEMM chains also hold z [T, H] and the low-rank
+ * intermediates.  A shape that needs more than the array returns
+ * CLEARMOE_ERR_TOO_LARGE before anything is launched.  Every call on a device
+ * shares that device's array and leaves its contents behind (the counters it
+ * needs are cleared by the call's own fill kernels): calls that overlap in
+ * time on one device -- on different streams or threads -- race and must
+ * not be issued. */
+int clearmoe_ffn_forward_noalloc(const clearmoe_shape* shape, const void* x, const void* W1,
+                                 const float* b1, const void* US, const void* Vt, const float* b2,
+                                 const void* P, const void* Q, const void* Wg, const float* bg,
+                                 void* y, int32_t* idx_out, float* gate_out, hipStream_t stream);
 
 /* The whole layer with any router (see clearmoe_router and
  * clearmoe_route_ex); the other arguments, layouts, results and workspace are

@@ -18,7 +18,7 @@ __all__ = ["ClearMoEError", "Shape", "lib", "version", "workspace_bytes", "alloc
            "route", "dispatch", "combine", "ffn_forward", "from_stored", "to_stored",
            "DISPATCH_HIST_IN_WS", "F32", "BF16", "SYMBOLS", "N_STAGES", "stage_names",
            "timing_start", "timing_stop", "make_shape", "dense_ffn_forward",
-           "padded_workspace_bytes", "ffn_forward_padded", "Router", "make_router", "route_ex",
+           "padded_workspace_bytes", "ffn_forward_padded", "ffn_forward_noalloc", "Router", "make_router", "route_ex",
            "ffn_forward_ex"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -29,7 +29,10 @@ SYMBOLS = ("clearmoe_version", "clearmoe_source_digest", "clearmoe_status_string
            "clearmoe_route", "clearmoe_dispatch", "clearmoe_combine", "clearmoe_ffn_forward",
            "clearmoe_dense_ffn_forward", "clearmoe_stage_name", "clearmoe_timing_start",
            "clearmoe_timing_start_sampled", "clearmoe_timing_stop", "clearmoe_padded_workspace_bytes",
-           "clearmoe_ffn_forward_padded", "clearmoe_route_ex", "clearmoe_ffn_forward_ex")
+           "clearmoe_ffn_forward_padded", "clearmoe_route_ex", "clearmoe_ffn_forward_ex",
+           "clearmoe_ffn_forward_noalloc")
+NOALLOC_SCRATCH_BYTES = 64 << 20
+ERR_TOO_LARGE = 5
 N_STAGES = 16
 
 
@@ -95,6 +98,8 @@ def lib():
         L.clearmoe_padded_workspace_bytes.argtypes = [sp]
         L.clearmoe_ffn_forward_padded.restype = ctypes.c_int
         L.clearmoe_ffn_forward_padded.argtypes = [sp] + [vp] * 13 + [vp, sz, vp]
+        L.clearmoe_ffn_forward_noalloc.restype = ctypes.c_int
+        L.clearmoe_ffn_forward_noalloc.argtypes = [sp] + [vp] * 13 + [vp]
         L.clearmoe_dense_ffn_forward.restype = ctypes.c_int
         L.clearmoe_dense_ffn_forward.argtypes = [sp] + [vp] * 6 + [vp, sz, vp]
         L.clearmoe_stage_name.restype = ctypes.c_char_p
@@ -261,6 +266,24 @@ def ffn_forward(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int, ws: Optional[torch.
     """clearmoe_ffn_forward: the whole layer.  Returns y [T, D]."""
     return _layer_call("clearmoe_ffn_forward", workspace_bytes, x, W1, b1, US, Vt, b2, P, Q, Wg,
                        bg, k, ws, out, idx_out, gate_out, stream)
+
+
+def ffn_forward_noalloc(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int,
+                        out: Optional[torch.Tensor] = None, idx_out=None, gate_out=None,
+                        stream=None):
+    """clearmoe_ffn_forward_noalloc: the whole layer with the library's own
+    fixed scratch (no workspace).  Returns y [T, D]."""
+    T, D = x.shape
+    H = W1.shape[0]
+    r = US.shape[1]
+    E, _, q = P.shape
+    s = make_shape(T, D, E, k, _dt(x), H=H, r=r, q=q)
+    y = torch.empty((T, D), dtype=x.dtype, device=x.device) if out is None else out
+    rc = lib().clearmoe_ffn_forward_noalloc(ctypes.byref(s), _p(x), _p(W1), _p(b1), _p(US), _p(Vt),
+                                            _p(b2), _p(P), _p(Q), _p(Wg), _p(bg), _p(y),
+                                            _p(idx_out), _p(gate_out), _stream(stream))
+    _check(rc, "clearmoe_ffn_forward_noalloc")
+    return y
 
 
 def ffn_forward_padded(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int,

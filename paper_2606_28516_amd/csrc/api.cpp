@@ -94,6 +94,58 @@ Layout layout(const clearmoe_shape& s) {
     return L;
 }
 
+// The regions clearmoe_ffn_forward (linear router, no class tokens) touches
+// for this shape, packed: the fused top-1 path needs only the routing arrays
+// (and, when it cannot dispatch in its own prologue, the dispatch arrays);
+// the GEMM chains add their intermediates.  Regions a path does not touch
+// keep offset 0 and are never read or written.
+Layout layout_min(const clearmoe_shape& s) {
+    Layout L{};
+    const int64_t T = s.T, k = s.k, E = s.E;
+    const size_t es = elem_size(s.dtype);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off += up(bytes > 0 ? bytes : 1);
+        return at;
+    };
+    const bool fused = k == 1 && s.dtype == CLEARMOE_BF16 && fused_top1_supported(s.D, s.H, s.r, s.q);
+    const bool own = fused && hist_tiles(T, static_cast<int>(E)) * E <= kInlineScanMax;
+    const int64_t ntiles = route_tiles(T);
+    L.tile_counts = take(sizeof(int32_t) * hist_tiles(T, static_cast<int>(E)) * E);
+    if (!own) {
+        L.tile_base = take(sizeof(int32_t) * ntiles * E);
+        L.chunk_tot = take(sizeof(int32_t) * scan_chunks(ntiles) * E);
+        L.counts = take(sizeof(int32_t) * E);
+        L.offsets = take(sizeof(int32_t) * (E + 1));
+        L.perm = take(sizeof(int32_t) * T * k);
+        L.inv = take(sizeof(int32_t) * T * k);
+    }
+    L.dispatch_end = off;
+    L.idx = take(sizeof(int32_t) * T * k);
+    L.gate = take(sizeof(float) * T * k);
+    if (fused) {
+        const size_t fpart = T > 0 ? fused_part_bytes(T, static_cast<int>(E), s.H, s.r, s.q) : 0;
+        if (fpart > 0) {
+            L.fpart = take(fpart);
+            L.fcount = take(sizeof(int32_t) * static_cast<size_t>(T / 64 + E + 1));
+        }
+    } else if (k == 1) {
+        L.z = take(es * T * s.H);
+        L.tu = take(es * T * (s.r + s.q));
+        L.fpart = take(kGemmKsplitBytes);
+        L.fcount = take(sizeof(int32_t) * kGemmKsplitTiles);
+    } else {
+        L.z = take(es * T * s.H);
+        L.tproj = take(es * T * s.r);
+        L.hsh = take(sizeof(float) * T * s.D);
+        L.u = take(es * T * k * s.q);
+        L.hres = take(sizeof(float) * T * k * s.D);
+    }
+    L.total = off;
+    return L;
+}
+
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 // Shape checks common to every entry point (which fields matter depends on
@@ -358,6 +410,8 @@ const char* clearmoe_status_string(int status) {
         case CLEARMOE_ERR_UNSUPPORTED: return "unsupported";
         case CLEARMOE_ERR_WORKSPACE: return "workspace missing or too small";
         case CLEARMOE_ERR_HIP: return "HIP launch failed";
+        case CLEARMOE_ERR_TOO_LARGE:
+            return "shape needs more scratch than the no-allocation entry point holds";
         default: return "unknown status";
     }
 }
@@ -479,7 +533,8 @@ int class_tokens_impl(const clearmoe_shape& s, const clearmoe_router& rt, const 
 int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router, const void* x,
                      const void* W1, const float* b1, const void* US, const void* Vt,
                      const float* b2, const void* P, const void* Q, void* y, int32_t* idx_out,
-                     float* gate_out, void* ws, size_t ws_bytes, hipStream_t stream) {
+                     float* gate_out, void* ws, size_t ws_bytes, hipStream_t stream,
+                     const Layout* packed = nullptr) {
     int rc = check_layer_args(shape, x, W1, b1, US, Vt, b2, P, Q, nullptr, nullptr, y, idx_out,
                               gate_out);
     if (rc != CLEARMOE_OK) return rc;
@@ -487,7 +542,11 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
     rc = check_router(s, router);
     if (rc != CLEARMOE_OK) return rc;
     if (router->dense_stride > 0 && router->W2 == nullptr) return CLEARMOE_ERR_INVALID_ARG;
-    const Layout L = layout(s);
+    // a packed layout (no-allocation variant) serves only the linear router
+    // without class tokens, whose regions it holds
+    if (packed != nullptr && (router->hidden != 0 || router->adaptive || router->dense_stride > 0))
+        return CLEARMOE_ERR_INVALID_ARG;
+    const Layout L = packed != nullptr ? *packed : layout(s);
     if (!ws || !aligned(ws, kAlign) || ws_bytes < L.total) return CLEARMOE_ERR_WORKSPACE;
     if (s.T == 0) return CLEARMOE_OK;
 
@@ -627,6 +686,57 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
     const clearmoe_router rt = linear_router(Wg, bg);
     return ffn_forward_impl(shape, &rt, x, W1, b1, US, Vt, b2, P, Q, y, idx_out, gate_out, ws,
                             ws_bytes, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+// Scratch of clearmoe_ffn_forward_noalloc: one fixed device array, which each
+// device the library runs on holds until the process ends.  In host code the
+// name `scratch` only stands for the symbol: its device address on the
+// current device comes from hipGetSymbolAddress, once per device, and only
+// that address is handed to kernels.
+static __device__ __align__(256) unsigned char scratch[CLEARMOE_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch` (looked up on the first call on
+// that device, with it current).
+int scratch_address(void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return CLEARMOE_ERR_HIP;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (g_scratch_ptr[dev] == nullptr) {
+        void* p = nullptr;
+        if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr)
+            return CLEARMOE_ERR_HIP;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return CLEARMOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int clearmoe_ffn_forward_noalloc(const clearmoe_shape* shape, const void* x, const void* W1,
+                                 const float* b1, const void* US, const void* Vt, const float* b2,
+                                 const void* P, const void* Q, const void* Wg, const float* bg,
+                                 void* y, int32_t* idx_out, float* gate_out, hipStream_t stream) {
+    int rc = check_layer_args(shape, x, W1, b1, US, Vt, b2, P, Q, Wg, bg, y, idx_out, gate_out);
+    if (rc != CLEARMOE_OK) return rc;
+    const Layout L = layout_min(*shape);
+    if (L.total > static_cast<size_t>(CLEARMOE_NOALLOC_SCRATCH_BYTES)) return CLEARMOE_ERR_TOO_LARGE;
+    void* ws = nullptr;
+    rc = scratch_address(&ws);
+    if (rc != CLEARMOE_OK) return rc;
+    const clearmoe_router rt = linear_router(Wg, bg);
+    return ffn_forward_impl(shape, &rt, x, W1, b1, US, Vt, b2, P, Q, y, idx_out, gate_out, ws,
+                            L.total, stream, &L);
 }
 
 int clearmoe_ffn_forward_ex(const clearmoe_shape* shape, const clearmoe_router* router,

@@ -128,6 +128,24 @@ def test_dispatch_combine_ffn_reject_before_launch():
     assert L.clearmoe_ffn_forward(ctypes.byref(s), *args, FAKE, n - 1, None) == 3
 
 
+def test_noalloc_rejects_before_launch():
+    """The no-allocation variant checks its arguments like clearmoe_ffn_forward
+    and refuses a shape whose regions exceed its fixed scratch, all before any
+    HIP call."""
+    L = cm.lib()
+    s = _shape()
+    args = [FAKE] * 13
+    a = list(args)
+    a[1] = None                                   # NULL W1
+    assert L.clearmoe_ffn_forward_noalloc(ctypes.byref(s), *a, None) == 1
+    bad = _shape(q=6)
+    assert L.clearmoe_ffn_forward_noalloc(ctypes.byref(bad), *args, None) == 1
+    # the DeiT-Base top-2 layer keeps z [T, H] (310 MB): too large
+    big = cm.make_shape(50432, 768, 8, 2, cm.BF16, H=3072, r=256, q=64)
+    assert L.clearmoe_ffn_forward_noalloc(ctypes.byref(big), *args, None) == cm.ERR_TOO_LARGE
+    assert L.clearmoe_status_string(cm.ERR_TOO_LARGE).startswith(b"shape needs more scratch")
+
+
 def _prototypes():
     src = re.sub(r"/\*.*?\*/", "", open(HEADER).read(), flags=re.S)
     out = {}
