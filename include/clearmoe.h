@@ -302,7 +302,10 @@ enum {
     CLEARMOE_STAGE_Y = 13,             /* top-1: y[perm] = [t|u] [US|P_e]^T + b2 (grouped) */
     CLEARMOE_STAGE_FUSED_TOP1 = 14,    /* top-1 bf16: fc1+GELU, [t|u] and y in one kernel */
     CLEARMOE_STAGE_PAD_INDEX = 15,     /* padded backend: padded row maps */
-    CLEARMOE_N_STAGES = 16
+    CLEARMOE_STAGE_PAIR_KEY = 16,      /* top-2: expert-pair keys and gates */
+    CLEARMOE_STAGE_TU_PAIR = 17,       /* top-2: [t|u_a|u_b] grouped by expert pair */
+    CLEARMOE_STAGE_Y_PAIR = 18,        /* top-2: y grouped by pair, rows scattered */
+    CLEARMOE_N_STAGES = 19
 };
 
 /* Name of a stage (static string; "?" if out of range). */

@@ -33,7 +33,7 @@ SYMBOLS = ("clearmoe_version", "clearmoe_source_digest", "clearmoe_status_string
            "clearmoe_ffn_forward_noalloc")
 NOALLOC_SCRATCH_BYTES = 64 << 20
 ERR_TOO_LARGE = 5
-N_STAGES = 16
+N_STAGES = 19
 
 
 class ClearMoEError(RuntimeError):

@@ -30,12 +30,19 @@ struct Layout {
     size_t tile_counts, tile_base, chunk_tot;     // route / dispatch
     size_t counts, offsets, idx, gate, perm, inv;  // ffn_forward
     size_t z, tproj, hsh, u, hres, tu, fpart, fcount;
+    // top-2 pair order (E * E <= kPairMaxKeys): keys, pair gates, the pair
+    // permutation with its sort arrays, and [t|u_a|u_b] [T, r + 2q]
+    size_t pkey, pgate, pperm, pinv, pcounts, poffsets, ptc, ptb, pct, ptu;
     size_t dispatch_end, total;
     // padded-batch backend only (after total): capacity E * T * k rows
     size_t perm_pad, inv_pad, seg, u_pad, hres_pad, padded_total;
 };
 
 size_t elem_size(int dtype) { return dtype == CLEARMOE_F32 ? 4 : 2; }
+
+// Top-2 layers with few experts run in pair order: tokens sorted by their
+// expert pair, one [t|u_a|u_b] product and one y product per pair segment.
+bool pair_path(const clearmoe_shape& s) { return s.k == 2 && s.E * s.E <= kPairMaxKeys; }
 
 Layout layout(const clearmoe_shape& s) {
     Layout L{};
@@ -67,6 +74,19 @@ Layout layout(const clearmoe_shape& s) {
     L.u = take(es * T * k * s.q);
     L.hres = take(sizeof(float) * T * k * s.D);
     L.tu = take(es * T * k * (s.r + s.q));
+    if (pair_path(s)) {
+        const int64_t P = E * E;
+        L.pkey = take(sizeof(int32_t) * T);
+        L.pgate = take(sizeof(float) * 2 * T);
+        L.pperm = take(sizeof(int32_t) * T);
+        L.pinv = take(sizeof(int32_t) * T);
+        L.pcounts = take(sizeof(int32_t) * P);
+        L.poffsets = take(sizeof(int32_t) * (P + 1));
+        L.ptc = take(sizeof(int32_t) * (T > 0 ? hist_tiles(T, static_cast<int>(P)) * P : 1));
+        L.ptb = take(sizeof(int32_t) * (ntiles * P > 0 ? ntiles * P : 1));
+        L.pct = take(sizeof(int32_t) * (scan_chunks(ntiles) * P > 0 ? scan_chunks(ntiles) * P : 1));
+        L.ptu = take(es * T * (s.r + 2 * s.q));
+    }
     // float32 partials and per-tile arrival counters: of the fused top-1
     // kernel's hidden split (small batches), or else, on the top-1 GEMM
     // chain, of the [t|u] product's split K
@@ -111,8 +131,27 @@ Layout layout_min(const clearmoe_shape& s) {
     };
     const bool fused = k == 1 && s.dtype == CLEARMOE_BF16 && fused_top1_supported(s.D, s.H, s.r, s.q);
     const bool own = fused && hist_tiles(T, static_cast<int>(E)) * E <= kInlineScanMax;
+    const bool pair = pair_path(s);
     const int64_t ntiles = route_tiles(T);
     L.tile_counts = take(sizeof(int32_t) * hist_tiles(T, static_cast<int>(E)) * E);
+    if (pair) {
+        const int64_t P = E * E;
+        L.idx = take(sizeof(int32_t) * T * k);
+        L.gate = take(sizeof(float) * T * k);
+        L.pkey = take(sizeof(int32_t) * T);
+        L.pgate = take(sizeof(float) * 2 * T);
+        L.pperm = take(sizeof(int32_t) * T);
+        L.pinv = take(sizeof(int32_t) * T);
+        L.pcounts = take(sizeof(int32_t) * P);
+        L.poffsets = take(sizeof(int32_t) * (P + 1));
+        L.ptc = take(sizeof(int32_t) * hist_tiles(T, static_cast<int>(P)) * P);
+        L.ptb = take(sizeof(int32_t) * ntiles * P);
+        L.pct = take(sizeof(int32_t) * scan_chunks(ntiles) * P);
+        L.z = take(es * T * s.H);
+        L.ptu = take(es * T * (s.r + 2 * s.q));
+        L.total = off;
+        return L;
+    }
     if (!own) {
         L.tile_base = take(sizeof(int32_t) * ntiles * E);
         L.chunk_tot = take(sizeof(int32_t) * scan_chunks(ntiles) * E);
@@ -660,6 +699,66 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
         return CLEARMOE_OK;
     }
 
+    if (pair_path(s)) {
+        // Top-2 in pair order: every token's two experts {a, b} (a < b) name
+        // its segment, so the shared basis and both residuals merge into two
+        // grouped products over the pair order p:
+        //   [t | u_a | u_b](p) = z[pt] [Vt ; Q_a ; Q_b]^T, u_a times gate_a,
+        //                        u_b times gate_b;
+        //   y[pt] = [t | u_a | u_b](p) [US | P_a | P_b]^T + b2,
+        // with pt = pperm[p]: each y row is written once, and neither h_sh
+        // nor h_res is formed.
+        const int npk = s.E * s.E;
+        int32_t* pkey = at<int32_t>(ws, L.pkey);
+        float* pgate = at<float>(ws, L.pgate);
+        int32_t* pperm = at<int32_t>(ws, L.pperm);
+        int32_t* poffsets = at<int32_t>(ws, L.poffsets);
+        CLEARMOE_STAGE(CLEARMOE_STAGE_PAIR_KEY, st,
+                       launch_pair_key(idx, gate, T, s.E, pkey, pgate, st));
+        clearmoe_shape sp = s;
+        sp.E = npk;
+        sp.k = 1;
+        Layout Lp = L;
+        Lp.tile_counts = L.ptc;
+        Lp.tile_base = L.ptb;
+        Lp.chunk_tot = L.pct;
+        rc = dispatch_impl(sp, Lp, pkey, ws, at<int32_t>(ws, L.pcounts), poffsets, pperm,
+                           at<int32_t>(ws, L.pinv), nullptr, nullptr, false, st);
+        if (rc != CLEARMOE_OK) return rc;
+        GemmDesc g = gemm_desc(T, s.H, s.D);
+        g.A = x; g.lda = s.D;
+        g.B = W1; g.ldb = s.D;
+        g.C = z; g.ldc = s.H; g.c_f32 = 0;
+        g.bias = b1; g.gelu = 1;
+        CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
+        void* ptu = at<void>(ws, L.ptu);
+        const int rqq = s.r + 2 * s.q;
+        g = gemm_desc(T, rqq, s.H);
+        g.A = z; g.lda = s.H; g.a_rows = pperm; g.a_div = 1;
+        g.B = Vt; g.ldb = s.H;
+        g.B1 = Q; g.ldb1 = s.H; g.b1_seg_stride = static_cast<int64_t>(s.q) * s.H;
+        g.B2 = Q; g.ldb2 = s.H; g.b2_seg_stride = static_cast<int64_t>(s.q) * s.H;
+        g.n_split = s.r; g.n_split2 = s.r + s.q; g.pair_E = s.E;
+        g.C = ptu; g.ldc = rqq; g.c_f32 = 0;
+        g.row_scale = pgate; g.scale_rows = pperm; g.rs_stride = 2;
+        g.scale_col0 = s.r; g.scale_col1 = s.r + s.q;
+        g.seg_offsets = poffsets; g.nseg = npk;
+        if (rqq > 0) CLEARMOE_STAGE(CLEARMOE_STAGE_TU_PAIR, st, launch_gemm(s.dtype, g, st));
+        g = gemm_desc(T, s.D, rqq);
+        g.A = ptu; g.lda = rqq;
+        g.B = US; g.ldb = s.r;
+        g.B1 = P; g.ldb1 = s.q; g.b1_seg_stride = static_cast<int64_t>(s.D) * s.q;
+        g.B2 = P; g.ldb2 = s.q; g.b2_seg_stride = static_cast<int64_t>(s.D) * s.q;
+        g.k_split = s.r; g.k_split2 = s.r + s.q; g.pair_E = s.E;
+        g.C = y; g.ldc = s.D; g.c_f32 = 0;
+        g.c_rows = pperm; g.c_div = 1;
+        g.bias = b2;
+        g.seg_offsets = poffsets; g.nseg = npk;
+        CLEARMOE_STAGE(CLEARMOE_STAGE_Y_PAIR, st, launch_gemm(s.dtype, g, st));
+        if (cls) return class_tokens_impl(s, *router, x, W1, b1, b2, z, true, y, st);
+        return CLEARMOE_OK;
+    }
+
     // 3. z = GELU(x W1^T + b1); 4. shared basis t = z Vt^T, h_sh = t US^T + b2
     rc = shared_impl(s, x, W1, b1, US, Vt, b2, z, tproj, hsh, st);
     if (rc != CLEARMOE_OK) return rc;
@@ -866,7 +965,7 @@ const char* clearmoe_stage_name(int stage) {
     static const char* names[CLEARMOE_N_STAGES] = {
         "route", "tile_hist", "scan", "permute", "combine", "fc1_gelu",
         "basis_t", "basis_h", "res_u", "res_h", "combine_res", "dense_fc2", "tu_grouped",
-        "y_grouped", "fused_top1", "pad_index"};
+        "y_grouped", "fused_top1", "pad_index", "pair_key", "tu_pair", "y_pair"};
     return (stage >= 0 && stage < CLEARMOE_N_STAGES) ? names[stage] : "?";
 }
 

@@ -68,11 +68,11 @@ __global__ __launch_bounds__(TILE) void k_tile_hist(const int32_t* __restrict__ 
     if (tid < E) tile_counts[static_cast<int64_t>(blockIdx.x) * E + tid] = s_run[tid];
 }
 
-// Exclusive scan over tiles of every expert column at once, in chunks of
-// kScanChunk tiles: workgroup c scans tiles [c kScanChunk, (c + 1)
-// kScanChunk), one per thread (a thread holds its tile's histogram, EP >= E
-// registers; the wave scans it with shuffles, wave totals meet in LDS), and
-// writes the within-chunk exclusive prefixes tb and the chunk's totals.  The
+// Exclusive scan over tiles of every expert column, in chunks of kScanChunk
+// tiles: workgroup c scans tiles [c kScanChunk, (c + 1) kScanChunk), one per
+// thread, EP expert columns at a time (a thread holds EP counts in registers;
+// the wave scans them with shuffles, wave totals meet in LDS), and writes the
+// within-chunk exclusive prefixes tb and the chunk's totals.  The
 // permutation adds the chunk prefixes, so every chunk runs in parallel.
 constexpr int kScanChunk = 256;
 
@@ -85,36 +85,39 @@ __global__ __launch_bounds__(kScanChunk) void k_scan(const int32_t* __restrict__
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int64_t b = static_cast<int64_t>(blockIdx.x) * kScanChunk + tid;
     const bool in = b < ntiles;
-    int v[EP], c[EP];
-#pragma unroll
-    for (int e = 0; e < EP; ++e) {
-        c[e] = (in && e < E) ? tc[b * E + e] : 0;
-        v[e] = c[e];
-    }
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
+    for (int e0 = 0; e0 < E; e0 += EP) {
+        int v[EP], c[EP];
 #pragma unroll
         for (int e = 0; e < EP; ++e) {
-            const int n = __shfl_up(v[e], o);
-            if (lane >= o) v[e] += n;
+            c[e] = (in && e0 + e < E) ? tc[b * E + e0 + e] : 0;
+            v[e] = c[e];
         }
-    }
-    if (lane == 63) {
 #pragma unroll
-        for (int e = 0; e < EP; ++e) s_wsum[w][e] = v[e];
-    }
-    __syncthreads();
+        for (int o = 1; o < 64; o <<= 1) {
 #pragma unroll
-    for (int e = 0; e < EP; ++e) {
-        int pre = 0;
-        for (int i = 0; i < w; ++i) pre += s_wsum[i][e];
-        if (in && e < E) tb[b * E + e] = pre + v[e] - c[e];
-    }
-    if (tid < E) {
-        int sum = 0;
+            for (int e = 0; e < EP; ++e) {
+                const int n = __shfl_up(v[e], o);
+                if (lane >= o) v[e] += n;
+            }
+        }
+        if (e0 > 0) __syncthreads();             // the previous block's sums are read
+        if (lane == 63) {
 #pragma unroll
-        for (int i = 0; i < kW; ++i) sum += s_wsum[i][tid];
-        chunk_tot[static_cast<int64_t>(blockIdx.x) * E + tid] = sum;
+            for (int e = 0; e < EP; ++e) s_wsum[w][e] = v[e];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int e = 0; e < EP; ++e) {
+            int pre = 0;
+            for (int i = 0; i < w; ++i) pre += s_wsum[i][e];
+            if (in && e0 + e < E) tb[b * E + e0 + e] = pre + v[e] - c[e];
+        }
+        if (tid < EP && e0 + tid < E) {
+            int sum = 0;
+#pragma unroll
+            for (int i = 0; i < kW; ++i) sum += s_wsum[i][tid];
+            chunk_tot[static_cast<int64_t>(blockIdx.x) * E + e0 + tid] = sum;
+        }
     }
 }
 
@@ -430,14 +433,11 @@ hipError_t launch_scan(const int32_t* tile_counts, int64_t ntiles, int E, int32_
                        int32_t* chunk_tot, hipStream_t st) {
     const dim3 grid(static_cast<unsigned>(scan_chunks(ntiles)));
     if (ntiles == 0) return hipSuccess;
+    // 16 columns at a time beyond 8 experts (64 per pass spilled registers)
     if (E <= 8)
         launch_kernel(k_scan<8>, grid, kScanChunk, 0, st, tile_counts, ntiles, E, tile_base, chunk_tot);
-    else if (E <= 16)
-        launch_kernel(k_scan<16>, grid, kScanChunk, 0, st, tile_counts, ntiles, E, tile_base, chunk_tot);
-    else if (E <= 32)
-        launch_kernel(k_scan<32>, grid, kScanChunk, 0, st, tile_counts, ntiles, E, tile_base, chunk_tot);
     else
-        launch_kernel(k_scan<64>, grid, kScanChunk, 0, st, tile_counts, ntiles, E, tile_base, chunk_tot);
+        launch_kernel(k_scan<16>, grid, kScanChunk, 0, st, tile_counts, ntiles, E, tile_base, chunk_tot);
     return hipGetLastError();
 }
 
@@ -487,6 +487,43 @@ hipError_t launch_combine_residual(int dtype, const float* hsh, const float* hre
     else
         launch_kernel(k_combine_residual<bf16_bits>, blocks, 256, 0, st,
             hsh, hres, inv, static_cast<bf16_bits*>(y), T, D, k, hres_rows);
+    return hipGetLastError();
+}
+
+// Pair keys of a top-2 routing: token t with experts {a, b}, a < b, gets key
+// a E + b and its two gates in that order, g2 = (gate of a, gate of b); a
+// token with one expert e (the other slot empty) gets the diagonal key e E + e
+// and gates (gate of e, 0); a token with none gets key -1 (no segment).
+__global__ __launch_bounds__(256) void k_pair_key(const int32_t* __restrict__ idx,
+                                                  const float* __restrict__ gate, int64_t T,
+                                                  int E, int32_t* __restrict__ key,
+                                                  float* __restrict__ g2) {
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (t >= T) return;
+    // idx and gate may be only 4-byte aligned (caller arrays): two loads each
+    const int2 e = make_int2(idx[2 * t], idx[2 * t + 1]);
+    const float2 g = make_float2(gate[2 * t], gate[2 * t + 1]);
+    const bool v0 = e.x >= 0 && e.x < E, v1 = e.y >= 0 && e.y < E;
+    int32_t k = -1;
+    float2 o = make_float2(0.0f, 0.0f);
+    if (v0 && v1) {
+        const bool lo0 = e.x < e.y;
+        k = lo0 ? e.x * E + e.y : e.y * E + e.x;
+        o = lo0 ? g : make_float2(g.y, g.x);
+    } else if (v0 || v1) {
+        const int ee = v0 ? e.x : e.y;
+        k = ee * E + ee;
+        o = make_float2(v0 ? g.x : g.y, 0.0f);
+    }
+    key[t] = k;
+    *reinterpret_cast<float2*>(g2 + 2 * t) = o;
+}
+
+hipError_t launch_pair_key(const int32_t* idx, const float* gate, int64_t T, int E, int32_t* key,
+                           float* g2, hipStream_t st) {
+    if (T == 0) return hipSuccess;
+    launch_kernel(k_pair_key, dim3(static_cast<unsigned>((T + 255) / 256)), 256, 0, st, idx, gate,
+                  T, E, key, g2);
     return hipGetLastError();
 }
 

@@ -35,15 +35,23 @@
 
 namespace clearmoe {
 
-constexpr int kStageBytes = 128;   // bytes of k per row per stage
+constexpr int kStageBytes = 128;   // bytes of k per row per stage (default)
 constexpr int kXcds = 8;           // MI355X: 8 XCDs of 32 CUs
 
 __device__ __attribute__((aligned(16))) const uint32_t g_zero_page[4] = {0u, 0u, 0u, 0u};
 
 typedef __attribute__((address_space(3))) uint32_t lds_u32;
 
-// Physical 16-byte chunk slot of logical chunk c in LDS row r is c ^ swz(r).
-__device__ __forceinline__ int swz(int r) { return (r >> 1) & 7; }
+// Physical 16-byte chunk slot of logical chunk c in LDS row r is c ^ swz(r),
+// for rows of SB bytes (CPR = SB / 16 chunks): a 256-byte bank window holds
+// 16 / CPR rows, and the swizzle spreads the CPR rows that share window
+// positions over the CPR chunk slots, so 16 consecutive rows of one logical
+// chunk hit 16 distinct 16-byte bank groups.
+template <int SB>
+__device__ __forceinline__ int swz(int r) {
+    constexpr int CPR = SB / 16, RW = 16 / CPR;
+    return (r / RW) % CPR;
+}
 
 // 16 bytes per lane, HBM -> LDS: lane i's bytes land at lds_base + 16*i.
 // Issued as inline asm so that the compiler does not model it: the waits for
@@ -82,21 +90,25 @@ template <> struct Mfma<float> {
     }
 };
 
-template <typename Tin, int BM, int BN, int WM, int WN, int NS>
-__global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, int ntiles, int per_xcd,
-                                                       int ksplit) {
+// WPE > 0 asks for WPE waves per SIMD (registers capped to fit them).
+template <typename Tin, int BM, int BN, int WM, int WN, int NS, int SB = kStageBytes, int WPE = 0>
+__global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(WPE > 0 ? WPE : 1)))
+void k_gemm(GemmDesc g, int mtiles, int ntiles, int per_xcd, int ksplit) {
     constexpr int NW = WM * WN;                     // waves: 4 (one per SIMD) or 8 (two)
     static_assert(NW == 4 || NW == 8, "4 or 8 waves");
     constexpr int WTM = BM / WM, WTN = BN / WN;
     constexpr int TM = WTM / 32, TN = WTN / 32;
     static_assert(TM >= 1 && TN >= 1, "wave tile at least 32x32");
-    static_assert(BM % (8 * NW) == 0 && BN % (8 * NW) == 0, "8-row load groups per wave");
+    static_assert(SB == 64 || SB == 128, "stage rows of 64 or 128 bytes");
+    constexpr int CPR = SB / 16;                    // 16-byte chunks per stage row
+    constexpr int RPL = 64 / CPR;                   // rows per load instruction (1 KB)
+    static_assert(BM % (RPL * NW) == 0 && BN % (RPL * NW) == 0, "whole load groups per wave");
     constexpr int PER16 = Elem<Tin>::per16;
-    constexpr int BK = kStageBytes / static_cast<int>(sizeof(Tin));
-    constexpr int AL = BM / (8 * NW), BL = BN / (8 * NW);   // load instructions per wave per stage
+    constexpr int BK = SB / static_cast<int>(sizeof(Tin));
+    constexpr int AL = BM / (RPL * NW), BL = BN / (RPL * NW);   // load instructions per wave per stage
     constexpr int LPS = AL + BL;
     static_assert(LPS * (NS - 1) < 64, "vmcnt range");
-    constexpr int STAGE_A = BM * kStageBytes, STAGE_B = BN * kStageBytes;
+    constexpr int STAGE_A = BM * SB, STAGE_B = BN * SB;
     // One LDS array per stage, so that with the stage index a compile-time
     // constant the LDS lowering gives each its own alias scope and the
     // compiler's own waits for the async loads cover only the stage read.
@@ -149,23 +161,31 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, i
     const Tin* B0 = g.B != nullptr
                         ? static_cast<const Tin*>(g.B) + static_cast<int64_t>(seg) * g.b_seg_stride
                         : nullptr;
+    // parts 1 and 2 belong to the segment's expert, or, for pair segments
+    // (s = a * pair_E + b), to its experts a and b
+    const int e1 = g.pair_E > 0 ? seg / g.pair_E : seg;
+    const int e2 = g.pair_E > 0 ? seg % g.pair_E : seg;
     const Tin* B1 = g.B1 != nullptr
-                        ? static_cast<const Tin*>(g.B1) + static_cast<int64_t>(seg) * g.b1_seg_stride
+                        ? static_cast<const Tin*>(g.B1) + static_cast<int64_t>(e1) * g.b1_seg_stride
+                        : nullptr;
+    const Tin* B2 = g.B2 != nullptr
+                        ? static_cast<const Tin*>(g.B2) + static_cast<int64_t>(e2) * g.b2_seg_stride
                         : nullptr;
     const uint32_t* zero = g_zero_page;
 
     // ---- per-lane source rows of its load instructions (row within the tile
     //      = (wave*AL + i)*8 + lane/8; LDS chunk lane%8 holds global chunk
-    //      (lane%8) ^ swz(row)).  A B row has a part-0 and a part-1 pointer
-    //      (the k split picks between them per chunk).
-    const int lrow8 = lane >> 3, cpos = lane & 7;
+    //      (lane%8) ^ swz(row)).  A B row has a pointer per k part (the k
+    //      split picks between them per chunk).
+    const int lrow8 = lane / CPR, cpos = lane % CPR;
     const Tin* arow[AL];
     const Tin* brow0[BL];
     const Tin* brow1[BL];
+    const Tin* brow2[BL];
     int achunk[AL], bchunk[BL];
 #pragma unroll
     for (int i = 0; i < AL; ++i) {
-        const int r = (wave * AL + i) * 8 + lrow8;
+        const int r = (wave * AL + i) * RPL + lrow8;
         const int64_t m = m_lo + r;
         arow[i] = nullptr;
         if (m < m_hi) {
@@ -173,22 +193,25 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, i
             const int64_t src = g.a_rows != nullptr ? static_cast<int64_t>(g.a_rows[m]) : m;
             if (src >= 0) arow[i] = A + (g.a_rows != nullptr ? src / g.a_div : src) * g.lda;
         }
-        achunk[i] = cpos ^ swz(r);
+        achunk[i] = cpos ^ swz<SB>(r);
     }
 #pragma unroll
     for (int i = 0; i < BL; ++i) {
-        const int r = (wave * BL + i) * 8 + lrow8;
+        const int r = (wave * BL + i) * RPL + lrow8;
         const int n = n0 + r;
-        brow0[i] = brow1[i] = nullptr;
+        brow0[i] = brow1[i] = brow2[i] = nullptr;
         if (n < g.N) {
             if (n < g.n_split) {
                 if (g.B != nullptr) brow0[i] = B0 + static_cast<int64_t>(n) * g.ldb;
                 if (B1 != nullptr) brow1[i] = B1 + static_cast<int64_t>(n) * g.ldb1;
-            } else if (B1 != nullptr) {
-                brow0[i] = B1 + static_cast<int64_t>(n - g.n_split) * g.ldb1;
+                if (B2 != nullptr) brow2[i] = B2 + static_cast<int64_t>(n) * g.ldb2;
+            } else if (n < g.n_split2) {
+                if (B1 != nullptr) brow0[i] = B1 + static_cast<int64_t>(n - g.n_split) * g.ldb1;
+            } else if (B2 != nullptr) {
+                brow0[i] = B2 + static_cast<int64_t>(n - g.n_split2) * g.ldb2;
             }
         }
-        bchunk[i] = cpos ^ swz(r);
+        bchunk[i] = cpos ^ swz<SB>(r);
     }
 
     // k stages of this part: [kb0, kb0 + nk)
@@ -219,8 +242,10 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, i
             if (kk < g.K) {
                 if (kk < g.k_split) {
                     if (brow0[i] != nullptr) src = brow0[i] + kk;
-                } else if (brow1[i] != nullptr) {
-                    src = brow1[i] + (kk - g.k_split);
+                } else if (kk < g.k_split2) {
+                    if (brow1[i] != nullptr) src = brow1[i] + (kk - g.k_split);
+                } else if (brow2[i] != nullptr) {
+                    src = brow2[i] + (kk - g.k_split2);
                 }
             }
             async_load16(src,
@@ -261,18 +286,18 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, i
             const unsigned char* sa = stage(b);
             const unsigned char* sb = sa + STAGE_A;
 #pragma unroll
-            for (int s = 0; s < kStageBytes / 32; ++s) {
+            for (int s = 0; s < SB / 32; ++s) {
                 const int c = 2 * s + lhalf;        // 16-byte chunk of k within the stage
                 uint4 fa[TM], fb[TN];
 #pragma unroll
                 for (int i = 0; i < TM; ++i) {
                     const int r = wm * WTM + i * 32 + lrow;
-                    fa[i] = *reinterpret_cast<const uint4*>(sa + r * kStageBytes + ((c ^ swz(r)) << 4));
+                    fa[i] = *reinterpret_cast<const uint4*>(sa + r * SB + ((c ^ swz<SB>(r)) << 4));
                 }
 #pragma unroll
                 for (int j = 0; j < TN; ++j) {
                     const int r = wn * WTN + j * 32 + lrow;
-                    fb[j] = *reinterpret_cast<const uint4*>(sb + r * kStageBytes + ((c ^ swz(r)) << 4));
+                    fb[j] = *reinterpret_cast<const uint4*>(sb + r * SB + ((c ^ swz<SB>(r)) << 4));
                 }
                 // B first: tile (i, j) accumulates C^T (see the epilogue)
 #pragma unroll
@@ -347,7 +372,11 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, i
         const int64_t m = m_lo + wm * WTM + i * 32 + lrow;
         if (m >= m_hi) continue;
         const int32_t sr = g.row_scale != nullptr ? g.scale_rows[m] : 0;
-        const float rs = g.row_scale == nullptr ? 1.0f : (sr >= 0 ? g.row_scale[sr] : 0.0f);
+        float rs = 1.0f, rs1 = 1.0f;
+        if (g.row_scale != nullptr) {
+            rs = sr >= 0 ? g.row_scale[static_cast<int64_t>(sr) * g.rs_stride] : 0.0f;
+            rs1 = g.rs_stride > 1 && sr >= 0 ? g.row_scale[static_cast<int64_t>(sr) * g.rs_stride + 1] : rs;
+        }
         // a negative scatter index is a padding row: it is not stored
         const int64_t cr = g.c_rows != nullptr ? static_cast<int64_t>(g.c_rows[m]) : m;
         if (cr < 0) continue;
@@ -366,7 +395,8 @@ __global__ __launch_bounds__(64 * WM * WN) void k_gemm(GemmDesc g, int mtiles, i
                 float val[4];
 #pragma unroll
                 for (int t = 0; t < 4; ++t) {
-                    val[t] = acc[i][j][4 * q4 + t] * (n + t >= g.scale_col0 ? rs : 1.0f) + bb[t];
+                    const float sc = n + t >= g.scale_col0 ? (n + t >= g.scale_col1 ? rs1 : rs) : 1.0f;
+                    val[t] = acc[i][j][4 * q4 + t] * sc + bb[t];
                     if (g.gelu) val[t] = gelu_erf(val[t]);
                 }
                 if (g.c_f32) {
@@ -395,14 +425,14 @@ int gemm_ksplit(int64_t tiles, int nk) {
     return s < 2 ? 1 : static_cast<int>(s);
 }
 
-template <typename Tin, int BM, int BN, int WM, int WN, int NS>
+template <typename Tin, int BM, int BN, int WM, int WN, int NS, int SB = kStageBytes, int WPE = 0>
 static hipError_t gemm_cfg(const GemmDesc& g, hipStream_t st) {
     int64_t mt = (g.M + BM - 1) / BM;
     if (g.seg_offsets != nullptr) mt += g.nseg;
     const int64_t nt = (g.N + BN - 1) / BN;
     const int64_t tiles = mt * nt;
     if (tiles == 0) return hipSuccess;
-    constexpr int BK = kStageBytes / static_cast<int>(sizeof(Tin));
+    constexpr int BK = SB / static_cast<int>(sizeof(Tin));
     // tiles x S <= 256 parts of BM x BN floats each fit kGemmKsplitBytes up
     // to 64 x 128 tiles (larger ones never have so few tiles here)
     int S = 1;
@@ -424,7 +454,7 @@ static hipError_t gemm_cfg(const GemmDesc& g, hipStream_t st) {
         const hipError_t err = hipGetLastError();
         if (err != hipSuccess) return err;
     }
-    launch_kernel(k_gemm<Tin, BM, BN, WM, WN, NS>, dim3(static_cast<unsigned>(grid)), 64 * WM * WN, 0, st,
+    launch_kernel(k_gemm<Tin, BM, BN, WM, WN, NS, SB, WPE>, dim3(static_cast<unsigned>(grid)), 64 * WM * WN, 0, st,
         d, static_cast<int>(mt), static_cast<int>(nt), static_cast<int>(per_xcd), S);
     return hipGetLastError();
 }
@@ -439,6 +469,20 @@ static hipError_t gemm_cfg(const GemmDesc& g, hipStream_t st) {
 template <typename Tin>
 static hipError_t gemm_dt(const GemmDesc& g, hipStream_t st) {
     const int64_t mt128 = (g.M + 127) / 128;
+    if constexpr (sizeof(Tin) == 2) {
+        // bfloat16, measured on the DeiT-Base layer's products (50432 rows):
+        // 64-byte stages, three in flight, and two workgroups per CU (72 KB
+        // of LDS each) beat 128-byte stages two deep, which leave the loads'
+        // latency exposed (fc1 + GELU 446 -> 407 us, the dense fc2 320 ->
+        // 302, the pair products 245 -> 209 and 138 -> 79 us)
+        const int64_t mnk = g.M * static_cast<int64_t>(g.N) * g.K;
+        if (g.N >= 512 && mnk >= (int64_t{1} << 35))
+            return gemm_cfg<Tin, 256, 128, 4, 2, 3, 64>(g, st);
+        if (g.N >= 512 && g.M >= 16384) return gemm_cfg<Tin, 128, 256, 4, 2, 3, 64>(g, st);
+        if (g.N > 128 && g.N <= 512 && g.K >= 1024 && g.M >= 16384)
+            return gemm_cfg<Tin, 128, 128, 2, 2, 3, 64, 2>(g, st);
+        if (g.N >= 1024 && g.K <= 512) return gemm_cfg<Tin, 128, 128, 4, 2, 2>(g, st);
+    }
     if (g.N >= 1024 && ((g.M + 255) / 256) * ((g.N + 255) / 256) >= 1024)
         return gemm_cfg<Tin, 256, 256, 4, 2, 2>(g, st);
     if (g.N <= 32) return gemm_cfg<Tin, 128, 32, 4, 1, 3>(g, st);

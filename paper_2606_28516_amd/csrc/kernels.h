@@ -192,6 +192,12 @@ hipError_t launch_combine_gated(int dtype, const void* ye, const int32_t* inv, c
 hipError_t launch_combine_residual(int dtype, const float* hsh, const float* hres,
                                    const int32_t* inv, void* y, int64_t T, int D, int k,
                                    int64_t hres_rows, hipStream_t st);
+// Pair order of a top-2 routing (idx, gate [T, 2]): key[t] = a E + b for
+// the token's experts a < b (e E + e with one expert, -1 with none) and
+// g2[t] = (gate of a, gate of b).  Pair segments need E * E <= kPairMaxKeys.
+constexpr int kPairMaxKeys = 64;
+hipError_t launch_pair_key(const int32_t* idx, const float* gate, int64_t T, int E, int32_t* key,
+                           float* g2, hipStream_t st);
 // Index maps of the padded-batch backend (expert e owns rows [e C, e C + C)):
 // perm_pad [E C] (-1 = padding), inv_pad [A], seg [E + 1] = e C.
 hipError_t launch_pad_index(const int32_t* idx, const int32_t* counts, const int32_t* offsets,
@@ -199,9 +205,12 @@ hipError_t launch_pad_index(const int32_t* idx, const int32_t* counts, const int
                             int32_t* perm_pad, int32_t* inv_pad, int32_t* seg, hipStream_t st);
 
 // NT GEMM  C[crow(m), n] = epi( sum_k A[arow(m), k] B_seg(m)[n, k] ).
-// B may come in two parts: rows n >= n_split from B1 (row n - n_split), or
-// columns k >= k_split from B1 (column k - k_split); each part has its own
-// per-segment stride (0 = shared by all segments).
+// B may come in up to three parts: rows n_split <= n < n_split2 from B1 (row
+// n - n_split) and rows n >= n_split2 from B2 (row n - n_split2), or columns
+// k_split <= k < k_split2 from B1 and k >= k_split2 from B2; each part has
+// its own per-segment stride (0 = shared by all segments).  Parts 1 and 2
+// take the segment's index, or with pair_E > 0 (segment s = a * pair_E + b of
+// a top-2 pair order) a for B1 and b for B2.
 struct GemmDesc {
     const void* A;            // [*, K] in dtype, row stride lda (elements)
     int64_t lda;
@@ -213,8 +222,14 @@ struct GemmDesc {
     const void* B1;           // optional part 1 (see n_split / k_split)
     int64_t ldb1;
     int64_t b1_seg_stride;
+    const void* B2;           // optional part 2
+    int64_t ldb2;
+    int64_t b2_seg_stride;
     int n_split;              // rows n >= n_split come from B1 (default: N)
+    int n_split2;             // rows n >= n_split2 come from B2 (default: N)
     int k_split;              // columns k >= k_split come from B1 (default: K)
+    int k_split2;             // columns k >= k_split2 come from B2 (default: K)
+    int pair_E;               // > 0: segments are expert pairs (see above)
     void* C;                  // output, row stride ldc
     int64_t ldc;
     int c_f32;                // 1: C is float32; 0: C is dtype
@@ -222,8 +237,10 @@ struct GemmDesc {
     int c_div;
     const float* bias;        // optional [N]
     const float* row_scale;   // optional: columns n >= scale_col0 of row m are
-    const int32_t* scale_rows;//   scaled by row_scale[scale_rows[m]]
-    int scale_col0;
+    const int32_t* scale_rows;//   scaled by row_scale[scale_rows[m] * rs_stride],
+    int scale_col0;           //   and columns n >= scale_col1 by the entry after
+    int scale_col1;           //   it (rs_stride 2); a negative scale row is 0
+    int rs_stride;
     int gelu;                 // 1: GELU after bias
     int64_t M;                // rows (sum of segments when grouped)
     int N, K;
@@ -243,7 +260,11 @@ inline GemmDesc gemm_desc(int64_t M, int N, int K) {
     g.a_div = 1;
     g.c_div = 1;
     g.n_split = N;
+    g.n_split2 = N;
     g.k_split = K;
+    g.k_split2 = K;
+    g.scale_col1 = N;
+    g.rs_stride = 1;
     g.M = M;
     g.N = N;
     g.K = K;
