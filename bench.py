@@ -592,49 +592,56 @@ def bench_layer(cm, synth, torch, np, stream, workload, steps, cfg=None, L=None,
 
 
 def bench_stack(cm, synth, torch, np, stream, L, steps):
-    """The FFN part of a DeiT-Small forward: 12 blocks, of which the 6 with the
-    best layer scores are CLEAR-MoE (Sec. III Phase 2 keeps the top L/2) and
-    the others stay dense, with each image's class token on the dense path in
-    the CLEAR-MoE layers (Table C6).  Every layer runs on the same resident
-    12608-token input with the same weights (timing only; attention, layer
-    norms and residual adds are not part of this path).  Compared with 12
-    dense FFN layers through the same kernels: the FFN-only analogue of the
-    paper's model-level CLEAR-MoE / dense latency ratio (Table III)."""
+    """The FFN part of a DeiT-Small forward as one chain (clearmoe_stack_forward):
+    12 blocks with their own weights, each adding its input back (x + f(x));
+    six are CLEAR-MoE (Sec. III Phase 2 keeps the best-scoring L/2; here
+    blocks 6..11, the order does not change the timing) with each image's
+    class token on the dense path (Table C6), six stay dense.  Compared with
+    the chain of 12 dense blocks through the same kernels: the FFN-only
+    analogue of the paper's model-level CLEAR-MoE / dense latency ratio
+    (Table III).  Attention and layer norms are not part of this path."""
     cfg = L["cfg"]
-    C = synth.with_class_tokens(L, stride=197)
-    d = {n: cm.from_stored(C[n]) for n in ("x", "W1", "b1", "US", "Vt", "b2", "P", "Q", "Wg",
-                                          "bg", "W2")}
-    router = cm.make_router(d["Wg"], d["bg"], dense_stride=197, W2=d["W2"])
-    shape = cm.make_shape(cfg.T, cfg.D, cfg.E, cfg.k, cm.BF16, H=cfg.H, r=cfg.r, q=cfg.q)
-    ws = cm.alloc_workspace(shape)
-    y = torch.empty_like(d["x"])
-    moe_layers = 6
+    x = cm.from_stored(L["x"])
+    keep, moe_stack, dense_stack = [], [], []
+    for l in range(12):
+        Ll = synth.make_layer(dataclasses.replace(cfg, name=f"block{l}", T=1, seed=100 + l,
+                                                  n_cal=4000))
+        W2 = cm.from_stored(synth.to_bf16_bits(Ll["W2"]))
+        d = {n: cm.from_stored(Ll[n]) for n in ("W1", "b1", "US", "Vt", "b2", "P", "Q", "Wg", "bg")}
+        d["W2"] = W2
+        keep.append(d)
+        dense = cm.make_stack_layer(d["W1"], d["b1"], d["b2"], W2=W2)
+        dense_stack.append(dense)
+        if l >= 6:
+            router = cm.make_router(d["Wg"], d["bg"], dense_stride=197, W2=W2)
+            moe_stack.append(cm.make_stack_layer(d["W1"], d["b1"], d["b2"], d["US"], d["Vt"],
+                                                 d["P"], d["Q"], router, k=cfg.k, W2=W2))
+        else:
+            moe_stack.append(dense)
+    shape = cm.stack_shape(x, cfg.H, cfg.E, cfg.r, cfg.q)
+    ws = torch.empty(cm.stack_workspace_bytes(shape, moe_stack), dtype=torch.uint8,
+                     device=x.device)
+    y = torch.empty_like(x)
 
-    def moe():
-        cm.ffn_forward_ex(d["x"], d["W1"], d["b1"], d["US"], d["Vt"], d["b2"], d["P"], d["Q"],
-                          router, cfg.k, ws=ws, out=y)
-
-    def dense():
-        cm.dense_ffn_forward(d["x"], d["W1"], d["b1"], d["W2"], d["b2"], ws=ws, out=y)
-
-    def timed(fn_list):
-        for f in fn_list:
-            f()
+    def timed(layers):
+        for _ in range(3):
+            cm.stack_forward(x, layers, cfg.H, cfg.E, cfg.r, cfg.q, ws=ws, out=y)
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
         for _ in range(steps):
-            for f in fn_list:
-                f()
+            cm.stack_forward(x, layers, cfg.H, cfg.E, cfg.r, cfg.q, ws=ws, out=y)
         e1.record(stream)
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / steps
 
-    mixed = timed([moe] * moe_layers + [dense] * (12 - moe_layers))
-    all_dense = timed([dense] * 12)
-    return {"workload": f"12 FFN layers at {cfg.name} (T={cfg.T}), {moe_layers} CLEAR-MoE "
-                        f"(class tokens on the dense path) + {12 - moe_layers} dense",
-            "ms": mixed, "tokens_per_s": cfg.T / (mixed * 1e-3), "dense_ms": all_dense,
+    mixed = timed(moe_stack)
+    all_dense = timed(dense_stack)
+    del keep
+    return {"workload": f"12 chained FFN blocks (x + f(x)) at {cfg.name} (T={cfg.T}), blocks 6..11 "
+                        f"CLEAR-MoE top-{cfg.k} with class tokens on the dense path, 0..5 dense; "
+                        f"own weights per block", "ms": mixed,
+            "tokens_per_s": cfg.T / (mixed * 1e-3), "dense_ms": all_dense,
             "moe_over_dense_time": mixed / all_dense, "steps": steps}
 
 

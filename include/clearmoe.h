@@ -305,8 +305,51 @@ enum {
     CLEARMOE_STAGE_PAIR_KEY = 16,      /* top-2: expert-pair keys and gates */
     CLEARMOE_STAGE_TU_PAIR = 17,       /* top-2: [t|u_a|u_b] grouped by expert pair */
     CLEARMOE_STAGE_Y_PAIR = 18,        /* top-2: y grouped by pair, rows scattered */
-    CLEARMOE_N_STAGES = 19
+    CLEARMOE_STAGE_RESIDUAL_ADD = 19,  /* stack: x_{l+1} = x_l + f_l(x_l) */
+    CLEARMOE_N_STAGES = 20
 };
+
+/* One layer of a chained FFN stack (clearmoe_stack_forward).  The paper
+ * expertises the L/2 best-scoring of a ViT's L blocks (Sec. III Phase 2; six
+ * of twelve for DeiT) and keeps the others dense.
+ *   moe == 0: the dense FFN  f(x) = GELU(x W1^T + b1) W2^T + b2
+ *             (W1 [H, D], b1 [H], W2 [D, H], b2 [D]; the other fields unused);
+ *   moe == 1: a CLEAR-MoE layer with k experts per token, weights as in
+ *             clearmoe_ffn_forward_ex (W1, b1, US, Vt, b2, P, Q and the router;
+ *             class tokens through router.dense_stride / router.W2).
+ * Every layer has the stack's T, D, H, E, r, q and dtype. */
+typedef struct {
+    int32_t moe;
+    int32_t k;
+    const void* W1;
+    const float* b1;
+    const void* US;
+    const void* Vt;
+    const float* b2;
+    const void* P;
+    const void* Q;
+    const void* W2;
+    clearmoe_router router;
+} clearmoe_stack_layer;
+
+/* Bytes of workspace clearmoe_stack_forward needs (the largest layer's
+ * workspace plus three [T, D] activation buffers); 0 if the shape or a
+ * layer's k is invalid or n < 1. */
+size_t clearmoe_stack_workspace_bytes(const clearmoe_shape* shape,
+                                      const clearmoe_stack_layer* layers, int32_t n);
+
+/* A chain of n FFN layers, each feeding the next (multi-layer integration of
+ * Sec. III Phase 2): with residual != 0 every layer adds its input back,
+ * x_{l+1} = x_l + f_l(x_l) (the FFN sublayer of a transformer block with its
+ * skip connection; layer norms and attention are outside this path), else
+ * x_{l+1} = f_l(x_l); y = x_n.  x [T, D] in, y [T, D] out (dtype), both
+ * caller-owned; x_l lives in the workspace between layers, rounded to dtype
+ * like y, and f_l is rounded to dtype before the add.  All layers run on
+ * `stream` in order; argument checks cover every layer before anything is
+ * launched.  shape->k is ignored (each layer has its own). */
+int clearmoe_stack_forward(const clearmoe_shape* shape, const clearmoe_stack_layer* layers,
+                           int32_t n, int32_t residual, const void* x, void* y, void* ws,
+                           size_t ws_bytes, hipStream_t stream);
 
 /* Name of a stage (static string; "?" if out of range). */
 const char* clearmoe_stage_name(int stage);

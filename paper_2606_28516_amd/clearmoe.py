@@ -18,7 +18,9 @@ __all__ = ["ClearMoEError", "Shape", "lib", "version", "workspace_bytes", "alloc
            "route", "dispatch", "combine", "ffn_forward", "from_stored", "to_stored",
            "DISPATCH_HIST_IN_WS", "F32", "BF16", "SYMBOLS", "N_STAGES", "stage_names",
            "timing_start", "timing_stop", "make_shape", "dense_ffn_forward",
-           "padded_workspace_bytes", "ffn_forward_padded", "ffn_forward_noalloc", "Router", "make_router", "route_ex",
+           "padded_workspace_bytes", "ffn_forward_padded", "ffn_forward_noalloc",
+           "StackLayer", "make_stack_layer", "stack_shape", "stack_workspace_bytes",
+           "stack_forward", "Router", "make_router", "route_ex",
            "ffn_forward_ex"]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -30,10 +32,11 @@ SYMBOLS = ("clearmoe_version", "clearmoe_source_digest", "clearmoe_status_string
            "clearmoe_dense_ffn_forward", "clearmoe_stage_name", "clearmoe_timing_start",
            "clearmoe_timing_start_sampled", "clearmoe_timing_stop", "clearmoe_padded_workspace_bytes",
            "clearmoe_ffn_forward_padded", "clearmoe_route_ex", "clearmoe_ffn_forward_ex",
-           "clearmoe_ffn_forward_noalloc")
+           "clearmoe_ffn_forward_noalloc", "clearmoe_stack_workspace_bytes",
+           "clearmoe_stack_forward")
 NOALLOC_SCRATCH_BYTES = 64 << 20
 ERR_TOO_LARGE = 5
-N_STAGES = 19
+N_STAGES = 20
 
 
 class ClearMoEError(RuntimeError):
@@ -51,6 +54,15 @@ class Router(ctypes.Structure):
                 ("bh", ctypes.c_void_p), ("W2", ctypes.c_void_p), ("hidden", ctypes.c_int32),
                 ("adaptive", ctypes.c_int32), ("dense_stride", ctypes.c_int32),
                 ("reserved", ctypes.c_int32), ("tau", ctypes.c_double)]
+
+
+class StackLayer(ctypes.Structure):
+    """clearmoe_stack_layer: a dense FFN (moe = 0) or a CLEAR-MoE layer
+    (moe = 1, k experts per token, with its router)."""
+    _fields_ = [("moe", ctypes.c_int32), ("k", ctypes.c_int32), ("W1", ctypes.c_void_p),
+                ("b1", ctypes.c_void_p), ("US", ctypes.c_void_p), ("Vt", ctypes.c_void_p),
+                ("b2", ctypes.c_void_p), ("P", ctypes.c_void_p), ("Q", ctypes.c_void_p),
+                ("W2", ctypes.c_void_p), ("router", Router)]
 
 
 _lib = None
@@ -100,6 +112,12 @@ def lib():
         L.clearmoe_ffn_forward_padded.argtypes = [sp] + [vp] * 13 + [vp, sz, vp]
         L.clearmoe_ffn_forward_noalloc.restype = ctypes.c_int
         L.clearmoe_ffn_forward_noalloc.argtypes = [sp] + [vp] * 13 + [vp]
+        lp = ctypes.POINTER(StackLayer)
+        L.clearmoe_stack_workspace_bytes.restype = sz
+        L.clearmoe_stack_workspace_bytes.argtypes = [sp, lp, ctypes.c_int32]
+        L.clearmoe_stack_forward.restype = ctypes.c_int
+        L.clearmoe_stack_forward.argtypes = [sp, lp, ctypes.c_int32, ctypes.c_int32, vp, vp, vp, sz,
+                                             vp]
         L.clearmoe_dense_ffn_forward.restype = ctypes.c_int
         L.clearmoe_dense_ffn_forward.argtypes = [sp] + [vp] * 6 + [vp, sz, vp]
         L.clearmoe_stage_name.restype = ctypes.c_char_p
@@ -325,6 +343,46 @@ def dense_ffn_forward(x, W1, b1, W2, b2, ws: Optional[torch.Tensor] = None,
     rc = lib().clearmoe_dense_ffn_forward(ctypes.byref(s), _p(x), _p(W1), _p(b1), _p(W2), _p(b2),
                                           _p(y), _p(ws), ws.numel(), _stream(stream))
     _check(rc, "clearmoe_dense_ffn_forward")
+    return y
+
+
+def make_stack_layer(W1, b1, b2, US=None, Vt=None, P=None, Q=None, router: Optional[Router] = None,
+                     k: int = 1, W2=None) -> StackLayer:
+    """A stack layer over device tensors (keep them alive while it is used):
+    dense when router is None (W1, b1, W2, b2), else a CLEAR-MoE layer."""
+    p = lambda t: None if t is None else _p(t).value  # noqa: E731
+    if router is None:
+        return StackLayer(0, 1, p(W1), p(b1), None, None, p(b2), None, None, p(W2), Router())
+    return StackLayer(1, int(k), p(W1), p(b1), p(US), p(Vt), p(b2), p(P), p(Q), p(W2), router)
+
+
+def stack_shape(x, H: int, E: int, r: int, q: int) -> Shape:
+    T, D = x.shape
+    return make_shape(T, D, E, 1, _dt(x), H=H, r=r, q=q)
+
+
+def stack_workspace_bytes(shape: Shape, layers) -> int:
+    arr = (StackLayer * len(layers))(*layers)
+    return int(lib().clearmoe_stack_workspace_bytes(ctypes.byref(shape), arr, len(layers)))
+
+
+def stack_forward(x, layers, H: int, E: int, r: int, q: int, residual: bool = True,
+                  ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                  stream=None):
+    """clearmoe_stack_forward: x through the chain of layers (each a
+    StackLayer), x_{l+1} = x_l + f_l(x_l) with residual, else f_l(x_l).
+    Returns y [T, D]."""
+    s = stack_shape(x, H, E, r, q)
+    arr = (StackLayer * len(layers))(*layers)
+    if ws is None:
+        n = int(lib().clearmoe_stack_workspace_bytes(ctypes.byref(s), arr, len(layers)))
+        if n == 0:
+            raise ClearMoEError("invalid stack")
+        ws = torch.empty(n, dtype=torch.uint8, device=x.device)
+    y = torch.empty_like(x) if out is None else out
+    rc = lib().clearmoe_stack_forward(ctypes.byref(s), arr, len(layers), 1 if residual else 0,
+                                      _p(x), _p(y), _p(ws), ws.numel(), _stream(stream))
+    _check(rc, "clearmoe_stack_forward")
     return y
 
 

@@ -961,11 +961,128 @@ int clearmoe_dense_ffn_forward(const clearmoe_shape* shape, const void* x, const
     return CLEARMOE_OK;
 }
 
+}  // extern "C"
+
+namespace {
+
+// The dense FFN y = GELU(x W1^T + b1) W2^T + b2 with z in the workspace.
+int dense_impl(const clearmoe_shape& s, const void* x, const void* W1, const float* b1,
+               const void* W2, const float* b2, void* y, void* z, hipStream_t st) {
+    GemmDesc g = gemm_desc(s.T, s.H, s.D);
+    g.A = x; g.lda = s.D;
+    g.B = W1; g.ldb = s.D;
+    g.C = z; g.ldc = s.H; g.c_f32 = 0;
+    g.bias = b1; g.gelu = 1;
+    CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
+    g = gemm_desc(s.T, s.D, s.H);
+    g.A = z; g.lda = s.H;
+    g.B = W2; g.ldb = s.H;
+    g.C = y; g.ldc = s.D; g.c_f32 = 0;
+    g.bias = b2;
+    CLEARMOE_STAGE(CLEARMOE_STAGE_DENSE_FC2, st, launch_gemm(s.dtype, g, st));
+    return CLEARMOE_OK;
+}
+
+// The shape of stack layer l (the stack's shape with the layer's k).
+clearmoe_shape stack_layer_shape(const clearmoe_shape& s, const clearmoe_stack_layer& L) {
+    clearmoe_shape sl = s;
+    sl.k = L.moe ? L.k : 1;
+    return sl;
+}
+
+// Largest per-layer workspace of a stack (0 if a layer is invalid).
+size_t stack_layer_bytes(const clearmoe_shape& s, const clearmoe_stack_layer* layers, int32_t n) {
+    size_t most = 0;
+    for (int32_t l = 0; l < n; ++l) {
+        if (layers[l].moe != 0 && layers[l].moe != 1) return 0;
+        const clearmoe_shape sl = stack_layer_shape(s, layers[l]);
+        if (check_shape(&sl, true) != CLEARMOE_OK) return 0;
+        const size_t b = layout(sl).total;
+        if (b > most) most = b;
+    }
+    return up(most);
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t clearmoe_stack_workspace_bytes(const clearmoe_shape* shape,
+                                      const clearmoe_stack_layer* layers, int32_t n) {
+    if (shape == nullptr || layers == nullptr || n < 1) return 0;
+    const size_t most = stack_layer_bytes(*shape, layers, n);
+    if (most == 0) return 0;
+    const size_t act = up(elem_size(shape->dtype) * static_cast<size_t>(shape->T > 0 ? shape->T : 0) *
+                          static_cast<size_t>(shape->D));
+    return most + 3 * act;
+}
+
+int clearmoe_stack_forward(const clearmoe_shape* shape, const clearmoe_stack_layer* layers,
+                           int32_t n, int32_t residual, const void* x, void* y, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+    if (shape == nullptr || layers == nullptr || n < 1) return CLEARMOE_ERR_INVALID_ARG;
+    if (residual != 0 && residual != 1) return CLEARMOE_ERR_INVALID_ARG;
+    const clearmoe_shape& s = *shape;
+    // every layer's arguments are checked before the first launch
+    for (int32_t l = 0; l < n; ++l) {
+        const clearmoe_stack_layer& L = layers[l];
+        if (L.moe != 0 && L.moe != 1) return CLEARMOE_ERR_INVALID_ARG;
+        const clearmoe_shape sl = stack_layer_shape(s, L);
+        int rc;
+        if (L.moe) {
+            rc = check_layer_args(&sl, x, L.W1, L.b1, L.US, L.Vt, L.b2, L.P, L.Q, nullptr, nullptr,
+                                  y, nullptr, nullptr);
+            if (rc == CLEARMOE_OK) rc = check_router(sl, &L.router);
+            if (rc == CLEARMOE_OK && L.router.dense_stride > 0 && L.router.W2 == nullptr)
+                rc = CLEARMOE_ERR_INVALID_ARG;
+        } else {
+            rc = check_shape(&sl, true);
+            if (rc == CLEARMOE_OK && (!L.W1 || !L.W2 || !aligned(L.W1, 16) || !aligned(L.W2, 16) ||
+                                      (L.b1 && !aligned(L.b1, 4)) || (L.b2 && !aligned(L.b2, 4))))
+                rc = CLEARMOE_ERR_INVALID_ARG;
+        }
+        if (rc != CLEARMOE_OK) return rc;
+    }
+    if (s.T > 0 && (!x || !y || !aligned(x, 16) || !aligned(y, 16))) return CLEARMOE_ERR_INVALID_ARG;
+    const size_t need = clearmoe_stack_workspace_bytes(shape, layers, n);
+    if (need == 0) return CLEARMOE_ERR_INVALID_ARG;
+    if (!ws || !aligned(ws, kAlign) || ws_bytes < need) return CLEARMOE_ERR_WORKSPACE;
+    if (s.T == 0) return CLEARMOE_OK;
+
+    // workspace: the layers' own region first, then activations A, B and the
+    // layer output F
+    const size_t most = stack_layer_bytes(s, layers, n);
+    const size_t act = up(elem_size(s.dtype) * static_cast<size_t>(s.T) * static_cast<size_t>(s.D));
+    void* buf[2] = {at<void>(ws, most), at<void>(ws, most + act)};
+    void* F = at<void>(ws, most + 2 * act);
+    const void* cur = x;
+    for (int32_t l = 0; l < n; ++l) {
+        const clearmoe_stack_layer& L = layers[l];
+        const clearmoe_shape sl = stack_layer_shape(s, L);
+        void* out = l == n - 1 ? y : buf[l % 2];
+        void* f = residual ? F : out;
+        int rc;
+        if (L.moe) {
+            rc = ffn_forward_impl(&sl, &L.router, cur, L.W1, L.b1, L.US, L.Vt, L.b2, L.P, L.Q, f,
+                                  nullptr, nullptr, ws, most, stream);
+        } else {
+            rc = dense_impl(sl, cur, L.W1, L.b1, L.W2, L.b2, f, at<void>(ws, layout(sl).z), stream);
+        }
+        if (rc != CLEARMOE_OK) return rc;
+        if (residual)
+            CLEARMOE_STAGE(CLEARMOE_STAGE_RESIDUAL_ADD, stream,
+                           launch_residual_add(s.dtype, cur, F, out, s.T, s.D, stream));
+        cur = out;
+    }
+    return CLEARMOE_OK;
+}
+
 const char* clearmoe_stage_name(int stage) {
     static const char* names[CLEARMOE_N_STAGES] = {
         "route", "tile_hist", "scan", "permute", "combine", "fc1_gelu",
         "basis_t", "basis_h", "res_u", "res_h", "combine_res", "dense_fc2", "tu_grouped",
-        "y_grouped", "fused_top1", "pad_index", "pair_key", "tu_pair", "y_pair"};
+        "y_grouped", "fused_top1", "pad_index", "pair_key", "tu_pair", "y_pair",
+        "residual_add"};
     return (stage >= 0 && stage < CLEARMOE_N_STAGES) ? names[stage] : "?";
 }
 

@@ -490,6 +490,44 @@ hipError_t launch_combine_residual(int dtype, const float* hsh, const float* hre
     return hipGetLastError();
 }
 
+// out = x + f element by element (float32 sum, one rounding to the storage
+// type): the skip connection around a stack's FFN layer.  16-byte pieces.
+template <typename T>
+__global__ __launch_bounds__(256) void k_residual_add(const T* __restrict__ x,
+                                                      const T* __restrict__ f,
+                                                      T* __restrict__ out, int64_t n16) {
+    const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= n16) return;
+    constexpr int P = Elem<T>::per16;
+    const uint4 xa = reinterpret_cast<const uint4*>(x)[i];
+    const uint4 fa = reinterpret_cast<const uint4*>(f)[i];
+    const T* xv = reinterpret_cast<const T*>(&xa);
+    const T* fv = reinterpret_cast<const T*>(&fa);
+    float v[P];
+#pragma unroll
+    for (int j = 0; j < P; ++j) v[j] = Elem<T>::to_f32(xv[j]) + Elem<T>::to_f32(fv[j]);
+    uint4 o;
+    T* ov = reinterpret_cast<T*>(&o);
+#pragma unroll
+    for (int j = 0; j < P; ++j) ov[j] = Elem<T>::from_f32(v[j]);
+    reinterpret_cast<uint4*>(out)[i] = o;
+}
+
+hipError_t launch_residual_add(int dtype, const void* x, const void* f, void* out, int64_t T, int D,
+                               hipStream_t st) {
+    const int per16 = dtype == 0 ? 4 : 8;
+    const int64_t n16 = T * (D / per16);
+    if (n16 == 0) return hipSuccess;
+    const unsigned blocks = static_cast<unsigned>((n16 + 255) / 256);
+    if (dtype == 0)
+        launch_kernel(k_residual_add<float>, blocks, 256, 0, st, static_cast<const float*>(x),
+                      static_cast<const float*>(f), static_cast<float*>(out), n16);
+    else
+        launch_kernel(k_residual_add<bf16_bits>, blocks, 256, 0, st, static_cast<const bf16_bits*>(x),
+                      static_cast<const bf16_bits*>(f), static_cast<bf16_bits*>(out), n16);
+    return hipGetLastError();
+}
+
 // Pair keys of a top-2 routing: token t with experts {a, b}, a < b, gets key
 // a E + b and its two gates in that order, g2 = (gate of a, gate of b); a
 // token with one expert e (the other slot empty) gets the diagonal key e E + e

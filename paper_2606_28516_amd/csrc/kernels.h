@@ -198,6 +198,9 @@ hipError_t launch_combine_residual(int dtype, const float* hsh, const float* hre
 constexpr int kPairMaxKeys = 64;
 hipError_t launch_pair_key(const int32_t* idx, const float* gate, int64_t T, int E, int32_t* key,
                            float* g2, hipStream_t st);
+// out = x + f (dtype, [T, D], D a multiple of 8 for bf16 / 4 for float32).
+hipError_t launch_residual_add(int dtype, const void* x, const void* f, void* out, int64_t T, int D,
+                               hipStream_t st);
 // Index maps of the padded-batch backend (expert e owns rows [e C, e C + C)):
 // perm_pad [E C] (-1 = padding), inv_pad [A], seg [E + 1] = e C.
 hipError_t launch_pad_index(const int32_t* idx, const int32_t* counts, const int32_t* offsets,

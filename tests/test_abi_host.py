@@ -245,3 +245,36 @@ def test_route_ex_and_ffn_ex_reject_bad_routers_before_launch():
                                      *args, FAKE, n, None) == 1
     assert L.clearmoe_ffn_forward_ex(ctypes.byref(s), ctypes.byref(_router()), *args, FAKE, n - 1,
                                      None) == 3
+
+
+def test_stack_workspace_and_rejections_before_launch():
+    """The stack entry point sizes its workspace from its largest layer plus
+    three activation buffers, and checks every layer before launching any."""
+    L = cm.lib()
+    s = _shape(k=1)
+    f = FAKE.value
+    router = cm.Router(f, None, None, None, None, 0, 0, 0, 0, 0.0)
+    moe1 = cm.StackLayer(1, 1, f, None, f, f, None, f, f, None, router)
+    moe2 = cm.StackLayer(1, 2, f, None, f, f, None, f, f, None, router)
+    dense = cm.StackLayer(0, 1, f, None, None, None, None, None, None, f, cm.Router())
+    arr = (cm.StackLayer * 3)(moe1, dense, moe2)
+    n = L.clearmoe_stack_workspace_bytes(ctypes.byref(s), arr, 3)
+    act = 100 * 64 * 2
+    assert n >= cm.workspace_bytes(_shape(k=2)) + 3 * act
+    assert L.clearmoe_stack_workspace_bytes(ctypes.byref(s), arr, 0) == 0
+    bad = (cm.StackLayer * 3)(moe1, dense, cm.StackLayer(2, 1, f, None, f, f, None, f, f, None,
+                                                         router))
+    assert L.clearmoe_stack_workspace_bytes(ctypes.byref(s), bad, 3) == 0
+    # the third layer has no W1: refused although the first two are valid
+    nw1 = cm.StackLayer(1, 2, None, None, f, f, None, f, f, None, router)
+    arr2 = (cm.StackLayer * 3)(moe1, dense, nw1)
+    assert L.clearmoe_stack_forward(ctypes.byref(s), arr2, 3, 1, FAKE, FAKE, FAKE, n, None) == 1
+    # k > E in a layer, a dense layer without W2, a bad residual flag
+    bigk = (cm.StackLayer * 1)(cm.StackLayer(1, 5, f, None, f, f, None, f, f, None, router))
+    assert L.clearmoe_stack_forward(ctypes.byref(s), bigk, 1, 1, FAKE, FAKE, FAKE, n, None) == 1
+    nw2 = (cm.StackLayer * 1)(cm.StackLayer(0, 1, f, None, None, None, None, None, None, None,
+                                            cm.Router()))
+    assert L.clearmoe_stack_forward(ctypes.byref(s), nw2, 1, 1, FAKE, FAKE, FAKE, n, None) == 1
+    assert L.clearmoe_stack_forward(ctypes.byref(s), arr, 3, 2, FAKE, FAKE, FAKE, n, None) == 1
+    # workspace one byte short
+    assert L.clearmoe_stack_forward(ctypes.byref(s), arr, 3, 1, FAKE, FAKE, FAKE, n - 1, None) == 3
