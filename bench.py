@@ -70,6 +70,9 @@ def parse():
     ap.add_argument("--traffic-probe", action="store_true",
                     help="for counter runs: one 1 GiB device copy from a cache-cold source "
                          "(known bytes, to scale the counters), then the timed steps only")
+    ap.add_argument("--dispatch-probe", action="store_true",
+                    help="for counter runs: the copy of --traffic-probe, then --steps passes "
+                         "of the 2^20-token dispatch workload only")
     return ap.parse_args()
 
 
@@ -77,6 +80,7 @@ KERNEL_SOURCES = {
     "route": ["route.hip"], "tile_hist": ["dispatch.hip"], "scan": ["dispatch.hip"],
     "permute": ["dispatch.hip"], "combine": ["dispatch.hip"], "combine_res": ["dispatch.hip"],
     "fused_top1": ["fused_kernel.h", "fused.hip", "fused_split.hip"],
+    "pair_key": ["dispatch.hip"], "residual_add": ["dispatch.hip"],
 }
 
 
@@ -160,6 +164,11 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs the GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.dispatch_probe:
+        copy_probe(torch, torch.device("cuda:0"))
+        bench_dispatch(cm, synth, torch, None, torch.cuda.current_stream(), args.steps, timed=False)
+        print(json.dumps({"dispatch_probe": True, "steps": args.steps}), flush=True)
+        return
     cfg = synth.CONFIGS[args.workload]
     L = synth.make_layer(cfg)
     core = measure_layer(cm, torch, cfg, L, args.steps, args.warmup, args.traffic_probe)
@@ -275,6 +284,19 @@ def time_dense(cm, synth, torch, np, cfg, L, d, ws, stream, steps, warmup, moe_m
             "tflops": 4 * cfg.T * cfg.D * cfg.H / (dms * 1e-3) / 1e12}
 
 
+def copy_probe(torch, dev):
+    """One device copy of exactly 1 GiB from a cache-cold source: the known
+    bytes that scale the FETCH_SIZE / WRITE_SIZE counters of a counter run."""
+    src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    flush.fill_(2)                  # evicts src from the 256 MB last-level cache
+    torch.cuda.synchronize()
+    dst.copy_(src)                  # reads and writes exactly 1 GiB
+    torch.cuda.synchronize()
+    del src, dst, flush
+
+
 def measure_layer(cm, torch, cfg, L, steps, warmup, traffic_probe=False):
     """Warm up, find the dominant kernel from a per-stage pass, then time
     exactly `steps` layer calls between two events on the stream, with the
@@ -299,14 +321,7 @@ def measure_layer(cm, torch, cfg, L, steps, warmup, traffic_probe=False):
         step()
     torch.cuda.synchronize()
     if traffic_probe:
-        src = torch.ones(1 << 30, dtype=torch.uint8, device=dev)
-        dst = torch.empty_like(src)
-        flush = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-        flush.fill_(2)                  # evicts src from the 256 MB last-level cache
-        torch.cuda.synchronize()
-        dst.copy_(src)                  # reads and writes exactly 1 GiB
-        torch.cuda.synchronize()
-        del src, dst, flush
+        copy_probe(torch, dev)
         for _ in range(steps):
             step()
         torch.cuda.synchronize()
@@ -359,7 +374,7 @@ def measure_layer(cm, torch, cfg, L, steps, warmup, traffic_probe=False):
             "wall_s": wall, "_step": step, "_d": d, "_ws": ws, "_y": y, "_stream": stream}
 
 
-def bench_dispatch(cm, synth, torch, np, stream, steps):
+def bench_dispatch(cm, synth, torch, np, stream, steps, timed=True):
     """Route -> dispatch (rows copied into expert order) -> gated combine on the
     2^20-token workload.  HBM fraction against compulsory bytes (x read once)
     and against the bytes this design moves (x read by route and by permute)."""
@@ -397,6 +412,11 @@ def bench_dispatch(cm, synth, torch, np, stream, steps):
     for _ in range(3):
         run()
     torch.cuda.synchronize()
+    if not timed:                   # counter runs: the passes alone
+        for _ in range(steps):
+            run()
+        torch.cuda.synchronize()
+        return None
     # untimed steps for the step time, then timed ones for the per-kernel times
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record(stream)

@@ -59,13 +59,27 @@ def built_digest(path: str = LIB) -> str:
     return data[i + len(DIGEST_MARKER): i + len(DIGEST_MARKER) + DIGEST_LEN].decode("ascii", "replace")
 
 
+# Translation units whose device assembly is kept beside the objects (with
+# the source digest), for the CPU check of the fused kernel's counted waits.
+KEEP_ASM = ("fused.hip", "fused_split.hip")
+
+
+def device_asm(src: str) -> str:
+    """Path of the kept gfx950 assembly of a translation unit."""
+    return os.path.join(BUILD_DIR, os.path.splitext(src)[0] + f"-hip-amdgcn-amd-amdhsa-{ARCH}.s")
+
+
 def _compile(src: str, digest: str) -> str:
     obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, "-x", "hip", *FLAGS, f'-DCLEARMOE_SOURCE_DIGEST="{digest}"', "-c",
+    keep = ["-save-temps=obj"] if src in KEEP_ASM else []
+    cmd = [HIPCC, "-x", "hip", *FLAGS, *keep, f'-DCLEARMOE_SOURCE_DIGEST="{digest}"', "-c",
            os.path.join(CSRC, src), "-o", obj]
-    r = subprocess.run(cmd, capture_output=True, text=True)
+    r = subprocess.run(cmd, capture_output=True, text=True, cwd=BUILD_DIR)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{r.stdout}\n{r.stderr}")
+    if keep:
+        with open(device_asm(src) + ".digest", "w") as f:
+            f.write(digest)
     return obj
 
 

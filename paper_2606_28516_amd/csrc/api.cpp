@@ -42,7 +42,7 @@ size_t elem_size(int dtype) { return dtype == CLEARMOE_F32 ? 4 : 2; }
 
 // Top-2 layers with few experts run in pair order: tokens sorted by their
 // expert pair, one [t|u_a|u_b] product and one y product per pair segment.
-bool pair_path(const clearmoe_shape& s) { return s.k == 2 && s.E * s.E <= kPairMaxKeys; }
+bool pair_path(const clearmoe_shape& s) { return s.k == 2 && pair_keys(s.E) <= kPairMaxKeys; }
 
 Layout layout(const clearmoe_shape& s) {
     Layout L{};
@@ -75,9 +75,9 @@ Layout layout(const clearmoe_shape& s) {
     L.hres = take(sizeof(float) * T * k * s.D);
     L.tu = take(es * T * k * (s.r + s.q));
     if (pair_path(s)) {
-        const int64_t P = E * E;
+        const int64_t P = pair_keys(static_cast<int>(E));
         L.pkey = take(sizeof(int32_t) * T);
-        L.pgate = take(sizeof(float) * 2 * T);
+        L.pgate = take(sizeof(float) * 2 * T);       // [2][T]: gates of a, of b
         L.pperm = take(sizeof(int32_t) * T);
         L.pinv = take(sizeof(int32_t) * T);
         L.pcounts = take(sizeof(int32_t) * P);
@@ -90,12 +90,14 @@ Layout layout(const clearmoe_shape& s) {
     // float32 partials and per-tile arrival counters: of the fused top-1
     // kernel's hidden split (small batches), or else, on the top-1 GEMM
     // chain, of the [t|u] product's split K
-    const bool fused = k == 1 && s.dtype == CLEARMOE_BF16 && fused_top1_supported(s.D, s.H, s.r, s.q);
+    // (a top-2 pair order's single-expert tokens take the top-1 path)
+    const bool fused_ok = s.dtype == CLEARMOE_BF16 && fused_top1_supported(s.D, s.H, s.r, s.q);
+    const bool top1 = k == 1 || pair_path(s);
     size_t fpart = 0, fcount = 0;
-    if (fused && T > 0) {
+    if (top1 && fused_ok && T > 0) {
         fpart = fused_part_bytes(T, static_cast<int>(E), s.H, s.r, s.q);
         fcount = fpart > 0 ? static_cast<size_t>(T / 64 + E + 1) : 0;
-    } else if (k == 1 && T > 0) {
+    } else if (top1 && T > 0) {
         fpart = kGemmKsplitBytes;
         fcount = kGemmKsplitTiles;
     }
@@ -135,11 +137,11 @@ Layout layout_min(const clearmoe_shape& s) {
     const int64_t ntiles = route_tiles(T);
     L.tile_counts = take(sizeof(int32_t) * hist_tiles(T, static_cast<int>(E)) * E);
     if (pair) {
-        const int64_t P = E * E;
+        const int64_t P = pair_keys(static_cast<int>(E));
         L.idx = take(sizeof(int32_t) * T * k);
         L.gate = take(sizeof(float) * T * k);
         L.pkey = take(sizeof(int32_t) * T);
-        L.pgate = take(sizeof(float) * 2 * T);
+        L.pgate = take(sizeof(float) * 2 * T);       // [2][T]: gates of a, of b
         L.pperm = take(sizeof(int32_t) * T);
         L.pinv = take(sizeof(int32_t) * T);
         L.pcounts = take(sizeof(int32_t) * P);
@@ -700,23 +702,27 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
     }
 
     if (pair_path(s)) {
-        // Top-2 in pair order: every token's two experts {a, b} (a < b) name
-        // its segment, so the shared basis and both residuals merge into two
-        // grouped products over the pair order p:
+        // Top-2 in pair order.  Tokens are sorted by key: first the tokens
+        // with one expert e (key e; only an adaptive router leaves a slot
+        // empty), then those with two experts {a, b}, a < b (key E + the
+        // pair's number).  Each pair segment merges the shared basis and both
+        // residuals into two grouped products over the pair order p:
         //   [t | u_a | u_b](p) = z[pt] [Vt ; Q_a ; Q_b]^T, u_a times gate_a,
         //                        u_b times gate_b;
         //   y[pt] = [t | u_a | u_b](p) [US | P_a | P_b]^T + b2,
         // with pt = pperm[p]: each y row is written once, and neither h_sh
-        // nor h_res is formed.
-        const int npk = s.E * s.E;
+        // nor h_res is formed.  Single-expert tokens take the top-1 path over
+        // the first E segments (the fused kernel where it applies).
+        const int nkeys = pair_keys(s.E), npairs = nkeys - s.E;
         int32_t* pkey = at<int32_t>(ws, L.pkey);
-        float* pgate = at<float>(ws, L.pgate);
+        float* pga = at<float>(ws, L.pgate);
+        float* pgb = pga + T;
         int32_t* pperm = at<int32_t>(ws, L.pperm);
         int32_t* poffsets = at<int32_t>(ws, L.poffsets);
         CLEARMOE_STAGE(CLEARMOE_STAGE_PAIR_KEY, st,
-                       launch_pair_key(idx, gate, T, s.E, pkey, pgate, st));
+                       launch_pair_key(idx, gate, T, s.E, pkey, pga, pgb, st));
         clearmoe_shape sp = s;
-        sp.E = npk;
+        sp.E = nkeys;
         sp.k = 1;
         Layout Lp = L;
         Lp.tile_counts = L.ptc;
@@ -725,24 +731,75 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
         rc = dispatch_impl(sp, Lp, pkey, ws, at<int32_t>(ws, L.pcounts), poffsets, pperm,
                            at<int32_t>(ws, L.pinv), nullptr, nullptr, false, st);
         if (rc != CLEARMOE_OK) return rc;
-        GemmDesc g = gemm_desc(T, s.H, s.D);
-        g.A = x; g.lda = s.D;
-        g.B = W1; g.ldb = s.D;
-        g.C = z; g.ldc = s.H; g.c_f32 = 0;
-        g.bias = b1; g.gelu = 1;
-        CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
+        const bool singles = router->adaptive != 0;
+        const bool fused_ok = s.dtype == CLEARMOE_BF16 && fused_top1_supported(s.D, s.H, s.r, s.q);
+        const int32_t* pair_seg = poffsets + s.E;
+        GemmDesc g;
+        bool z_pair_order = false;
+        if (singles && fused_ok) {
+            // single-expert tokens: the fused top-1 kernel over the first E
+            // segments, with the gate of their one expert
+            CLEARMOE_STAGE(CLEARMOE_STAGE_FUSED_TOP1, st,
+                           launch_fused_top1(x, W1, b1, US, Vt, b2, P, Q, pperm, poffsets, nullptr,
+                                             nullptr, pga, y, T, s.D, s.H, s.E, s.r, s.q,
+                                             at<float>(ws, L.fpart), at<int32_t>(ws, L.fcount), st));
+            // two-expert tokens: fc1 + GELU on their rows only, z in pair order
+            g = gemm_desc(T, s.H, s.D);
+            g.A = x; g.lda = s.D; g.a_rows = pperm; g.a_div = 1;
+            g.B = W1; g.ldb = s.D;
+            g.C = z; g.ldc = s.H; g.c_f32 = 0;
+            g.bias = b1; g.gelu = 1;
+            g.seg_offsets = pair_seg; g.nseg = npairs; g.seg_merge = 1;
+            CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
+            z_pair_order = true;
+        } else {
+            g = gemm_desc(T, s.H, s.D);
+            g.A = x; g.lda = s.D;
+            g.B = W1; g.ldb = s.D;
+            g.C = z; g.ldc = s.H; g.c_f32 = 0;
+            g.bias = b1; g.gelu = 1;
+            CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
+            if (singles) {
+                // single-expert tokens: the top-1 chain's two grouped products
+                void* tu = at<void>(ws, L.tu);
+                const int rq = s.r + s.q;
+                g = gemm_desc(T, rq, s.H);
+                g.A = z; g.lda = s.H; g.a_rows = pperm; g.a_div = 1;
+                g.B = Vt; g.ldb = s.H;
+                g.B1 = Q; g.ldb1 = s.H; g.b1_seg_stride = static_cast<int64_t>(s.q) * s.H;
+                g.n_split = s.r;
+                g.C = tu; g.ldc = rq; g.c_f32 = 0;
+                g.row_scale = pga; g.scale_rows = pperm; g.scale_col0 = s.r;
+                g.seg_offsets = poffsets; g.nseg = s.E;
+                g.ks_part = at<float>(ws, L.fpart); g.ks_count = at<int32_t>(ws, L.fcount);
+                if (rq > 0) CLEARMOE_STAGE(CLEARMOE_STAGE_TU, st, launch_gemm(s.dtype, g, st));
+                g = gemm_desc(T, s.D, rq);
+                g.A = tu; g.lda = rq;
+                g.B = US; g.ldb = s.r;
+                g.B1 = P; g.ldb1 = s.q; g.b1_seg_stride = static_cast<int64_t>(s.D) * s.q;
+                g.k_split = s.r;
+                g.C = y; g.ldc = s.D; g.c_f32 = 0;
+                g.c_rows = pperm; g.c_div = 1;
+                g.bias = b2;
+                g.seg_offsets = poffsets; g.nseg = s.E;
+                CLEARMOE_STAGE(CLEARMOE_STAGE_Y, st, launch_gemm(s.dtype, g, st));
+            }
+        }
         void* ptu = at<void>(ws, L.ptu);
         const int rqq = s.r + 2 * s.q;
         g = gemm_desc(T, rqq, s.H);
-        g.A = z; g.lda = s.H; g.a_rows = pperm; g.a_div = 1;
+        g.A = z; g.lda = s.H;
+        if (!z_pair_order) {
+            g.a_rows = pperm; g.a_div = 1;
+        }
         g.B = Vt; g.ldb = s.H;
         g.B1 = Q; g.ldb1 = s.H; g.b1_seg_stride = static_cast<int64_t>(s.q) * s.H;
         g.B2 = Q; g.ldb2 = s.H; g.b2_seg_stride = static_cast<int64_t>(s.q) * s.H;
         g.n_split = s.r; g.n_split2 = s.r + s.q; g.pair_E = s.E;
         g.C = ptu; g.ldc = rqq; g.c_f32 = 0;
-        g.row_scale = pgate; g.scale_rows = pperm; g.rs_stride = 2;
+        g.row_scale = pga; g.row_scale2 = pgb; g.scale_rows = pperm;
         g.scale_col0 = s.r; g.scale_col1 = s.r + s.q;
-        g.seg_offsets = poffsets; g.nseg = npk;
+        g.seg_offsets = pair_seg; g.nseg = npairs;
         if (rqq > 0) CLEARMOE_STAGE(CLEARMOE_STAGE_TU_PAIR, st, launch_gemm(s.dtype, g, st));
         g = gemm_desc(T, s.D, rqq);
         g.A = ptu; g.lda = rqq;
@@ -753,9 +810,11 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
         g.C = y; g.ldc = s.D; g.c_f32 = 0;
         g.c_rows = pperm; g.c_div = 1;
         g.bias = b2;
-        g.seg_offsets = poffsets; g.nseg = npk;
+        g.seg_offsets = pair_seg; g.nseg = npairs;
         CLEARMOE_STAGE(CLEARMOE_STAGE_Y_PAIR, st, launch_gemm(s.dtype, g, st));
-        if (cls) return class_tokens_impl(s, *router, x, W1, b1, b2, z, true, y, st);
+        // class tokens: their dense FFN output, from the token-order z when
+        // there is one
+        if (cls) return class_tokens_impl(s, *router, x, W1, b1, b2, z, !z_pair_order, y, st);
         return CLEARMOE_OK;
     }
 

@@ -528,14 +528,15 @@ hipError_t launch_residual_add(int dtype, const void* x, const void* f, void* ou
     return hipGetLastError();
 }
 
-// Pair keys of a top-2 routing: token t with experts {a, b}, a < b, gets key
-// a E + b and its two gates in that order, g2 = (gate of a, gate of b); a
-// token with one expert e (the other slot empty) gets the diagonal key e E + e
-// and gates (gate of e, 0); a token with none gets key -1 (no segment).
+// Pair keys of a top-2 routing (see launch_pair_key): a token with one expert
+// e gets key e and gates (gate of e, 0); one with experts a < b gets key
+// E + (number of the pair (a, b) in lexicographic order) and gates (gate of
+// a, gate of b); one with none gets -1 (no segment).
 __global__ __launch_bounds__(256) void k_pair_key(const int32_t* __restrict__ idx,
                                                   const float* __restrict__ gate, int64_t T,
                                                   int E, int32_t* __restrict__ key,
-                                                  float* __restrict__ g2) {
+                                                  float* __restrict__ ga,
+                                                  float* __restrict__ gb) {
     const int64_t t = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
     if (t >= T) return;
     // idx and gate may be only 4-byte aligned (caller arrays): two loads each
@@ -544,24 +545,25 @@ __global__ __launch_bounds__(256) void k_pair_key(const int32_t* __restrict__ id
     const bool v0 = e.x >= 0 && e.x < E, v1 = e.y >= 0 && e.y < E;
     int32_t k = -1;
     float2 o = make_float2(0.0f, 0.0f);
-    if (v0 && v1) {
+    if (v0 && v1 && e.x != e.y) {
         const bool lo0 = e.x < e.y;
-        k = lo0 ? e.x * E + e.y : e.y * E + e.x;
+        const int a = lo0 ? e.x : e.y, b = lo0 ? e.y : e.x;
+        k = E + a * (2 * E - a - 1) / 2 + (b - a - 1);
         o = lo0 ? g : make_float2(g.y, g.x);
     } else if (v0 || v1) {
-        const int ee = v0 ? e.x : e.y;
-        k = ee * E + ee;
+        k = v0 ? e.x : e.y;
         o = make_float2(v0 ? g.x : g.y, 0.0f);
     }
     key[t] = k;
-    *reinterpret_cast<float2*>(g2 + 2 * t) = o;
+    ga[t] = o.x;
+    gb[t] = o.y;
 }
 
 hipError_t launch_pair_key(const int32_t* idx, const float* gate, int64_t T, int E, int32_t* key,
-                           float* g2, hipStream_t st) {
+                           float* ga, float* gb, hipStream_t st) {
     if (T == 0) return hipSuccess;
     launch_kernel(k_pair_key, dim3(static_cast<unsigned>((T + 255) / 256)), 256, 0, st, idx, gate,
-                  T, E, key, g2);
+                  T, E, key, ga, gb);
     return hipGetLastError();
 }
 

@@ -26,9 +26,10 @@
 //     own loads of stage kt before the workgroup barrier;
 //   * lanes whose row or k chunk is outside the operand load a 16-byte zero
 //     page instead, so tails need no special path and never read out of bounds;
-//   * tiles are ordered XCD-major: workgroup i runs on XCD i % 8, and each XCD
-//     walks a contiguous range of tiles (N fastest), so the A rows of a tile
-//     stay in one XCD's L2;
+//   * tiles are spread by row tile over the XCDs: workgroup i runs on XCD
+//     i % 8, which takes every eighth row tile with all its column tiles, so
+//     the A rows of a tile stay in one XCD's L2 and the leading row tiles
+//     (all a grouped product's rows when its segments hold few) use every XCD;
 //   * grouped mode: the tile index enumerates (segment, M-tile) pairs in
 //     segment order, read from the device offsets; surplus workgroups exit.
 #include "kernels.h"
@@ -121,17 +122,31 @@ void k_gemm(GemmDesc g, int mtiles, int ntiles, int per_xcd, int ksplit) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave / WN, wn = wave % WN;
 
-    // ---- tile of this workgroup (XCD-major order); with split K, S
-    //      consecutive workgroups (one XCD) share a tile, part kp taking its
-    //      share of the k stages
-    const int wg = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    // ---- tile of this workgroup.  Workgroup b runs on XCD x = b % 8 as its
+    //      i-th (i = b / 8); XCD x takes the row tiles x, x + 8, x + 16, ...,
+    //      each with all its column tiles in turn, so one XCD's L2 serves the
+    //      A rows of a row tile, and the first row tiles -- the only ones
+    //      with rows when a grouped product's segments hold fewer rows than
+    //      its bound M -- spread over every XCD.  With split K, S consecutive
+    //      workgroups of one XCD share a tile, part kp taking its share of
+    //      the k stages.
+    (void)per_xcd;
     const int S = g.ks_part != nullptr ? ksplit : 1;
-    const int tile = wg / S, kp = wg - tile * S;
-    if (tile >= mtiles * ntiles) return;
-    const int mt = tile / ntiles, nt = tile % ntiles;
+    const int xcd = blockIdx.x % kXcds, local = blockIdx.x / kXcds;
+    const int tile_local = local / S, kp = local - tile_local * S;
+    const int mt = (tile_local / ntiles) * kXcds + xcd, nt = tile_local % ntiles;
+    if (mt >= mtiles) return;
+    const int tile = mt * ntiles + nt;
     int64_t m_lo, m_hi;
     int seg = 0;
-    if (g.seg_offsets != nullptr) {
+    if (g.seg_offsets != nullptr && g.seg_merge) {
+        int64_t lo = g.seg_offsets[0], hi = g.seg_offsets[g.nseg];
+        lo = lo < 0 ? 0 : (lo > g.M ? g.M : lo);
+        hi = hi < lo ? lo : (hi > g.M ? g.M : hi);
+        m_lo = lo + static_cast<int64_t>(mt) * BM;
+        if (m_lo >= hi) return;
+        m_hi = m_lo + BM < hi ? m_lo + BM : hi;
+    } else if (g.seg_offsets != nullptr) {
         int64_t before = 0;
         bool found = false;
         for (int e = 0; e < g.nseg; ++e) {
@@ -163,8 +178,8 @@ void k_gemm(GemmDesc g, int mtiles, int ntiles, int per_xcd, int ksplit) {
                         : nullptr;
     // parts 1 and 2 belong to the segment's expert, or, for pair segments
     // (s = a * pair_E + b), to its experts a and b
-    const int e1 = g.pair_E > 0 ? seg / g.pair_E : seg;
-    const int e2 = g.pair_E > 0 ? seg % g.pair_E : seg;
+    int e1 = seg, e2 = seg;
+    if (g.pair_E > 0) pair_experts(seg, g.pair_E, e1, e2);
     const Tin* B1 = g.B1 != nullptr
                         ? static_cast<const Tin*>(g.B1) + static_cast<int64_t>(e1) * g.b1_seg_stride
                         : nullptr;
@@ -374,8 +389,8 @@ void k_gemm(GemmDesc g, int mtiles, int ntiles, int per_xcd, int ksplit) {
         const int32_t sr = g.row_scale != nullptr ? g.scale_rows[m] : 0;
         float rs = 1.0f, rs1 = 1.0f;
         if (g.row_scale != nullptr) {
-            rs = sr >= 0 ? g.row_scale[static_cast<int64_t>(sr) * g.rs_stride] : 0.0f;
-            rs1 = g.rs_stride > 1 && sr >= 0 ? g.row_scale[static_cast<int64_t>(sr) * g.rs_stride + 1] : rs;
+            rs = sr >= 0 ? g.row_scale[sr] : 0.0f;
+            rs1 = g.row_scale2 == nullptr ? rs : (sr >= 0 ? g.row_scale2[sr] : 0.0f);
         }
         // a negative scatter index is a padding row: it is not stored
         const int64_t cr = g.c_rows != nullptr ? static_cast<int64_t>(g.c_rows[m]) : m;
@@ -440,8 +455,8 @@ static hipError_t gemm_cfg(const GemmDesc& g, hipStream_t st) {
         S = gemm_ksplit(tiles, (g.K + BK - 1) / BK);
     GemmDesc d = g;
     if (S == 1) d.ks_part = nullptr;
-    int64_t per_xcd = (tiles * S + kXcds - 1) / kXcds;
-    per_xcd = (per_xcd + S - 1) / S * S;             // a tile's parts on one XCD
+    // every XCD takes ceil(mt / 8) row tiles of nt tiles of S parts
+    const int64_t per_xcd = (mt + kXcds - 1) / kXcds * nt * S;
     const int64_t grid = per_xcd * kXcds;
     if (S > 1) {
         // the fill kernel must not take the timing events meant for the GEMM

@@ -192,12 +192,25 @@ hipError_t launch_combine_gated(int dtype, const void* ye, const int32_t* inv, c
 hipError_t launch_combine_residual(int dtype, const float* hsh, const float* hres,
                                    const int32_t* inv, void* y, int64_t T, int D, int k,
                                    int64_t hres_rows, hipStream_t st);
-// Pair order of a top-2 routing (idx, gate [T, 2]): key[t] = a E + b for
-// the token's experts a < b (e E + e with one expert, -1 with none) and
-// g2[t] = (gate of a, gate of b).  Pair segments need E * E <= kPairMaxKeys.
+// Pair order of a top-2 routing (idx, gate [T, 2]): a token with one expert
+// e (the other slot empty, as the adaptive router leaves it) gets key e; one
+// with experts a < b gets key E + pair_index(a, b), the pairs numbered in
+// lexicographic order (pair_index(a, b) = a (2E - a - 1) / 2 + b - a - 1); one
+// with none gets -1.  ga[t], gb[t] = the gates of a and b (gate of e and 0
+// for one expert).  The E (E + 1) / 2 keys must not exceed kPairMaxKeys.
 constexpr int kPairMaxKeys = 64;
+__host__ __device__ inline int pair_keys(int E) { return E * (E + 1) / 2; }
+// Experts (a, b) of pair number s (0 <= s < E (E - 1) / 2).
+__host__ __device__ inline void pair_experts(int s, int E, int& a, int& b) {
+    a = 0;
+    while (s >= E - 1 - a) {
+        s -= E - 1 - a;
+        ++a;
+    }
+    b = a + 1 + s;
+}
 hipError_t launch_pair_key(const int32_t* idx, const float* gate, int64_t T, int E, int32_t* key,
-                           float* g2, hipStream_t st);
+                           float* ga, float* gb, hipStream_t st);
 // out = x + f (dtype, [T, D], D a multiple of 8 for bf16 / 4 for float32).
 hipError_t launch_residual_add(int dtype, const void* x, const void* f, void* out, int64_t T, int D,
                                hipStream_t st);
@@ -212,8 +225,10 @@ hipError_t launch_pad_index(const int32_t* idx, const int32_t* counts, const int
 // n - n_split) and rows n >= n_split2 from B2 (row n - n_split2), or columns
 // k_split <= k < k_split2 from B1 and k >= k_split2 from B2; each part has
 // its own per-segment stride (0 = shared by all segments).  Parts 1 and 2
-// take the segment's index, or with pair_E > 0 (segment s = a * pair_E + b of
-// a top-2 pair order) a for B1 and b for B2.
+// take the segment's index, or with pair_E > 0 (segment s = the s-th expert
+// pair (a, b), a < b, of a top-2 pair order; see pair_experts) a for B1 and b
+// for B2.  With seg_merge the segments' rows form one range, all with the
+// parts of segment 0.
 struct GemmDesc {
     const void* A;            // [*, K] in dtype, row stride lda (elements)
     int64_t lda;
@@ -233,17 +248,18 @@ struct GemmDesc {
     int k_split;              // columns k >= k_split come from B1 (default: K)
     int k_split2;             // columns k >= k_split2 come from B2 (default: K)
     int pair_E;               // > 0: segments are expert pairs (see above)
+    int seg_merge;            // 1: rows [seg_offsets[0], seg_offsets[nseg]) as one segment
     void* C;                  // output, row stride ldc
     int64_t ldc;
     int c_f32;                // 1: C is float32; 0: C is dtype
     const int32_t* c_rows;    // optional scatter: C row = c_rows[m] / c_div
     int c_div;
     const float* bias;        // optional [N]
-    const float* row_scale;   // optional: columns n >= scale_col0 of row m are
-    const int32_t* scale_rows;//   scaled by row_scale[scale_rows[m] * rs_stride],
-    int scale_col0;           //   and columns n >= scale_col1 by the entry after
-    int scale_col1;           //   it (rs_stride 2); a negative scale row is 0
-    int rs_stride;
+    const float* row_scale;   // optional: columns scale_col0 <= n < scale_col1 of
+    const int32_t* scale_rows;//   row m are scaled by row_scale[scale_rows[m]],
+    int scale_col0;           //   columns n >= scale_col1 by row_scale2[...]
+    int scale_col1;           //   (a negative scale row scales by 0)
+    const float* row_scale2;
     int gelu;                 // 1: GELU after bias
     int64_t M;                // rows (sum of segments when grouped)
     int N, K;
@@ -267,7 +283,6 @@ inline GemmDesc gemm_desc(int64_t M, int N, int K) {
     g.k_split = K;
     g.k_split2 = K;
     g.scale_col1 = N;
-    g.rs_stride = 1;
     g.M = M;
     g.N = N;
     g.K = K;

@@ -31,7 +31,7 @@ PADDED_LAYERS = [
     (700, 384, 1536, 4, 1, 128, 32, "bf16", 0.6),
     (411, 192, 384, 8, 2, 64, 32, "bf16", None),
     (250, 64, 64, 3, 3, 0, 8, "bf16", 0.8),          # k = E, r = 0
-    (300, 64, 128, 9, 2, 16, 8, "bf16", 0.4),        # top-2 beyond the pair order
+    (300, 64, 128, 11, 2, 16, 8, "bf16", 0.4),       # top-2 beyond the pair order
 ]
 
 
@@ -68,12 +68,12 @@ def test_padded_against_oracle(T, D, H, E, k, r, q, dt, imb):
     _check_against_oracle(L, g)
     # same routing as the grouped backend.  For k > 1 the grouped backend
     # forms h_sh and h_res apart like the padded one (same y, bit for bit),
-    # except for top-2 with E * E <= 64, which runs in expert-pair order (one
-    # product per pair segment): there the two agree to the bars.
+    # except for top-2 with E (E + 1) / 2 <= 64, which runs in expert-pair
+    # order (one product per pair segment): there the two agree to the bars.
     grouped = gpu_ffn(L)
     assert np.array_equal(g["idx"], grouped["idx"])
     assert np.array_equal(g["gate"], grouped["gate"])
-    if k == 2 and E * E <= 64:
+    if k == 2 and E * (E + 1) // 2 <= 64:
         if dt == "f32":
             assert max_rel(g["y"], grouped["y"]) <= F32_MAXREL
         else:

@@ -142,10 +142,12 @@ SMALL_LAYERS = [
     ("bf16", 257, 128, 256, 8, 1, 64, 16, "random"),
     ("bf16", 400, 64, 192, 6, 2, 32, 24, "random"),
     ("bf16", 333, 192, 384, 5, 3, 64, 32, "svd_tail"),
-    # top-2 with more experts than the pair order covers (E * E > 64): the
-    # chain with h_sh, h_res and the combine
-    ("bf16", 700, 64, 128, 9, 2, 16, 8, "random"),
+    # top-2 with more experts than the pair order covers (E (E + 1) / 2 >
+    # 64): the chain with h_sh, h_res and the combine
+    ("bf16", 700, 64, 128, 11, 2, 16, 8, "random"),
     ("f32", 301, 64, 96, 12, 2, 16, 8, "random"),
+    # the pair order at its largest key count (E = 10: 55 keys)
+    ("bf16", 1500, 64, 128, 10, 2, 32, 16, "random"),
 ]
 
 
