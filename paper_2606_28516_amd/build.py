@@ -19,7 +19,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libclearmoe.so")
 BUILD_DIR = os.path.join(ROOT, "_build", "clearmoe")
-SOURCES = ["api.cpp", "route.hip", "dispatch.hip", "gemm.hip", "fused.hip", "fused_split.hip"]
+SOURCES = ["api.cpp", "route.hip", "dispatch.hip", "gemm.hip", "fused.hip", "fused_split.hip",
+           "class_ffn.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # The library carries the digest of the sources it was built from after this

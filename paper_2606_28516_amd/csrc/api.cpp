@@ -8,6 +8,7 @@
 #include <mutex>
 #include <vector>
 
+#include "class_ffn.h"
 #include "kernels.h"
 
 using namespace clearmoe;
@@ -30,6 +31,7 @@ struct Layout {
     size_t tile_counts, tile_base, chunk_tot;     // route / dispatch
     size_t counts, offsets, idx, gate, perm, inv;  // ffn_forward
     size_t z, tproj, hsh, u, hres, tu, fpart, fcount;
+    size_t cpart, ccount;   // class rows' split over the hidden width: partial sums, arrivals
     // top-2 pair order (E * E <= kPairMaxKeys): keys, pair gates, the pair
     // permutation with its sort arrays, and [t|u_a|u_b] [T, r + 2q]
     size_t pkey, pgate, pperm, pinv, pcounts, poffsets, ptc, ptb, pct, ptu;
@@ -103,6 +105,8 @@ Layout layout(const clearmoe_shape& s) {
     }
     L.fpart = take(fpart > 0 ? fpart : 1);
     L.fcount = take(sizeof(int32_t) * (fcount > 0 ? fcount : 1));
+    L.cpart = take(kClsPartBytes);
+    L.ccount = take(sizeof(uint64_t) * kClsCountWords);
     L.total = off;
     // A padded batch holds E sub-batches of the largest expert count, which
     // can be every assignment: room for E * T * k rows.
@@ -548,10 +552,27 @@ namespace {
 // into the workspace's z region first.
 int class_tokens_impl(const clearmoe_shape& s, const clearmoe_router& rt, const void* x,
                       const void* W1, const float* b1, const float* b2, void* z, bool z_all,
-                      void* y, hipStream_t st) {
+                      void* y, const Layout& L, void* ws, hipStream_t st) {
     const int64_t sd = rt.dense_stride;
     const int64_t ncls = (s.T + sd - 1) / sd;
     int64_t zld = s.H;
+    if (!z_all && s.dtype == CLEARMOE_BF16 && class_ffn_supported(s.D, s.H)) {
+        // both products in one pass per 32 class rows (z stays on chip)
+        ClassArgs c{};
+        c.x = static_cast<const bf16_bits*>(x);
+        c.W1 = static_cast<const bf16_bits*>(W1);
+        c.b1 = b1;
+        c.W2 = static_cast<const bf16_bits*>(rt.W2);
+        c.b2 = b2;
+        c.y = static_cast<bf16_bits*>(y);
+        c.ncls = ncls;
+        c.stride = sd;
+        c.D = s.D;
+        c.H = s.H;
+        class_ffn_plan(c, at<float>(ws, L.cpart), at<uint64_t>(ws, L.ccount));
+        CLEARMOE_STAGE(CLEARMOE_STAGE_DENSE_FC2, st, launch_class_ffn(c, st));
+        return CLEARMOE_OK;
+    }
     if (z_all) {
         zld = static_cast<int64_t>(s.H) * sd;
     } else {
@@ -607,8 +628,9 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
     void* u = at<void>(ws, L.u);
     float* hres = at<float>(ws, L.hres);
 
-    // With the fused top-1 kernel the class tokens' dense path needs only x:
-    // it runs on the side stream beside routing, dispatch and the fused
+    // With the fused top-1 kernel the class tokens' dense path needs only x.
+    // Without the hidden split it runs inside the fused launch; with it (a
+    // small batch), on a side stream beside routing, dispatch and the fused
     // kernel (which leave compute units idle), into the workspace's z region
     // (unused by the fused path).
     std::unique_lock<std::mutex> side_lock;
@@ -622,14 +644,18 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
             if (!done && *side != nullptr) (void)hipStreamWaitEvent(st, (*side)->join, 0);
         }
     } join_guard{st, &side};
-    if (cls && fused) {
+    // The fused launch without the hidden split runs the class rows itself,
+    // on workgroups past its tiles.
+    const bool cls_in_fused = cls && fused && s.dtype == CLEARMOE_BF16 && fused_split(T, s.E, s.H) == 1 &&
+                              class_ffn_supported(s.D, s.H);
+    if (cls && fused && !cls_in_fused) {
         side_lock = std::unique_lock<std::mutex>(g_side_mu);
         rc = side_stream(&side);
         if (rc != CLEARMOE_OK) return rc;
         if (hipEventRecord(side->fork, st) != hipSuccess ||
             hipStreamWaitEvent(side->s, side->fork, 0) != hipSuccess)
             return CLEARMOE_ERR_HIP;
-        rc = class_tokens_impl(s, *router, x, W1, b1, b2, z, false, y, side->s);
+        rc = class_tokens_impl(s, *router, x, W1, b1, b2, z, false, y, L, ws, side->s);
         if (rc != CLEARMOE_OK) return rc;
         if (hipEventRecord(side->join, side->s) != hipSuccess) return CLEARMOE_ERR_HIP;
     }
@@ -648,11 +674,25 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
     // Top-1 in bf16: fc1 + GELU, [t|u] and y in one kernel (z stays on chip).
     if (fused) {
         const int32_t* tc = own_dispatch ? at<int32_t>(ws, L.tile_counts) : nullptr;
+        ClassArgs c{};
+        if (cls_in_fused) {
+            c.x = static_cast<const bf16_bits*>(x);
+            c.W1 = static_cast<const bf16_bits*>(W1);
+            c.b1 = b1;
+            c.W2 = static_cast<const bf16_bits*>(router->W2);
+            c.b2 = b2;
+            c.y = static_cast<bf16_bits*>(y);
+            c.ncls = (T + router->dense_stride - 1) / router->dense_stride;
+            c.stride = router->dense_stride;
+            c.D = s.D;
+            c.H = s.H;
+            class_ffn_plan(c, at<float>(ws, L.cpart), at<uint64_t>(ws, L.ccount));
+        }
         CLEARMOE_STAGE(CLEARMOE_STAGE_FUSED_TOP1, st,
                        launch_fused_top1(x, W1, b1, US, Vt, b2, P, Q, perm, offsets,
                                          own_dispatch ? idx : nullptr, tc, gate, y, T, s.D, s.H,
                                          s.E, s.r, s.q, at<float>(ws, L.fpart),
-                                         at<int32_t>(ws, L.fcount), st));
+                                         at<int32_t>(ws, L.fcount), st, cls_in_fused ? &c : nullptr));
         // join: the class rows of y (written on the side stream) are complete
         // before anything later on the caller's stream
         if (side != nullptr) {
@@ -697,7 +737,7 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
         g.bias = b2;
         g.seg_offsets = offsets; g.nseg = s.E;
         CLEARMOE_STAGE(CLEARMOE_STAGE_Y, st, launch_gemm(s.dtype, g, st));
-        if (cls) return class_tokens_impl(s, *router, x, W1, b1, b2, z, true, y, st);
+        if (cls) return class_tokens_impl(s, *router, x, W1, b1, b2, z, true, y, L, ws, st);
         return CLEARMOE_OK;
     }
 
@@ -814,7 +854,7 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
         CLEARMOE_STAGE(CLEARMOE_STAGE_Y_PAIR, st, launch_gemm(s.dtype, g, st));
         // class tokens: their dense FFN output, from the token-order z when
         // there is one
-        if (cls) return class_tokens_impl(s, *router, x, W1, b1, b2, z, !z_pair_order, y, st);
+        if (cls) return class_tokens_impl(s, *router, x, W1, b1, b2, z, !z_pair_order, y, L, ws, st);
         return CLEARMOE_OK;
     }
 
@@ -828,7 +868,7 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
     CLEARMOE_STAGE(CLEARMOE_STAGE_COMBINE_RES, st,
                    launch_combine_residual(s.dtype, hsh, hres, inv, y, T, s.D, s.k, A, st));
     // 7. class tokens: the dense FFN's output replaces theirs
-    if (cls) return class_tokens_impl(s, *router, x, W1, b1, b2, z, true, y, st);
+    if (cls) return class_tokens_impl(s, *router, x, W1, b1, b2, z, true, y, L, ws, st);
     return CLEARMOE_OK;
 }
 

@@ -91,11 +91,14 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
                              const int32_t* perm, const int32_t* offsets, const int32_t* idx,
                              const int32_t* tile_counts, const float* gate, void* y, int64_t T,
                              int D, int H, int E, int r, int q, float* part, int32_t* counters,
-                             hipStream_t st) {
+                             hipStream_t st, const ClassArgs* cls) {
     if (!fused_top1_supported(D, H, r, q)) return hipErrorInvalidValue;
     if (T == 0) return hipSuccess;
     const int split = fused_split(T, E, H);
     if (split > 1 && (part == nullptr || counters == nullptr)) return hipErrorInvalidValue;
+    if (cls != nullptr && (split > 1 || !class_ffn_supported(cls->D, cls->H) || cls->D != D ||
+                           cls->H != H || cls->nparts < 1))
+        return hipErrorInvalidValue;
     FusedArgs a{};
     a.x = static_cast<const bf16_bits*>(x);
     a.W1 = static_cast<const bf16_bits*>(W1);
@@ -159,6 +162,20 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
         if (err != hipSuccess) return err;
     }
     if (split > 1) return fused_launch_split(a, lds, grid, nft, st);
+    if (cls != nullptr && cls->ncls > 0) {
+        // the class rows' workgroups after the tiles' (their LDS plan is far
+        // smaller than the tiles')
+        const int64_t cgrid = grid + class_blocks(cls->ncls) * cls->nparts;
+        if (cgrid > INT32_MAX || class_lds_bytes(H) > lds) return hipErrorInvalidValue;
+        const int g = static_cast<int>(cgrid);
+        switch (nft) {
+            case 1: return fused_cfg_cls<1>(a, *cls, lds, g, st);
+            case 2: return fused_cfg_cls<2>(a, *cls, lds, g, st);
+            case 3: return fused_cfg_cls<3>(a, *cls, lds, g, st);
+            case 4: return fused_cfg_cls<4>(a, *cls, lds, g, st);
+            default: return fused_cfg_cls<5>(a, *cls, lds, g, st);
+        }
+    }
     switch (nft) {
         case 1: return fused_cfg<1, false>(a, lds, grid, st);
         case 2: return fused_cfg<2, false>(a, lds, grid, st);

@@ -301,12 +301,16 @@ constexpr int kFusedMaxD = 384;      // six 64-wide input groups; x rows of a 64
 constexpr int kFusedMaxH = 8192;     // ... beside b1
 constexpr int kFusedMaxRQ = 160;     // [t|u] accumulators live in registers
 bool fused_top1_supported(int D, int H, int r, int q);
+struct ClassArgs;
+// With cls (a planned class_ffn pass, class_ffn.h) the class rows' dense FFN
+// runs on extra workgroups of the same launch; only for a launch without
+// the hidden split (fused_split(T, E, H) == 1), else an invalid-value error.
 hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, const void* US,
                              const void* Vt, const float* b2, const void* P, const void* Q,
                              const int32_t* perm, const int32_t* offsets, const int32_t* idx,
                              const int32_t* tile_counts, const float* gate, void* y, int64_t T,
                              int D, int H, int E, int r, int q, float* part, int32_t* counters,
-                             hipStream_t st);
+                             hipStream_t st, const ClassArgs* cls = nullptr);
 // Small batches (fewer 64-row tiles than CUs) split each tile's hidden units
 // over fused_split(T, E, H) workgroups; the launch then needs part
 // (fused_part_bytes) and counters (T / 64 + E + 1 int32) of workspace, else

@@ -26,6 +26,9 @@ import isa_check
 VALIDATED = {("fused.hip", n, 0): (0, 0) for n in range(1, 6)}
 VALIDATED.update({("fused_split.hip", n, 1): (0, 0) for n in range(1, 5)})
 VALIDATED[("fused_split.hip", 5, 1)] = (2, 12)
+# the variants with the class rows' workgroups (k_fused_top1_cls; "split"
+# 2 marks them): the same body after a branch on the workgroup index
+VALIDATED.update({("fused.hip", n, 2): (0, 0) for n in range(1, 6)})
 
 
 @pytest.fixture(scope="module")
@@ -55,7 +58,10 @@ def _meta(text, name):
 
 @pytest.mark.parametrize("src,nft,split", sorted(VALIDATED))
 def test_fused_kernel_isa(asm, src, nft, split):
-    name = f"_ZN8clearmoe12_GLOBAL__N_112k_fused_top1ILi{nft}ELb{split}EEEvNS_9FusedArgsE"
+    if split == 2:
+        name = f"_ZN8clearmoe12_GLOBAL__N_116k_fused_top1_clsILi{nft}EEEvNS_9FusedArgsENS_9ClassArgsE"
+    else:
+        name = f"_ZN8clearmoe12_GLOBAL__N_112k_fused_top1ILi{nft}ELb{split}EEEvNS_9FusedArgsE"
     text = asm[src]
     assert _meta(text, name) == VALIDATED[(src, nft, split)], _meta(text, name)
     insts, labels = isa_check.kernel_body(text, name)

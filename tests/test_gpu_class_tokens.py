@@ -134,6 +134,49 @@ def test_class_tokens_at_deit_small():
         assert e <= BF16_FROB_REGRESS, e
 
 
+IN_LAUNCH = [
+    # T, D, H, E, r, q, stride: enough 64-row tiles for one workgroup per tile,
+    # so the class rows run on extra workgroups of the fused launch
+    (9000, 264, 1000, 4, 64, 32, 150),   # D % 16 = 8, H % 128 = 104; 60 class rows: two blocks
+                                         # of 32, the second partial, each split over the hidden width
+    (9000, 320, 512, 4, 32, 16, 5),      # 1800 class rows: 57 blocks, too many to split
+]
+
+
+@pytest.mark.parametrize("T,D,H,E,r,q,stride", IN_LAUNCH)
+def test_class_rows_inside_fused_launch(T, D, H, E, r, q, stride):
+    """The fused launch's class-row workgroups: no launch of their own (no
+    dense-path stage runs), every class row and a sample of the others
+    against the oracle."""
+    cfg = synth.LayerConfig("clsin", T=T, D=D, H=H, E=E, k=1, r=r, q=q, dtype="bf16", seed=T + stride,
+                            residual="random", n_cal=2000)
+    L = synth.make_layer(cfg)
+    rng = np.random.default_rng(stride)
+    L["b1"] = (0.1 * rng.standard_normal(H)).astype(np.float32)
+    L["b2"] = (0.1 * rng.standard_normal(D)).astype(np.float32)
+    C = synth.with_class_tokens(L, stride=stride)
+    cm.timing_start(cm.stage_names(), max_records=64)
+    try:
+        g = gpu_ffn_ex(C)
+    finally:
+        t = cm.timing_stop()
+    launched = {k for k, v in t.items() if v[1] > 0}
+    assert "fused_top1" in launched and not launched & {"fc1_gelu", "dense_fc2"}, launched
+    lg = oracle.router_logits(C["x"], C["Wg"], C["bg"])
+    cls = np.arange(T) % stride == 0
+    assert np.all(g["idx"][cls] == -1)
+    ok = ~cls & ~bound_excluded(oracle.margins(lg, 1) < MARGIN)
+    assert np.array_equal(g["idx"][ok, 0], oracle.topk(lg, 1)[0][ok, 0])
+    rows = np.unique(np.concatenate([np.nonzero(cls)[0], _sample_rows(T, 256, 5)]))
+    rows = rows[cls[rows] | ok[rows]]
+    ref = oracle.ffn_forward_layer(C, rows=rows)
+    for what, sel in (("class", ref["cls"]), ("routed", ~ref["cls"])):
+        e = frob_rel(g["y"][rows][sel], ref["y"][sel])
+        print(f"{what} rows: relative Frobenius error {e:.3e}")
+        assert e <= BF16_FROB_REGRESS, e
+    assert np.all(np.isfinite(g["y"]))
+
+
 def test_class_rows_ordered_on_the_callers_stream():
     """The class rows come from a side stream that the caller's stream joins:
     work queued after the call on a user stream (here a copy of y, with no
