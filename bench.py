@@ -79,7 +79,7 @@ def parse():
 KERNEL_SOURCES = {
     "route": ["route.hip"], "tile_hist": ["dispatch.hip"], "scan": ["dispatch.hip"],
     "permute": ["dispatch.hip"], "combine": ["dispatch.hip"], "combine_res": ["dispatch.hip"],
-    "fused_top1": ["fused_kernel.h", "fused.hip", "fused_split.hip"],
+    "fused_top1": ["fused_kernel.h", "fused_body.inc", "class_ffn.h", "fused.hip", "fused_split.hip"],
     "pair_key": ["dispatch.hip"], "residual_add": ["dispatch.hip"],
 }
 
@@ -485,13 +485,15 @@ def bench_imbalance(cm, synth, torch, np, stream, steps):
                     for _ in range(5):
                         run()
                     torch.cuda.synchronize()
-                    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-                    e0.record(stream)
-                    for _ in range(steps):
-                        run()
-                    e1.record(stream)
-                    torch.cuda.synchronize()
-                    ms = e0.elapsed_time(e1) / steps
+                    ms = float("inf")
+                    for _ in range(2):   # best of two passes
+                        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                        e0.record(stream)
+                        for _ in range(steps):
+                            run()
+                        e1.record(stream)
+                        torch.cuda.synchronize()
+                        ms = min(ms, e0.elapsed_time(e1) / steps)
                     row[name] = {"ms": ms, "tokens_per_s": T / (ms * 1e-3)}
                 counts = torch.bincount(idx.flatten().long(), minlength=E).cpu().numpy()
                 row["counts"] = counts.tolist()
@@ -655,8 +657,12 @@ def bench_stack(cm, synth, torch, np, stream, L, steps):
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / steps
 
-    mixed = timed(moe_stack)
-    all_dense = timed(dense_stack)
+    # three interleaved passes of each, the best of each kept (clock and
+    # cache state drift between passes hits both alike)
+    mixed, all_dense = float("inf"), float("inf")
+    for _ in range(3):
+        mixed = min(mixed, timed(moe_stack))
+        all_dense = min(all_dense, timed(dense_stack))
     del keep
     return {"workload": f"12 chained FFN blocks (x + f(x)) at {cfg.name} (T={cfg.T}), blocks 6..11 "
                         f"CLEAR-MoE top-{cfg.k} with class tokens on the dense path, 0..5 dense; "

@@ -497,6 +497,15 @@ static hipError_t gemm_dt(const GemmDesc& g, hipStream_t st) {
         if (g.N > 128 && g.N <= 512 && g.K >= 1024 && g.M >= 16384)
             return gemm_cfg<Tin, 128, 128, 2, 2, 3, 64, 2>(g, st);
         if (g.N >= 1024 && g.K <= 512) return gemm_cfg<Tin, 128, 128, 4, 2, 2>(g, st);
+        // long k rows (2 KB or more) over a few hundred 64x64 tiles (e.g. the
+        // pair products of an adaptive layer at DeiT-Small widths, 28 -> 20
+        // us): four stages in flight; with more tiles, 128x128 over 8 waves
+        // (the DeiT-Small dense fc2, 35 -> 32 us)
+        if (g.K >= 1024 && g.N > 128 && g.N <= 512) {
+            const int64_t t64 = ((g.M + 63) / 64 + (g.seg_offsets != nullptr ? g.nseg : 0)) * ((g.N + 63) / 64);
+            if (t64 <= 1024) return gemm_cfg<Tin, 64, 64, 2, 2, 4>(g, st);
+            return gemm_cfg<Tin, 128, 128, 4, 2, 2>(g, st);
+        }
     }
     if (g.N >= 1024 && ((g.M + 255) / 256) * ((g.N + 255) / 256) >= 1024)
         return gemm_cfg<Tin, 256, 256, 4, 2, 2>(g, st);
