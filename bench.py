@@ -79,7 +79,8 @@ def parse():
 KERNEL_SOURCES = {
     "route": ["route.hip"], "tile_hist": ["dispatch.hip"], "scan": ["dispatch.hip"],
     "permute": ["dispatch.hip"], "combine": ["dispatch.hip"], "combine_res": ["dispatch.hip"],
-    "fused_top1": ["fused_kernel.h", "fused_body.inc", "class_ffn.h", "fused.hip", "fused_split.hip"],
+    "fused_top1": ["fused_kernel.h", "fused_body.inc", "class_ffn.h", "fused.hip", "fused_split.hip",
+                   "fused_cls.hip"],
     "pair_key": ["dispatch.hip"], "residual_add": ["dispatch.hip"],
 }
 

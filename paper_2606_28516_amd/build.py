@@ -20,7 +20,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libclearmoe.so")
 BUILD_DIR = os.path.join(ROOT, "_build", "clearmoe")
 SOURCES = ["api.cpp", "route.hip", "dispatch.hip", "gemm.hip", "fused.hip", "fused_split.hip",
-           "class_ffn.hip"]
+           "fused_cls.hip", "class_ffn.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 # The library carries the digest of the sources it was built from after this
@@ -62,7 +62,7 @@ def built_digest(path: str = LIB) -> str:
 
 # Translation units whose device assembly is kept beside the objects (with
 # the source digest), for the CPU check of the fused kernel's counted waits.
-KEEP_ASM = ("fused.hip", "fused_split.hip")
+KEEP_ASM = ("fused.hip", "fused_split.hip", "fused_cls.hip")
 
 
 def device_asm(src: str) -> str:

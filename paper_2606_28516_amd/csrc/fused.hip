@@ -1,6 +1,7 @@
 // Fused top-1 CLEAR-MoE FFN in bfloat16 for gfx950 (kernel in fused_kernel.h):
-// host side, LDS plan, the one-workgroup-per-tile instantiations, and the
-// choice of the hidden split for small batches.
+// host side, LDS plan, the one-workgroup-per-tile instantiations (those with
+// the class rows' workgroups: fused_cls.hip), and the choice of the hidden
+// split for small batches.
 #include "fused_kernel.h"
 
 namespace clearmoe {
@@ -167,14 +168,7 @@ hipError_t launch_fused_top1(const void* x, const void* W1, const float* b1, con
         // smaller than the tiles')
         const int64_t cgrid = grid + class_blocks(cls->ncls) * cls->nparts;
         if (cgrid > INT32_MAX || class_lds_bytes(H) > lds) return hipErrorInvalidValue;
-        const int g = static_cast<int>(cgrid);
-        switch (nft) {
-            case 1: return fused_cfg_cls<1>(a, *cls, lds, g, st);
-            case 2: return fused_cfg_cls<2>(a, *cls, lds, g, st);
-            case 3: return fused_cfg_cls<3>(a, *cls, lds, g, st);
-            case 4: return fused_cfg_cls<4>(a, *cls, lds, g, st);
-            default: return fused_cfg_cls<5>(a, *cls, lds, g, st);
-        }
+        return fused_launch_cls(a, *cls, lds, static_cast<int>(cgrid), nft, st);
     }
     switch (nft) {
         case 1: return fused_cfg<1, false>(a, lds, grid, st);

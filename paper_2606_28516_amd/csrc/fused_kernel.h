@@ -1,8 +1,8 @@
 // Fused top-1 CLEAR-MoE FFN in bfloat16 for gfx950: one kernel from x to y.
 // The kernel templates (their body is fused_body.inc); fused.hip
-// instantiates the one-workgroup-per-tile variants, with and without the
-// class rows' dense FFN on extra workgroups, and holds the host side,
-// fused_split.hip the hidden-split ones.
+// instantiates the one-workgroup-per-tile variants and holds the host side,
+// fused_cls.hip the ones with the class rows' dense FFN on extra
+// workgroups, fused_split.hip the hidden-split ones.
 //
 // With k = 1 every row p of the expert order is one token, and the layer is
 //     z      = GELU(x W1^T + b1)                        shared fc1 (Eq. 2)
@@ -87,6 +87,11 @@ struct FusedArgs {
 // Launch of the hidden-split variant (fused_split.hip) for nft 32-row [t|u]
 // tiles.
 hipError_t fused_launch_split(const FusedArgs& a, size_t lds, int grid, int nft, hipStream_t st);
+struct ClassArgs;
+// Launch of the variant with the class rows' workgroups (fused_cls.hip);
+// grid counts the tiles' workgroups and the class rows'.
+hipError_t fused_launch_cls(const FusedArgs& a, const ClassArgs& c, size_t lds, int grid, int nft,
+                            hipStream_t st);
 
 namespace {
 

@@ -3,7 +3,7 @@
 The kernel waits for its inline-assembly loads with hand-counted vmcnt
 values; the compiler does not see those loads.  Two properties of the built
 code keep those counts valid, and both are checked here on the gfx950
-assembly of the two translation units that instantiate the kernel:
+assembly of the three translation units that instantiate the kernel:
   * no instruction touches a register that an inline load is still filling
     (every control-flow path from the load to a covering wait);
   * the register allocation is the validated one: the spill slots (the
@@ -28,12 +28,12 @@ VALIDATED.update({("fused_split.hip", n, 1): (0, 0) for n in range(1, 5)})
 VALIDATED[("fused_split.hip", 5, 1)] = (2, 12)
 # the variants with the class rows' workgroups (k_fused_top1_cls; "split"
 # 2 marks them): the same body after a branch on the workgroup index
-VALIDATED.update({("fused.hip", n, 2): (0, 0) for n in range(1, 6)})
+VALIDATED.update({("fused_cls.hip", n, 2): (0, 0) for n in range(1, 6)})
 
 
 @pytest.fixture(scope="module")
 def asm():
-    """The device assembly the library build kept for the two translation
+    """The device assembly the library build kept for the translation
     units (built from the sources in the tree)."""
     from paper_2606_28516_amd import build as hb
     out = {}
