@@ -33,6 +33,15 @@
  *     required pointers non-NULL and 16-byte aligned, the workspace large
  *     enough.  A failed check returns its status and has no side effect.  A
  *     launch failure returns CLEARMOE_ERR_HIP (hipGetLastError).
+ *   - The layer entry points clearmoe_ffn_forward, clearmoe_ffn_forward_ex
+ *     and clearmoe_dense_ffn_forward also take D, H, r, q that are not such
+ *     multiples: those shapes run on zero-padded copies of the operands in
+ *     the workspace (clearmoe_workspace_bytes counts them), with the same
+ *     routing and y as unpadded (padding adds only zero products, and an
+ *     extra hidden unit's activation is GELU(0) = 0); their pointers need
+ *     only element alignment (the router's Wg stays 16-byte aligned when it
+ *     is an MLP router's [E, hidden] output layer).  The other entry points
+ *     keep the multiples.
  *   - No C++ exception crosses this interface.  Calls on one stream are
  *     ordered; calls that share a workspace must not overlap in time.
  */

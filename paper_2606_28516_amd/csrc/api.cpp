@@ -194,14 +194,16 @@ Layout layout_min(const clearmoe_shape& s) {
 bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 // Shape checks common to every entry point (which fields matter depends on
-// the entry point; unused fields must still be in range).
-int check_shape(const clearmoe_shape* s, bool layer) {
+// the entry point; unused fields must still be in range).  D, H, r and q
+// must be multiples of the elements of a 16-byte piece, except for the
+// layer entry points (unaligned_ok), which pad such shapes.
+int check_shape(const clearmoe_shape* s, bool layer, bool unaligned_ok = false) {
     if (s == nullptr) return CLEARMOE_ERR_INVALID_ARG;
     if (s->dtype != CLEARMOE_F32 && s->dtype != CLEARMOE_BF16) return CLEARMOE_ERR_UNSUPPORTED;
     if (s->T < 0 || s->D < 1 || s->D > kMaxDim) return CLEARMOE_ERR_INVALID_ARG;
     if (s->E < 1 || s->E > 64 || s->k < 1 || s->k > s->E) return CLEARMOE_ERR_INVALID_ARG;
     if (static_cast<int64_t>(s->T) * s->k >= (int64_t{1} << 31)) return CLEARMOE_ERR_INVALID_ARG;
-    const int mult = s->dtype == CLEARMOE_F32 ? 4 : 8;
+    const int mult = unaligned_ok ? 1 : (s->dtype == CLEARMOE_F32 ? 4 : 8);
     if (s->D % mult != 0) return CLEARMOE_ERR_INVALID_ARG;
     if (layer) {
         if (s->H < 1 || s->H > kMaxDim || s->H % mult != 0) return CLEARMOE_ERR_INVALID_ARG;
@@ -210,6 +212,62 @@ int check_shape(const clearmoe_shape* s, bool layer) {
         if (s->r % mult != 0 || s->q % mult != 0) return CLEARMOE_ERR_INVALID_ARG;
     }
     return CLEARMOE_OK;
+}
+
+// Unaligned layer shapes (D, H, r or q not a multiple of the elements of a
+// 16-byte piece) run on zero-padded copies of their operands in the
+// workspace.  Padding changes no result: an extra input feature or basis
+// component multiplies zeros, and an extra hidden unit has z = GELU(0 + 0) =
+// 0; the router's logits are the same sums, so the routing is the same, and
+// the padded layer's y cropped to D columns is the layer's y.
+int piece_elems(int dtype) { return dtype == CLEARMOE_F32 ? 4 : 8; }
+int round_up(int v, int m) { return (v + m - 1) / m * m; }
+bool unaligned_layer(const clearmoe_shape& s) {
+    const int m = piece_elems(s.dtype);
+    return s.D % m != 0 || s.H % m != 0 || s.r % m != 0 || s.q % m != 0;
+}
+clearmoe_shape aligned_shape(const clearmoe_shape& s) {
+    const int m = piece_elems(s.dtype);
+    clearmoe_shape a = s;
+    a.D = round_up(s.D, m);
+    a.H = round_up(s.H, m);
+    a.r = round_up(s.r, m);
+    a.q = round_up(s.q, m);
+    return a;
+}
+// Workspace of an unaligned layer: the aligned layer's own workspace first,
+// then the padded copies (every operand a layer entry point may take).
+struct PadLayout {
+    size_t inner, x, y, W1, b1, US, Vt, b2, P, Q, Wg, Wh, W2, total;
+};
+PadLayout pad_layout(const clearmoe_shape& s) {
+    const clearmoe_shape a = aligned_shape(s);
+    const size_t es = elem_size(s.dtype);
+    const size_t T = static_cast<size_t>(s.T), E = static_cast<size_t>(s.E);
+    const size_t D = static_cast<size_t>(a.D), H = static_cast<size_t>(a.H);
+    const size_t r = static_cast<size_t>(a.r), q = static_cast<size_t>(a.q);
+    PadLayout p{};
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t o = off;
+        off = up(off + bytes);
+        return o;
+    };
+    p.inner = take(layout(a).total);
+    p.x = take(es * T * D);
+    p.y = take(es * T * D);
+    p.W1 = take(es * H * D);
+    p.b1 = take(4 * H);
+    p.US = take(es * D * r);
+    p.Vt = take(es * r * H);
+    p.b2 = take(4 * D);
+    p.P = take(es * E * D * q);
+    p.Q = take(es * E * q * H);
+    p.Wg = take(es * E * D);
+    p.Wh = take(es * static_cast<size_t>(kMlpHiddenMax) * D);
+    p.W2 = take(es * D * H);
+    p.total = off;
+    return p;
 }
 
 // ---- stage timing: two events per timed launch, recorded on its stream ----
@@ -462,6 +520,8 @@ const char* clearmoe_status_string(int status) {
 }
 
 size_t clearmoe_workspace_bytes(const clearmoe_shape* shape) {
+    if (shape != nullptr && check_shape(shape, true, true) == CLEARMOE_OK && unaligned_layer(*shape))
+        return pad_layout(*shape).total;
     if (check_shape(shape, false) != CLEARMOE_OK) return 0;
     clearmoe_shape s = *shape;
     if (check_shape(shape, true) != CLEARMOE_OK) {  // route / dispatch-only shape
@@ -874,6 +934,87 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
 
 }  // namespace
 
+namespace {
+
+// Copies [batches][rows][cols] of src into the workspace region at off as
+// [batches][prow][pcol] with zeros around; a NULL src (an operand the path
+// does not read) stays NULL.
+int pad_operand(int eb, const void* src, void* ws, size_t off, int64_t batches, int64_t rows,
+                int64_t cols, int64_t prow, int64_t pcol, hipStream_t st, const void** out) {
+    *out = nullptr;
+    if (src == nullptr) return CLEARMOE_OK;
+    void* dst = at<void>(ws, off);
+    if (launch_pad_copy(eb, src, dst, batches, rows, cols, prow, pcol, st) != hipSuccess)
+        return CLEARMOE_ERR_HIP;
+    *out = dst;
+    return CLEARMOE_OK;
+}
+
+bool elem_aligned(const void* p, size_t a) { return p == nullptr || aligned(p, a); }
+
+// The layer on an unaligned shape: padded copies of its operands, the
+// aligned layer on them, y cropped back (see pad_layout).  Operands are read
+// element by element, so element alignment suffices.
+int ffn_forward_unaligned(const clearmoe_shape& s, const clearmoe_router* router, const void* x,
+                          const void* W1, const float* b1, const void* US, const void* Vt,
+                          const float* b2, const void* P, const void* Q, void* y, int32_t* idx_out,
+                          float* gate_out, void* ws, size_t ws_bytes, hipStream_t st) {
+    const size_t es = elem_size(s.dtype);
+    if (router == nullptr || router->Wg == nullptr || !W1 || (s.T > 0 && (!x || !y)))
+        return CLEARMOE_ERR_INVALID_ARG;
+    if ((s.r > 0 && (!US || !Vt)) || (s.q > 0 && (!P || !Q))) return CLEARMOE_ERR_INVALID_ARG;
+    if (router->hidden < 0 || router->hidden > kMlpHiddenMax || (router->hidden > 0 && !router->Wh))
+        return CLEARMOE_ERR_INVALID_ARG;
+    const void* ve[] = {x, W1, US, Vt, P, Q, y, router->Wg, router->Wh, router->W2};
+    for (const void* p : ve)
+        if (!elem_aligned(p, es)) return CLEARMOE_ERR_INVALID_ARG;
+    const void* v4[] = {b1, b2, idx_out, gate_out};
+    for (const void* p : v4)
+        if (!elem_aligned(p, 4)) return CLEARMOE_ERR_INVALID_ARG;
+    const PadLayout pl = pad_layout(s);
+    if (!ws || !aligned(ws, kAlign) || ws_bytes < pl.total) return CLEARMOE_ERR_WORKSPACE;
+    const clearmoe_shape a = aligned_shape(s);
+    const int eb = static_cast<int>(es);
+    const int64_t T = s.T, E = s.E;
+    const void *xp, *W1p, *b1p, *USp, *Vtp, *b2p, *Pp, *Qp;
+    int rc = pad_operand(eb, x, ws, pl.x, 1, T, s.D, T, a.D, st, &xp);
+    if (rc == CLEARMOE_OK) rc = pad_operand(eb, W1, ws, pl.W1, 1, s.H, s.D, a.H, a.D, st, &W1p);
+    if (rc == CLEARMOE_OK) rc = pad_operand(4, b1, ws, pl.b1, 1, 1, s.H, 1, a.H, st, &b1p);
+    if (rc == CLEARMOE_OK) rc = pad_operand(eb, s.r > 0 ? US : nullptr, ws, pl.US, 1, s.D, s.r, a.D, a.r, st, &USp);
+    if (rc == CLEARMOE_OK) rc = pad_operand(eb, s.r > 0 ? Vt : nullptr, ws, pl.Vt, 1, s.r, s.H, a.r, a.H, st, &Vtp);
+    if (rc == CLEARMOE_OK) rc = pad_operand(4, b2, ws, pl.b2, 1, 1, s.D, 1, a.D, st, &b2p);
+    if (rc == CLEARMOE_OK) rc = pad_operand(eb, s.q > 0 ? P : nullptr, ws, pl.P, E, s.D, s.q, a.D, a.q, st, &Pp);
+    if (rc == CLEARMOE_OK) rc = pad_operand(eb, s.q > 0 ? Q : nullptr, ws, pl.Q, E, s.q, s.H, a.q, a.H, st, &Qp);
+    clearmoe_router rt = *router;
+    if (rc == CLEARMOE_OK && rt.hidden == 0)   // linear router: Wg [E, D]
+        rc = pad_operand(eb, router->Wg, ws, pl.Wg, 1, E, s.D, E, a.D, st, &rt.Wg);
+    if (rc == CLEARMOE_OK && rt.hidden > 0)    // MLP router: Wh [hidden, D] (Wg is [E, hidden])
+        rc = pad_operand(eb, router->Wh, ws, pl.Wh, 1, rt.hidden, s.D, rt.hidden, a.D, st, &rt.Wh);
+    if (rc == CLEARMOE_OK && rt.W2 != nullptr)  // class tokens' fc2 [D, H]
+        rc = pad_operand(eb, router->W2, ws, pl.W2, 1, s.D, s.H, a.D, a.H, st, &rt.W2);
+    if (rc != CLEARMOE_OK) return rc;
+    void* yp = at<void>(ws, pl.y);
+    rc = ffn_forward_impl(&a, &rt, xp, W1p, static_cast<const float*>(b1p), USp, Vtp,
+                          static_cast<const float*>(b2p), Pp, Qp, yp, idx_out, gate_out,
+                          at<void>(ws, pl.inner), layout(a).total, st);
+    if (rc != CLEARMOE_OK || T == 0) return rc;
+    return launch_pad_copy(eb, yp, y, 1, T, a.D, T, s.D, st) == hipSuccess ? CLEARMOE_OK : CLEARMOE_ERR_HIP;
+}
+
+// Layer entry: unaligned shapes through the padded copies, others directly.
+int ffn_forward_any(const clearmoe_shape* shape, const clearmoe_router* router, const void* x,
+                    const void* W1, const float* b1, const void* US, const void* Vt, const float* b2,
+                    const void* P, const void* Q, void* y, int32_t* idx_out, float* gate_out, void* ws,
+                    size_t ws_bytes, hipStream_t st) {
+    if (shape != nullptr && check_shape(shape, true, true) == CLEARMOE_OK && unaligned_layer(*shape))
+        return ffn_forward_unaligned(*shape, router, x, W1, b1, US, Vt, b2, P, Q, y, idx_out, gate_out,
+                                     ws, ws_bytes, st);
+    return ffn_forward_impl(shape, router, x, W1, b1, US, Vt, b2, P, Q, y, idx_out, gate_out, ws, ws_bytes,
+                            st);
+}
+
+}  // namespace
+
 extern "C" {
 
 int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void* W1,
@@ -882,8 +1023,8 @@ int clearmoe_ffn_forward(const clearmoe_shape* shape, const void* x, const void*
                          int32_t* idx_out, float* gate_out, void* ws, size_t ws_bytes,
                          hipStream_t stream) {
     const clearmoe_router rt = linear_router(Wg, bg);
-    return ffn_forward_impl(shape, &rt, x, W1, b1, US, Vt, b2, P, Q, y, idx_out, gate_out, ws,
-                            ws_bytes, stream);
+    return ffn_forward_any(shape, &rt, x, W1, b1, US, Vt, b2, P, Q, y, idx_out, gate_out, ws, ws_bytes,
+                           stream);
 }
 
 }  // extern "C"
@@ -942,8 +1083,8 @@ int clearmoe_ffn_forward_ex(const clearmoe_shape* shape, const clearmoe_router* 
                             const void* Vt, const float* b2, const void* P, const void* Q,
                             void* y, int32_t* idx_out, float* gate_out, void* ws,
                             size_t ws_bytes, hipStream_t stream) {
-    return ffn_forward_impl(shape, router, x, W1, b1, US, Vt, b2, P, Q, y, idx_out, gate_out, ws,
-                            ws_bytes, stream);
+    return ffn_forward_any(shape, router, x, W1, b1, US, Vt, b2, P, Q, y, idx_out, gate_out, ws, ws_bytes,
+                           stream);
 }
 
 size_t clearmoe_padded_workspace_bytes(const clearmoe_shape* shape) {
@@ -1030,6 +1171,34 @@ int clearmoe_ffn_forward_padded(const clearmoe_shape* shape, const void* x, cons
 int clearmoe_dense_ffn_forward(const clearmoe_shape* shape, const void* x, const void* W1,
                                const float* b1, const void* W2, const float* b2, void* y,
                                void* ws, size_t ws_bytes, hipStream_t stream) {
+    if (shape != nullptr && check_shape(shape, true, true) == CLEARMOE_OK && unaligned_layer(*shape)) {
+        // padded copies, the aligned FFN on them, y cropped (see pad_layout)
+        const clearmoe_shape& s = *shape;
+        const size_t es = elem_size(s.dtype);
+        if (!W1 || !W2 || (s.T > 0 && (!x || !y))) return CLEARMOE_ERR_INVALID_ARG;
+        const void* ve[] = {x, W1, W2, y};
+        for (const void* p : ve)
+            if (!elem_aligned(p, es)) return CLEARMOE_ERR_INVALID_ARG;
+        if (!elem_aligned(b1, 4) || !elem_aligned(b2, 4)) return CLEARMOE_ERR_INVALID_ARG;
+        const PadLayout pl = pad_layout(s);
+        if (!ws || !aligned(ws, kAlign) || ws_bytes < pl.total) return CLEARMOE_ERR_WORKSPACE;
+        const clearmoe_shape a = aligned_shape(s);
+        const int eb = static_cast<int>(es);
+        const void *xp, *W1p, *b1p, *W2p, *b2p;
+        int rc = pad_operand(eb, x, ws, pl.x, 1, s.T, s.D, s.T, a.D, stream, &xp);
+        if (rc == CLEARMOE_OK) rc = pad_operand(eb, W1, ws, pl.W1, 1, s.H, s.D, a.H, a.D, stream, &W1p);
+        if (rc == CLEARMOE_OK) rc = pad_operand(4, b1, ws, pl.b1, 1, 1, s.H, 1, a.H, stream, &b1p);
+        if (rc == CLEARMOE_OK) rc = pad_operand(eb, W2, ws, pl.W2, 1, s.D, s.H, a.D, a.H, stream, &W2p);
+        if (rc == CLEARMOE_OK) rc = pad_operand(4, b2, ws, pl.b2, 1, 1, s.D, 1, a.D, stream, &b2p);
+        if (rc != CLEARMOE_OK) return rc;
+        void* yp = at<void>(ws, pl.y);
+        rc = clearmoe_dense_ffn_forward(&a, xp, W1p, static_cast<const float*>(b1p), W2p,
+                                        static_cast<const float*>(b2p), yp, at<void>(ws, pl.inner),
+                                        layout(a).total, stream);
+        if (rc != CLEARMOE_OK || s.T == 0) return rc;
+        return launch_pad_copy(eb, yp, y, 1, s.T, a.D, s.T, s.D, stream) == hipSuccess ? CLEARMOE_OK
+                                                                                       : CLEARMOE_ERR_HIP;
+    }
     int rc = check_shape(shape, true);
     if (rc != CLEARMOE_OK) return rc;
     const clearmoe_shape& s = *shape;

@@ -528,6 +528,38 @@ hipError_t launch_residual_add(int dtype, const void* x, const void* f, void* ou
     return hipGetLastError();
 }
 
+template <typename T>
+__global__ __launch_bounds__(256) void k_pad_copy(const T* __restrict__ src, T* __restrict__ dst,
+                                                  int64_t batches, int64_t srows, int64_t scols,
+                                                  int64_t drows, int64_t dcols) {
+    const int64_t n = batches * drows * dcols;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t c = i % dcols, br = i / dcols;
+        const int64_t r = br % drows, b = br / drows;
+        dst[i] = (r < srows && c < scols) ? src[(b * srows + r) * scols + c] : T(0);
+    }
+}
+
+hipError_t launch_pad_copy(int elem_bytes, const void* src, void* dst, int64_t batches, int64_t srows,
+                           int64_t scols, int64_t drows, int64_t dcols, hipStream_t st) {
+    if (batches < 0 || srows < 0 || scols < 0 || drows < 0 || dcols < 0) return hipErrorInvalidValue;
+    const int64_t n = batches * drows * dcols;
+    if (n == 0) return hipSuccess;
+    if (src == nullptr || dst == nullptr) return hipErrorInvalidValue;
+    const int64_t b = (n + 255) / 256;
+    const unsigned blocks = static_cast<unsigned>(b < 8192 ? b : 8192);
+    if (elem_bytes == 4)
+        launch_kernel(k_pad_copy<uint32_t>, blocks, 256, 0, st, static_cast<const uint32_t*>(src),
+                      static_cast<uint32_t*>(dst), batches, srows, scols, drows, dcols);
+    else if (elem_bytes == 2)
+        launch_kernel(k_pad_copy<uint16_t>, blocks, 256, 0, st, static_cast<const uint16_t*>(src),
+                      static_cast<uint16_t*>(dst), batches, srows, scols, drows, dcols);
+    else
+        return hipErrorInvalidValue;
+    return hipGetLastError();
+}
+
 // Pair keys of a top-2 routing (see launch_pair_key): a token with one expert
 // e gets key e and gates (gate of e, 0); one with experts a < b gets key
 // E + (number of the pair (a, b) in lexicographic order) and gates (gate of

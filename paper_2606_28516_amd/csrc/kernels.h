@@ -214,6 +214,12 @@ hipError_t launch_pair_key(const int32_t* idx, const float* gate, int64_t T, int
 // out = x + f (dtype, [T, D], D a multiple of 8 for bf16 / 4 for float32).
 hipError_t launch_residual_add(int dtype, const void* x, const void* f, void* out, int64_t T, int D,
                                hipStream_t st);
+// dst[b][r][c] = src[b][r][c] for r < srows, c < scols, else 0, over
+// b < batches, r < drows, c < dcols (elements of elem_bytes = 2 or 4 bytes;
+// src and dst each contiguous).  Pads with zeros (drows >= srows, dcols >=
+// scols) or crops (drows <= srows, dcols <= scols).
+hipError_t launch_pad_copy(int elem_bytes, const void* src, void* dst, int64_t batches, int64_t srows,
+                           int64_t scols, int64_t drows, int64_t dcols, hipStream_t st);
 // Index maps of the padded-batch backend (expert e owns rows [e C, e C + C)):
 // perm_pad [E C] (-1 = padding), inv_pad [A], seg [E + 1] = e C.
 hipError_t launch_pad_index(const int32_t* idx, const int32_t* counts, const int32_t* offsets,

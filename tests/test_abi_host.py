@@ -65,8 +65,10 @@ def test_workspace_bytes_grows_with_shape_and_rejects_bad_shapes():
     assert 0 < a < b and a % 256 == 0
     assert cm.workspace_bytes(_shape(k=5)) == 0          # k > E
     assert cm.workspace_bytes(_shape(E=65, k=1)) == 0    # E > 64
-    assert cm.workspace_bytes(_shape(D=12)) == 0         # D not a multiple of 8 for bf16
+    assert cm.workspace_bytes(_shape(D=12)) == 0         # r > min(D, H)
     assert cm.workspace_bytes(_shape(D=12, dtype=cm.F32, H=128, r=4, q=4)) > 0
+    # unaligned layer shapes: the aligned layer's workspace plus padded copies
+    assert cm.workspace_bytes(_shape(D=60, H=100, r=12, q=6)) > cm.workspace_bytes(_shape(H=104, r=16))
     assert cm.workspace_bytes(_shape(T=0)) > 0
     # the configurations of the benchmark and tests are all valid
     for c in synth.CONFIGS.values():
@@ -121,9 +123,14 @@ def test_dispatch_combine_ffn_reject_before_launch():
     # r > min(D, H)
     bad = _shape(r=72)
     assert L.clearmoe_ffn_forward(ctypes.byref(bad), *args, FAKE, n, None) == 1
-    # q not a multiple of 8 in bf16
-    bad = _shape(q=6)
-    assert L.clearmoe_ffn_forward(ctypes.byref(bad), *args, FAKE, n, None) == 1
+    # q not a multiple of 8 in bf16: a valid layer shape that runs on padded
+    # copies, which the workspace of the aligned shape cannot hold
+    odd = _shape(q=6)
+    assert cm.workspace_bytes(odd) > n
+    assert L.clearmoe_ffn_forward(ctypes.byref(odd), *args, FAKE, n, None) == 3
+    # ... and a component entry point keeps the multiples
+    assert L.clearmoe_route(ctypes.byref(_shape(D=60, r=8)), FAKE, FAKE, None, FAKE, FAKE, FAKE, n,
+                            None) == 1
     # workspace one byte short
     assert L.clearmoe_ffn_forward(ctypes.byref(s), *args, FAKE, n - 1, None) == 3
 
