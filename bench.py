@@ -53,7 +53,7 @@ TIME_EVERY = 8          # sampling of the dominant kernel's timed launches in sh
 MIN_TIMED = 20          # timed launches of the dominant kernel, at least
 # stages whose kernels are matrix products (the router's flops are not its bound)
 MFMA_STAGES = ("fc1_gelu", "basis_t", "basis_h", "res_u", "res_h", "tu_grouped", "y_grouped",
-               "dense_fc2", "fused_top1")
+               "tu_pair", "y_pair", "dense_fc2", "fused_top1")
 
 
 def parse():
@@ -120,6 +120,11 @@ def stage_work(stage, cfg, b):
         "dense_fc2": (2 * T * D * H, T * H * b + D * H * b + T * D * b),
         "tu_grouped": (2 * A * (r + q) * H, A * H * b + (r + E * q) * H * b + A * (r + q) * b),
         "y_grouped": (2 * A * D * (r + q), A * (r + q) * b + D * (r + E * q) * b + T * D * b),
+        # top-2 in expert-pair order: one row per token with its two experts
+        "tu_pair": (2 * T * (r + 2 * q) * H, T * H * b + (r + E * q) * H * b + T * (r + 2 * q) * b),
+        "y_pair": (2 * T * D * (r + 2 * q), T * (r + 2 * q) * b + D * (r + E * q) * b + T * D * b),
+        "pair_key": (0, A * 8 + T * 12),
+        "tile_hist": (0, T * 4 + 4 * ((T + 63) // 64) * (E + E * (E - 1) // 2)),
         # x in, y out; W1, [Vt;Q_e] and [US|P_e] once each; b1, b2; the expert
         # index of every token and the router's tile histogram
         "fused_top1": (2 * T * (D * H + H * (r + q) + (r + q) * D),
@@ -354,6 +359,18 @@ def measure_layer(cm, torch, cfg, L, steps, warmup, traffic_probe=False):
     wall = time.perf_counter() - t0
     dom_ms, dom_n = cm.timing_stop()[dominant]
     ms_step = ev0.elapsed_time(ev1) / steps
+    # spread of single steps (a separate pass after the timed one, an event
+    # pair around each call)
+    pairs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+             for _ in range(max(steps, 1))]
+    for e0, e1 in pairs:
+        e0.record(stream)
+        step()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    per_step = sorted(e0.elapsed_time(e1) for e0, e1 in pairs)
+    pct = {f"p{p}": per_step[min(len(per_step) - 1, round(p / 100 * (len(per_step) - 1)))]
+           for p in (10, 50, 90)}
 
     flops, byts = stage_work(dominant, cfg, b)
     dom_avg_s = dom_ms / dom_n * 1e-3
@@ -369,7 +386,11 @@ def measure_layer(cm, torch, cfg, L, steps, warmup, traffic_probe=False):
     roof["avg_launch_us"] = dom_avg_s * 1e6
     roof["timed_launches"] = dom_n
     roof["algorithmic_per_launch"] = flops if flops > 0 else byts
+    if flops > 0:
+        roof["attainable"] = min(roof["peak"], flops / byts * HBM_PEAK_GBS / 1e3)
+        roof["frac_attainable"] = roof["achieved"] / roof["attainable"]
     return {"value": cfg.T / (ms_step * 1e-3), "ms_per_step": ms_step, "roofline": roof,
+            "step_ms": pct,
             "layer_tflops": layer_flops(cfg) / (ms_step * 1e-3) / 1e12,
             "stages_us": {s_: v * 1e3 for s_, v in sorted(stages.items(), key=lambda kv: -kv[1])},
             "wall_s": wall, "_step": step, "_d": d, "_ws": ws, "_y": y, "_stream": stream}
@@ -606,6 +627,12 @@ def bench_layer(cm, synth, torch, np, stream, workload, steps, cfg=None, L=None,
         if flops:
             e["tflops"] = flops / (us * 1e-6) / 1e12
             e["mfma_frac"] = e["tflops"] / peak
+            # against the attainable rate min(peak, AI x HBM) of its
+            # algorithmic flops and bytes
+            byts = stage_work(s_, cfg, b)[1]
+            attain = min(peak, flops / byts * HBM_PEAK_GBS / 1e3)
+            e["attainable_tflops"] = attain
+            e["attainable_frac"] = e["tflops"] / attain
         stages[s_] = e
     del ws, y, d
     return {"workload": f"{cfg.name} (T={cfg.T} D={cfg.D} H={cfg.H} E={cfg.E} k={cfg.k} "
