@@ -201,6 +201,7 @@ def main():
         "config": {"workload": cfg.name, "tokens": cfg.T, "D": cfg.D, "H": cfg.H, "E": cfg.E,
                    "k": cfg.k, "r": cfg.r, "q": cfg.q, "seed": cfg.seed},
         "roofline": core["roofline"],
+        "step_ms": core["step_ms"],
         "layer_tflops": core["layer_tflops"],
         "stages_us": core["stages_us"],
         "wall_s": core["wall_s"],

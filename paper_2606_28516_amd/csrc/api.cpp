@@ -820,7 +820,7 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
         int32_t* pperm = at<int32_t>(ws, L.pperm);
         int32_t* poffsets = at<int32_t>(ws, L.poffsets);
         CLEARMOE_STAGE(CLEARMOE_STAGE_PAIR_KEY, st,
-                       launch_pair_key(idx, gate, T, s.E, pkey, pga, pgb, st));
+                       launch_pair_key(idx, gate, T, s.E, pkey, pga, pgb, at<int32_t>(ws, L.ptc), st));
         clearmoe_shape sp = s;
         sp.E = nkeys;
         sp.k = 1;
@@ -829,7 +829,7 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
         Lp.tile_base = L.ptb;
         Lp.chunk_tot = L.pct;
         rc = dispatch_impl(sp, Lp, pkey, ws, at<int32_t>(ws, L.pcounts), poffsets, pperm,
-                           at<int32_t>(ws, L.pinv), nullptr, nullptr, false, st);
+                           at<int32_t>(ws, L.pinv), nullptr, nullptr, true, st);
         if (rc != CLEARMOE_OK) return rc;
         const bool singles = router->adaptive != 0;
         const bool fused_ok = s.dtype == CLEARMOE_BF16 && fused_top1_supported(s.D, s.H, s.r, s.q);

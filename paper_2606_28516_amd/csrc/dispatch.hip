@@ -563,39 +563,61 @@ hipError_t launch_pad_copy(int elem_bytes, const void* src, void* dst, int64_t b
 // Pair keys of a top-2 routing (see launch_pair_key): a token with one expert
 // e gets key e and gates (gate of e, 0); one with experts a < b gets key
 // E + (number of the pair (a, b) in lexicographic order) and gates (gate of
-// a, gate of b); one with none gets -1 (no segment).
-__global__ __launch_bounds__(256) void k_pair_key(const int32_t* __restrict__ idx,
-                                                  const float* __restrict__ gate, int64_t T,
-                                                  int E, int32_t* __restrict__ key,
-                                                  float* __restrict__ ga,
-                                                  float* __restrict__ gb) {
-    const int64_t t = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-    if (t >= T) return;
-    // idx and gate may be only 4-byte aligned (caller arrays): two loads each
-    const int2 e = make_int2(idx[2 * t], idx[2 * t + 1]);
-    const float2 g = make_float2(gate[2 * t], gate[2 * t + 1]);
-    const bool v0 = e.x >= 0 && e.x < E, v1 = e.y >= 0 && e.y < E;
-    int32_t k = -1;
-    float2 o = make_float2(0.0f, 0.0f);
-    if (v0 && v1 && e.x != e.y) {
-        const bool lo0 = e.x < e.y;
-        const int a = lo0 ? e.x : e.y, b = lo0 ? e.y : e.x;
-        k = E + a * (2 * E - a - 1) / 2 + (b - a - 1);
-        o = lo0 ? g : make_float2(g.y, g.x);
-    } else if (v0 || v1) {
-        k = v0 ? e.x : e.y;
-        o = make_float2(v0 ? g.x : g.y, 0.0f);
+// a, gate of b); one with none gets -1 (no segment).  Workgroup i takes the
+// TILE tokens of histogram tile i and also writes the tile's key counts, so
+// the dispatch over keys needs no histogram pass of its own.
+template <int TILE>
+__global__ __launch_bounds__(TILE) void k_pair_key(const int32_t* __restrict__ idx,
+                                                   const float* __restrict__ gate, int64_t T, int E,
+                                                   int nkeys, int32_t* __restrict__ key,
+                                                   float* __restrict__ ga, float* __restrict__ gb,
+                                                   int32_t* __restrict__ tile_counts) {
+    constexpr int kW = TILE / 64;
+    __shared__ int s_wc[kW][64];
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int64_t t = static_cast<int64_t>(blockIdx.x) * TILE + tid;
+    int32_t kk = -1;
+    if (t < T) {
+        // idx and gate may be only 4-byte aligned (caller arrays): two loads each
+        const int2 e = make_int2(idx[2 * t], idx[2 * t + 1]);
+        const float2 g = make_float2(gate[2 * t], gate[2 * t + 1]);
+        const bool v0 = e.x >= 0 && e.x < E, v1 = e.y >= 0 && e.y < E;
+        float2 o = make_float2(0.0f, 0.0f);
+        if (v0 && v1 && e.x != e.y) {
+            const bool lo0 = e.x < e.y;
+            const int a = lo0 ? e.x : e.y, b = lo0 ? e.y : e.x;
+            kk = E + a * (2 * E - a - 1) / 2 + (b - a - 1);
+            o = lo0 ? g : make_float2(g.y, g.x);
+        } else if (v0 || v1) {
+            kk = v0 ? e.x : e.y;
+            o = make_float2(v0 ? g.x : g.y, 0.0f);
+        }
+        key[t] = kk;
+        ga[t] = o.x;
+        gb[t] = o.y;
     }
-    key[t] = k;
-    ga[t] = o.x;
-    gb[t] = o.y;
+    (void)wave_rank(kk >= 0, kk, nkeys, lane, w, s_wc);
+    __syncthreads();
+    if (tid < nkeys) {
+        int c = 0;
+#pragma unroll
+        for (int i = 0; i < kW; ++i) c += s_wc[i][tid];
+        tile_counts[static_cast<int64_t>(blockIdx.x) * nkeys + tid] = c;
+    }
 }
 
 hipError_t launch_pair_key(const int32_t* idx, const float* gate, int64_t T, int E, int32_t* key,
-                           float* ga, float* gb, hipStream_t st) {
-    if (T == 0) return hipSuccess;
-    launch_kernel(k_pair_key, dim3(static_cast<unsigned>((T + 255) / 256)), 256, 0, st, idx, gate,
-                  T, E, key, ga, gb);
+                           float* ga, float* gb, int32_t* tile_counts, hipStream_t st) {
+    const int nkeys = pair_keys(E);
+    if (nkeys > kPairMaxKeys) return hipErrorInvalidValue;
+    const int64_t nt = hist_tiles(T, nkeys);
+    if (nt == 0) return hipSuccess;
+    if (hist_tile(T, nkeys) == kSmallTile)
+        launch_kernel(k_pair_key<kSmallTile>, dim3(static_cast<unsigned>(nt)), kSmallTile, 0, st, idx, gate, T,
+                      E, nkeys, key, ga, gb, tile_counts);
+    else
+        launch_kernel(k_pair_key<kRouteTile>, dim3(static_cast<unsigned>(nt)), kRouteTile, 0, st, idx, gate, T,
+                      E, nkeys, key, ga, gb, tile_counts);
     return hipGetLastError();
 }
 

@@ -209,8 +209,11 @@ __host__ __device__ inline void pair_experts(int s, int E, int& a, int& b) {
     }
     b = a + 1 + s;
 }
+// Also writes the key histogram of every tile of hist_tile(T, pair_keys(E))
+// tokens into tile_counts [hist_tiles(T, pair_keys(E))][pair_keys(E)], as
+// the dispatch over keys reads it.
 hipError_t launch_pair_key(const int32_t* idx, const float* gate, int64_t T, int E, int32_t* key,
-                           float* ga, float* gb, hipStream_t st);
+                           float* ga, float* gb, int32_t* tile_counts, hipStream_t st);
 // out = x + f (dtype, [T, D], D a multiple of 8 for bf16 / 4 for float32).
 hipError_t launch_residual_add(int dtype, const void* x, const void* f, void* out, int64_t T, int D,
                                hipStream_t st);
