@@ -719,14 +719,35 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
         if (rc != CLEARMOE_OK) return rc;
         if (hipEventRecord(side->join, side->s) != hipSuccess) return CLEARMOE_ERR_HIP;
     }
+    // Top-2 in pair order with every token on two experts: fc1 + GELU in
+    // token order needs only x, so it runs on the side stream while routing
+    // and the pair dispatch run here (they leave most of the chip idle); the
+    // pair products wait for it.
+    const bool fc1_aside = pair_path(s) && !router->adaptive && T > 0;
+    if (fc1_aside) {
+        side_lock = std::unique_lock<std::mutex>(g_side_mu);
+        rc = side_stream(&side);
+        if (rc != CLEARMOE_OK) return rc;
+        if (hipEventRecord(side->fork, st) != hipSuccess ||
+            hipStreamWaitEvent(side->s, side->fork, 0) != hipSuccess)
+            return CLEARMOE_ERR_HIP;
+        GemmDesc g = gemm_desc(T, s.H, s.D);
+        g.A = x; g.lda = s.D;
+        g.B = W1; g.ldb = s.D;
+        g.C = z; g.ldc = s.H; g.c_f32 = 0;
+        g.bias = b1; g.gelu = 1;
+        CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, side->s, launch_gemm(s.dtype, g, side->s));
+        if (hipEventRecord(side->join, side->s) != hipSuccess) return CLEARMOE_ERR_HIP;
+    }
 
     // 1. router + top-k + per-tile histogram; 2. scan + stable permutation
     // (the fused top-1 kernel does the latter itself from the histogram
-    // when it is small enough for one workgroup's scan)
+    // when it is small enough for one workgroup's scan; the pair order
+    // dispatches pair keys instead, below)
     rc = route_impl(s, L, *router, x, idx, gate, ws, st);
     if (rc != CLEARMOE_OK) return rc;
     const bool own_dispatch = fused && hist_tiles(T, s.E) * s.E <= kInlineScanMax;
-    if (!own_dispatch) {
+    if (!own_dispatch && !pair_path(s)) {
         rc = dispatch_impl(s, L, idx, ws, counts, offsets, perm, inv, nullptr, nullptr, true, st);
         if (rc != CLEARMOE_OK) return rc;
     }
@@ -853,12 +874,14 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
             CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
             z_pair_order = true;
         } else {
-            g = gemm_desc(T, s.H, s.D);
-            g.A = x; g.lda = s.D;
-            g.B = W1; g.ldb = s.D;
-            g.C = z; g.ldc = s.H; g.c_f32 = 0;
-            g.bias = b1; g.gelu = 1;
-            CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
+            if (!fc1_aside) {
+                g = gemm_desc(T, s.H, s.D);
+                g.A = x; g.lda = s.D;
+                g.B = W1; g.ldb = s.D;
+                g.C = z; g.ldc = s.H; g.c_f32 = 0;
+                g.bias = b1; g.gelu = 1;
+                CLEARMOE_STAGE(CLEARMOE_STAGE_FC1, st, launch_gemm(s.dtype, g, st));
+            }
             if (singles) {
                 // single-expert tokens: the top-1 chain's two grouped products
                 void* tu = at<void>(ws, L.tu);
@@ -884,6 +907,10 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
                 g.seg_offsets = poffsets; g.nseg = s.E;
                 CLEARMOE_STAGE(CLEARMOE_STAGE_Y, st, launch_gemm(s.dtype, g, st));
             }
+        }
+        if (fc1_aside) {   // z from the side stream
+            join_guard.done = true;
+            if (hipStreamWaitEvent(st, side->join, 0) != hipSuccess) return CLEARMOE_ERR_HIP;
         }
         void* ptu = at<void>(ws, L.ptu);
         const int rqq = s.r + 2 * s.q;

@@ -200,6 +200,28 @@ def test_ffn_forward_configs(name):
         assert e <= BF16_FROB and e <= BF16_FROB_REGRESS, e
 
 
+def test_pair_order_launches():
+    """The top-2 layer in pair order: one key pass (with its tile histogram),
+    one permutation (over keys; no expert-order dispatch), fc1 once (beside
+    the routing, on the side stream), the two pair products; the result
+    against the oracle."""
+    cfg = synth.LayerConfig("pairlaunch", T=1500, D=128, H=256, E=6, k=2, r=32, q=16, dtype="bf16",
+                            seed=12, residual="random", n_cal=2000)
+    L = synth.make_layer(cfg)
+    cm.timing_start(cm.stage_names(), max_records=64)
+    try:
+        g = gpu_ffn(L)
+    finally:
+        t = cm.timing_stop()
+    launched = {k: v[1] for k, v in t.items() if v[1] > 0}
+    assert launched == {"route": 1, "pair_key": 1, "permute": 1, "fc1_gelu": 1, "tu_pair": 1,
+                        "y_pair": 1}, launched
+    ref = oracle.ffn_forward_layer(L)
+    tie = assert_routing(g["idx"], ref["logits"], 2)
+    e = frob_rel(g["y"][~tie], ref["y"][~tie])
+    assert e <= BF16_FROB_REGRESS, e
+
+
 @pytest.mark.parametrize("dt,r", [("bf16", 32), ("f32", 16), ("bf16", 0)])
 def test_pair_order_every_pair(dt, r):
     """Top-2 over E = 8 experts in pair order: tokens spread over all 28
