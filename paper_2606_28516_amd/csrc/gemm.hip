@@ -27,9 +27,13 @@
 //   * lanes whose row or k chunk is outside the operand load a 16-byte zero
 //     page instead, so tails need no special path and never read out of bounds;
 //   * tiles are spread by row tile over the XCDs: workgroup i runs on XCD
-//     i % 8, which takes every eighth row tile with all its column tiles, so
-//     the A rows of a tile stay in one XCD's L2 and the leading row tiles
-//     (all a grouped product's rows when its segments hold few) use every XCD;
+//     i % 8, which takes every eighth row tile, in groups of four row tiles
+//     whose column tiles it runs column by column, so the A rows and the B
+//     rows that the concurrent workgroups of an XCD read are shared among
+//     them in its L2, and the leading row tiles (all a grouped product's rows
+//     when its segments hold few) use every XCD;
+//   * long-K products stage each wave's output rows through LDS and store
+//     whole rows (16 bytes per lane) instead of 8-byte pieces;
 //   * grouped mode: the tile index enumerates (segment, M-tile) pairs in
 //     segment order, read from the device offsets; surplus workgroups exit.
 #include "kernels.h"
@@ -94,7 +98,7 @@ template <> struct Mfma<float> {
 // WPE > 0 asks for WPE waves per SIMD (registers capped to fit them).
 template <typename Tin, int BM, int BN, int WM, int WN, int NS, int SB = kStageBytes, int WPE = 0>
 __global__ __launch_bounds__(64 * WM * WN) __attribute__((amdgpu_waves_per_eu(WPE > 0 ? WPE : 1)))
-void k_gemm(GemmDesc g, int mtiles, int ntiles, int per_xcd, int ksplit) {
+void k_gemm(GemmDesc g, int mtiles, int ntiles, int group, int ksplit, int staged) {
     constexpr int NW = WM * WN;                     // waves: 4 (one per SIMD) or 8 (two)
     static_assert(NW == 4 || NW == 8, "4 or 8 waves");
     constexpr int WTM = BM / WM, WTN = BN / WN;
@@ -123,18 +127,32 @@ void k_gemm(GemmDesc g, int mtiles, int ntiles, int per_xcd, int ksplit) {
     const int wm = wave / WN, wn = wave % WN;
 
     // ---- tile of this workgroup.  Workgroup b runs on XCD x = b % 8 as its
-    //      i-th (i = b / 8); XCD x takes the row tiles x, x + 8, x + 16, ...,
-    //      each with all its column tiles in turn, so one XCD's L2 serves the
-    //      A rows of a row tile, and the first row tiles -- the only ones
+    //      i-th (i = b / 8); XCD x owns the row tiles x, x + 8, x + 16, ...
+    //      (mx of them) and takes them in groups of `group` row tiles (the
+    //      last group may be short), each group column tile by column tile,
+    //      so the workgroups in flight on one XCD share both their A rows and
+    //      their B rows in its L2, and the first row tiles -- the only ones
     //      with rows when a grouped product's segments hold fewer rows than
     //      its bound M -- spread over every XCD.  With split K, S consecutive
     //      workgroups of one XCD share a tile, part kp taking its share of
     //      the k stages.
-    (void)per_xcd;
     const int S = g.ks_part != nullptr ? ksplit : 1;
     const int xcd = blockIdx.x % kXcds, local = blockIdx.x / kXcds;
     const int tile_local = local / S, kp = local - tile_local * S;
-    const int mt = (tile_local / ntiles) * kXcds + xcd, nt = tile_local % ntiles;
+    const int mx = (mtiles - xcd + kXcds - 1) / kXcds;
+    const int full = mx / group;
+    int mi, nt;
+    if (tile_local < full * group * ntiles) {
+        const int gi = tile_local / (group * ntiles), r = tile_local - gi * group * ntiles;
+        mi = gi * group + r % group;
+        nt = r / group;
+    } else {
+        const int r = tile_local - full * group * ntiles, gm = mx - full * group;
+        if (gm <= 0 || r >= gm * ntiles) return;
+        mi = full * group + r % gm;
+        nt = r / gm;
+    }
+    const int mt = mi * kXcds + xcd;
     if (mt >= mtiles) return;
     const int tile = mt * ntiles + nt;
     int64_t m_lo, m_hi;
@@ -376,6 +394,71 @@ void k_gemm(GemmDesc g, int mtiles, int ntiles, int per_xcd, int ksplit) {
                 }
     }
 
+    // ---- staged epilogue (2-byte outputs, N and ldc multiples of 8): each
+    //      wave writes a 32-row block of its tile, rounded, to its own slot of
+    //      the stage buffers (rows padded by 8 bytes, so the 32 rows of one
+    //      8-byte write start on distinct bank pairs), then reads it back as
+    //      whole rows, WTN / 8 lanes per row with 16 bytes each, and stores
+    //      them; the row scatter applies per stored row.  Same values and
+    //      rounding as the direct epilogue below.
+    constexpr int kPitch = WTN * 2 + 8;
+    constexpr bool kStaged =
+        sizeof(Tin) == 2 && WTN % 8 == 0 && (NW / 2) * 32 * kPitch <= STAGE_A + STAGE_B;
+    if (kStaged && staged && !g.c_f32 && g.N % 8 == 0 && g.ldc % 8 == 0) {
+        __syncthreads();                   // every wave is done with the stage buffers
+        unsigned char* slot = (wave < NW / 2 ? st0 : st1) + (wave % (NW / 2)) * 32 * kPitch;
+        constexpr int LPR = WTN / 8, RPI = 64 / LPR;      // lanes per row, rows per read
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+            const int64_t m = m_lo + wm * WTM + i * 32 + lrow;
+            float rs = 1.0f, rs1 = 1.0f;
+            if (g.row_scale != nullptr && m < m_hi) {
+                const int32_t sr = g.scale_rows[m];
+                rs = sr >= 0 ? g.row_scale[sr] : 0.0f;
+                rs1 = g.row_scale2 == nullptr ? rs : (sr >= 0 ? g.row_scale2[sr] : 0.0f);
+            }
+#pragma unroll
+            for (int j = 0; j < TN; ++j) {
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4) {
+                    const int nl = j * 32 + 8 * q4 + 4 * lhalf;
+                    const int n = n0 + wn * WTN + nl;
+                    float val[4];
+#pragma unroll
+                    for (int t = 0; t < 4; ++t) {
+                        const float bb = (g.bias != nullptr && n + t < g.N) ? g.bias[n + t] : 0.0f;
+                        const float sc = n + t >= g.scale_col0 ? (n + t >= g.scale_col1 ? rs1 : rs) : 1.0f;
+                        val[t] = acc[i][j][4 * q4 + t] * sc + bb;
+                        if (g.gelu) val[t] = gelu_erf(val[t]);
+                    }
+                    uint2 w;
+                    w.x = pack2_bf16(val[0], val[1]);
+                    w.y = pack2_bf16(val[2], val[3]);
+                    *reinterpret_cast<uint2*>(slot + lrow * kPitch + nl * 2) = w;
+                }
+            }
+            // the slot is the wave's own: LDS accesses of one wave complete
+            // in order, so only the compiler must keep them in place
+            __builtin_amdgcn_wave_barrier();
+#pragma unroll
+            for (int it = 0; it < 32 / RPI; ++it) {
+                const int rr = it * RPI + lane / LPR, ch = lane % LPR;
+                const uint4 v = *reinterpret_cast<const uint4*>(slot + rr * kPitch + ch * 16);
+                const int64_t mm = m_lo + wm * WTM + i * 32 + rr;
+                const int n = n0 + wn * WTN + ch * 8;
+                if (mm < m_hi && n < g.N) {
+                    const int64_t cr = g.c_rows != nullptr ? static_cast<int64_t>(g.c_rows[mm]) : mm;
+                    if (cr >= 0) {
+                        const int64_t cm = g.c_rows != nullptr ? cr / g.c_div : cr;
+                        *reinterpret_cast<uint4*>(static_cast<Tin*>(g.C) + cm * g.ldc + n) = v;
+                    }
+                }
+            }
+            __builtin_amdgcn_wave_barrier();
+        }
+        return;
+    }
+
     // ---- epilogue.  The MFMAs took B as the first operand, so tile (i, j)
     //      holds C^T: lane l owns row m = .. + i*32 + l%32, and its value v is
     //      column n = .. + j*32 + 8*(v/4) + 4*(l/32) + v%4 -- four consecutive
@@ -457,6 +540,11 @@ static hipError_t gemm_cfg(const GemmDesc& g, hipStream_t st) {
     if (S == 1) d.ks_part = nullptr;
     // every XCD takes ceil(mt / 8) row tiles of nt tiles of S parts
     const int64_t per_xcd = (mt + kXcds - 1) / kXcds * nt * S;
+    // measured on the DeiT-Base products: groups of four row tiles (fc1 +
+    // GELU 391 -> 377 us, the others unchanged); the staged epilogue pays
+    // off for long K (dense fc2 298 -> 288, pair [t|u] product 183 -> 178 us)
+    // and costs for short K (fc1 +1 %, DeiT-Small fc1 +5 %)
+    const int group = 4, staged = g.K >= 2048 ? 1 : 0;
     const int64_t grid = per_xcd * kXcds;
     if (S > 1) {
         // the fill kernel must not take the timing events meant for the GEMM
@@ -470,7 +558,7 @@ static hipError_t gemm_cfg(const GemmDesc& g, hipStream_t st) {
         if (err != hipSuccess) return err;
     }
     launch_kernel(k_gemm<Tin, BM, BN, WM, WN, NS, SB, WPE>, dim3(static_cast<unsigned>(grid)), 64 * WM * WN, 0, st,
-        d, static_cast<int>(mt), static_cast<int>(nt), static_cast<int>(per_xcd), S);
+        d, static_cast<int>(mt), static_cast<int>(nt), group, S, staged);
     return hipGetLastError();
 }
 

@@ -23,6 +23,7 @@ SPLIT_LAYERS = [
     ("f32", 1576, 192, 768, 4, 64, 16),     # DeiT-Tiny widths: S = 4
     ("f32", 70, 64, 2048, 3, 32, 8),        # 4 tiles of 128x64, 64 k stages: S = 8
     ("bf16", 300, 128, 1024, 4, 48, 16),    # r % 32 != 0: GEMM chain, 7 tiles, S = 4
+    ("bf16", 300, 128, 2056, 4, 48, 16),    # K >= 2048: the staged epilogue after the part sum
 ]
 
 

@@ -367,6 +367,8 @@ def test_dense_comparator(name):
     (16411, 520, 1032),    # both products: 128x256 tiles, 64-byte stages
     (16411, 264, 1032),    # fc2 (N = 264, K = 1032): 128x128 tiles, four waves, 64-byte stages
     (5003, 136, 1032),     # fc1 (N = 1032, K = 136): 128x128 tiles over eight waves
+    (20011, 1672, 2056),   # fc2 with K >= 2048: 256x128 tiles, the staged epilogue, last column tile 8 wide
+    (9001, 264, 2056),     # fc2 (N = 264, K = 2056): 64x64 tiles, the staged epilogue
 ])
 def test_dense_gemm_tile_rules_ragged(T, D, H):
     """The dense FFN (bf16) at shapes that select each bf16 tile rule of the
