@@ -402,8 +402,8 @@ void k_gemm(GemmDesc g, int mtiles, int ntiles, int group, int ksplit, int stage
     //      them; the row scatter applies per stored row.  Same values and
     //      rounding as the direct epilogue below.
     constexpr int kPitch = WTN * 2 + 8;
-    constexpr bool kStaged =
-        sizeof(Tin) == 2 && WTN % 8 == 0 && (NW / 2) * 32 * kPitch <= STAGE_A + STAGE_B;
+    constexpr bool kStaged = sizeof(Tin) == 2 && WTN % 8 == 0 && 64 % (WTN / 8) == 0 &&
+                             32 % (64 / (WTN / 8)) == 0 && (NW / 2) * 32 * kPitch <= STAGE_A + STAGE_B;
     if (kStaged && staged && !g.c_f32 && g.N % 8 == 0 && g.ldc % 8 == 0) {
         __syncthreads();                   // every wave is done with the stage buffers
         unsigned char* slot = (wave < NW / 2 ? st0 : st1) + (wave % (NW / 2)) * 32 * kPitch;
@@ -577,13 +577,16 @@ static hipError_t gemm_dt(const GemmDesc& g, hipStream_t st) {
         // 64-byte stages, three in flight, and two workgroups per CU (72 KB
         // of LDS each) beat 128-byte stages two deep, which leave the loads'
         // latency exposed (fc1 + GELU 446 -> 407 us, the dense fc2 320 ->
-        // 302, the pair products 245 -> 209 and 138 -> 79 us)
+        // 302); 256x128 over eight waves then beat every other tile of that
+        // kind for the long products with N >= 512 (the pair y product, N =
+        // 768, K = 384: 67 -> 58 us against 128x256) and for the long-K ones
+        // with 128 < N <= 512 (the pair [t|u_a|u_b] product, N = 384, K =
+        // 3072: 180 -> 173 us against 128x128 over four waves)
         const int64_t mnk = g.M * static_cast<int64_t>(g.N) * g.K;
-        if (g.N >= 512 && mnk >= (int64_t{1} << 35))
+        if (g.N >= 512 && (mnk >= (int64_t{1} << 35) || g.M >= 16384))
             return gemm_cfg<Tin, 256, 128, 4, 2, 3, 64>(g, st);
-        if (g.N >= 512 && g.M >= 16384) return gemm_cfg<Tin, 128, 256, 4, 2, 3, 64>(g, st);
         if (g.N > 128 && g.N <= 512 && g.K >= 1024 && g.M >= 16384)
-            return gemm_cfg<Tin, 128, 128, 2, 2, 3, 64, 2>(g, st);
+            return gemm_cfg<Tin, 256, 128, 4, 2, 3, 64>(g, st);
         if (g.N >= 1024 && g.K <= 512) return gemm_cfg<Tin, 128, 128, 4, 2, 2>(g, st);
         // long k rows (2 KB or more) over a few hundred 64x64 tiles (e.g. the
         // pair products of an adaptive layer at DeiT-Small widths, 28 -> 20

@@ -364,8 +364,8 @@ def test_dense_comparator(name):
 
 @pytest.mark.parametrize("T,D,H", [
     (20011, 1672, 1032),   # both products: 256x128 tiles, 64-byte stages (largest)
-    (16411, 520, 1032),    # both products: 128x256 tiles, 64-byte stages
-    (16411, 264, 1032),    # fc2 (N = 264, K = 1032): 128x128 tiles, four waves, 64-byte stages
+    (16411, 520, 1032),    # both products: 256x128 tiles by row count (M >= 16384)
+    (16411, 264, 1032),    # fc2 (N = 264, K = 1032): 256x128 tiles, long K with N <= 512
     (5003, 136, 1032),     # fc1 (N = 1032, K = 136): 128x128 tiles over eight waves
     (20011, 1672, 2056),   # fc2 with K >= 2048: 256x128 tiles, the staged epilogue, last column tile 8 wide
     (9001, 264, 2056),     # fc2 (N = 264, K = 2056): 64x64 tiles, the staged epilogue
