@@ -69,10 +69,20 @@ typedef enum {
 typedef enum { CLEARMOE_F32 = 0, CLEARMOE_BF16 = 1 } clearmoe_dtype;
 
 /* Layer shape.  T tokens, D model width, H fc1 width (d_ffn), E experts,
- * k experts per token, r shared SVD rank, q residual rank per expert. */
+ * k experts per token, r shared SVD rank, q residual rank per expert.
+ * renorm selects the gates of the chosen experts (Sec. III Phase 4 treats
+ * the router's scores as a distribution over the E experts; the paper does
+ * not say whether the top-k gates are renormalised):
+ *   1  the softmax of the k selected logits, renormalised over them (k = 1:
+ *      gate 1) -- the reading the benchmark workloads use;
+ *   0  the selected experts' probabilities under the softmax over all E
+ *      logits (they sum to less than 1 unless k = E).
+ * Any other value is rejected (CLEARMOE_ERR_INVALID_ARG); a zero-filled
+ * struct therefore asks for the unrenormalised gates. */
 typedef struct {
     int32_t T, D, H, E, k, r, q;
     int32_t dtype;                 /* clearmoe_dtype */
+    int32_t renorm;                /* 1: renormalised top-k gates; 0: full-softmax gates */
 } clearmoe_shape;
 
 /* Flags of clearmoe_dispatch. */
@@ -96,19 +106,22 @@ const char* clearmoe_status_string(int status);
 size_t clearmoe_workspace_bytes(const clearmoe_shape* shape);
 
 /* Router and top-k (Sec. III Phase 4 linear router, with the bias counted in
- * Table C5; Algorithm 3 "a <- argmax(g(x))"; top-k with renormalised softmax
- * gates).
+ * Table C5; Algorithm 3 "a <- argmax(g(x))"; top-k with softmax gates,
+ * renormalised over the selected experts unless shape->renorm is 0).
  *   x   [T, D], Wg [E, D] (dtype); bg [E] float32 or NULL.
  *   idx [T, k] int32 out: experts by logit descending, ties to the lower
  *       index; slot 0 is the best.
- *   gate [T, k] float32 out: softmax over the k selected logits (1.0 at k=1).
+ *   gate [T, k] float32 out: renorm 1: softmax over the k selected logits
+ *       (1.0 at k=1); renorm 0: the selected experts' probabilities under
+ *       the softmax over all E logits.
  * The choice is exact: logits are accumulated in float32 by MFMA together
  * with a rigorous bound on their rounding error, and every token whose top-k
  * gaps do not clear that bound is recomputed in double (so ties are decided
  * by the index rule on exact sums).  Gates come from the same logits.
  * ws (required) receives the per-tile expert histogram of the result, which a
  * following clearmoe_dispatch with CLEARMOE_DISPATCH_HIST_IN_WS and the same
- * T, E, k reuses instead of recounting.  Uses shape fields T, D, E, k, dtype. */
+ * T, E, k reuses instead of recounting.  Uses shape fields T, D, E, k,
+ * dtype, renorm. */
 int clearmoe_route(const clearmoe_shape* shape, const void* x, const void* Wg, const float* bg,
                    int32_t* idx, float* gate, void* ws, size_t ws_bytes, hipStream_t stream);
 
@@ -125,7 +138,8 @@ int clearmoe_route(const clearmoe_shape* shape, const void* x, const void* Wg, c
  *             token is its largest softmax probability over all E experts,
  *             p = 1 / sum_e exp(l_e - l_max); p >= tau keeps it at top-1
  *             (idx = (best, -1), gate = (1, 0): slot 1 is empty), otherwise
- *             it takes the top 2 with their softmax renormalised.
+ *             it takes the top 2 with their softmax renormalised (with
+ *             shape->renorm 0: gates (p, 0), or the two probabilities).
  *   Class tokens (Table C6 excludes the class token of each image from
  *   expert dispatch and runs it on the dense path): with dense_stride s > 0
  *   every token t with t % s == 0 gets no expert (all k slots -1, gate 0);

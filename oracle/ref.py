@@ -22,7 +22,7 @@ __all__ = ["build", "lib", "widen", "num_threads", "set_num_threads", "gelu", "r
            "topk", "route", "dispatch", "permute_rows", "fc1_gelu", "shared", "residual",
            "ffn_forward", "ffn_forward_layer", "combine", "margins", "adaptive_topk",
            "round_to_storage", "mlp_router_logits", "route_layer", "ffn_forward_routed",
-           "confidence", "dense_fc2", "class_tokens"]
+           "confidence", "dense_fc2", "class_tokens", "full_softmax_gates"]
 
 
 def build(force: bool = True) -> str:
@@ -128,6 +128,24 @@ def adaptive_topk(logits, tau: float):
     return idx, gate
 
 
+def full_softmax_gates(logits, idx) -> np.ndarray:
+    """Gates without renormalisation (shape field renorm = 0): the chosen
+    experts' probabilities under the softmax over all E logits of the token
+    (Sec. III Phase 4: the router's scores as a distribution over experts).
+    An empty slot (idx -1) gets 0.  Plain loops over tokens and slots."""
+    lg = np.asarray(logits, dtype=np.float64)
+    idx = np.asarray(idx)
+    T, k = idx.shape
+    gate = np.zeros((T, k))
+    for t in range(T):
+        m = lg[t].max()
+        den = np.sum(np.exp(lg[t] - m))
+        for j in range(k):
+            if idx[t, j] >= 0:
+                gate[t, j] = np.exp(lg[t, idx[t, j]] - m) / den
+    return gate
+
+
 def confidence(logits) -> np.ndarray:
     """Largest softmax probability of each token (the adaptive router's
     confidence), in double."""
@@ -170,6 +188,8 @@ def route_layer(layer: dict, rows=None):
         idx, gate = adaptive_topk(lg, rt["tau"])
     else:
         idx, gate = topk(lg, k)
+    if int(layer.get("renorm", 1)) == 0:
+        gate = full_softmax_gates(lg, idx)
     return idx, gate, lg
 
 
@@ -287,6 +307,7 @@ def ffn_forward_layer(layer: dict, rows=None):
     of the layer depends on its own token alone, so a sample of rows gives the
     same values as the full run at those rows.  A "router" entry (MLP or
     adaptive) routes through route_layer; without it the linear router runs.
+    A "renorm" entry 0 gives the unrenormalised gates (full_softmax_gates).
     A "dense_stride" entry s > 0 makes every token t with t % s == 0 a class
     token (Table C6): it takes no expert slot (idx -1, gate 0) and its output
     is the dense FFN's, GELU(x W1^T + b1) W2^T + b2 with the layer's "W2".
@@ -305,7 +326,8 @@ def ffn_forward_layer(layer: dict, rows=None):
                                                                         idx, gate)
         y[cls] = dense_fc2(z[cls], layer["W2"], layer["b2"])
         return dict(y=y, idx=idx, gate=gate, logits=lg, cls=cls)
-    if layer.get("router") is not None and layer["router"]["kind"] != "linear":
+    if (layer.get("router") is not None and layer["router"]["kind"] != "linear") or \
+            int(layer.get("renorm", 1)) == 0:
         idx, gate, lg = route_layer(layer, rows)
         y = ffn_forward_routed(x, layer["W1"], layer["b1"], layer["US"], layer["Vt"],
                                layer["b2"], layer["P"], layer["Q"], idx, gate)

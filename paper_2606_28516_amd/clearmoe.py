@@ -44,7 +44,7 @@ class ClearMoEError(RuntimeError):
 
 
 class Shape(ctypes.Structure):
-    _fields_ = [(n, ctypes.c_int32) for n in ("T", "D", "H", "E", "k", "r", "q", "dtype")]
+    _fields_ = [(n, ctypes.c_int32) for n in ("T", "D", "H", "E", "k", "r", "q", "dtype", "renorm")]
 
 
 class Router(ctypes.Structure):
@@ -166,8 +166,10 @@ def _stream(stream) -> ctypes.c_void_p:
     return ctypes.c_void_p(s.cuda_stream)
 
 
-def make_shape(T, D, E, k, dtype, H=0, r=0, q=0) -> Shape:
-    return Shape(int(T), int(D), int(H), int(E), int(k), int(r), int(q), int(dtype))
+def make_shape(T, D, E, k, dtype, H=0, r=0, q=0, renorm=1) -> Shape:
+    """renorm = 1: the top-k gates renormalised over the selected experts;
+    0: their probabilities under the softmax over all E."""
+    return Shape(int(T), int(D), int(H), int(E), int(k), int(r), int(q), int(dtype), int(renorm))
 
 
 def workspace_bytes(shape: Shape) -> int:
@@ -181,11 +183,11 @@ def alloc_workspace(shape: Shape, device="cuda") -> torch.Tensor:
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
-def route(x, Wg, bg, k: int, ws: Optional[torch.Tensor] = None, stream=None):
+def route(x, Wg, bg, k: int, ws: Optional[torch.Tensor] = None, stream=None, renorm: int = 1):
     """clearmoe_route: returns (idx [T,k] int32, gate [T,k] float32)."""
     T, D = x.shape
     E = Wg.shape[0]
-    s = make_shape(T, D, E, k, _dt(x))
+    s = make_shape(T, D, E, k, _dt(x), renorm=renorm)
     ws = alloc_workspace(s, x.device) if ws is None else ws
     idx = torch.empty((T, k), dtype=torch.int32, device=x.device)
     gate = torch.empty((T, k), dtype=torch.float32, device=x.device)
@@ -206,10 +208,11 @@ def make_router(Wg, bg=None, Wh=None, bh=None, adaptive: bool = False, tau: floa
                   1 if adaptive else 0, int(dense_stride), 0, float(tau))
 
 
-def route_ex(x, router: Router, E: int, k: int, ws: Optional[torch.Tensor] = None, stream=None):
+def route_ex(x, router: Router, E: int, k: int, ws: Optional[torch.Tensor] = None, stream=None,
+             renorm: int = 1):
     """clearmoe_route_ex: returns (idx [T,k] int32, -1 = empty slot; gate [T,k])."""
     T, D = x.shape
-    s = make_shape(T, D, E, k, _dt(x))
+    s = make_shape(T, D, E, k, _dt(x), renorm=renorm)
     ws = alloc_workspace(s, x.device) if ws is None else ws
     idx = torch.empty((T, k), dtype=torch.int32, device=x.device)
     gate = torch.empty((T, k), dtype=torch.float32, device=x.device)
@@ -260,12 +263,12 @@ def padded_workspace_bytes(shape: Shape) -> int:
 
 
 def _layer_call(name, ws_bytes, x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k, ws, out, idx_out,
-                gate_out, stream):
+                gate_out, stream, renorm=1):
     T, D = x.shape
     H = W1.shape[0]
     r = US.shape[1]
     E, _, q = P.shape
-    s = make_shape(T, D, E, k, _dt(x), H=H, r=r, q=q)
+    s = make_shape(T, D, E, k, _dt(x), H=H, r=r, q=q, renorm=renorm)
     if ws is None:
         n = ws_bytes(s)
         if n == 0:
@@ -280,22 +283,23 @@ def _layer_call(name, ws_bytes, x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k, ws, out,
 
 
 def ffn_forward(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int, ws: Optional[torch.Tensor] = None,
-                out: Optional[torch.Tensor] = None, idx_out=None, gate_out=None, stream=None):
+                out: Optional[torch.Tensor] = None, idx_out=None, gate_out=None, stream=None,
+                renorm: int = 1):
     """clearmoe_ffn_forward: the whole layer.  Returns y [T, D]."""
     return _layer_call("clearmoe_ffn_forward", workspace_bytes, x, W1, b1, US, Vt, b2, P, Q, Wg,
-                       bg, k, ws, out, idx_out, gate_out, stream)
+                       bg, k, ws, out, idx_out, gate_out, stream, renorm)
 
 
 def ffn_forward_noalloc(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int,
                         out: Optional[torch.Tensor] = None, idx_out=None, gate_out=None,
-                        stream=None):
+                        stream=None, renorm: int = 1):
     """clearmoe_ffn_forward_noalloc: the whole layer with the library's own
     fixed scratch (no workspace).  Returns y [T, D]."""
     T, D = x.shape
     H = W1.shape[0]
     r = US.shape[1]
     E, _, q = P.shape
-    s = make_shape(T, D, E, k, _dt(x), H=H, r=r, q=q)
+    s = make_shape(T, D, E, k, _dt(x), H=H, r=r, q=q, renorm=renorm)
     y = torch.empty((T, D), dtype=x.dtype, device=x.device) if out is None else out
     rc = lib().clearmoe_ffn_forward_noalloc(ctypes.byref(s), _p(x), _p(W1), _p(b1), _p(US), _p(Vt),
                                             _p(b2), _p(P), _p(Q), _p(Wg), _p(bg), _p(y),
@@ -306,22 +310,22 @@ def ffn_forward_noalloc(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int,
 
 def ffn_forward_padded(x, W1, b1, US, Vt, b2, P, Q, Wg, bg, k: int,
                        ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
-                       idx_out=None, gate_out=None, stream=None):
+                       idx_out=None, gate_out=None, stream=None, renorm: int = 1):
     """clearmoe_ffn_forward_padded: the whole layer through the padded batched
     backend (blocks the host until dispatch is done).  Returns y [T, D]."""
     return _layer_call("clearmoe_ffn_forward_padded", padded_workspace_bytes, x, W1, b1, US, Vt,
-                       b2, P, Q, Wg, bg, k, ws, out, idx_out, gate_out, stream)
+                       b2, P, Q, Wg, bg, k, ws, out, idx_out, gate_out, stream, renorm)
 
 
 def ffn_forward_ex(x, W1, b1, US, Vt, b2, P, Q, router: Router, k: int,
                    ws: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
-                   idx_out=None, gate_out=None, stream=None):
+                   idx_out=None, gate_out=None, stream=None, renorm: int = 1):
     """clearmoe_ffn_forward_ex: the whole layer with any router.  Returns y."""
     T, D = x.shape
     H = W1.shape[0]
     r = US.shape[1]
     E, _, q = P.shape
-    s = make_shape(T, D, E, k, _dt(x), H=H, r=r, q=q)
+    s = make_shape(T, D, E, k, _dt(x), H=H, r=r, q=q, renorm=renorm)
     ws = alloc_workspace(s, x.device) if ws is None else ws
     y = torch.empty((T, D), dtype=x.dtype, device=x.device) if out is None else out
     rc = lib().clearmoe_ffn_forward_ex(ctypes.byref(s), ctypes.byref(router), _p(x), _p(W1),

@@ -136,7 +136,7 @@ Layout layout_min(const clearmoe_shape& s) {
         return at;
     };
     const bool fused = k == 1 && s.dtype == CLEARMOE_BF16 && fused_top1_supported(s.D, s.H, s.r, s.q);
-    const bool own = fused && hist_tiles(T, static_cast<int>(E)) * E <= kInlineScanMax;
+    const bool own = fused && s.renorm && hist_tiles(T, static_cast<int>(E)) * E <= kInlineScanMax;
     const bool pair = pair_path(s);
     const int64_t ntiles = route_tiles(T);
     L.tile_counts = take(sizeof(int32_t) * hist_tiles(T, static_cast<int>(E)) * E);
@@ -202,6 +202,7 @@ int check_shape(const clearmoe_shape* s, bool layer, bool unaligned_ok = false) 
     if (s->dtype != CLEARMOE_F32 && s->dtype != CLEARMOE_BF16) return CLEARMOE_ERR_UNSUPPORTED;
     if (s->T < 0 || s->D < 1 || s->D > kMaxDim) return CLEARMOE_ERR_INVALID_ARG;
     if (s->E < 1 || s->E > 64 || s->k < 1 || s->k > s->E) return CLEARMOE_ERR_INVALID_ARG;
+    if (s->renorm != 0 && s->renorm != 1) return CLEARMOE_ERR_INVALID_ARG;
     if (static_cast<int64_t>(s->T) * s->k >= (int64_t{1} << 31)) return CLEARMOE_ERR_INVALID_ARG;
     const int mult = unaligned_ok ? 1 : (s->dtype == CLEARMOE_F32 ? 4 : 8);
     if (s->D % mult != 0) return CLEARMOE_ERR_INVALID_ARG;
@@ -352,13 +353,13 @@ int route_impl(const clearmoe_shape& s, const Layout& L, const clearmoe_router& 
     if (rt.hidden == 0) {
         CLEARMOE_STAGE(CLEARMOE_STAGE_ROUTE, st,
                        launch_route(s.dtype, x, rt.Wg, rt.bg, s.T, s.D, s.E, s.k, rt.adaptive,
-                                    rt.tau, rt.dense_stride, idx, gate, tc, st));
+                                    s.renorm, rt.tau, rt.dense_stride, idx, gate, tc, st));
         return CLEARMOE_OK;
     }
     CLEARMOE_STAGE(CLEARMOE_STAGE_ROUTE, st,
                    launch_route_mlp(s.dtype, x, rt.Wh, rt.bh, rt.Wg, rt.bg, s.T, s.D, rt.hidden,
-                                    s.E, s.k, rt.adaptive, rt.tau, rt.dense_stride, idx, gate,
-                                    st));
+                                    s.E, s.k, rt.adaptive, s.renorm, rt.tau, rt.dense_stride,
+                                    idx, gate, st));
     CLEARMOE_STAGE(CLEARMOE_STAGE_TILE_HIST, st,
                    launch_tile_histogram(idx, s.T, s.E, s.k, tc, st));
     return CLEARMOE_OK;
@@ -746,7 +747,10 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
     // dispatches pair keys instead, below)
     rc = route_impl(s, L, *router, x, idx, gate, ws, st);
     if (rc != CLEARMOE_OK) return rc;
-    const bool own_dispatch = fused && hist_tiles(T, s.E) * s.E <= kInlineScanMax;
+    // (the fused kernel's own dispatch takes every top-1 gate as 1, which
+    // holds for renormalised gates only; with renorm == 0 it reads them
+    // from the dispatch kernels' order)
+    const bool own_dispatch = fused && s.renorm && hist_tiles(T, s.E) * s.E <= kInlineScanMax;
     if (!own_dispatch && !pair_path(s)) {
         rc = dispatch_impl(s, L, idx, ws, counts, offsets, perm, inv, nullptr, nullptr, true, st);
         if (rc != CLEARMOE_OK) return rc;

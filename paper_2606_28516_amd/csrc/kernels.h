@@ -153,14 +153,14 @@ __host__ __device__ inline int64_t hist_tiles(int64_t T, int E) {
 // per-tile expert histogram (tile_counts may be NULL).  dense_stride > 0:
 // tokens t with t % dense_stride == 0 get no expert (all slots -1, gate 0).
 hipError_t launch_route(int dtype, const void* x, const void* Wg, const float* bg, int64_t T,
-                        int D, int E, int k, int adaptive, double tau, int dense_stride,
+                        int D, int E, int k, int adaptive, int renorm, double tau, int dense_stride,
                         int32_t* idx, float* gate, int32_t* tile_counts, hipStream_t st);
 // MLP router: hidden GELU(x Wh^T + bh) of width Hr (1..kMlpHiddenMax) rounded
 // to the storage type, logits hr Wo^T + bo in double; then as launch_route
 // (no histogram).
 hipError_t launch_route_mlp(int dtype, const void* x, const void* Wh, const float* bh,
                             const void* Wo, const float* bo, int64_t T, int D, int Hr, int E,
-                            int k, int adaptive, double tau, int dense_stride, int32_t* idx,
+                            int k, int adaptive, int renorm, double tau, int dense_stride, int32_t* idx,
                             float* gate, hipStream_t st);
 constexpr int kMlpHiddenMax = 256;
 // Per-tile expert histogram of an index array (tiles of hist_tile(T, E) tokens).

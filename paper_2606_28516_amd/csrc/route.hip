@@ -137,16 +137,22 @@ __device__ __forceinline__ double route_confidence(const double (&lg)[EP], int E
 }
 
 // Choice of one token from its logits (descending, ties to the lower index):
-// the top k with the softmax of the selected logits renormalised (k = 1:
-// gate 1), or, adaptive (k = 2 slots), top-1 when the confidence reaches tau
-// and top-2 otherwise, the unused second slot being expert -1 with gate 0.
-// Writes idx/gate of token t; returns the bit set of the chosen experts.
+// the top k, or, adaptive (k = 2 slots), top-1 when the confidence reaches
+// tau and top-2 otherwise, the unused second slot being expert -1 with gate
+// 0.  Gates: renorm != 0, the softmax of the selected logits renormalised
+// over them (k = 1: gate 1); renorm == 0, the selected experts' probabilities
+// under the softmax over all E logits (their sum is below 1 unless every
+// expert is selected).  Writes idx/gate of token t; returns the bit set of
+// the chosen experts.
 template <int EP>
 __device__ __forceinline__ uint64_t route_select(const double (&lg)[EP], int E, int k,
-                                                 int adaptive, double tau, int64_t t,
+                                                 int adaptive, int renorm, double tau, int64_t t,
                                                  int32_t* __restrict__ idx,
                                                  float* __restrict__ gate) {
-    const int kk = (adaptive && route_confidence<EP>(lg, E) >= tau) ? 1 : k;
+    // the largest probability under the softmax over all E (adaptive choice;
+    // renorm == 0: an expert's gate is exp(l - l_max) times it)
+    const double conf = (adaptive || !renorm) ? route_confidence<EP>(lg, E) : 1.0;
+    const int kk = (adaptive && conf >= tau) ? 1 : k;
     if (kk == 2) {
         // two experts: gates 1 / (1 + e1) and e1 / (1 + e1), e1 = exp(l1 - l0)
         // (the general loop's arithmetic: exp(0) = 1 exactly), one exp
@@ -154,7 +160,7 @@ __device__ __forceinline__ uint64_t route_select(const double (&lg)[EP], int E, 
         const int b0 = pick<EP>(lg, E, 0ull, v0);
         const int b1 = pick<EP>(lg, E, 1ull << b0, v1);
         const double e1 = exp_ool(v1 - v0);
-        const double den = 1.0 + e1;
+        const double den = renorm ? 1.0 + e1 : 1.0 / conf;
         idx[t * k] = b0;
         idx[t * k + 1] = b1;
         gate[t * k] = static_cast<float>(1.0 / den);
@@ -168,11 +174,12 @@ __device__ __forceinline__ uint64_t route_select(const double (&lg)[EP], int E, 
         const int best = pick<EP>(lg, E, mine, bv);
         mine |= 1ull << best;
         if (j == 0) top = bv;
-        if (kk > 1) den += exp_ool(bv - top);         // one expert: its gate is 1
+        if (kk > 1 && renorm) den += exp_ool(bv - top);   // one expert: its gate is 1
         idx[t * k + j] = best;
     }
+    if (!renorm) den = 1.0 / conf;           // top is the largest logit
     if (kk == 1) {
-        gate[t * k] = 1.0f;
+        gate[t * k] = renorm ? 1.0f : static_cast<float>(conf);
     } else {
         uint64_t tk = 0;
         for (int j = 0; j < kk; ++j) {
@@ -207,7 +214,7 @@ template <typename Tin, int EG, int NB, int KP>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(EG == 1 ? 2 : 1)))
 void k_route(
     const Tin* __restrict__ x, const Tin* __restrict__ Wg, const float* __restrict__ bg, int64_t T,
-    int D, int E, int k, int adaptive, double tau, int dense_stride, int32_t* __restrict__ idx,
+    int D, int E, int k, int adaptive, int renorm, double tau, int dense_stride, int32_t* __restrict__ idx,
     float* __restrict__ gate, int32_t* __restrict__ tile_counts, int w_lds) {
     extern __shared__ __attribute__((aligned(16))) unsigned char s_w[];
     constexpr int EP = 16 * EG;                      // experts padded to MFMA rows
@@ -473,7 +480,7 @@ void k_route(
     }
     // ---- top-k (or adaptive top-1 / top-2), gates, outputs
     uint64_t mine = 0;
-    if (valid) mine = route_select<EP>(lg, E, k, adaptive, tau, t, idx, gate);
+    if (valid) mine = route_select<EP>(lg, E, k, adaptive, renorm, tau, t, idx, gate);
     if (cls && lane < kTok && t < T) {
         for (int j = 0; j < k; ++j) {
             idx[t * k + j] = -1;
@@ -543,7 +550,7 @@ template <typename Tin, int EG>
 __global__ __launch_bounds__(256) void k_route_mlp(
     const Tin* __restrict__ x, const Tin* __restrict__ Wh, const float* __restrict__ bh,
     const Tin* __restrict__ Wo, const float* __restrict__ bo, int64_t T, int D, int Hr, int E,
-    int k, int adaptive, double tau, int dense_stride, int32_t* __restrict__ idx,
+    int k, int adaptive, int renorm, double tau, int dense_stride, int32_t* __restrict__ idx,
     float* __restrict__ gate) {
     constexpr int EP = 16 * EG;
     static_assert(EG <= 4, "one wave per 16 experts");
@@ -623,7 +630,7 @@ __global__ __launch_bounds__(256) void k_route_mlp(
 #pragma unroll
             for (int e = 0; e < EP; ++e)
                 lg[e] = s_lg[lane][e] + ((bo != nullptr && e < E) ? static_cast<double>(bo[e]) : 0.0);
-            (void)route_select<EP>(lg, E, k, adaptive, tau, t, idx, gate);
+            (void)route_select<EP>(lg, E, k, adaptive, renorm, tau, t, idx, gate);
         }
     }
 }
@@ -631,36 +638,36 @@ __global__ __launch_bounds__(256) void k_route_mlp(
 template <typename Tin>
 static hipError_t route_mlp_dt(const Tin* x, const Tin* Wh, const float* bh, const Tin* Wo,
                                const float* bo, int64_t T, int D, int Hr, int E, int k,
-                               int adaptive, double tau, int dense_stride, int32_t* idx,
+                               int adaptive, int renorm, double tau, int dense_stride, int32_t* idx,
                                float* gate, hipStream_t st) {
     const int64_t blocks = (T + kMlpTokens - 1) / kMlpTokens;
     if (blocks == 0) return hipSuccess;
     const dim3 grid(static_cast<unsigned>(blocks));
     if (E <= 16)
-        launch_kernel(k_route_mlp<Tin, 1>, grid, 256, 0, st, x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau,
+        launch_kernel(k_route_mlp<Tin, 1>, grid, 256, 0, st, x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, renorm, tau,
                                                     dense_stride, idx, gate);
     else if (E <= 32)
-        launch_kernel(k_route_mlp<Tin, 2>, grid, 256, 0, st, x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau,
+        launch_kernel(k_route_mlp<Tin, 2>, grid, 256, 0, st, x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, renorm, tau,
                                                     dense_stride, idx, gate);
     else
-        launch_kernel(k_route_mlp<Tin, 4>, grid, 256, 0, st, x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, tau,
+        launch_kernel(k_route_mlp<Tin, 4>, grid, 256, 0, st, x, Wh, bh, Wo, bo, T, D, Hr, E, k, adaptive, renorm, tau,
                                                     dense_stride, idx, gate);
     return hipGetLastError();
 }
 
 hipError_t launch_route_mlp(int dtype, const void* x, const void* Wh, const float* bh,
                             const void* Wo, const float* bo, int64_t T, int D, int Hr, int E,
-                            int k, int adaptive, double tau, int dense_stride, int32_t* idx,
+                            int k, int adaptive, int renorm, double tau, int dense_stride, int32_t* idx,
                             float* gate, hipStream_t st) {
     if (Hr < 1 || Hr > kMlpHiddenMax) return hipErrorInvalidValue;
     if (dtype == 0)
         return route_mlp_dt<float>(static_cast<const float*>(x), static_cast<const float*>(Wh), bh,
                                    static_cast<const float*>(Wo), bo, T, D, Hr, E, k, adaptive,
-                                   tau, dense_stride, idx, gate, st);
+                                   renorm, tau, dense_stride, idx, gate, st);
     return route_mlp_dt<bf16_bits>(static_cast<const bf16_bits*>(x),
                                    static_cast<const bf16_bits*>(Wh), bh,
                                    static_cast<const bf16_bits*>(Wo), bo, T, D, Hr, E, k, adaptive,
-                                   tau, dense_stride, idx, gate, st);
+                                   renorm, tau, dense_stride, idx, gate, st);
 }
 
 constexpr int64_t kRouteWLds = 32 * 1024;
@@ -668,7 +675,7 @@ constexpr int64_t kRouteWLds = 32 * 1024;
 
 template <typename Tin>
 static hipError_t route_dt(const Tin* x, const Tin* Wg, const float* bg, int64_t T, int D, int E,
-                           int k, int adaptive, double tau, int dense_stride, int32_t* idx,
+                           int k, int adaptive, int renorm, double tau, int dense_stride, int32_t* idx,
                            float* gate, int32_t* tc, hipStream_t st) {
     const int64_t blocks = hist_tiles(T, E);
     if (blocks == 0) return hipSuccess;
@@ -678,31 +685,31 @@ static hipError_t route_dt(const Tin* x, const Tin* Wg, const float* bg, int64_t
     const int64_t wbytes = static_cast<int64_t>(E) * D * static_cast<int64_t>(sizeof(Tin));
     const int w_lds = wbytes <= kRouteWLds ? static_cast<int>((wbytes + 1023) / 1024 * 1024) : 0;
     if (small)
-        launch_kernel(k_route<Tin, 1, 1, 12>, grid, 256, w_lds, st, x, Wg, bg, T, D, E, k, adaptive, tau,
+        launch_kernel(k_route<Tin, 1, 1, 12>, grid, 256, w_lds, st, x, Wg, bg, T, D, E, k, adaptive, renorm, tau,
                                                           dense_stride, idx, gate, tc, w_lds);
     else if (E <= 16)
         launch_kernel(k_route<Tin, 1, 4, KPRE>, grid, kRouteTile, w_lds, st, x, Wg, bg, T, D, E, k, adaptive,
-                                                                   tau, dense_stride, idx, gate, tc,
+                                                                   renorm, tau, dense_stride, idx, gate, tc,
                                                                    w_lds);
     else if (E <= 32)
         launch_kernel(k_route<Tin, 2, 4, KPRE>, grid, kRouteTile, w_lds, st, x, Wg, bg, T, D, E, k, adaptive,
-                                                                   tau, dense_stride, idx, gate, tc,
+                                                                   renorm, tau, dense_stride, idx, gate, tc,
                                                                    w_lds);
     else
         launch_kernel(k_route<Tin, 4, 4, KPRE>, grid, kRouteTile, w_lds, st, x, Wg, bg, T, D, E, k, adaptive,
-                                                                   tau, dense_stride, idx, gate, tc,
+                                                                   renorm, tau, dense_stride, idx, gate, tc,
                                                                    w_lds);
     return hipGetLastError();
 }
 
 hipError_t launch_route(int dtype, const void* x, const void* Wg, const float* bg, int64_t T,
-                        int D, int E, int k, int adaptive, double tau, int dense_stride,
+                        int D, int E, int k, int adaptive, int renorm, double tau, int dense_stride,
                         int32_t* idx, float* gate, int32_t* tile_counts, hipStream_t st) {
     if (dtype == 0)
         return route_dt<float>(static_cast<const float*>(x), static_cast<const float*>(Wg), bg, T,
-                               D, E, k, adaptive, tau, dense_stride, idx, gate, tile_counts, st);
+                               D, E, k, adaptive, renorm, tau, dense_stride, idx, gate, tile_counts, st);
     return route_dt<bf16_bits>(static_cast<const bf16_bits*>(x), static_cast<const bf16_bits*>(Wg),
-                               bg, T, D, E, k, adaptive, tau, dense_stride, idx, gate, tile_counts,
+                               bg, T, D, E, k, adaptive, renorm, tau, dense_stride, idx, gate, tile_counts,
                                st);
 }
 

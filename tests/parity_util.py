@@ -44,7 +44,7 @@ def gpu_ffn(L, ws=None, with_routing=True, padded=False):
     gate = torch.empty((T, k), dtype=torch.float32, device="cuda") if with_routing else None
     fwd = cm.ffn_forward_padded if padded else cm.ffn_forward
     y = fwd(d["x"], d["W1"], d["b1"], d["US"], d["Vt"], d["b2"], d["P"], d["Q"], d["Wg"],
-            d["bg"], k, ws=ws, idx_out=idx, gate_out=gate)
+            d["bg"], k, ws=ws, idx_out=idx, gate_out=gate, renorm=int(L.get("renorm", 1)))
     torch.cuda.synchronize()
     out = dict(y=oracle.widen(cm.to_stored(y)))
     if with_routing:
@@ -99,15 +99,19 @@ def assert_routing(idx_gpu, logits_ref, k):
     return tie
 
 
-def assert_gates(gate_gpu, logits_ref, idx_gpu, k, tie):
+def assert_gates(gate_gpu, logits_ref, idx_gpu, k, tie, renorm=1):
     """Gates against the oracle's double gates (float32 rounding), on the tokens
-    where the GPU made the oracle's choice."""
-    _, g = oracle.topk(logits_ref, k)
+    where the GPU made the oracle's choice: renormalised over the chosen
+    experts (renorm 1) or their probabilities under the softmax over all E
+    (renorm 0)."""
+    i, g = oracle.topk(logits_ref, k)
+    if not renorm:
+        g = oracle.full_softmax_gates(logits_ref, i)
     ok = ~tie
     err = np.abs(gate_gpu[ok] - g[ok])
     # gates come from float32 logits whose choice is certified (double for near ties)
     assert np.all(err <= 2e-5), float(err.max())
-    if k == 1:
+    if k == 1 and renorm:
         assert np.all(gate_gpu == 1.0)
 
 
@@ -144,7 +148,7 @@ def gpu_ffn_ex(L):
     idx = torch.empty((T, k), dtype=torch.int32, device="cuda")
     gate = torch.empty((T, k), dtype=torch.float32, device="cuda")
     y = cm.ffn_forward_ex(d["x"], d["W1"], d["b1"], d["US"], d["Vt"], d["b2"], d["P"], d["Q"], r,
-                          k, idx_out=idx, gate_out=gate)
+                          k, idx_out=idx, gate_out=gate, renorm=int(L.get("renorm", 1)))
     torch.cuda.synchronize()
     del keep
     return dict(y=oracle.widen(cm.to_stored(y)), idx=idx.cpu().numpy(), gate=gate.cpu().numpy())

@@ -54,9 +54,10 @@ def test_timing_start_rejects_bad_arguments_before_creating_events():
 
 
 def _shape(**kw):
-    d = dict(T=100, D=64, H=128, E=4, k=2, r=16, q=8, dtype=cm.BF16)
+    d = dict(T=100, D=64, H=128, E=4, k=2, r=16, q=8, dtype=cm.BF16, renorm=1)
     d.update(kw)
-    return cm.make_shape(d["T"], d["D"], d["E"], d["k"], d["dtype"], H=d["H"], r=d["r"], q=d["q"])
+    return cm.make_shape(d["T"], d["D"], d["E"], d["k"], d["dtype"], H=d["H"], r=d["r"], q=d["q"],
+                         renorm=d["renorm"])
 
 
 def test_workspace_bytes_grows_with_shape_and_rejects_bad_shapes():
@@ -70,6 +71,10 @@ def test_workspace_bytes_grows_with_shape_and_rejects_bad_shapes():
     # unaligned layer shapes: the aligned layer's workspace plus padded copies
     assert cm.workspace_bytes(_shape(D=60, H=100, r=12, q=6)) > cm.workspace_bytes(_shape(H=104, r=16))
     assert cm.workspace_bytes(_shape(T=0)) > 0
+    # the gate rule: 1 (renormalised) or 0 (softmax over all E); nothing else
+    assert cm.workspace_bytes(_shape(renorm=0)) == a
+    assert cm.workspace_bytes(_shape(renorm=2)) == 0
+    assert cm.workspace_bytes(_shape(renorm=-1)) == 0
     # the configurations of the benchmark and tests are all valid
     for c in synth.CONFIGS.values():
         s = cm.make_shape(c.T, c.D, c.E, c.k, cm.F32 if c.dtype == "f32" else cm.BF16,
@@ -97,6 +102,8 @@ def test_route_rejects_before_launch():
     assert L.clearmoe_route(ctypes.byref(bad), FAKE, FAKE, None, FAKE, FAKE, FAKE, ws_n, None) == 1
     bad = _shape(dtype=7)
     assert L.clearmoe_route(ctypes.byref(bad), FAKE, FAKE, None, FAKE, FAKE, FAKE, ws_n, None) == 2
+    bad = _shape(renorm=3)
+    assert L.clearmoe_route(ctypes.byref(bad), FAKE, FAKE, None, FAKE, FAKE, FAKE, ws_n, None) == 1
     big = _shape(T=1 << 30, k=2)                                    # T*k >= 2^31
     assert L.clearmoe_route(ctypes.byref(big), FAKE, FAKE, None, FAKE, FAKE, FAKE, ws_n, None) == 1
     assert L.clearmoe_route(None, FAKE, FAKE, None, FAKE, FAKE, FAKE, ws_n, None) == 1
@@ -200,6 +207,13 @@ def _router(**kw):
     d.update(kw)
     return cm.Router(d["Wg"], d["bg"], d["Wh"], d["bh"], d["W2"], d["hidden"], d["adaptive"],
                      d["dense_stride"], d["reserved"], d["tau"])
+
+
+def test_shape_descriptor_layout():
+    """The ctypes mirror of clearmoe_shape: nine int32 (the gate rule last)."""
+    assert ctypes.sizeof(cm.Shape) == 36
+    assert cm.Shape.dtype.offset == 28 and cm.Shape.renorm.offset == 32
+    assert cm.make_shape(1, 8, 2, 1, cm.BF16).renorm == 1
 
 
 def test_router_descriptor_layout():

@@ -591,3 +591,40 @@ def test_class_tokens_on_a_row_sample_use_global_positions():
     full = oracle.ffn_forward_layer(C)
     assert np.array_equal(part["cls"], [True, False, True, False, True, False])
     assert np.max(np.abs(part["y"] - full["y"][rows])) < 1e-13
+
+
+def test_full_softmax_gates_hand_computed():
+    """Unrenormalised gates (shape field renorm = 0): each chosen expert's
+    probability under the softmax over all E logits.  Logits ln 1 .. ln 4
+    give probabilities 1/10 .. 4/10 exactly; the top two are experts 3 and 2
+    with 4/10 and 3/10 (renormalised: 4/7, 3/7); top-1 gives 4/10."""
+    lg = np.log(np.array([[1.0, 2.0, 3.0, 4.0], [4.0, 3.0, 2.0, 1.0]]))
+    idx, g2 = oracle.topk(lg, 2)
+    assert idx.tolist() == [[3, 2], [0, 1]]
+    assert np.allclose(g2, [[4 / 7, 3 / 7], [4 / 7, 3 / 7]], rtol=0, atol=1e-15)
+    full = oracle.full_softmax_gates(lg, idx)
+    assert np.allclose(full, [[0.4, 0.3], [0.4, 0.3]], rtol=0, atol=1e-15)
+    i1, _ = oracle.topk(lg, 1)
+    assert np.allclose(oracle.full_softmax_gates(lg, i1), [[0.4], [0.4]], rtol=0, atol=1e-15)
+    # an empty slot (adaptive top-1) gets 0; equal logits split evenly
+    assert oracle.full_softmax_gates(np.zeros((1, 5)), np.array([[2, -1]])).tolist() == [[0.2, 0.0]]
+
+
+@pytest.mark.parametrize("E,k", [(2, 1), (4, 2), (8, 2), (6, 3), (5, 5)])
+def test_full_softmax_gates_against_the_renormalised(E, k):
+    """Properties that tie the two gate rules together: the unrenormalised
+    gates divided by their sum over the k slots are the renormalised gates of
+    the C oracle's top-k; each is below 1 and their sum is the probability
+    mass of the chosen experts, which is 1 when every expert is chosen (k =
+    E) and at most 1 otherwise; with k = 1 the gate is the confidence."""
+    rng = np.random.default_rng(7 * E + k)
+    lg = 2.0 * rng.standard_normal((50, E))
+    idx, g = oracle.topk(lg, k)
+    full = oracle.full_softmax_gates(lg, idx)
+    s = full.sum(axis=1)
+    assert np.allclose(full / s[:, None], g, rtol=1e-13, atol=0)
+    assert np.all(full < 1.0 + 1e-15) and np.all(s <= 1.0 + 1e-13)
+    if k == E:
+        assert np.allclose(s, 1.0, rtol=0, atol=1e-13)
+    if k == 1:
+        assert np.allclose(full[:, 0], oracle.confidence(lg), rtol=1e-14, atol=0)
