@@ -40,8 +40,13 @@
  *     routing and y as unpadded (padding adds only zero products, and an
  *     extra hidden unit's activation is GELU(0) = 0); their pointers need
  *     only element alignment (the router's Wg stays 16-byte aligned when it
- *     is an MLP router's [E, hidden] output layer).  The other entry points
- *     keep the multiples.
+ *     is an MLP router's [E, hidden] output layer).  clearmoe_route and
+ *     clearmoe_route_ex take any D the same way (padded copies of x and the
+ *     router's D-wide matrix, counted by clearmoe_workspace_bytes);
+ *     clearmoe_dispatch (with rows) and clearmoe_combine take any D
+ *     directly, copying and combining rows one element at a time (same
+ *     results; their row pointers need element alignment only).  The padded
+ *     backend and the stack keep the multiples.
  *   - No C++ exception crosses this interface.  Calls on one stream are
  *     ordered; calls that share a workspace must not overlap in time.
  */

@@ -195,8 +195,9 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 
 // Shape checks common to every entry point (which fields matter depends on
 // the entry point; unused fields must still be in range).  D, H, r and q
-// must be multiples of the elements of a 16-byte piece, except for the
-// layer entry points (unaligned_ok), which pad such shapes.
+// must be multiples of the elements of a 16-byte piece, except where the
+// entry point takes other shapes (unaligned_ok): the layer entry points and
+// routing pad them, dispatch and combine copy their rows element by element.
 int check_shape(const clearmoe_shape* s, bool layer, bool unaligned_ok = false) {
     if (s == nullptr) return CLEARMOE_ERR_INVALID_ARG;
     if (s->dtype != CLEARMOE_F32 && s->dtype != CLEARMOE_BF16) return CLEARMOE_ERR_UNSUPPORTED;
@@ -271,6 +272,42 @@ PadLayout pad_layout(const clearmoe_shape& s) {
     return p;
 }
 
+// Routing with a row width D that is not a multiple of the elements of a
+// 16-byte piece runs on padded copies of x and the router's input matrix
+// (Wg, or an MLP router's Wh), placed after the aligned shape's own regions;
+// a valid layer shape uses the layer's padded copies (pad_layout).
+struct RoutePads {
+    clearmoe_shape a;     // the aligned routing shape (H = r = q = 0)
+    size_t x, Wg, Wh, total;
+};
+RoutePads route_pads(const clearmoe_shape& s) {
+    RoutePads r{};
+    r.a = s;
+    r.a.D = round_up(s.D, piece_elems(s.dtype));
+    r.a.H = r.a.r = r.a.q = 0;
+    if (check_shape(&s, true, true) == CLEARMOE_OK) {
+        const PadLayout p = pad_layout(s);
+        r.x = p.x;
+        r.Wg = p.Wg;
+        r.Wh = p.Wh;
+        r.total = p.total;
+        return r;
+    }
+    const size_t es = elem_size(s.dtype), D = static_cast<size_t>(r.a.D);
+    size_t off = up(layout(r.a).total);
+    r.x = off;
+    off = up(off + es * static_cast<size_t>(s.T) * D);
+    r.Wg = off;
+    off = up(off + es * static_cast<size_t>(s.E) * D);
+    r.Wh = off;
+    off = up(off + es * static_cast<size_t>(kMlpHiddenMax) * D);
+    r.total = off;
+    return r;
+}
+bool unaligned_rows(const clearmoe_shape& s) { return s.D % piece_elems(s.dtype) != 0; }
+int route_unaligned(const clearmoe_shape& s, const clearmoe_router& router, const void* x,
+                    int32_t* idx, float* gate, void* ws, size_t ws_bytes, hipStream_t st);
+
 // ---- stage timing: two events per timed launch, recorded on its stream ----
 struct StageTimer {
     bool on = false;
@@ -333,16 +370,18 @@ clearmoe_router linear_router(const void* Wg, const float* bg) {
 }
 
 // Router checks (before any HIP call).
-int check_router(const clearmoe_shape& s, const clearmoe_router* r) {
-    if (r == nullptr || r->Wg == nullptr || !aligned(r->Wg, 16)) return CLEARMOE_ERR_INVALID_ARG;
+// wa: the alignment the router's matrices need (16 bytes; one element when
+// they are read into padded copies).
+int check_router(const clearmoe_shape& s, const clearmoe_router* r, size_t wa = 16) {
+    if (r == nullptr || r->Wg == nullptr || !aligned(r->Wg, wa)) return CLEARMOE_ERR_INVALID_ARG;
     if (r->bg && !aligned(r->bg, 4)) return CLEARMOE_ERR_INVALID_ARG;
     if (r->hidden < 0 || r->hidden > kMlpHiddenMax) return CLEARMOE_ERR_INVALID_ARG;
-    if (r->hidden > 0 && (r->Wh == nullptr || !aligned(r->Wh, 16) || (r->bh && !aligned(r->bh, 4))))
+    if (r->hidden > 0 && (r->Wh == nullptr || !aligned(r->Wh, wa) || (r->bh && !aligned(r->bh, 4))))
         return CLEARMOE_ERR_INVALID_ARG;
     if (r->adaptive != 0 && r->adaptive != 1) return CLEARMOE_ERR_INVALID_ARG;
     if (r->adaptive && (s.k != 2 || s.E < 2 || r->tau != r->tau)) return CLEARMOE_ERR_INVALID_ARG;
     if (r->dense_stride < 0 || r->reserved != 0) return CLEARMOE_ERR_INVALID_ARG;
-    if (r->W2 && !aligned(r->W2, 16)) return CLEARMOE_ERR_INVALID_ARG;
+    if (r->W2 && !aligned(r->W2, wa)) return CLEARMOE_ERR_INVALID_ARG;
     return CLEARMOE_OK;
 }
 
@@ -368,6 +407,17 @@ int route_impl(const clearmoe_shape& s, const Layout& L, const clearmoe_router& 
 int dispatch_impl(const clearmoe_shape& s, const Layout& L, const int32_t* idx, void* ws,
                   int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv, const void* x,
                   void* xperm, bool hist_in_ws, hipStream_t st) {
+    if (x != nullptr && s.D % piece_elems(s.dtype) != 0) {
+        // rows that are not whole 16-byte pieces: the indices first, then the
+        // rows one element at a time
+        const int rc = dispatch_impl(s, L, idx, ws, counts, offsets, perm, inv, nullptr, nullptr,
+                                     hist_in_ws, st);
+        if (rc != CLEARMOE_OK) return rc;
+        CLEARMOE_STAGE(CLEARMOE_STAGE_PERMUTE, st,
+                       launch_gather_rows_elem(s.dtype, x, perm, offsets + s.E,
+                                               static_cast<int64_t>(s.T) * s.k, s.k, s.D, xperm, st));
+        return CLEARMOE_OK;
+    }
     int32_t* tc = at<int32_t>(ws, L.tile_counts);
     int32_t* tb = at<int32_t>(ws, L.tile_base);
     const int64_t nt = route_tiles(s.T);
@@ -523,6 +573,8 @@ const char* clearmoe_status_string(int status) {
 size_t clearmoe_workspace_bytes(const clearmoe_shape* shape) {
     if (shape != nullptr && check_shape(shape, true, true) == CLEARMOE_OK && unaligned_layer(*shape))
         return pad_layout(*shape).total;
+    if (shape != nullptr && check_shape(shape, false, true) == CLEARMOE_OK && unaligned_rows(*shape))
+        return route_pads(*shape).total;     // route / dispatch-only shape
     if (check_shape(shape, false) != CLEARMOE_OK) return 0;
     clearmoe_shape s = *shape;
     if (check_shape(shape, true) != CLEARMOE_OK) {  // route / dispatch-only shape
@@ -535,9 +587,11 @@ size_t clearmoe_workspace_bytes(const clearmoe_shape* shape) {
 
 int clearmoe_route(const clearmoe_shape* shape, const void* x, const void* Wg, const float* bg,
                    int32_t* idx, float* gate, void* ws, size_t ws_bytes, hipStream_t stream) {
-    int rc = check_shape(shape, false);
+    int rc = check_shape(shape, false, true);
     if (rc != CLEARMOE_OK) return rc;
     const clearmoe_shape& s = *shape;
+    if (unaligned_rows(s))
+        return route_unaligned(s, linear_router(Wg, bg), x, idx, gate, ws, ws_bytes, stream);
     const bool tok = s.T > 0;                 // per-token arrays may be NULL when T == 0
     if (!Wg || (tok && (!x || !idx || !gate))) return CLEARMOE_ERR_INVALID_ARG;
     if (!aligned(x, 16) || !aligned(Wg, 16) || !aligned(idx, 4) || !aligned(gate, 4) ||
@@ -552,9 +606,14 @@ int clearmoe_route(const clearmoe_shape* shape, const void* x, const void* Wg, c
 
 int clearmoe_route_ex(const clearmoe_shape* shape, const clearmoe_router* router, const void* x,
                       int32_t* idx, float* gate, void* ws, size_t ws_bytes, hipStream_t stream) {
-    int rc = check_shape(shape, false);
+    int rc = check_shape(shape, false, true);
     if (rc != CLEARMOE_OK) return rc;
     const clearmoe_shape& s = *shape;
+    if (unaligned_rows(s)) {
+        rc = check_router(s, router, elem_size(s.dtype));
+        if (rc != CLEARMOE_OK) return rc;
+        return route_unaligned(s, *router, x, idx, gate, ws, ws_bytes, stream);
+    }
     rc = check_router(s, router);
     if (rc != CLEARMOE_OK) return rc;
     const bool tok = s.T > 0;
@@ -570,17 +629,21 @@ int clearmoe_route_ex(const clearmoe_shape* shape, const clearmoe_router* router
 int clearmoe_dispatch(const clearmoe_shape* shape, const int32_t* idx, void* ws, size_t ws_bytes,
                       int32_t* counts, int32_t* offsets, int32_t* perm, int32_t* inv,
                       const void* x, void* xperm, unsigned flags, hipStream_t stream) {
-    int rc = check_shape(shape, false);
+    int rc = check_shape(shape, false, true);
     if (rc != CLEARMOE_OK) return rc;
     const clearmoe_shape& s = *shape;
     const bool tok = s.T > 0;
     if (!counts || !offsets || (tok && (!idx || !perm || !inv))) return CLEARMOE_ERR_INVALID_ARG;
     if (tok && (x == nullptr) != (xperm == nullptr)) return CLEARMOE_ERR_INVALID_ARG;
+    // rows that are whole 16-byte pieces are copied as such; others element
+    // by element
+    const size_t ra = unaligned_rows(s) ? elem_size(s.dtype) : 16;
     if (!aligned(idx, 4) || !aligned(counts, 4) || !aligned(offsets, 4) || !aligned(perm, 4) ||
-        !aligned(inv, 4) || (x && (!aligned(x, 16) || !aligned(xperm, 16))))
+        !aligned(inv, 4) || (x && (!aligned(x, ra) || !aligned(xperm, ra))))
         return CLEARMOE_ERR_INVALID_ARG;
     if (flags & ~static_cast<unsigned>(CLEARMOE_DISPATCH_HIST_IN_WS)) return CLEARMOE_ERR_INVALID_ARG;
     clearmoe_shape sl = s;
+    sl.D = round_up(s.D, piece_elems(s.dtype));
     sl.H = sl.r = sl.q = 0;
     const Layout L = layout(sl);
     if (!ws || !aligned(ws, kAlign) || ws_bytes < L.dispatch_end) return CLEARMOE_ERR_WORKSPACE;
@@ -590,12 +653,18 @@ int clearmoe_dispatch(const clearmoe_shape* shape, const int32_t* idx, void* ws,
 
 int clearmoe_combine(const clearmoe_shape* shape, const void* ye, const int32_t* inv,
                      const float* gate, void* y, hipStream_t stream) {
-    int rc = check_shape(shape, false);
+    int rc = check_shape(shape, false, true);
     if (rc != CLEARMOE_OK) return rc;
     const clearmoe_shape& s = *shape;
     if (s.T > 0 && (!ye || !inv || !gate || !y)) return CLEARMOE_ERR_INVALID_ARG;
-    if (!aligned(ye, 16) || !aligned(y, 16) || !aligned(inv, 4) || !aligned(gate, 4))
+    const size_t ra = unaligned_rows(s) ? elem_size(s.dtype) : 16;
+    if (!aligned(ye, ra) || !aligned(y, ra) || !aligned(inv, 4) || !aligned(gate, 4))
         return CLEARMOE_ERR_INVALID_ARG;
+    if (unaligned_rows(s)) {
+        CLEARMOE_STAGE(CLEARMOE_STAGE_COMBINE, stream,
+                       launch_combine_gated_elem(s.dtype, ye, inv, gate, y, s.T, s.D, s.k, stream));
+        return CLEARMOE_OK;
+    }
     CLEARMOE_STAGE(CLEARMOE_STAGE_COMBINE, stream,
                    launch_combine_gated(s.dtype, ye, inv, gate, y, s.T, s.D, s.k, stream));
     return CLEARMOE_OK;
@@ -1030,6 +1099,30 @@ int ffn_forward_unaligned(const clearmoe_shape& s, const clearmoe_router* router
                           at<void>(ws, pl.inner), layout(a).total, st);
     if (rc != CLEARMOE_OK || T == 0) return rc;
     return launch_pad_copy(eb, yp, y, 1, T, a.D, T, s.D, st) == hipSuccess ? CLEARMOE_OK : CLEARMOE_ERR_HIP;
+}
+
+// Routing on padded copies (see route_pads).  The router has been checked
+// with element alignment; x too is read element by element.
+int route_unaligned(const clearmoe_shape& s, const clearmoe_router& router, const void* x,
+                    int32_t* idx, float* gate, void* ws, size_t ws_bytes, hipStream_t st) {
+    const size_t es = elem_size(s.dtype);
+    if (router.Wg == nullptr || (s.T > 0 && (!x || !idx || !gate))) return CLEARMOE_ERR_INVALID_ARG;
+    if (!elem_aligned(x, es) || !elem_aligned(router.Wg, es) || !elem_aligned(idx, 4) ||
+        !elem_aligned(gate, 4) || !elem_aligned(router.bg, 4))
+        return CLEARMOE_ERR_INVALID_ARG;
+    const RoutePads rp = route_pads(s);
+    if (!ws || !aligned(ws, kAlign) || ws_bytes < rp.total) return CLEARMOE_ERR_WORKSPACE;
+    const int eb = static_cast<int>(es);
+    const int64_t T = s.T, E = s.E;
+    const void* xp;
+    int rc = pad_operand(eb, x, ws, rp.x, 1, T, s.D, T, rp.a.D, st, &xp);
+    clearmoe_router rt = router;
+    if (rc == CLEARMOE_OK && rt.hidden == 0)   // linear router: Wg [E, D]
+        rc = pad_operand(eb, router.Wg, ws, rp.Wg, 1, E, s.D, E, rp.a.D, st, &rt.Wg);
+    if (rc == CLEARMOE_OK && rt.hidden > 0)    // MLP router: Wh [hidden, D] (Wg is [E, hidden])
+        rc = pad_operand(eb, router.Wh, ws, rp.Wh, 1, rt.hidden, s.D, rt.hidden, rp.a.D, st, &rt.Wh);
+    if (rc != CLEARMOE_OK) return rc;
+    return route_impl(rp.a, layout(rp.a), rt, xp, idx, gate, ws, st);
 }
 
 // Layer entry: unaligned shapes through the padded copies, others directly.

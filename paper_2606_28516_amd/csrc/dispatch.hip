@@ -475,6 +475,80 @@ hipError_t launch_combine_gated(int dtype, const void* ye, const int32_t* inv, c
     return hipGetLastError();
 }
 
+// Row width D that is not a multiple of the elements of a 16-byte piece:
+// the same row gather and gated combine one element per thread (the
+// combine's arithmetic is the 16-byte kernel's: float32 fma in slot order
+// from 0, one rounding to the storage type).
+template <typename T>
+__global__ __launch_bounds__(256) void k_gather_rows_elem(const T* __restrict__ x,
+                                                          const int32_t* __restrict__ perm,
+                                                          const int32_t* __restrict__ nreal,
+                                                          int64_t A, int k, int D,
+                                                          T* __restrict__ xperm) {
+    int64_t rows = *nreal;                        // rows past offsets[E] are not written
+    rows = rows < 0 ? 0 : (rows > A ? A : rows);
+    const int64_t n = rows * D;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t p = i / D, c = i - p * D;
+        const int64_t a = perm[p];
+        if (a >= 0 && a < A) xperm[i] = x[(a / k) * D + c];
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void k_combine_gated_elem(const T* __restrict__ ye,
+                                                            const int32_t* __restrict__ inv,
+                                                            const float* __restrict__ gate,
+                                                            T* __restrict__ y, int64_t Tn, int D,
+                                                            int k) {
+    const int64_t n = Tn * D, A = Tn * k;
+    for (int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; i < n;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t t = i / D, c = i - t * D;
+        float acc = 0.0f;
+        for (int j = 0; j < k; ++j) {
+            const int64_t p = inv[t * k + j];
+            if (p >= 0 && p < A)                  // never follow an invalid index
+                acc = __builtin_fmaf(gate[t * k + j], Elem<T>::to_f32(ye[p * D + c]), acc);
+        }
+        y[i] = Elem<T>::from_f32(acc);
+    }
+}
+
+static unsigned elem_blocks(int64_t n) {
+    const int64_t b = (n + 255) / 256;
+    return static_cast<unsigned>(b < 8192 ? b : 8192);
+}
+
+hipError_t launch_gather_rows_elem(int dtype, const void* x, const int32_t* perm,
+                                   const int32_t* nreal, int64_t A, int k, int D, void* xperm,
+                                   hipStream_t st) {
+    if (A * D == 0) return hipSuccess;
+    if (dtype == 0)
+        launch_kernel(k_gather_rows_elem<float>, elem_blocks(A * D), 256, 0, st,
+                      static_cast<const float*>(x), perm, nreal, A, k, D, static_cast<float*>(xperm));
+    else
+        launch_kernel(k_gather_rows_elem<bf16_bits>, elem_blocks(A * D), 256, 0, st,
+                      static_cast<const bf16_bits*>(x), perm, nreal, A, k, D,
+                      static_cast<bf16_bits*>(xperm));
+    return hipGetLastError();
+}
+
+hipError_t launch_combine_gated_elem(int dtype, const void* ye, const int32_t* inv,
+                                     const float* gate, void* y, int64_t T, int D, int k,
+                                     hipStream_t st) {
+    if (T * D == 0) return hipSuccess;
+    if (dtype == 0)
+        launch_kernel(k_combine_gated_elem<float>, elem_blocks(T * D), 256, 0, st,
+                      static_cast<const float*>(ye), inv, gate, static_cast<float*>(y), T, D, k);
+    else
+        launch_kernel(k_combine_gated_elem<bf16_bits>, elem_blocks(T * D), 256, 0, st,
+                      static_cast<const bf16_bits*>(ye), inv, gate, static_cast<bf16_bits*>(y), T,
+                      D, k);
+    return hipGetLastError();
+}
+
 hipError_t launch_combine_residual(int dtype, const float* hsh, const float* hres,
                                    const int32_t* inv, void* y, int64_t T, int D, int k,
                                    int64_t hres_rows, hipStream_t st) {

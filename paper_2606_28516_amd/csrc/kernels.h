@@ -223,6 +223,16 @@ hipError_t launch_residual_add(int dtype, const void* x, const void* f, void* ou
 // scols) or crops (drows <= srows, dcols <= scols).
 hipError_t launch_pad_copy(int elem_bytes, const void* src, void* dst, int64_t batches, int64_t srows,
                            int64_t scols, int64_t drows, int64_t dcols, hipStream_t st);
+// Any row width D, one element per thread: xperm[p] = x[perm[p] / k] for
+// p < *nreal (a device count, e.g. offsets[E]; A = T k rows at most), and
+// the gated combine y[t] = sum_j gate[t, j] ye[inv[t k + j]] (as
+// launch_combine_gated).
+hipError_t launch_gather_rows_elem(int dtype, const void* x, const int32_t* perm,
+                                   const int32_t* nreal, int64_t A, int k, int D, void* xperm,
+                                   hipStream_t st);
+hipError_t launch_combine_gated_elem(int dtype, const void* ye, const int32_t* inv,
+                                     const float* gate, void* y, int64_t T, int D, int k,
+                                     hipStream_t st);
 // Index maps of the padded-batch backend (expert e owns rows [e C, e C + C)):
 // perm_pad [E C] (-1 = padding), inv_pad [A], seg [E + 1] = e C.
 hipError_t launch_pad_index(const int32_t* idx, const int32_t* counts, const int32_t* offsets,

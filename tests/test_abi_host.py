@@ -66,7 +66,10 @@ def test_workspace_bytes_grows_with_shape_and_rejects_bad_shapes():
     assert 0 < a < b and a % 256 == 0
     assert cm.workspace_bytes(_shape(k=5)) == 0          # k > E
     assert cm.workspace_bytes(_shape(E=65, k=1)) == 0    # E > 64
-    assert cm.workspace_bytes(_shape(D=12)) == 0         # r > min(D, H)
+    # r > min(D, H): not a layer, so the routing / dispatch workspace (D = 12
+    # routes on padded copies)
+    assert cm.workspace_bytes(_shape(D=12)) == cm.workspace_bytes(_shape(D=12, H=0, r=0, q=0)) > 0
+    assert cm.workspace_bytes(_shape(D=0)) == 0
     assert cm.workspace_bytes(_shape(D=12, dtype=cm.F32, H=128, r=4, q=4)) > 0
     # unaligned layer shapes: the aligned layer's workspace plus padded copies
     assert cm.workspace_bytes(_shape(D=60, H=100, r=12, q=6)) > cm.workspace_bytes(_shape(H=104, r=16))
@@ -135,9 +138,21 @@ def test_dispatch_combine_ffn_reject_before_launch():
     odd = _shape(q=6)
     assert cm.workspace_bytes(odd) > n
     assert L.clearmoe_ffn_forward(ctypes.byref(odd), *args, FAKE, n, None) == 3
-    # ... and a component entry point keeps the multiples
-    assert L.clearmoe_route(ctypes.byref(_shape(D=60, r=8)), FAKE, FAKE, None, FAKE, FAKE, FAKE, n,
-                            None) == 1
+    # routing with D = 60 runs on padded copies too: it needs their workspace,
+    # and element alignment of x and Wg
+    odd_d = _shape(D=60, r=8)
+    big_n = cm.workspace_bytes(odd_d)
+    assert big_n > n
+    assert L.clearmoe_route(ctypes.byref(odd_d), FAKE, FAKE, None, FAKE, FAKE, FAKE, n, None) == 3
+    assert L.clearmoe_route(ctypes.byref(odd_d), ctypes.c_void_p(0x10001), FAKE, None, FAKE, FAKE,
+                            FAKE, big_n, None) == 1
+    route_only = _shape(D=60, H=0, r=0, q=0)          # no layer fields: routing's own pads
+    assert 0 < cm.workspace_bytes(route_only) < big_n
+    # dispatch / combine rows of 60 elements need element alignment only
+    assert L.clearmoe_combine(ctypes.byref(route_only), ctypes.c_void_p(0x10001), FAKE, FAKE, FAKE,
+                              None) == 1
+    assert L.clearmoe_dispatch(ctypes.byref(route_only), FAKE, FAKE, 4, FAKE, FAKE, FAKE, FAKE,
+                               ctypes.c_void_p(0x10002), FAKE, 0, None) == 3
     # workspace one byte short
     assert L.clearmoe_ffn_forward(ctypes.byref(s), *args, FAKE, n - 1, None) == 3
 

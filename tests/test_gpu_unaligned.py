@@ -1,7 +1,8 @@
-"""GPU parity of the layer entry points on unaligned shapes (D, H, r or q not
-a multiple of the elements of a 16-byte piece), which run on zero-padded
-copies of their operands: routing bit-exact and y within the bars against
-the oracle, which computes the unpadded layer.  Cases: top-1 and top-2, both
+"""GPU parity of the entry points on unaligned shapes (D, H, r or q not a
+multiple of the elements of a 16-byte piece): the layer entry points and
+routing run on zero-padded copies of their operands, dispatch and combine
+copy rows element by element.  Routing bit-exact and y within the bars
+against the oracle, which computes the unpadded layer.  Cases: top-1 and top-2, both
 dtypes, class tokens, the MLP router, the dense FFN, and a shape that pads
 into the fused top-1 kernel's range (one workgroup per tile, class rows in
 its launch)."""
@@ -13,8 +14,9 @@ import oracle
 from paper_2606_28516_amd import clearmoe as cm
 from paper_2606_28516_amd import synth
 
-from parity_util import (BF16_FROB_REGRESS, F32_MAXREL, MARGIN, assert_elementwise, bound_excluded, dev,
-                         frob_rel, gpu_ffn, gpu_ffn_ex, max_rel)
+from parity_util import (BF16_FROB_REGRESS, F32_MAXREL, MARGIN, assert_elementwise, assert_gates,
+                         assert_routing, bound_excluded, check_dispatch, confidence_gap, dev, frob_rel,
+                         gpu_ffn, gpu_ffn_ex, gpu_router, max_rel)
 
 pytestmark = pytest.mark.gpu
 
@@ -112,3 +114,66 @@ def test_unaligned_dense_ffn(dt, T, D, H):
         assert max_rel(got, ref) <= F32_MAXREL
     else:
         assert frob_rel(got, ref) <= BF16_FROB_REGRESS
+
+
+@pytest.mark.parametrize("dt,T,D,E,k", [
+    ("bf16", 3001, 60, 8, 2),       # 64-token histogram tiles, inline scan
+    ("f32", 1500, 30, 5, 1),
+    ("bf16", 70001, 100, 8, 2),     # 256-token tiles, chunked scan
+])
+def test_unaligned_route_dispatch_combine(dt, T, D, E, k):
+    """Routing on padded copies of x and Wg, dispatch with element-wise row
+    copies and the element-wise gated combine (D not a multiple of the
+    elements of a 16-byte piece): routing bit-exact (near ties excluded),
+    gates within 2e-5, the dispatch bit-exact against the oracle's of the
+    same indices, every copied row bit for bit, and the combine of the
+    copied rows (identity experts) against the oracle's combine."""
+    L = synth.make_dispatch(T=T, D=D, E=E, k=k, dtype=dt, seed=T + D)
+    x, Wg, bg = dev(L["x"]), dev(L["Wg"]), dev(L["bg"])
+    s = cm.make_shape(T, D, E, k, cm.BF16 if dt == "bf16" else cm.F32)
+    ws = cm.alloc_workspace(s)
+    idx, gate = cm.route(x, Wg, bg, k, ws=ws)
+    counts, offsets, perm, inv, xperm = cm.dispatch(idx, E, ws=ws, x=x, hist_in_ws=True)
+    y = cm.combine(xperm, inv, gate)
+    torch.cuda.synchronize()
+    idx_np, gate_np = idx.cpu().numpy(), gate.cpu().numpy()
+    lg = oracle.router_logits(L["x"], L["Wg"], L["bg"])
+    tie = assert_routing(idx_np, lg, k)
+    assert_gates(gate_np, lg, idx_np, k, tie)
+    perm_np, inv_np = perm.cpu().numpy(), inv.cpu().numpy()
+    check_dispatch(idx_np, E, counts.cpu().numpy(), offsets.cpu().numpy(), perm_np, inv_np)
+    xs = cm.to_stored(x)
+    rows = cm.to_stored(xperm)
+    assert np.array_equal(rows, xs[perm_np // k])
+    ref = oracle.combine(rows, inv_np, gate_np, k)
+    got = oracle.widen(cm.to_stored(y))
+    bound = (2.0 ** -8 if dt == "bf16" else 1e-6) * np.abs(ref) + 1e-6
+    assert np.all(np.abs(got - ref) <= bound)
+
+
+def test_unaligned_route_ex_mlp_and_adaptive():
+    """route_ex with D = 60: the MLP router (its Wh padded) and the adaptive
+    router, against the oracle."""
+    L = synth.make_dispatch(T=2000, D=60, E=6, k=2, dtype="bf16", seed=3)
+    lay = {"x": L["x"], "Wg": L["Wg"], "bg": L["bg"],
+           "cfg": synth.LayerConfig("u", T=2000, D=60, H=8, E=6, k=2, r=0, q=0, dtype="bf16", seed=3)}
+    M = synth.with_mlp_router(lay, h=16, seed=5)
+    r, keep = gpu_router(M)
+    s = cm.make_shape(2000, 60, 6, 2, cm.BF16)
+    idx, gate = cm.route_ex(dev(L["x"]), r, 6, 2, ws=cm.alloc_workspace(s))
+    torch.cuda.synchronize()
+    lg, _ = oracle.mlp_router_logits(L["x"], M["router"]["Wh"], M["router"]["bh"], M["Wg"], M["bg"], "bf16")
+    tie = assert_routing(idx.cpu().numpy(), lg, 2)
+    assert_gates(gate.cpu().numpy(), lg, idx.cpu().numpy(), 2, tie)
+    del keep
+    lg = oracle.router_logits(L["x"], L["Wg"], L["bg"])
+    tau = float(np.quantile(oracle.confidence(lg), 0.5))
+    A = dict(lay, router={"kind": "adaptive", "tau": tau})
+    r, keep = gpu_router(A)
+    idx, gate = cm.route_ex(dev(L["x"]), r, 6, 2, ws=cm.alloc_workspace(s))
+    torch.cuda.synchronize()
+    i_ref, g_ref = oracle.adaptive_topk(lg, tau)
+    ok = ~bound_excluded((oracle.margins(lg, 2) < MARGIN) | (confidence_gap(lg, tau) < 1e-9))
+    assert np.array_equal(idx.cpu().numpy()[ok], i_ref[ok])
+    assert np.all(np.abs(gate.cpu().numpy()[ok] - g_ref[ok]) <= 2e-5)
+    del keep
