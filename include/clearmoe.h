@@ -16,8 +16,10 @@
  *     resources that an entry point creates on first use and keeps until
  *     the process ends: clearmoe_ffn_forward_padded, a pinned 256-byte host
  *     buffer per calling thread (and an event per call, destroyed before it
- *     returns); clearmoe_ffn_forward_ex with class tokens, a side stream and
- *     two events per device; the stage timer, the events it is started with.
+ *     returns); clearmoe_ffn_forward and _ex on a top-2 layer in expert-pair
+ *     order, or with class tokens, a side stream and two events per device
+ *     (clearmoe_ffn_forward_noalloc creates none); the stage timer, the
+ *     events it is started with.
  *   - Matrices are row-major and contiguous.  Weights are stored [out, in]
  *     (the nn.Linear convention), so every product is A[M,K] B[N,K]^T.
  *   - x, W1, US, Vt, P, Q, Wg, ye and y have element type shape->dtype

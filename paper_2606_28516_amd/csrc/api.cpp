@@ -793,7 +793,8 @@ int ffn_forward_impl(const clearmoe_shape* shape, const clearmoe_router* router,
     // token order needs only x, so it runs on the side stream while routing
     // and the pair dispatch run here (they leave most of the chip idle); the
     // pair products wait for it.
-    const bool fc1_aside = pair_path(s) && !router->adaptive && T > 0;
+    // (not in the no-allocation variant: it creates no stream or event)
+    const bool fc1_aside = pair_path(s) && !router->adaptive && T > 0 && packed == nullptr;
     if (fc1_aside) {
         side_lock = std::unique_lock<std::mutex>(g_side_mu);
         rc = side_stream(&side);
