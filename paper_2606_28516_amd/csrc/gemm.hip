@@ -565,10 +565,10 @@ static hipError_t gemm_cfg(const GemmDesc& g, hipStream_t st) {
 // Tile choice by shape (measured on MI355X at the layer's sizes): with few
 // 128x128 tiles the GEMM is latency bound, so 64-row tiles (more workgroups
 // per CU) win; long-K skinny products want 64x64 with four stages in flight;
-// large products (a thousand 256x256 tiles or more, e.g. fc1 of a 50432-token
-// DeiT-Base layer) take 256x256 tiles over 8 waves, two per SIMD (half the
-// operand bytes per flop of 128x128, and one wave's waits overlap the other's
-// MFMAs).
+// the large bfloat16 products take 256x128 tiles over 8 waves with 64-byte
+// stages (two workgroups per CU), and large float32 ones 256x256 tiles over
+// 8 waves, two per SIMD (half the operand bytes per flop of 128x128, and one
+// wave's waits overlap the other's MFMAs).
 template <typename Tin>
 static hipError_t gemm_dt(const GemmDesc& g, hipStream_t st) {
     const int64_t mt128 = (g.M + 127) / 128;
