@@ -115,3 +115,33 @@ def test_mlp_router_full_softmax_gates():
     M["renorm"] = 0
     g = gpu_ffn_ex(M)
     _check(M, g)
+
+
+def test_class_tokens_in_the_fused_launch_full_softmax_gates():
+    """renorm = 0 with class tokens: the dispatch kernels order the expert
+    tokens (the fused kernel's own dispatch assumes gates of 1) and the class
+    rows still run inside the fused launch (one workgroup per tile)."""
+    L = _layer("bf16", 9000, 384, 1536, 8, 1, 128, 32, seed=21)
+    C = synth.with_class_tokens(L, stride=197)
+    C["renorm"] = 0
+    cm.timing_start(cm.stage_names(), max_records=64)
+    try:
+        g = gpu_ffn_ex(C)
+    finally:
+        t = cm.timing_stop()
+    assert t.get("fused_top1", (0, 0))[1] == 1 and t.get("permute", (0, 0))[1] >= 1, t
+    ref = oracle.ffn_forward_layer(C)
+    tie = bound_excluded(oracle.margins(ref["logits"], 1) < MARGIN) & ~ref["cls"]
+    ok = ~tie
+    assert np.array_equal(g["idx"][ok], ref["idx"][ok])
+    assert np.all(np.abs(g["gate"][ok] - ref["gate"][ok]) <= 2e-5)
+    e = frob_rel(g["y"][ok], ref["y"][ok])
+    assert e <= BF16_FROB_REGRESS, e
+    assert_elementwise(g["y"][ok], ref["y"][ok], "bf16")
+
+
+def test_unaligned_layer_full_softmax_gates():
+    """An unaligned shape (padded copies) keeps the gate rule."""
+    L = _layer("bf16", 700, 100, 250, 5, 2, 20, 12, seed=8)
+    g = gpu_ffn(L)
+    _check(L, g)
